@@ -1,0 +1,153 @@
+/* saturn.h -- C ABI of the MI355X fine-tuning-step library (libsaturn.so).
+ *
+ * The Saturn paper (Nagrecha & Kumar, arXiv 2309.01226) schedules a set of
+ * model-training tasks, each given by a model, its data and its own
+ * hyper-parameters (Sec. 3.1 "Workload Specification", the Task / HParams
+ * API), drawn from model selection: grid or random search over batch size and
+ * learning rate, and layer-wise fine-tuning, i.e. choosing which layers to
+ * train (Abstract; Sec. 2 "Model selection"; Table 3).  The work it orders is
+ * the fine-tuning step of each task.  This library runs that step on one
+ * gfx950 GPU: one opaque model per task, advanced by sat_train_step.
+ *
+ * Conventions for every call:
+ *   - returns SAT_OK or a negative sat_status; out-parameters are written only
+ *     on SAT_OK; sat_last_error() gives a message (thread-local);
+ *   - no call aborts the process;
+ *   - "device pointer" means memory of the model's GPU; "host pointer" means
+ *     ordinary CPU memory;
+ *   - distinct models may be driven from one host thread on distinct streams;
+ *     a single model is not re-entrant.
+ */
+#ifndef SATURN_H
+#define SATURN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct sat_model sat_model; /* opaque, owned by the library */
+
+typedef enum {
+  SAT_OK = 0,
+  SAT_EINVAL = -1,      /* invalid configuration or argument */
+  SAT_ENOMEM = -2,      /* the arena is too small (or device allocation failed) */
+  SAT_EHIP = -3,        /* a HIP runtime call failed */
+  SAT_ESTATE = -4,      /* the model is in a failed state */
+  SAT_ENONFINITE = -5,  /* the loss read back is NaN or infinite */
+  SAT_ENOTSUP = -6      /* the operation does not apply to this model */
+} sat_status;
+
+typedef enum { SAT_GPT2 = 0, SAT_GPTJ = 1, SAT_VIT = 2 } sat_arch;
+
+/* Per-task configuration: architecture, depth, width, batch size, learning
+ * rate and frozen-layer count of one model (the hyper-parameters a model
+ * selection task carries, Sec. 3.1).
+ *   GPT2: pre-LN decoder, learned positions, bias on every linear, untied head
+ *         without bias, tanh GELU, causal attention.
+ *   GPTJ: one LN per block feeding attention and MLP in parallel, rotary on the
+ *         first rotary_dim dims of every head, no q/k/v/out bias, head bias.
+ *   VIT : pre-LN encoder over (img/patch)^2 patches + a CLS token, erf GELU,
+ *         bidirectional attention, class head on the CLS row. */
+typedef struct {
+  uint32_t struct_size; /* must equal sizeof(sat_config) */
+  int32_t arch;         /* sat_arch */
+  int32_t n_layers, d_model, n_heads, d_mlp;
+  int32_t vocab;        /* decoders: vocabulary size; VIT: number of classes */
+  int32_t seq_len;      /* decoders: tokens per row; VIT: ignored (derived) */
+  int32_t img_size, patch, channels; /* VIT only */
+  int32_t rotary_dim;   /* GPTJ: even, <= head dim; others 0 */
+  int32_t batch;        /* rows per step, fixed per model */
+  int32_t frozen_layers;/* k in [0, n_layers]: k > 0 freezes the embeddings and blocks [0, k) */
+  double lr, beta1, beta2, eps, weight_decay; /* AdamW, decoupled decay on every trainable
+                          tensor; double so that 1 - beta is exact to float precision */
+  float init_std;       /* std of the N(0, std^2) initialisation of matrices and tables */
+  float ln_eps;
+  uint64_t seed;        /* counter-based initialisation seed */
+} sat_config;
+
+/* Bytes of device memory a model of this configuration needs (parameters,
+ * bf16 shadow, gradients, AdamW moments, activations, workspace).
+ * Errors: SAT_EINVAL for an invalid configuration. */
+sat_status sat_model_arena_bytes(const sat_config* cfg, size_t* bytes);
+
+/* Create a model on the current HIP device.
+ *   arena: device pointer of at least arena_bytes bytes, borrowed until
+ *          sat_model_destroy; NULL makes the library allocate (and own) it.
+ *   hip_stream: hipStream_t every kernel of this model is enqueued on (NULL =
+ *          the null stream); borrowed.
+ * Initialises parameters (matrices and tables ~ N(0, init_std^2) from `seed`,
+ * biases 0, LN gains 1) and zeroes AdamW state; t = 0.
+ * Errors: SAT_EINVAL (configuration), SAT_ENOMEM (arena_bytes too small or
+ * allocation failure), SAT_EHIP. */
+sat_status sat_model_create(const sat_config* cfg, void* arena, size_t arena_bytes,
+                            void* hip_stream, sat_model** out);
+
+/* One fine-tuning step: forward, backward down to block k, AdamW on the
+ * trainable tensors (t += 1), all enqueued on the model's stream.
+ *   inputs: device pointer; decoders int32 tokens [batch, seq_len] in
+ *           [0, vocab); VIT fp32 images [batch, channels, img, img].
+ *   labels: device pointer, int32; decoders [batch, seq_len], VIT [batch];
+ *           -1 = ignore, otherwise in [0, vocab).
+ *   loss_out: host pointer or NULL.  Non-NULL: the call waits for the step and
+ *           writes the mean loss over non-ignored labels.  NULL: the call
+ *           returns as soon as the work is enqueued.
+ * Out-of-range token ids or labels are not checked on the device.
+ * Errors: SAT_EINVAL (null model or pointers), SAT_ESTATE, SAT_EHIP,
+ * SAT_ENONFINITE (loss read back is not finite; the update was applied). */
+sat_status sat_train_step(sat_model* m, const void* inputs, const int32_t* labels,
+                          float* loss_out);
+
+/* Forward only; writes the mean loss to the host pointer loss_out (waits for
+ * the stream).  Changes no parameter or optimizer state. */
+sat_status sat_eval_loss(sat_model* m, const void* inputs, const int32_t* labels,
+                         float* loss_out);
+
+/* Release the model (and the arena when the library allocated it).  Waits for
+ * the model's stream.  NULL is accepted. */
+sat_status sat_model_destroy(sat_model* m);
+
+/* ---- parameter table and test / resume accessors --------------------------
+ * Tensors are numbered 0..n-1 bottom to top (embeddings, blocks 0..L-1, final
+ * LN, head).  Linear weights are [out, in] (y = x W^T + b).  All host buffers
+ * are fp32 (t: int64) of the tensor's element count; every accessor waits for
+ * the model's stream. */
+int32_t sat_num_params(const sat_model* m);
+/* name: static string owned by the library; shape: [rows, cols] (cols = 1 for vectors). */
+sat_status sat_param_info(const sat_model* m, int32_t i, const char** name, int64_t shape[2],
+                          int32_t* trainable);
+sat_status sat_param_read(sat_model* m, int32_t i, float* host);
+/* Writes the fp32 master and refreshes the bf16 shadow. */
+sat_status sat_param_write(sat_model* m, int32_t i, const float* host);
+/* Gradient of the last sat_train_step; zeros for frozen tensors. */
+sat_status sat_grad_read(sat_model* m, int32_t i, float* host);
+/* Residual stream entering block `layer` (fp32 [batch * seq, d_model]) after
+ * the last forward; layer = n_layers gives the stream entering the final LN. */
+sat_status sat_activation_read(sat_model* m, int32_t layer, float* host);
+/* Logits of the last forward, fp32 [rows, vocab] (rows = batch * seq, VIT: batch). */
+sat_status sat_logits_read(sat_model* m, float* host);
+sat_status sat_state_read(sat_model* m, int32_t i, float* mom, float* vel, int64_t* t);
+sat_status sat_state_write(sat_model* m, int32_t i, const float* mom, const float* vel, int64_t t);
+/* Number of trainable parameters (elements) and algorithmic FLOPs of one step. */
+sat_status sat_model_stats(const sat_model* m, int64_t* n_params, int64_t* n_trainable,
+                           double* step_flops);
+
+/* ---- measurement ---------------------------------------------------------
+ * Per-launch timing of one kernel class with HIP events recorded on the
+ * model's stream around each matching launch (at most max_launches between
+ * two reads; later launches are not timed).  kind: 0 off, 1 the forward QKV
+ * product (GPT-J: the fused QKV + fc1 product), 2 every GEMM, 3 the AdamW
+ * update, 4 attention forward, 5 attention backward.  Waits for the stream. */
+sat_status sat_model_set_timing(sat_model* m, int32_t kind, int32_t max_launches);
+/* Sum of the timed launches' durations (ms), their count and their
+ * algorithmic work (FLOPs; bytes for AdamW), then resets the counters. */
+sat_status sat_model_timing_read(sat_model* m, double* total_ms, int64_t* launches, double* work);
+
+const char* sat_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SATURN_H */

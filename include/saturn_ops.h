@@ -1,0 +1,121 @@
+/* saturn_ops.h -- kernel-level C ABI of libsaturn.so.
+ *
+ * Each call enqueues one kernel of the fine-tuning step (the step that the
+ * Saturn paper, arXiv 2309.01226, schedules for every model-selection task;
+ * Sec. 3.1, Table 3) on `stream` (a hipStream_t, NULL = null stream) and
+ * returns without waiting.  All tensor pointers are device pointers owned by
+ * the caller; matrices are row-major with the given leading dimension (in
+ * elements).  bf16 means IEEE bfloat16 storage (uint16).  The calls exist so
+ * that every kernel can be checked and timed on its own; the model calls in
+ * saturn.h use the same kernels.  Errors: SAT_EINVAL for bad sizes or null
+ * pointers, SAT_EHIP when the launch fails.  Status codes as in saturn.h.
+ */
+#ifndef SATURN_OPS_H
+#define SATURN_OPS_H
+
+#include <stdint.h>
+
+#include "saturn.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Dense contraction C[m, n] = sum_k A(m, k) B(n, k) (bf16 operands, fp32
+ * accumulation), the forward, input-gradient and weight-gradient products of
+ * every linear layer.  Layout 0: A(m, k) = A[m*lda + k], B(n, k) = B[n*ldb + k];
+ * layout 1: A(m, k) = A[k*lda + m], B(n, k) = B[k*ldb + n].
+ * Epilogue 0: fp32 out = C + bias.  1: fp32 out = resid + C + bias (resid may
+ * equal out).  2: bf16 out = C + bias, and, when out2 != NULL, bf16
+ * out2[m, n - gelu_col0] = GELU(C + bias) for n >= gelu_col0.  3: bf16 out =
+ * C * GELU'(aux[m, n]).  bias (fp32, may be NULL) applies to columns
+ * n >= bias_col0 as bias[n - bias_col0].  gelu_erf: 0 tanh form, 1 erf form. */
+typedef struct {
+  const void* A;
+  const void* B;
+  int32_t M, N, K;
+  int64_t lda, ldb;
+  int32_t a_layout, b_layout, epilogue;
+  void* out;
+  int64_t ldo;
+  const float* bias;
+  int32_t bias_col0;
+  const float* resid;
+  int64_t ldr;
+  void* out2;
+  int64_t ldo2;
+  int32_t gelu_col0;
+  const void* aux;
+  int64_t ldaux;
+  int32_t gelu_erf;
+} sat_gemm_desc;
+sat_status sat_op_gemm(const sat_gemm_desc* d, void* stream);
+
+/* LayerNorm forward over `rows` rows of length d: x fp32 (row r at
+ * x + r*row_stride*ldx), y bf16 [rows, ldy], mean / rstd fp32 [rows]. */
+sat_status sat_op_layernorm_fwd(const float* x, int64_t ldx, int64_t row_stride, const float* g,
+                                const float* b, void* y, int64_t ldy, float* mean, float* rstd,
+                                int32_t rows, int32_t d, float eps, void* stream);
+/* LayerNorm backward: dres[r] += dx[r] (fp32, same row addressing as x);
+ * dg, db fp32 [d] (overwritten).  work: fp32 scratch of 2*n_part*d floats,
+ * n_part = min(rows, 256). */
+sat_status sat_op_layernorm_bwd(const float* dy, int64_t lddy, const float* x, int64_t ldx,
+                                int64_t row_stride, const float* g, const float* mean,
+                                const float* rstd, float* dres, int64_t ldres, float* dg,
+                                float* db, float* work, int32_t rows, int32_t d, void* stream);
+
+/* Flash-style attention forward.  q, k, v, o: bf16, element (b, h, s, j) at
+ * ptr[(b*S + s)*ld + h*dh + j].  lse: fp32 [B, H, S] natural-log
+ * log-sum-exp of the scaled scores.  scale multiplies q.k. */
+sat_status sat_op_attention_fwd(const void* q, const void* k, const void* v, int64_t ldq,
+                                int64_t ldk, int64_t ldv, void* o, int64_t ldo, float* lse,
+                                int32_t B, int32_t H, int32_t S, int32_t dh, int32_t causal,
+                                float scale, void* stream);
+/* Attention backward from dO (bf16, addressed like o), the forward's o and
+ * lse; writes dq, dk, dv (bf16, addressed like q, k, v).  delta: fp32
+ * [B, H, S] scratch. */
+sat_status sat_op_attention_bwd(const void* q, const void* k, const void* v, int64_t ldq,
+                                int64_t ldk, int64_t ldv, const void* o, int64_t ldo,
+                                const float* lse, const void* dout, int64_t lddo, float* delta,
+                                void* dq, void* dk, void* dv, int64_t lddq, int64_t lddk,
+                                int64_t lddv, int32_t B, int32_t H, int32_t S, int32_t dh,
+                                int32_t causal, float scale, void* stream);
+
+/* Rotary on interleaved pairs of the first rd dims of every q and k head, in
+ * place; qk bf16 [B*S, ld] with q at column 0 and k at column H*dh.
+ * inverse = 1 applies the transpose rotation (backward). */
+sat_status sat_op_rotary(void* qk, int64_t ld, int32_t B, int32_t S, int32_t H, int32_t dh,
+                         int32_t rd, int32_t inverse, void* stream);
+
+/* Softmax cross-entropy forward + backward over fp32 logits z [N, ldz]:
+ * row_loss fp32 [N] (0 for label -1), dz bf16 [N, lddz] = (softmax - onehot)
+ * * inv_n (0 rows for label -1), where inv_n = 1 / (number of labels != -1). */
+sat_status sat_op_cross_entropy(const float* z, int64_t ldz, const int32_t* labels, int32_t N,
+                                int32_t V, float* row_loss, void* dz, int64_t lddz, float* inv_n,
+                                void* stream);
+
+/* Fused AdamW over n fp32 values (torch semantics, decoupled decay) at step t
+ * (t >= 1); refreshes the bf16 shadow when shadow != NULL. */
+sat_status sat_op_adamw(float* p, const float* g, float* m, float* v, void* shadow, int64_t n,
+                        double lr, double beta1, double beta2, double eps, double wd, int64_t t,
+                        void* stream);
+
+/* Token embedding forward h[t] = wte[tok[t]] (+ wpe[t % S]) and its
+ * deterministic backward dwte[v] = sum over t with tok[t] == v of dh[t] in
+ * increasing t, written for every v < V (zero rows for absent tokens).
+ * work: int32 scratch of T entries.  Backward limits: T <= 16384, V < 65536
+ * (SAT_EINVAL otherwise). */
+sat_status sat_op_embed_fwd(const int32_t* tok, const float* wte, const float* wpe, float* h,
+                            int32_t T, int32_t S, int32_t d, int32_t V, void* stream);
+sat_status sat_op_embed_bwd(const int32_t* tok, const float* dh, float* dwte, int32_t T,
+                            int32_t d, int32_t V, int32_t* work, void* stream);
+
+/* Column sum out[c] = sum_r X[r, c] of an fp32 [rows, ldx] matrix,
+ * deterministic; work: fp32 scratch of min(rows, 256) * cols floats. */
+sat_status sat_op_colsum(const float* X, int64_t ldx, int32_t rows, int32_t cols, float* out,
+                         float* work, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SATURN_OPS_H */

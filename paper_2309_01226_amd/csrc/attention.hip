@@ -1,0 +1,507 @@
+// Flash-style attention forward and backward on gfx950 MFMA (bf16 operands,
+// fp32 accumulation), causal (decoders) or bidirectional (ViT).
+//
+// Per head: P = softmax(scale * q k^T + mask), o = P v, saved per query:
+// lse = log sum_j exp(scale * q.k_j).  The S x S matrix never touches HBM:
+// key/value (or query/gradient) blocks are staged through LDS and the softmax
+// runs online.
+//
+// Layout trick.  With v_mfma_f32_32x32x16_bf16 a lane of the 32 x 32
+// accumulator owns one column and 16 rows.  The forward and the dQ kernel
+// compute the transposed score tile S^T = K Q^T, so each lane owns one query
+// (column) and its running max / sum / rescale are per-lane scalars; its 16
+// probabilities are then already an MFMA operand for O^T += V^T P^T, provided
+// V^T is read from LDS with the same key permutation.  The dK/dV kernel owns
+// keys instead and computes S = Q K^T the other way round.
+//
+// Backward without atomics: one kernel accumulates dK and dV per key block
+// over all query blocks, a second accumulates dQ per query block over all key
+// blocks (the score and dP tiles are recomputed in both).  Large head dims are
+// split into output slices so the accumulators fit in registers.
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr float LOG2E = 1.4426950408889634f;
+constexpr float LN2 = 0.6931471805599453f;
+constexpr int NT = 256;  // 4 waves
+constexpr int WROWS = 32;  // rows (queries or keys) owned by each wave
+constexpr int WG_ROWS = 4 * WROWS;
+
+__device__ __forceinline__ floatx16 zero16() {
+  floatx16 z;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) z[r] = 0.f;
+  return z;
+}
+
+// Copy rows [row0, row0 + ROWS) x cols [0, DH) of a bf16 matrix (row r at
+// src + r * ld) into LDS dst[r][c] (pitch P), zero for rows >= nvalid.
+template <int ROWS, int DH, int P>
+__device__ __forceinline__ void stage_rows(const bf16* __restrict__ src, long ld, int row0,
+                                           int nvalid, bf16* dst) {
+  constexpr int VPR = DH / 8;
+  constexpr int NV = ROWS * VPR;
+  for (int v = threadIdx.x; v < NV; v += NT) {
+    int r = v / VPR, c = (v % VPR) * 8;
+    u32x4 x = {0u, 0u, 0u, 0u};
+    if (row0 + r < nvalid) x = *reinterpret_cast<const u32x4*>(src + (long)(row0 + r) * ld + c);
+    *reinterpret_cast<u32x4*>(dst + r * P + c) = x;
+  }
+}
+
+// Transposed copy: dst[c][r] = src[row0 + r][col0 + c] for r < ROWS, c < COLS
+// (zero for rows >= nvalid or columns >= DH), via 8 x 8 register transposes.
+template <int ROWS, int COLS, int DH, int P>
+__device__ __forceinline__ void stage_rows_T(const bf16* __restrict__ src, long ld, int row0,
+                                             int nvalid, int col0, bf16* dst) {
+  constexpr int RB = ROWS / 8, CB = COLS / 8, NB = RB * CB;
+  for (int b = threadIdx.x; b < NB; b += NT) {
+    int rb = b % RB, cb = b / RB;
+    int c = col0 + cb * 8;
+    u32x4 x[8];
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) {
+      int r = row0 + rb * 8 + kk;
+      u32x4 z = {0u, 0u, 0u, 0u};
+      x[kk] = (r < nvalid && c < DH) ? *reinterpret_cast<const u32x4*>(src + (long)r * ld + c) : z;
+    }
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      u32x4 lo, hi;
+#pragma unroll
+      for (int w2 = 0; w2 < 4; ++w2) {
+        uint32_t a = x[2 * w2][w], e = x[2 * w2 + 1][w];
+        lo[w2] = __builtin_amdgcn_perm(e, a, 0x05040100u);
+        hi[w2] = __builtin_amdgcn_perm(e, a, 0x07060302u);
+      }
+      *reinterpret_cast<u32x4*>(dst + (cb * 8 + 2 * w) * P + rb * 8) = lo;
+      *reinterpret_cast<u32x4*>(dst + (cb * 8 + 2 * w + 1) * P + rb * 8) = hi;
+    }
+  }
+}
+
+// MFMA operand of 8 consecutive bf16 from LDS.
+__device__ __forceinline__ bf16x8 lds8(const bf16* p) {
+  return *reinterpret_cast<const bf16x8*>(p);
+}
+// Operand in the accumulator's row permutation: for lane group g the 16-wide
+// chunk starting at `base` contributes elements base + 4g + {0..3} and
+// base + 8 + 4g + {0..3}.
+__device__ __forceinline__ bf16x8 lds8_perm(const bf16* row, int base, int g) {
+  bf16x4 a = *reinterpret_cast<const bf16x4*>(row + base + 4 * g);
+  bf16x4 b = *reinterpret_cast<const bf16x4*>(row + base + 8 + 4 * g);
+  bf16x8 r;
+  r[0] = a[0]; r[1] = a[1]; r[2] = a[2]; r[3] = a[3];
+  r[4] = b[0]; r[5] = b[1]; r[6] = b[2]; r[7] = b[3];
+  return r;
+}
+// Eight accumulator values r = 8h .. 8h+7 as a bf16 operand.
+__device__ __forceinline__ bf16x8 acc_to_bf16(const floatx16& x, int h) {
+  bf16x8 r;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r[e] = f2bf(x[8 * h + e]);
+  return r;
+}
+// Row (within a 32 x 32 tile) held by accumulator register r of lane group g.
+__device__ __forceinline__ int acc_row(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
+
+// Load a 32-row x DH operand slice for this lane (row = lane % 32) from global.
+template <int DH>
+__device__ __forceinline__ void load_row_operand(const bf16* __restrict__ base, long ld, int row,
+                                                 int nvalid, int g, bf16x8* out) {
+#pragma unroll
+  for (int c = 0; c < DH / 16; ++c) {
+    u32x4 z = {0u, 0u, 0u, 0u};
+    u32x4 x = (row < nvalid) ? *reinterpret_cast<const u32x4*>(base + (long)row * ld + c * 16 + 8 * g) : z;
+    out[c] = *reinterpret_cast<bf16x8*>(&x);
+  }
+}
+
+constexpr int round32(int x) { return (x + 31) / 32 * 32; }
+
+// Heavy (late) causal blocks first.
+__device__ __forceinline__ int block_index(int nblk, int causal) {
+  return causal ? (nblk - 1 - (int)blockIdx.x) : (int)blockIdx.x;
+}
+
+// ================================================================ forward
+template <int DH, int BKV>
+__global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
+  constexpr int DHP = round32(DH);
+  constexpr int PK = DH + 8;    // K tile pitch
+  constexpr int PV = BKV + 8;   // V^T tile pitch
+  __shared__ __attribute__((aligned(16))) bf16 Ks[BKV * PK];
+  __shared__ __attribute__((aligned(16))) bf16 Vt[DHP * PV];
+
+  const int S = a.S;
+  const int nqb = (S + WG_ROWS - 1) / WG_ROWS;
+  const int qb = block_index(nqb, a.causal);
+  const int bh = blockIdx.y, b = bh / a.H, h = bh % a.H;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, g = lane >> 5;
+  const int q0 = qb * WG_ROWS;
+  const int q = q0 + wave * WROWS + (lane & 31);
+
+  const bf16* Qb = a.q + (long)b * S * a.ldq + (long)h * DH;
+  const bf16* Kb = a.k + (long)b * S * a.ldk + (long)h * DH;
+  const bf16* Vb = a.v + (long)b * S * a.ldv + (long)h * DH;
+
+  bf16x8 qf[DH / 16];
+  load_row_operand<DH>(Qb, a.ldq, q, S, g, qf);
+
+  floatx16 o[DHP / 32];
+#pragma unroll
+  for (int t = 0; t < DHP / 32; ++t) o[t] = zero16();
+  float m = -INFINITY, l = 0.f;
+  const float sc = a.scale * LOG2E;
+  const int wave_qmax = q0 + wave * WROWS + WROWS - 1;
+
+  const int kv_end = a.causal ? min(S, q0 + WG_ROWS) : S;
+  for (int kv0 = 0; kv0 < kv_end; kv0 += BKV) {
+    __syncthreads();
+    stage_rows<BKV, DH, PK>(Kb, a.ldk, kv0, S, Ks);
+    stage_rows_T<BKV, DHP, DH, PV>(Vb, a.ldv, kv0, S, 0, Vt);
+    __syncthreads();
+    if (a.causal && kv0 > wave_qmax) continue;
+
+    floatx16 s[BKV / 32];
+#pragma unroll
+    for (int t = 0; t < BKV / 32; ++t) {
+      s[t] = zero16();
+#pragma unroll
+      for (int c = 0; c < DH / 16; ++c)
+        s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            lds8(Ks + (t * 32 + (lane & 31)) * PK + c * 16 + 8 * g), qf[c], s[t], 0, 0, 0);
+    }
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < BKV / 32; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        int key = kv0 + t * 32 + acc_row(r, g);
+        float x = s[t][r] * sc;
+        if (key >= S || (a.causal && key > q)) x = -INFINITY;
+        s[t][r] = x;
+        mloc = fmaxf(mloc, x);
+      }
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+    const float mnew = fmaxf(m, mloc);
+    const float alpha = (mnew == -INFINITY) ? 1.f : exp2f(m - mnew);
+    float lsum = 0.f;
+#pragma unroll
+    for (int t = 0; t < BKV / 32; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float p = (mnew == -INFINITY) ? 0.f : exp2f(s[t][r] - mnew);
+        s[t][r] = p;
+        lsum += p;
+      }
+    lsum += __shfl_xor(lsum, 32, 64);
+    l = l * alpha + lsum;
+    m = mnew;
+#pragma unroll
+    for (int t = 0; t < DHP / 32; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
+#pragma unroll
+    for (int t = 0; t < BKV / 32; ++t)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        bf16x8 pb = acc_to_bf16(s[t], hh);
+#pragma unroll
+        for (int ot = 0; ot < DHP / 32; ++ot)
+          o[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              lds8_perm(Vt + (ot * 32 + (lane & 31)) * PV, t * 32 + hh * 16, g), pb, o[ot], 0, 0, 0);
+      }
+  }
+  if (q < S) {
+    const float inv = (l > 0.f) ? 1.f / l : 0.f;
+    bf16* Ob = a.o + ((long)b * S + q) * a.ldo + (long)h * DH;
+#pragma unroll
+    for (int ot = 0; ot < DHP / 32; ++ot)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        int j = ot * 32 + acc_row(r, g);
+        if (j < DH) Ob[j] = f2bf(o[ot][r] * inv);
+      }
+    if (g == 0) a.lse[((long)b * a.H + h) * S + q] = (m + log2f(l)) * LN2;
+  }
+}
+
+// ================================================================ backward
+// delta[b, h, s] = sum_j dO[s, j] * O[s, j]; one wave per (b, s, h).
+__global__ __launch_bounds__(256) void attn_delta_kernel(AttnBwdArgs a) {
+  const int lane = threadIdx.x & 63;
+  const long row = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const long total = (long)a.f.B * a.f.S * a.f.H;
+  if (row >= total) return;
+  const int h = row % a.f.H;
+  const long bs = row / a.f.H;
+  const int dh = a.f.dh;
+  const bf16* o = a.f.o + bs * a.f.ldo + (long)h * dh;
+  const bf16* d = a.dout + bs * a.lddo + (long)h * dh;
+  float acc = 0.f;
+  for (int j = lane; j < dh; j += 64) acc += bf2f(o[j]) * bf2f(d[j]);
+  acc = wave_sum(acc);
+  const int b = bs / a.f.S, s = bs % a.f.S;
+  if (lane == 0) a.delta[((long)b * a.f.H + h) * a.f.S + s] = acc;
+}
+
+// dQ: workgroup = 128 queries of one (b, h); grid.z = output dh slice.
+template <int DH, int DHS, int BKV>
+__global__ __launch_bounds__(NT) void attn_bwd_dq_kernel(AttnBwdArgs a) {
+  constexpr int PK = DH + 8;
+  constexpr int PT = BKV + 8;
+  __shared__ __attribute__((aligned(16))) bf16 Ks[BKV * PK];
+  __shared__ __attribute__((aligned(16))) bf16 Vs[BKV * PK];
+  __shared__ __attribute__((aligned(16))) bf16 Kt[DHS * PT];
+
+  const int S = a.f.S;
+  const int nqb = (S + WG_ROWS - 1) / WG_ROWS;
+  const int qb = block_index(nqb, a.f.causal);
+  const int bh = blockIdx.y, b = bh / a.f.H, h = bh % a.f.H;
+  const int col0 = blockIdx.z * DHS;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, g = lane >> 5;
+  const int q0 = qb * WG_ROWS;
+  const int q = q0 + wave * WROWS + (lane & 31);
+  const long hs = ((long)b * a.f.H + h) * S;
+
+  const bf16* Qb = a.f.q + (long)b * S * a.f.ldq + (long)h * DH;
+  const bf16* Kb = a.f.k + (long)b * S * a.f.ldk + (long)h * DH;
+  const bf16* Vb = a.f.v + (long)b * S * a.f.ldv + (long)h * DH;
+  const bf16* dOb = a.dout + (long)b * S * a.lddo + (long)h * DH;
+
+  bf16x8 qf[DH / 16], df[DH / 16];
+  load_row_operand<DH>(Qb, a.f.ldq, q, S, g, qf);
+  load_row_operand<DH>(dOb, a.lddo, q, S, g, df);
+  const float sc = a.f.scale * LOG2E;
+  const float lse2 = (q < S) ? a.f.lse[hs + q] * LOG2E : 0.f;
+  const float dlt = (q < S) ? a.delta[hs + q] : 0.f;
+
+  floatx16 dq[DHS / 32];
+#pragma unroll
+  for (int t = 0; t < DHS / 32; ++t) dq[t] = zero16();
+  const int wave_qmax = q0 + wave * WROWS + WROWS - 1;
+  const int kv_end = a.f.causal ? min(S, q0 + WG_ROWS) : S;
+  for (int kv0 = 0; kv0 < kv_end; kv0 += BKV) {
+    __syncthreads();
+    stage_rows<BKV, DH, PK>(Kb, a.f.ldk, kv0, S, Ks);
+    stage_rows<BKV, DH, PK>(Vb, a.f.ldv, kv0, S, Vs);
+    stage_rows_T<BKV, DHS, DH, PT>(Kb, a.f.ldk, kv0, S, col0, Kt);
+    __syncthreads();
+    if (a.f.causal && kv0 > wave_qmax) continue;
+#pragma unroll
+    for (int t = 0; t < BKV / 32; ++t) {
+      floatx16 s = zero16(), dp = zero16();
+#pragma unroll
+      for (int c = 0; c < DH / 16; ++c) {
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            lds8(Ks + (t * 32 + (lane & 31)) * PK + c * 16 + 8 * g), qf[c], s, 0, 0, 0);
+        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            lds8(Vs + (t * 32 + (lane & 31)) * PK + c * 16 + 8 * g), df[c], dp, 0, 0, 0);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        int key = kv0 + t * 32 + acc_row(r, g);
+        bool ok = key < S && q < S && !(a.f.causal && key > q);
+        float p = ok ? exp2f(s[r] * sc - lse2) : 0.f;
+        s[r] = p * (dp[r] - dlt);
+      }
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        bf16x8 db = acc_to_bf16(s, hh);
+#pragma unroll
+        for (int ot = 0; ot < DHS / 32; ++ot)
+          dq[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              lds8_perm(Kt + (ot * 32 + (lane & 31)) * PT, t * 32 + hh * 16, g), db, dq[ot], 0, 0, 0);
+      }
+    }
+  }
+  if (q < S) {
+    bf16* out = a.dq + ((long)b * S + q) * a.lddq + (long)h * DH;
+#pragma unroll
+    for (int ot = 0; ot < DHS / 32; ++ot)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        int j = col0 + ot * 32 + acc_row(r, g);
+        if (j < DH && j < col0 + DHS) out[j] = f2bf(dq[ot][r] * a.f.scale);
+      }
+  }
+}
+
+// dK, dV: workgroup = 128 keys of one (b, h); grid.z = output dh slice.
+template <int DH, int DHS, int BQ>
+__global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnBwdArgs a) {
+  constexpr int PK = DH + 8;
+  constexpr int PT = BQ + 8;
+  __shared__ __attribute__((aligned(16))) bf16 Qs[BQ * PK];
+  __shared__ __attribute__((aligned(16))) bf16 dOs[BQ * PK];
+  __shared__ __attribute__((aligned(16))) bf16 Qt[DHS * PT];
+  __shared__ __attribute__((aligned(16))) bf16 dOt[DHS * PT];
+  __shared__ float lse_s[BQ], dlt_s[BQ];
+
+  const int S = a.f.S;
+  const int nkb = (S + WG_ROWS - 1) / WG_ROWS;
+  // causal: early key blocks see the most queries; schedule them first
+  const int kb = (int)blockIdx.x;
+  (void)nkb;
+  const int bh = blockIdx.y, b = bh / a.f.H, h = bh % a.f.H;
+  const int col0 = blockIdx.z * DHS;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, g = lane >> 5;
+  const int k0 = kb * WG_ROWS;
+  const int key = k0 + wave * WROWS + (lane & 31);
+  const long hs = ((long)b * a.f.H + h) * S;
+
+  const bf16* Qb = a.f.q + (long)b * S * a.f.ldq + (long)h * DH;
+  const bf16* Kb = a.f.k + (long)b * S * a.f.ldk + (long)h * DH;
+  const bf16* Vb = a.f.v + (long)b * S * a.f.ldv + (long)h * DH;
+  const bf16* dOb = a.dout + (long)b * S * a.lddo + (long)h * DH;
+
+  bf16x8 kf[DH / 16], vf[DH / 16];
+  load_row_operand<DH>(Kb, a.f.ldk, key, S, g, kf);
+  load_row_operand<DH>(Vb, a.f.ldv, key, S, g, vf);
+  const float sc = a.f.scale * LOG2E;
+
+  floatx16 dk[DHS / 32], dv[DHS / 32];
+#pragma unroll
+  for (int t = 0; t < DHS / 32; ++t) {
+    dk[t] = zero16();
+    dv[t] = zero16();
+  }
+  const int wave_kmin = k0 + wave * WROWS;
+  const int q_start = a.f.causal ? (k0 / BQ) * BQ : 0;
+  for (int qs0 = q_start; qs0 < S; qs0 += BQ) {
+    __syncthreads();
+    stage_rows<BQ, DH, PK>(Qb, a.f.ldq, qs0, S, Qs);
+    stage_rows<BQ, DH, PK>(dOb, a.lddo, qs0, S, dOs);
+    stage_rows_T<BQ, DHS, DH, PT>(Qb, a.f.ldq, qs0, S, col0, Qt);
+    stage_rows_T<BQ, DHS, DH, PT>(dOb, a.lddo, qs0, S, col0, dOt);
+    for (int i = threadIdx.x; i < BQ; i += NT) {
+      int qq = qs0 + i;
+      lse_s[i] = (qq < S) ? a.f.lse[hs + qq] * LOG2E : 0.f;
+      dlt_s[i] = (qq < S) ? a.delta[hs + qq] : 0.f;
+    }
+    __syncthreads();
+    if (a.f.causal && qs0 + BQ - 1 < wave_kmin) continue;
+#pragma unroll
+    for (int t = 0; t < BQ / 32; ++t) {
+      floatx16 s = zero16(), dp = zero16();
+#pragma unroll
+      for (int c = 0; c < DH / 16; ++c) {
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            lds8(Qs + (t * 32 + (lane & 31)) * PK + c * 16 + 8 * g), kf[c], s, 0, 0, 0);
+        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            lds8(dOs + (t * 32 + (lane & 31)) * PK + c * 16 + 8 * g), vf[c], dp, 0, 0, 0);
+      }
+      // s, dp: rows = queries (acc_row), column = this lane's key
+      floatx16 p;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        int qi = t * 32 + acc_row(r, g);
+        int qq = qs0 + qi;
+        bool ok = qq < S && key < S && !(a.f.causal && key > qq);
+        float pr = ok ? exp2f(s[r] * sc - lse_s[qi]) : 0.f;
+        p[r] = pr;
+        s[r] = pr * (dp[r] - dlt_s[qi]);
+      }
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        bf16x8 pb = acc_to_bf16(p, hh);
+        bf16x8 db = acc_to_bf16(s, hh);
+#pragma unroll
+        for (int ot = 0; ot < DHS / 32; ++ot) {
+          dv[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              lds8_perm(dOt + (ot * 32 + (lane & 31)) * PT, t * 32 + hh * 16, g), pb, dv[ot], 0, 0, 0);
+          dk[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              lds8_perm(Qt + (ot * 32 + (lane & 31)) * PT, t * 32 + hh * 16, g), db, dk[ot], 0, 0, 0);
+        }
+      }
+    }
+  }
+  if (key < S) {
+    bf16* ok_ = a.dk + ((long)b * S + key) * a.lddk + (long)h * DH;
+    bf16* ov = a.dv + ((long)b * S + key) * a.lddv + (long)h * DH;
+#pragma unroll
+    for (int ot = 0; ot < DHS / 32; ++ot)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        int j = col0 + ot * 32 + acc_row(r, g);
+        if (j < DH && j < col0 + DHS) {
+          ok_[j] = f2bf(dk[ot][r] * a.f.scale);
+          ov[j] = f2bf(dv[ot][r]);
+        }
+      }
+  }
+}
+
+template <int DH>
+struct AttnCfg {
+  static constexpr int BKV = (DH >= 256) ? 32 : 64;
+  static constexpr int DHS = (DH > 128) ? 128 : round32(DH);
+  static constexpr int NSLICE = (round32(DH) + DHS - 1) / DHS;
+  static constexpr int BQ = (DH >= 256) ? 32 : 64;
+};
+
+template <int DH>
+hipError_t fwd_launch(const AttnArgs& a, hipStream_t s) {
+  dim3 grid((a.S + WG_ROWS - 1) / WG_ROWS, a.B * a.H);
+  hipLaunchKernelGGL((attn_fwd_kernel<DH, AttnCfg<DH>::BKV>), grid, dim3(NT), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int DH>
+hipError_t bwd_launch(const AttnBwdArgs& a, hipStream_t s) {
+  using C = AttnCfg<DH>;
+  long rows = (long)a.f.B * a.f.S * a.f.H;
+  hipLaunchKernelGGL(attn_delta_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  dim3 grid((a.f.S + WG_ROWS - 1) / WG_ROWS, a.f.B * a.f.H, C::NSLICE);
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<DH, C::DHS, C::BQ>), grid, dim3(NT), 0, s, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<DH, C::DHS, C::BKV>), grid, dim3(NT), 0, s, a);
+  return hipGetLastError();
+}
+
+bool ok16(const void* p, long ld) {
+  return (reinterpret_cast<uintptr_t>(p) & 15) == 0 && ld % 8 == 0;
+}
+
+}  // namespace
+
+hipError_t launch_attention_fwd(const AttnArgs& a, hipStream_t s) {
+  if (a.B * a.H * a.S == 0) return hipSuccess;
+  if (!ok16(a.q, a.ldq) || !ok16(a.k, a.ldk) || !ok16(a.v, a.ldv)) return hipErrorInvalidValue;
+  switch (a.dh) {
+    case 16: return fwd_launch<16>(a, s);
+    case 32: return fwd_launch<32>(a, s);
+    case 64: return fwd_launch<64>(a, s);
+    case 80: return fwd_launch<80>(a, s);
+    case 128: return fwd_launch<128>(a, s);
+    case 256: return fwd_launch<256>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_attention_bwd(const AttnBwdArgs& a, hipStream_t s) {
+  if (a.f.B * a.f.H * a.f.S == 0) return hipSuccess;
+  if (!ok16(a.f.q, a.f.ldq) || !ok16(a.f.k, a.f.ldk) || !ok16(a.f.v, a.f.ldv) ||
+      !ok16(a.dout, a.lddo))
+    return hipErrorInvalidValue;
+  switch (a.f.dh) {
+    case 16: return bwd_launch<16>(a, s);
+    case 32: return bwd_launch<32>(a, s);
+    case 64: return bwd_launch<64>(a, s);
+    case 80: return bwd_launch<80>(a, s);
+    case 128: return bwd_launch<128>(a, s);
+    case 256: return bwd_launch<256>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+// Supported head dims (host query for argument checks).
+bool attention_supports_dh(int dh) {
+  return dh == 16 || dh == 32 || dh == 64 || dh == 80 || dh == 128 || dh == 256;
+}

@@ -1,0 +1,498 @@
+// Bandwidth-bound kernels of the fine-tuning step: rotary embedding, token
+// embedding forward / deterministic backward, ViT patch extraction and token
+// assembly, softmax cross-entropy, the fused AdamW update, the counter-based
+// parameter initialisation and small helpers.  All reductions run in a fixed
+// order (no floating-point atomics), so every step is bitwise reproducible.
+#include <math.h>
+
+#include <algorithm>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+// ---------------------------------------------------------------- rotary
+// One thread per (token, q|k, head, pair); angle = pos * 10000^(-2i/rd) in
+// double precision, then the 2x2 rotation (or its transpose for backward).
+__global__ void rotary_kernel(bf16* __restrict__ qk, long ld, int T, int S, int H, int dh, int rd,
+                              int inverse) {
+  const int half = rd / 2;
+  long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  long total = (long)T * 2 * H * half;
+  if (idx >= total) return;
+  int i = idx % half;
+  long r = idx / half;
+  int h = r % H;
+  r /= H;
+  int which = r % 2;
+  int t = (int)(r / 2);
+  int pos = t % S;
+  double ang = (double)pos * pow(10000.0, -2.0 * i / (double)rd);
+  double sn, cs;
+  sincos(ang, &sn, &cs);
+  float c = (float)cs, s = (float)sn;
+  if (inverse) s = -s;
+  bf16* p = qk + (long)t * ld + (long)which * H * dh + (long)h * dh + 2 * i;
+  float x0 = bf2f(p[0]), x1 = bf2f(p[1]);
+  p[0] = f2bf(x0 * c - x1 * s);
+  p[1] = f2bf(x0 * s + x1 * c);
+}
+
+// ---------------------------------------------------------------- embedding
+__global__ void embed_fwd_kernel(const int32_t* __restrict__ tok, const float* __restrict__ wte,
+                                 const float* __restrict__ wpe, float* __restrict__ h, int T,
+                                 int S, int d) {
+  const int d4 = d / 4;
+  long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long)T * d4) return;
+  int t = idx / d4, c = (idx % d4) * 4;
+  float4 v = *reinterpret_cast<const float4*>(wte + (long)tok[t] * d + c);
+  if (wpe != nullptr) {
+    float4 w = *reinterpret_cast<const float4*>(wpe + (long)(t % S) * d + c);
+    v.x += w.x; v.y += w.y; v.z += w.z; v.w += w.w;
+  }
+  *reinterpret_cast<float4*>(h + (long)t * d + c) = v;
+}
+
+// Sorts the keys (token << 15 | position) of T <= 16384 tokens with a bitonic
+// network in LDS (one workgroup); keys are unique, so the order is unique.
+constexpr int EMB_MAXT = 16384;
+__global__ __launch_bounds__(1024) void embed_sort_kernel(const int32_t* __restrict__ tok, int T,
+                                                          int32_t* __restrict__ sorted) {
+  __shared__ uint32_t key[EMB_MAXT];
+  int n = 1;
+  while (n < T) n <<= 1;
+  for (int i = threadIdx.x; i < n; i += blockDim.x)
+    key[i] = (i < T) ? (((uint32_t)tok[i] << 15) | (uint32_t)i) : 0xFFFFFFFFu;
+  __syncthreads();
+  for (int k = 2; k <= n; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = threadIdx.x; i < n; i += blockDim.x) {
+        int ixj = i ^ j;
+        if (ixj > i) {
+          uint32_t a = key[i], b = key[ixj];
+          bool up = (i & k) == 0;
+          if ((a > b) == up) {
+            key[i] = b;
+            key[ixj] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  for (int i = threadIdx.x; i < T; i += blockDim.x) sorted[i] = (int32_t)key[i];
+}
+
+// One wavefront per vocabulary row v: binary-search v's run in the sorted
+// keys, sum the matching dh rows in increasing position order, write the row
+// (zeros when v does not occur).
+__global__ __launch_bounds__(256) void embed_bwd_rows_kernel(const int32_t* __restrict__ sorted,
+                                                             int T, const float* __restrict__ dh,
+                                                             float* __restrict__ dwte, int d,
+                                                             int V) {
+  const int lane = threadIdx.x & 63;
+  const int v = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (v >= V) return;
+  const uint32_t lo_key = (uint32_t)v << 15;
+  int lo = 0, hi = T;
+  while (lo < hi) {
+    int mid = (lo + hi) >> 1;
+    if ((uint32_t)sorted[mid] < lo_key) lo = mid + 1;
+    else hi = mid;
+  }
+  int end = lo;
+  while (end < T && ((uint32_t)sorted[end] >> 15) == (uint32_t)v) ++end;
+  float* out = dwte + (long)v * d;
+  for (int c = lane * 4; c < d; c += 256) {
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int j = lo; j < end; ++j) {
+      int t = sorted[j] & 0x7FFF;
+      float4 x = *reinterpret_cast<const float4*>(dh + (long)t * d + c);
+      s.x += x.x; s.y += x.y; s.z += x.z; s.w += x.w;
+    }
+    *reinterpret_cast<float4*>(out + c) = s;
+  }
+}
+
+// ---------------------------------------------------------------- ViT
+__global__ void patchify_kernel(const float* __restrict__ img, bf16* __restrict__ out, int B,
+                                int C, int I, int p) {
+  const int g = I / p, np = g * g, pd = C * p * p;
+  long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long)B * np * pd) return;
+  int col = idx % pd;
+  long row = idx / pd;
+  int i = row % np, b = row / np;
+  int c = col / (p * p), kh = (col / p) % p, kw = col % p;
+  int pr = i / g, pc = i % g;
+  out[idx] = f2bf(img[(((long)b * C + c) * I + pr * p + kh) * I + pc * p + kw]);
+}
+
+__global__ void vit_assemble_kernel(const float* __restrict__ z, const float* __restrict__ cls,
+                                    const float* __restrict__ pos, float* __restrict__ h, int B,
+                                    int np, int d) {
+  const int S = np + 1;
+  long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long)B * S * d) return;
+  int c = idx % d;
+  long r = idx / d;
+  int s = r % S, b = r / S;
+  float base = (s == 0) ? cls[c] : z[((long)b * np + s - 1) * d + c];
+  h[idx] = base + pos[(long)s * d + c];
+}
+
+// dz[b*np + i, :] = bf16(dh[b*S + 1 + i, :])
+__global__ void vit_patch_grad_kernel(const float* __restrict__ dh, bf16* __restrict__ dz, int B,
+                                      int np, int d) {
+  long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long)B * np * d) return;
+  int c = idx % d;
+  long r = idx / d;
+  int i = r % np, b = r / np;
+  dz[idx] = f2bf(dh[((long)b * (np + 1) + 1 + i) * d + c]);
+}
+
+__global__ void f32_to_bf16_kernel(const float* __restrict__ x, long ldx, bf16* __restrict__ y,
+                                   long ldy, int rows, int cols) {
+  long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long)rows * cols) return;
+  int c = idx % cols;
+  long r = idx / cols;
+  y[r * ldy + c] = f2bf(x[r * ldx + c]);
+}
+
+// out[s, c] = sum_b dh[(b*S + s) * d + c]
+__global__ void sum_rows_batched_kernel(const float* __restrict__ dh, float* __restrict__ out,
+                                        int B, int S, int d) {
+  long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long)S * d) return;
+  float s = 0.f;
+  for (int b = 0; b < B; ++b) s += dh[(long)b * S * d + idx];
+  out[idx] = s;
+}
+
+// ---------------------------------------------------------------- cross-entropy
+__device__ __forceinline__ float block_reduce_sum_256(float v, float* sh) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sh[w] = v;
+  __syncthreads();
+  return sh[0] + sh[1] + sh[2] + sh[3];
+}
+__device__ __forceinline__ float block_reduce_max_256(float v, float* sh) {
+  v = wave_max(v);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sh[w] = v;
+  __syncthreads();
+  return fmaxf(fmaxf(sh[0], sh[1]), fmaxf(sh[2], sh[3]));
+}
+
+// One 256-thread block per row: online (max, sum exp) in one pass, block
+// combine, then dz = (exp(z - lse) - onehot) * inv_n in a second pass.
+__global__ __launch_bounds__(256) void xent_kernel(const float* __restrict__ z, long ldz,
+                                                   const int32_t* __restrict__ labels, int V,
+                                                   float* __restrict__ row_loss,
+                                                   bf16* __restrict__ dz, long lddz,
+                                                   const float* __restrict__ inv_n_p) {
+  __shared__ float sh[4];
+  const int row = blockIdx.x;
+  const float* zr = z + (long)row * ldz;
+  const int y = labels[row];
+  float m = -INFINITY, s = 0.f;
+  for (int c = threadIdx.x; c < V; c += 256) {
+    float x = zr[c];
+    if (x > m) {
+      s = s * __expf(m - x) + 1.f;
+      m = x;
+    } else {
+      s += __expf(x - m);
+    }
+  }
+  const float M = block_reduce_max_256(m, sh);
+  float sl = (m == -INFINITY) ? 0.f : s * __expf(m - M);
+  const float tot = block_reduce_sum_256(sl, sh);
+  const float lse = M + __logf(tot);
+  bf16* dr = dz + (long)row * lddz;
+  if (y < 0) {
+    const int cend = min((long)((V + 7) & ~7), lddz);
+    for (int c = threadIdx.x; c < cend; c += 256) dr[c] = f2bf(0.f);
+    if (threadIdx.x == 0) row_loss[row] = 0.f;
+    return;
+  }
+  const float inv_n = *inv_n_p;
+  for (int c = threadIdx.x; c < V; c += 256) {
+    float pr = __expf(zr[c] - lse);
+    dr[c] = f2bf((pr - (c == y ? 1.f : 0.f)) * inv_n);
+  }
+  // zero the row padding up to the next multiple of 8 columns (within lddz)
+  const int cpad = min((long)((V + 7) & ~7), lddz);
+  for (int c = V + threadIdx.x; c < cpad; c += 256) dr[c] = f2bf(0.f);
+  if (threadIdx.x == 0) row_loss[row] = lse - zr[y];
+}
+
+// Single block: out[0] = (sum of row_loss in a fixed tree order) * inv_n.
+__global__ __launch_bounds__(256) void loss_finalize_kernel(const float* __restrict__ row_loss,
+                                                            int n, const float* __restrict__ inv_n,
+                                                            float* __restrict__ out) {
+  __shared__ float sh[4];
+  double acc = 0.0;
+  for (int i = threadIdx.x; i < n; i += 256) acc += row_loss[i];
+  float v = block_reduce_sum_256((float)acc, sh);
+  if (threadIdx.x == 0) out[0] = v * inv_n[0];
+}
+
+__global__ __launch_bounds__(256) void count_valid_kernel(const int32_t* __restrict__ labels,
+                                                          int n, float* __restrict__ inv_n) {
+  __shared__ float sh[4];
+  float c = 0.f;
+  for (int i = threadIdx.x; i < n; i += 256) c += (labels[i] >= 0) ? 1.f : 0.f;
+  float tot = block_reduce_sum_256(c, sh);
+  if (threadIdx.x == 0) inv_n[0] = 1.f / fmaxf(tot, 1.f);
+}
+
+// ---------------------------------------------------------------- AdamW
+__device__ __forceinline__ void adamw_one(float& p, float g, float& m, float& v,
+                                          const AdamWConsts& c) {
+  p = p - c.lr_wd * p;
+  m = c.b1 * m + c.omb1 * g;
+  v = c.b2 * v + c.omb2 * g * g;
+  p = p - c.step * m / (sqrtf(v) / c.bc2s + c.eps);
+}
+
+__global__ __launch_bounds__(256) void adamw_kernel(float* __restrict__ p,
+                                                    const float* __restrict__ g,
+                                                    float* __restrict__ m, float* __restrict__ v,
+                                                    bf16* __restrict__ shadow, long n4, long n,
+                                                    AdamWConsts c) {
+  const long stride = (long)gridDim.x * blockDim.x;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+    float4 pp = reinterpret_cast<float4*>(p)[i];
+    float4 gg = reinterpret_cast<const float4*>(g)[i];
+    float4 mm = reinterpret_cast<float4*>(m)[i];
+    float4 vv = reinterpret_cast<float4*>(v)[i];
+    adamw_one(pp.x, gg.x, mm.x, vv.x, c);
+    adamw_one(pp.y, gg.y, mm.y, vv.y, c);
+    adamw_one(pp.z, gg.z, mm.z, vv.z, c);
+    adamw_one(pp.w, gg.w, mm.w, vv.w, c);
+    reinterpret_cast<float4*>(p)[i] = pp;
+    reinterpret_cast<float4*>(m)[i] = mm;
+    reinterpret_cast<float4*>(v)[i] = vv;
+    if (shadow != nullptr) {
+      bf16x4 o;
+      o[0] = f2bf(pp.x); o[1] = f2bf(pp.y); o[2] = f2bf(pp.z); o[3] = f2bf(pp.w);
+      reinterpret_cast<bf16x4*>(shadow)[i] = o;
+    }
+  }
+  // scalar tail (n not a multiple of 4, or unaligned pointers)
+  long t = n4 * 4 + (long)blockIdx.x * blockDim.x + threadIdx.x;
+  for (; t < n; t += stride) {
+    float pp = p[t], mm = m[t], vv = v[t];
+    adamw_one(pp, g[t], mm, vv, c);
+    p[t] = pp; m[t] = mm; v[t] = vv;
+    if (shadow != nullptr) shadow[t] = f2bf(pp);
+  }
+}
+
+// ---------------------------------------------------------------- init
+// Philox4x32-10 (Salmon et al., SC'11) keyed by the seed, counter =
+// (pair index, tensor id); Box-Muller turns its outputs into two normals.
+__device__ __forceinline__ void philox_round(uint32_t& c0, uint32_t& c1, uint32_t& c2,
+                                             uint32_t& c3, uint32_t k0, uint32_t k1) {
+  const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
+  uint32_t hi0 = __umulhi(M0, c0), lo0 = M0 * c0;
+  uint32_t hi1 = __umulhi(M1, c2), lo1 = M1 * c2;
+  uint32_t n0 = hi1 ^ c1 ^ k0, n1 = lo1, n2 = hi0 ^ c3 ^ k1, n3 = lo0;
+  c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+}
+__device__ __forceinline__ void philox4x32_10(uint32_t ctr[4], uint32_t k0, uint32_t k1) {
+  const uint32_t W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    philox_round(ctr[0], ctr[1], ctr[2], ctr[3], k0, k1);
+    k0 += W0;
+    k1 += W1;
+  }
+}
+
+__global__ void init_normal_kernel(float* __restrict__ p, bf16* __restrict__ shadow, long n,
+                                   uint32_t k0, uint32_t k1, uint32_t stream_id, float std) {
+  long pair = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  long i0 = pair * 2;
+  if (i0 >= n) return;
+  uint32_t c[4] = {(uint32_t)pair, (uint32_t)(pair >> 32), stream_id, 0x5A17u};
+  philox4x32_10(c, k0, k1);
+  // uniforms in (0, 1]: (x + 1) * 2^-32 with 24-bit mantissa safety
+  float u1 = ((c[0] >> 8) + 1) * (1.0f / 16777216.0f);
+  float u2 = (c[1] >> 8) * (1.0f / 16777216.0f);
+  float r = sqrtf(-2.f * __logf(u1));
+  float sn, cs;
+  __sincosf(6.283185307179586f * u2, &sn, &cs);
+  float z0 = r * cs * std, z1 = r * sn * std;
+  p[i0] = z0;
+  if (shadow) shadow[i0] = f2bf(z0);
+  if (i0 + 1 < n) {
+    p[i0 + 1] = z1;
+    if (shadow) shadow[i0 + 1] = f2bf(z1);
+  }
+}
+
+__global__ void fill_kernel(float* __restrict__ p, bf16* __restrict__ shadow, long n, float v) {
+  long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  p[i] = v;
+  if (shadow) shadow[i] = f2bf(v);
+}
+
+__global__ void zero_kernel(uint32_t* __restrict__ p, long n) {
+  const long stride = (long)gridDim.x * blockDim.x;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = 0u;
+}
+
+inline unsigned blocks_for(long n, int bs = 256) { return (unsigned)((n + bs - 1) / bs); }
+
+}  // namespace
+
+hipError_t launch_rotary(bf16* qk, long ld, int B, int S, int H, int dh, int rd, int inverse,
+                         hipStream_t s) {
+  if (rd <= 0) return hipSuccess;
+  if (rd % 2 || rd > dh) return hipErrorInvalidValue;
+  long total = (long)B * S * 2 * H * (rd / 2);
+  hipLaunchKernelGGL(rotary_kernel, dim3(blocks_for(total)), dim3(256), 0, s, qk, ld, B * S, S, H,
+                     dh, rd, inverse);
+  return hipGetLastError();
+}
+
+hipError_t launch_embed_fwd(const int32_t* tok, const float* wte, const float* wpe, float* h,
+                            int T, int S, int d, int V, hipStream_t s) {
+  (void)V;
+  if (T <= 0) return hipSuccess;
+  if (d % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(embed_fwd_kernel, dim3(blocks_for((long)T * d / 4)), dim3(256), 0, s, tok,
+                     wte, wpe, h, T, S, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_embed_bwd(const int32_t* tok, const float* dh, float* dwte, int T, int d, int V,
+                            int32_t* work, hipStream_t s) {
+  if (T <= 0 || T > EMB_MAXT || d % 4 || V <= 0 || V >= (1 << 16)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(embed_sort_kernel, dim3(1), dim3(1024), 0, s, tok, T, work);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(embed_bwd_rows_kernel, dim3(sat_cdiv(V, 4)), dim3(256), 0, s, work, T, dh,
+                     dwte, d, V);
+  return hipGetLastError();
+}
+
+hipError_t launch_patchify(const float* img, bf16* out, int B, int C, int I, int p,
+                           hipStream_t s) {
+  long total = (long)B * (I / p) * (I / p) * C * p * p;
+  if (total <= 0) return hipSuccess;
+  hipLaunchKernelGGL(patchify_kernel, dim3(blocks_for(total)), dim3(256), 0, s, img, out, B, C, I,
+                     p);
+  return hipGetLastError();
+}
+
+hipError_t launch_vit_assemble(const float* z, const float* cls, const float* pos, float* h,
+                               int B, int np, int d, hipStream_t s) {
+  long total = (long)B * (np + 1) * d;
+  hipLaunchKernelGGL(vit_assemble_kernel, dim3(blocks_for(total)), dim3(256), 0, s, z, cls, pos,
+                     h, B, np, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_vit_patch_grad(const float* dh, bf16* dz, int B, int np, int d, hipStream_t s) {
+  long total = (long)B * np * d;
+  hipLaunchKernelGGL(vit_patch_grad_kernel, dim3(blocks_for(total)), dim3(256), 0, s, dh, dz, B,
+                     np, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_f32_to_bf16(const float* x, long ldx, bf16* y, long ldy, int rows, int cols,
+                              hipStream_t s) {
+  long total = (long)rows * cols;
+  if (total <= 0) return hipSuccess;
+  hipLaunchKernelGGL(f32_to_bf16_kernel, dim3(blocks_for(total)), dim3(256), 0, s, x, ldx, y, ldy,
+                     rows, cols);
+  return hipGetLastError();
+}
+
+hipError_t launch_sum_rows_batched(const float* dh, float* out, int B, int S, int d,
+                                   hipStream_t s) {
+  long total = (long)S * d;
+  hipLaunchKernelGGL(sum_rows_batched_kernel, dim3(blocks_for(total)), dim3(256), 0, s, dh, out,
+                     B, S, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_xent(const float* z, long ldz, const int32_t* labels, int N, int V,
+                       float* row_loss, bf16* dz, long lddz, const float* inv_n, hipStream_t s) {
+  if (N <= 0) return hipSuccess;
+  hipLaunchKernelGGL(xent_kernel, dim3(N), dim3(256), 0, s, z, ldz, labels, V, row_loss, dz, lddz,
+                     inv_n);
+  return hipGetLastError();
+}
+
+hipError_t launch_loss_finalize(const float* row_loss, int n, const float* inv_n, float* out,
+                                hipStream_t s) {
+  hipLaunchKernelGGL(loss_finalize_kernel, dim3(1), dim3(256), 0, s, row_loss, n, inv_n, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_count_valid(const int32_t* labels, int n, float* inv_n, hipStream_t s) {
+  hipLaunchKernelGGL(count_valid_kernel, dim3(1), dim3(256), 0, s, labels, n, inv_n);
+  return hipGetLastError();
+}
+
+AdamWConsts adamw_consts(double lr, double beta1, double beta2, double eps, double wd, long t) {
+  AdamWConsts c;
+  c.lr_wd = (float)(lr * wd);
+  c.b1 = (float)beta1;
+  c.omb1 = (float)(1.0 - beta1);
+  c.b2 = (float)beta2;
+  c.omb2 = (float)(1.0 - beta2);
+  c.step = (float)(lr / (1.0 - pow(beta1, (double)t)));
+  c.bc2s = (float)sqrt(1.0 - pow(beta2, (double)t));
+  c.eps = (float)eps;
+  return c;
+}
+
+hipError_t launch_adamw(float* p, const float* g, float* m, float* v, bf16* shadow, long n,
+                        const AdamWConsts& c, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  bool al = ((reinterpret_cast<uintptr_t>(p) | reinterpret_cast<uintptr_t>(g) |
+              reinterpret_cast<uintptr_t>(m) | reinterpret_cast<uintptr_t>(v)) & 15) == 0 &&
+            (shadow == nullptr || (reinterpret_cast<uintptr_t>(shadow) & 7) == 0);
+  long n4 = al ? n / 4 : 0;
+  long work = n4 > 0 ? n4 : n;
+  unsigned grid = (unsigned)std::min<long>(blocks_for(work), 256L * 64);
+  hipLaunchKernelGGL(adamw_kernel, dim3(grid), dim3(256), 0, s, p, g, m, v, shadow, n4, n, c);
+  return hipGetLastError();
+}
+
+hipError_t launch_init_normal(float* p, bf16* shadow, long n, uint64_t seed, uint32_t stream_id,
+                              float std, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  long pairs = (n + 1) / 2;
+  hipLaunchKernelGGL(init_normal_kernel, dim3(blocks_for(pairs)), dim3(256), 0, s, p, shadow, n,
+                     (uint32_t)seed, (uint32_t)(seed >> 32), stream_id, std);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill(float* p, bf16* shadow, long n, float value, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_kernel, dim3(blocks_for(n)), dim3(256), 0, s, p, shadow, n, value);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero(void* p, long bytes, hipStream_t s) {
+  if (bytes <= 0) return hipSuccess;
+  if (bytes % 4) return hipErrorInvalidValue;
+  long n = bytes / 4;
+  unsigned grid = (unsigned)std::min<long>(blocks_for(n), 256L * 64);
+  hipLaunchKernelGGL(zero_kernel, dim3(grid), dim3(256), 0, s, (uint32_t*)p, n);
+  return hipGetLastError();
+}

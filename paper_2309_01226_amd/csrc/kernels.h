@@ -1,0 +1,142 @@
+// Host-side launchers of the gfx950 kernels.  Every launcher enqueues work on
+// the given stream and returns hipSuccess or the launch error; none of them
+// synchronises or allocates.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16;
+
+// ---------------------------------------------------------------- GEMM
+// C[m, n] = sum_k A(m, k) * B(n, k) on bf16 operands, fp32 accumulation.
+//   A layout 0: A(m, k) = A[m * lda + k]      layout 1: A(m, k) = A[k * lda + m]
+//   B layout 0: B(n, k) = B[n * ldb + k]      layout 1: B(n, k) = B[k * ldb + n]
+enum GemmLayout { LAY_K = 0, LAY_MN = 1 };
+enum GemmEpilogue {
+  EPI_F32 = 0,        // out_f32[m, n] = C + bias
+  EPI_RESID_F32 = 1,  // out_f32[m, n] = resid[m, n] + C + bias   (resid may alias out)
+  EPI_BF16 = 2,       // out_bf16[m, n] = C + bias; and out2[m, n - gelu_col0] = GELU(C + bias)
+  EPI_DGELU_BF16 = 3, // out_bf16[m, n] = C * GELU'(aux[m, n])
+};
+
+struct GemmArgs {
+  const bf16* A;
+  const bf16* B;
+  int M, N, K;
+  long lda, ldb;
+  void* out;
+  long ldo;
+  const float* bias;  // bias[n - bias_col0] added for n >= bias_col0; null = none
+  int bias_col0;
+  const float* resid;
+  long ldr;
+  bf16* out2;         // EPI_BF16: GELU outputs for n >= gelu_col0; null = none
+  long ldo2;
+  int gelu_col0;
+  const bf16* aux;    // EPI_DGELU_BF16: GELU pre-activation
+  long ldaux;
+  int gelu_erf;       // 0 = tanh form, 1 = erf form
+};
+
+hipError_t launch_gemm(const GemmArgs& a, int alay, int blay, int epi, hipStream_t s);
+
+// ---------------------------------------------------------------- LayerNorm
+// y = (x - mean) * rstd * g + b over rows of length d; x fp32, y bf16.
+// mean / rstd saved per row (fp32).  Row r of x is x + rows_idx(r) * ldx where
+// rows_idx(r) = r * row_stride (row_stride lets the ViT head pick CLS rows).
+hipError_t launch_layernorm_fwd(const float* x, long ldx, long row_stride, const float* g,
+                                const float* b, bf16* y, long ldy, float* mean, float* rstd,
+                                int rows, int d, float eps, hipStream_t s);
+// dx = rstd * (gy - mean(gy) - xhat * mean(gy * xhat)), gy = dy * g; written as
+// dres[r] += dx (fp32 residual gradient, row stride as in the forward).
+// Per-row partials of dg / db go to part_g / part_b [n_part, d] and are then
+// reduced by launch_colsum_partials (deterministic, no atomics).
+hipError_t launch_layernorm_bwd(const float* dy, long lddy, const float* x, long ldx,
+                                long row_stride, const float* g, const float* mean,
+                                const float* rstd, float* dres, long ldres, float* part_g,
+                                float* part_b, int rows, int d, int n_part, hipStream_t s);
+hipError_t launch_colsum_partials(const float* part, int n_part, int d, float* out,
+                                  hipStream_t s);
+// out[c] = sum_r X[r, c] for a bf16 or fp32 matrix, deterministic two-pass.
+hipError_t launch_colsum_bf16(const bf16* X, long ldx, int rows, int cols, float* part,
+                              int n_part, float* out, hipStream_t s);
+hipError_t launch_colsum_f32(const float* X, long ldx, int rows, int cols, float* part,
+                             int n_part, float* out, hipStream_t s);
+
+// ---------------------------------------------------------------- attention
+struct AttnArgs {
+  const bf16* q;   // q(b, h, s, :) = q[(b * S + s) * ldq + h * dh]
+  const bf16* k;
+  const bf16* v;
+  long ldq, ldk, ldv;
+  bf16* o;         // o(b, h, s, :) = o[(b * S + s) * ldo + h * dh]
+  long ldo;
+  float* lse;      // [B, H, S] log-sum-exp of the scaled scores (natural log)
+  int B, H, S, dh;
+  int causal;
+  float scale;
+};
+struct AttnBwdArgs {
+  AttnArgs f;
+  const bf16* dout;  long lddo;
+  float* delta;      // [B, H, S] rowsum(dO * O)
+  bf16* dq; bf16* dk; bf16* dv;
+  long lddq, lddk, lddv;
+};
+hipError_t launch_attention_fwd(const AttnArgs& a, hipStream_t s);
+hipError_t launch_attention_bwd(const AttnBwdArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- elementwise
+// GPT-J rotary on interleaved pairs of the first rd dims of every q and k head,
+// in place on the bf16 [T, ld] buffer (q at column 0, k at column d).
+hipError_t launch_rotary(bf16* qk, long ld, int B, int S, int H, int dh, int rd, int inverse,
+                         hipStream_t s);
+// h0[t, :] = wte[tok[t], :] (+ wpe[t % S, :])
+hipError_t launch_embed_fwd(const int32_t* tok, const float* wte, const float* wpe, float* h,
+                            int T, int S, int d, int V, hipStream_t s);
+// dwte[v, :] = sum over t with tok[t] == v of dh[t, :], in increasing t (deterministic).
+// Sorts (token, position) keys in `work` (int32, >= T entries); T <= 16384, V < 65536.
+hipError_t launch_embed_bwd(const int32_t* tok, const float* dh, float* dwte, int T, int d,
+                            int V, int32_t* work, hipStream_t s);
+// ViT: images [B, C, I, I] fp32 -> patches [B * np, C * p * p] bf16, (c, kh, kw) order.
+hipError_t launch_patchify(const float* img, bf16* out, int B, int C, int I, int p,
+                           hipStream_t s);
+// ViT: h[b, 0] = cls + pos[0]; h[b, 1 + i] = z[b * np + i] + pos[1 + i]  (z holds bias).
+hipError_t launch_vit_assemble(const float* z, const float* cls, const float* pos, float* h,
+                               int B, int np, int d, hipStream_t s);
+// ViT backward: dz[b * np + i, :] = bf16(dh[b * (np + 1) + 1 + i, :])
+hipError_t launch_vit_patch_grad(const float* dh, bf16* dz, int B, int np, int d, hipStream_t s);
+// fp32 -> bf16 copy of a strided matrix (rows x cols)
+hipError_t launch_f32_to_bf16(const float* x, long ldx, bf16* y, long ldy, int rows, int cols,
+                              hipStream_t s);
+// Cross-entropy fwd+bwd over fp32 logits [N, V]: per-row loss (0 for ignored
+// rows), dz = (softmax - onehot) * inv_n as bf16, count of valid rows.
+// inv_n: device pointer to 1 / (number of labels != -1).
+hipError_t launch_xent(const float* z, long ldz, const int32_t* labels, int N, int V,
+                       float* row_loss, bf16* dz, long lddz, const float* inv_n, hipStream_t s);
+// out[0] = inv_n[0] * sum of row_loss[0..n), summed in a fixed order.
+hipError_t launch_loss_finalize(const float* row_loss, int n, const float* inv_n, float* out,
+                                hipStream_t s);
+// inv_n[0] = 1 / max(1, number of labels >= 0)
+hipError_t launch_count_valid(const int32_t* labels, int n, float* inv_n, hipStream_t s);
+// Fused AdamW over n contiguous fp32 parameters with bf16 shadow refresh.
+// The scalar constants are formed on the host in double precision:
+//   p <- p - lr_wd * p;  m <- b1 m + omb1 g;  v <- b2 v + omb2 g^2;
+//   p <- p - step * m / (sqrt(v) / bc2s + eps)
+// with lr_wd = lr * wd, omb = 1 - beta, step = lr / (1 - beta1^t),
+// bc2s = sqrt(1 - beta2^t).
+struct AdamWConsts {
+  float lr_wd, b1, omb1, b2, omb2, step, bc2s, eps;
+};
+AdamWConsts adamw_consts(double lr, double beta1, double beta2, double eps, double wd, long t);
+hipError_t launch_adamw(float* p, const float* g, float* m, float* v, bf16* shadow, long n,
+                        const AdamWConsts& c, hipStream_t s);
+// Counter-based N(0, std^2) init of n fp32 values (Philox-style hash of
+// (seed, tensor id, index) fed to Box-Muller); also writes the bf16 shadow.
+hipError_t launch_init_normal(float* p, bf16* shadow, long n, uint64_t seed, uint32_t stream_id,
+                              float std, hipStream_t s);
+hipError_t launch_fill(float* p, bf16* shadow, long n, float value, hipStream_t s);
+hipError_t launch_zero(void* p, long bytes, hipStream_t s);
+hipError_t launch_sum_rows_batched(const float* dh, float* out, int B, int S, int d,
+                                   hipStream_t s);

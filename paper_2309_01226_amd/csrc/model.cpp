@@ -1,0 +1,273 @@
+// Model runtime: configuration checks, the per-model arena layout, parameter
+// table, and the forward / backward / AdamW launch sequence of one
+// fine-tuning step on the model's HIP stream.
+//
+// Arena (one per model, caller-provided or owned):
+//   fp32 master parameters | bf16 shadow | fp32 gradients | fp32 m | fp32 v |
+//   activations saved for backward | backward workspace.
+// Parameters run bottom to top (embeddings, blocks 0..L-1, final LN, head),
+// so the tensors frozen by k > 0 form a prefix and AdamW is a single flat
+// kernel over the trainable suffix; frozen gradients and moments are never
+// written.  Blocks below k share one scratch activation set.
+#include <math.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/saturn.h"
+#include "abi_common.h"
+#include "kernels.h"
+#include "model.h"
+
+bool attention_supports_dh(int dh);
+
+namespace {
+
+constexpr size_t kAlignElems = 64;  // parameter offsets (elements)
+constexpr size_t kAlignBytes = 256; // arena sections
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+}  // namespace
+
+// ------------------------------------------------------------------ config
+
+sat_status sat_validate_config(const sat_config* c) {
+  SAT_CHECK_ARG(c != nullptr, "null config");
+  SAT_CHECK_ARG(c->struct_size == sizeof(sat_config), "struct_size %u != sizeof(sat_config) %zu",
+                c->struct_size, sizeof(sat_config));
+  SAT_CHECK_ARG(c->arch >= SAT_GPT2 && c->arch <= SAT_VIT, "unknown arch %d", c->arch);
+  SAT_CHECK_ARG(c->n_layers >= 1, "n_layers must be >= 1");
+  SAT_CHECK_ARG(c->d_model >= 8 && c->d_model % 8 == 0 && c->d_model <= 4096,
+                "d_model must be a multiple of 8 in [8, 4096]");
+  SAT_CHECK_ARG(c->n_heads >= 1 && c->d_model % c->n_heads == 0, "d_model %% n_heads != 0");
+  int dh = c->d_model / c->n_heads;
+  SAT_CHECK_ARG(attention_supports_dh(dh), "head dim %d not in {16, 32, 64, 80, 128, 256}", dh);
+  SAT_CHECK_ARG(c->d_mlp >= 8 && c->d_mlp % 8 == 0, "d_mlp must be a positive multiple of 8");
+  SAT_CHECK_ARG(c->vocab >= 2, "vocab / classes must be >= 2");
+  SAT_CHECK_ARG(c->batch >= 1, "batch must be >= 1");
+  SAT_CHECK_ARG(c->frozen_layers >= 0 && c->frozen_layers <= c->n_layers,
+                "frozen_layers %d not in [0, n_layers]", c->frozen_layers);
+  SAT_CHECK_ARG(c->lr >= 0.f && c->beta1 >= 0.f && c->beta1 < 1.f && c->beta2 >= 0.f &&
+                    c->beta2 < 1.f && c->eps > 0.f && c->weight_decay >= 0.f,
+                "invalid AdamW hyper-parameters");
+  SAT_CHECK_ARG(c->ln_eps > 0.f && c->init_std >= 0.f, "invalid ln_eps / init_std");
+  if (c->arch == SAT_VIT) {
+    SAT_CHECK_ARG(c->patch >= 1 && c->img_size >= c->patch && c->img_size % c->patch == 0,
+                  "img_size must be a positive multiple of patch");
+    SAT_CHECK_ARG(c->channels >= 1, "channels must be >= 1");
+    SAT_CHECK_ARG(c->rotary_dim == 0, "rotary_dim must be 0 for VIT");
+  } else {
+    SAT_CHECK_ARG(c->seq_len >= 1, "seq_len must be >= 1");
+    if (c->arch == SAT_GPTJ)
+      SAT_CHECK_ARG(c->rotary_dim >= 0 && c->rotary_dim % 2 == 0 && c->rotary_dim <= dh,
+                    "rotary_dim must be even and <= head dim");
+    else
+      SAT_CHECK_ARG(c->rotary_dim == 0, "rotary_dim must be 0 for GPT2");
+    long T = (long)c->batch * c->seq_len;
+    SAT_CHECK_ARG(c->frozen_layers > 0 || (T <= 16384 && c->vocab < 65536),
+                  "training the token embedding needs batch*seq_len <= 16384 and vocab < 65536");
+  }
+  return SAT_OK;
+}
+
+// ------------------------------------------------------------------ layout
+
+void sat_model_dims(const sat_config& c, Dims* d) {
+  d->arch = c.arch;
+  d->L = c.n_layers;
+  d->d = c.d_model;
+  d->H = c.n_heads;
+  d->dh = c.d_model / c.n_heads;
+  d->m = c.d_mlp;
+  d->V = c.vocab;
+  d->Vp = (int)align_up(c.vocab, 8);
+  d->B = c.batch;
+  d->k = c.frozen_layers;
+  d->rd = c.rotary_dim;
+  if (c.arch == SAT_VIT) {
+    int g = c.img_size / c.patch;
+    d->np = g * g;
+    d->pd = c.channels * c.patch * c.patch;
+    d->S = d->np + 1;
+  } else {
+    d->np = 0;
+    d->pd = 0;
+    d->S = c.seq_len;
+  }
+  d->T = d->B * d->S;
+  d->rows_head = (c.arch == SAT_VIT) ? d->B : d->T;
+  d->qkv_ld = (c.arch == SAT_GPTJ) ? 3 * d->d + d->m : 3 * d->d;
+}
+
+static void add_param(std::vector<ParamDesc>& P, size_t& off, const std::string& name, long rows,
+                      long cols, int group, int kind) {
+  ParamDesc p;
+  p.name = name;
+  p.rows = rows;
+  p.cols = cols;
+  p.off = off;
+  p.group = group;
+  p.kind = kind;
+  P.push_back(p);
+  off = align_up(off + (size_t)rows * cols, kAlignElems);
+}
+
+// kind: 0 = normal init, 1 = zeros (bias), 2 = ones (LN gain)
+void sat_build_params(const sat_config& c, const Dims& D, std::vector<ParamDesc>& P,
+                      size_t* n_total) {
+  P.clear();
+  size_t off = 0;
+  const int d = D.d, m = D.m;
+  if (c.arch == SAT_VIT) {
+    add_param(P, off, "patch.w", d, D.pd, -1, 0);
+    add_param(P, off, "patch.b", d, 1, -1, 1);
+    add_param(P, off, "cls", d, 1, -1, 0);
+    add_param(P, off, "pos", D.S, d, -1, 0);
+  } else {
+    add_param(P, off, "wte", D.V, d, -1, 0);
+    if (c.arch == SAT_GPT2) add_param(P, off, "wpe", D.S, d, -1, 0);
+  }
+  for (int l = 0; l < D.L; ++l) {
+    std::string p = "h" + std::to_string(l) + ".";
+    if (c.arch == SAT_GPTJ) {
+      add_param(P, off, p + "ln1.g", d, 1, l, 2);
+      add_param(P, off, p + "ln1.b", d, 1, l, 1);
+      add_param(P, off, p + "attn.qkv.w", 3 * d, d, l, 0);
+      add_param(P, off, p + "mlp.fc1.w", m, d, l, 0);  // contiguous with attn.qkv.w
+      add_param(P, off, p + "mlp.fc1.b", m, 1, l, 1);
+      add_param(P, off, p + "attn.proj.w", d, d, l, 0);
+      add_param(P, off, p + "mlp.fc2.w", d, m, l, 0);
+      add_param(P, off, p + "mlp.fc2.b", d, 1, l, 1);
+    } else {
+      add_param(P, off, p + "ln1.g", d, 1, l, 2);
+      add_param(P, off, p + "ln1.b", d, 1, l, 1);
+      add_param(P, off, p + "attn.qkv.w", 3 * d, d, l, 0);
+      add_param(P, off, p + "attn.qkv.b", 3 * d, 1, l, 1);
+      add_param(P, off, p + "attn.proj.w", d, d, l, 0);
+      add_param(P, off, p + "attn.proj.b", d, 1, l, 1);
+      add_param(P, off, p + "ln2.g", d, 1, l, 2);
+      add_param(P, off, p + "ln2.b", d, 1, l, 1);
+      add_param(P, off, p + "mlp.fc1.w", m, d, l, 0);
+      add_param(P, off, p + "mlp.fc1.b", m, 1, l, 1);
+      add_param(P, off, p + "mlp.fc2.w", d, m, l, 0);
+      add_param(P, off, p + "mlp.fc2.b", d, 1, l, 1);
+    }
+  }
+  add_param(P, off, "lnf.g", d, 1, D.L, 2);
+  add_param(P, off, "lnf.b", d, 1, D.L, 1);
+  add_param(P, off, "head.w", D.V, d, D.L, 0);
+  if (c.arch != SAT_GPT2) add_param(P, off, "head.b", D.V, 1, D.L, 1);
+  for (auto& p : P) p.trainable = (p.group < 0) ? (D.k == 0) : (p.group >= D.k);
+  // Zero tail: the head's input-gradient product reads up to 7 rows past the
+  // last weight matrix when the vocabulary is not a multiple of 8.
+  off = align_up(off + (size_t)8 * (d > m ? d : m), kAlignElems);
+  *n_total = off;
+}
+
+namespace {
+
+struct Carver {
+  size_t off = 0;
+  char* base = nullptr;  // null during the sizing pass
+  template <typename T>
+  T* take(size_t count) {
+    size_t o = align_up(off, kAlignBytes);
+    off = o + count * sizeof(T);
+    return base ? reinterpret_cast<T*>(base + o) : nullptr;
+  }
+};
+
+// Lays out every buffer; with base == nullptr it only measures.
+size_t carve(sat_model* M, char* base) {
+  const Dims& D = M->D;
+  Carver c;
+  c.base = base;
+  const size_t NP = M->n_param_elems;
+  M->master = c.take<float>(NP);
+  M->shadow = c.take<bf16>(NP);
+  M->grad = c.take<float>(NP);
+  M->mom = c.take<float>(NP);
+  M->vel = c.take<float>(NP);
+  const long T = D.T, d = D.d, m = D.m;
+  const bool gptj = D.arch == SAT_GPTJ;
+  // residual stream entering every block and the final LN
+  M->h_in.assign(D.L + 1, nullptr);
+  for (int l = 0; l <= D.L; ++l) M->h_in[l] = c.take<float>(T * d);
+  // per-layer saved activations: blocks >= k get their own, frozen blocks share one set
+  const int nsets = (D.k > 0) ? D.L - D.k + 1 : D.L;
+  M->acts.assign(nsets, LayerActs());
+  for (int s = 0; s < nsets; ++s) {
+    LayerActs& A = M->acts[s];
+    A.a = c.take<bf16>(T * d);
+    A.mean1 = c.take<float>(T);
+    A.rstd1 = c.take<float>(T);
+    A.qkv = c.take<bf16>(T * D.qkv_ld);
+    A.o = c.take<bf16>(T * d);
+    A.lse = c.take<float>((size_t)D.B * D.H * D.S);
+    A.g = c.take<bf16>(T * m);
+    if (!gptj) {
+      A.h_mid = c.take<float>(T * d);
+      A.c = c.take<bf16>(T * d);
+      A.mean2 = c.take<float>(T);
+      A.rstd2 = c.take<float>(T);
+      A.u = c.take<bf16>(T * m);
+    } else {
+      A.h_mid = nullptr;
+      A.c = nullptr;
+      A.mean2 = A.rstd2 = nullptr;
+      A.u = nullptr;  // u lives in qkv[:, 3d:]
+    }
+  }
+  // head
+  const long R = D.rows_head;
+  M->f = c.take<bf16>(R * d);
+  M->meanf = c.take<float>(R);
+  M->rstdf = c.take<float>(R);
+  M->logits = c.take<float>(R * D.Vp);
+  M->dz = c.take<bf16>(R * D.Vp);
+  M->row_loss = c.take<float>(R);
+  M->scal = c.take<float>(8);  // [0] loss, [1] 1 / n_valid
+  // ViT input side
+  if (D.arch == SAT_VIT) {
+    M->patches = c.take<bf16>((size_t)D.B * D.np * D.pd);
+    M->zpatch = c.take<float>((size_t)D.B * D.np * d);
+    M->dzpatch = c.take<bf16>((size_t)D.B * D.np * d);
+  }
+  // backward workspace
+  M->dh = c.take<float>(T * d);
+  M->dh_bf = c.take<bf16>(T * d);
+  M->dA = c.take<float>(T * d);
+  M->dqkv = c.take<bf16>(T * D.qkv_ld);
+  M->du = gptj ? nullptr : c.take<bf16>(T * m);
+  M->dout = c.take<bf16>(T * d);
+  M->delta = c.take<float>((size_t)D.B * D.H * D.S);
+  M->n_part = (int)(T < 256 ? T : 256);
+  long wide = D.qkv_ld > D.Vp ? D.qkv_ld : D.Vp;
+  if (D.arch == SAT_VIT && D.pd > wide) wide = D.pd;
+  M->part = c.take<float>((size_t)2 * M->n_part * (wide > d ? wide : d));
+  M->sortbuf = c.take<int32_t>(T > 0 ? T : 1);
+  return align_up(c.off, kAlignBytes);
+}
+
+}  // namespace
+
+size_t sat_model_layout(sat_model* M, char* base) { return carve(M, base); }
+
+double sat_step_flops(const Dims& D) {
+  const double T = D.T, d = D.d, m = D.m;
+  const double gemm_layer = 2.0 * T * (3 * d * d + d * d + 2 * d * m);
+  const double causal = (D.arch == SAT_VIT) ? 1.0 : 0.5;
+  const double attn_layer = 4.0 * D.B * D.H * (double)D.S * D.S * D.dh * causal;
+  const double fwd_layer = gemm_layer + attn_layer;
+  double f = D.L * fwd_layer;                              // forward
+  f += (D.L - D.k) * 2.0 * fwd_layer;                      // dgrad + wgrad, attention backward
+  const double head = 2.0 * D.rows_head * d * D.V;
+  f += 3.0 * head;
+  if (D.arch == SAT_VIT) {
+    const double pe = 2.0 * D.B * D.np * (double)D.pd * d;
+    f += pe + (D.k == 0 ? pe : 0.0);
+  }
+  return f;
+}

@@ -1,0 +1,114 @@
+// Internal model state shared by the runtime translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/saturn.h"
+
+typedef __bf16 bf16;
+
+struct Dims {
+  int arch;
+  int L, d, H, dh, m, V, Vp, B, S, T, k, rd;
+  int np, pd;      // ViT: patches per image, values per patch
+  int rows_head;   // rows entering the head (T, or B for ViT)
+  int qkv_ld;      // row pitch of the q|k|v (|u for GPT-J) buffer
+};
+
+struct ParamDesc {
+  std::string name;
+  long rows, cols;
+  size_t off;      // element offset in the parameter arena
+  int group;       // -1 embeddings, l = block, L = final LN + head
+  int kind;        // 0 normal init, 1 zeros, 2 ones
+  bool trainable;
+};
+
+struct LayerActs {
+  bf16* a;          // LN1 output [T, d]
+  float* mean1;
+  float* rstd1;
+  bf16* qkv;        // [T, qkv_ld]: q | k | v (GPT-J: | u, the MLP pre-activation)
+  bf16* o;          // attention output [T, d]
+  float* lse;       // [B, H, S]
+  bf16* g;          // GELU output [T, m]
+  float* h_mid;     // GPT-2 / ViT: residual after attention [T, d]
+  bf16* c;          // LN2 output
+  float* mean2;
+  float* rstd2;
+  bf16* u;          // GPT-2 / ViT: MLP pre-activation [T, m]
+};
+
+struct TimingRec {
+  hipEvent_t e0, e1;
+  double flops;
+};
+
+struct sat_model {
+  sat_config cfg;
+  Dims D;
+  hipStream_t stream;
+  int device;
+  char* arena;
+  size_t arena_bytes;
+  bool own_arena;
+  bool failed;
+  int64_t t;
+  std::vector<ParamDesc> params;
+  size_t n_param_elems;
+  size_t train_off;  // first trainable element
+  // parameter-sized sections
+  float* master;
+  bf16* shadow;
+  float* grad;
+  float* mom;
+  float* vel;
+  // activations
+  std::vector<float*> h_in;
+  std::vector<LayerActs> acts;
+  bf16* f;
+  float* meanf;
+  float* rstdf;
+  float* logits;
+  bf16* dz;
+  float* row_loss;
+  float* scal;
+  bf16* patches;
+  float* zpatch;
+  bf16* dzpatch;
+  // backward workspace
+  float* dh;
+  bf16* dh_bf;
+  float* dA;
+  bf16* dqkv;
+  bf16* du;
+  bf16* dout;
+  float* delta;
+  float* part;
+  int n_part;
+  int32_t* sortbuf;
+  // optional per-launch timing of one kernel class
+  int timing_kind;
+  std::vector<TimingRec> timing;
+  size_t timing_used;
+};
+
+sat_status sat_validate_config(const sat_config* c);
+void sat_model_dims(const sat_config& c, Dims* d);
+void sat_build_params(const sat_config& c, const Dims& D, std::vector<ParamDesc>& P,
+                      size_t* n_total);
+size_t sat_model_layout(sat_model* M, char* base);
+double sat_step_flops(const Dims& D);
+
+// step.cpp
+sat_status sat_run_forward(sat_model* M, const void* inputs, const int32_t* labels);
+sat_status sat_run_backward(sat_model* M, const void* inputs);
+sat_status sat_run_adamw(sat_model* M);
+sat_status sat_run_init(sat_model* M);
+
+const LayerActs& sat_layer_acts(const sat_model* M, int l);

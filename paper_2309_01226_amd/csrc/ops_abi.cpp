@@ -1,0 +1,192 @@
+// Kernel-level C ABI (include/saturn_ops.h): argument checks, then one launch.
+#include <math.h>
+#include <string.h>
+
+#include <string>
+
+#include "../../include/saturn_ops.h"
+#include "abi_common.h"
+#include "kernels.h"
+
+static thread_local std::string g_last_error;
+
+void sat_set_error(const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+}
+
+extern "C" const char* sat_last_error(void) { return g_last_error.c_str(); }
+
+static inline hipStream_t S(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+extern "C" sat_status sat_op_gemm(const sat_gemm_desc* d, void* stream) {
+  SAT_CHECK_ARG(d != nullptr, "sat_op_gemm: null descriptor");
+  SAT_CHECK_ARG(d->A && d->B && d->out, "sat_op_gemm: null operand");
+  SAT_CHECK_ARG(d->M >= 0 && d->N >= 0 && d->K > 0, "sat_op_gemm: bad sizes M=%d N=%d K=%d",
+                d->M, d->N, d->K);
+  SAT_CHECK_ARG(d->a_layout == 0 || d->a_layout == 1, "sat_op_gemm: bad a_layout");
+  SAT_CHECK_ARG(d->b_layout == 0 || d->b_layout == 1, "sat_op_gemm: bad b_layout");
+  SAT_CHECK_ARG(d->epilogue >= 0 && d->epilogue <= 3, "sat_op_gemm: bad epilogue");
+  SAT_CHECK_ARG(d->lda >= (d->a_layout == 0 ? d->K : d->M), "sat_op_gemm: lda too small");
+  SAT_CHECK_ARG(d->ldb >= (d->b_layout == 0 ? d->K : d->N), "sat_op_gemm: ldb too small");
+  SAT_CHECK_ARG(d->ldo >= d->N, "sat_op_gemm: ldo too small");
+  SAT_CHECK_ARG(d->epilogue != 1 || (d->resid && d->ldr >= d->N), "sat_op_gemm: resid");
+  SAT_CHECK_ARG(d->epilogue != 3 || (d->aux && d->ldaux >= d->N), "sat_op_gemm: aux");
+  SAT_CHECK_ARG(d->epilogue != 2 || d->out2 == nullptr ||
+                    (d->gelu_col0 >= 0 && d->ldo2 >= d->N - d->gelu_col0),
+                "sat_op_gemm: out2");
+  GemmArgs a;
+  memset(&a, 0, sizeof a);
+  a.A = (const bf16*)d->A;
+  a.B = (const bf16*)d->B;
+  a.M = d->M; a.N = d->N; a.K = d->K;
+  a.lda = d->lda; a.ldb = d->ldb;
+  a.out = d->out; a.ldo = d->ldo;
+  a.bias = d->bias; a.bias_col0 = d->bias_col0;
+  a.resid = d->resid; a.ldr = d->ldr;
+  a.out2 = (bf16*)d->out2; a.ldo2 = d->ldo2; a.gelu_col0 = d->gelu_col0;
+  a.aux = (const bf16*)d->aux; a.ldaux = d->ldaux;
+  a.gelu_erf = d->gelu_erf;
+  SAT_HIP(launch_gemm(a, d->a_layout, d->b_layout, d->epilogue, S(stream)));
+  return SAT_OK;
+}
+
+bool attention_supports_dh(int dh);
+
+extern "C" sat_status sat_op_layernorm_fwd(const float* x, int64_t ldx, int64_t row_stride,
+                                           const float* g, const float* b, void* y, int64_t ldy,
+                                           float* mean, float* rstd, int32_t rows, int32_t d,
+                                           float eps, void* stream) {
+  SAT_CHECK_ARG(x && g && b && y && mean && rstd, "layernorm_fwd: null pointer");
+  SAT_CHECK_ARG(rows >= 0 && d > 0 && d % 4 == 0 && d <= 8192, "layernorm_fwd: d=%d must be a positive multiple of 4 <= 8192", d);
+  SAT_CHECK_ARG(ldx >= d && ldx % 4 == 0 && ldy >= d && ldy % 4 == 0 && row_stride >= 1,
+                "layernorm_fwd: bad leading dimensions");
+  SAT_HIP(launch_layernorm_fwd(x, ldx, row_stride, g, b, (bf16*)y, ldy, mean, rstd, rows, d, eps,
+                               S(stream)));
+  return SAT_OK;
+}
+
+extern "C" sat_status sat_op_layernorm_bwd(const float* dy, int64_t lddy, const float* x,
+                                           int64_t ldx, int64_t row_stride, const float* g,
+                                           const float* mean, const float* rstd, float* dres,
+                                           int64_t ldres, float* dg, float* db, float* work,
+                                           int32_t rows, int32_t d, void* stream) {
+  SAT_CHECK_ARG(dy && x && g && mean && rstd && dres && dg && db && work,
+                "layernorm_bwd: null pointer");
+  SAT_CHECK_ARG(rows > 0 && d > 0 && d % 4 == 0 && d <= 4096, "layernorm_bwd: d=%d must be a positive multiple of 4 <= 4096", d);
+  SAT_CHECK_ARG(lddy >= d && lddy % 4 == 0 && ldx >= d && ldx % 4 == 0 && ldres >= d &&
+                    ldres % 4 == 0 && row_stride >= 1,
+                "layernorm_bwd: bad leading dimensions");
+  int n_part = rows < 256 ? rows : 256;
+  SAT_HIP(launch_layernorm_bwd(dy, lddy, x, ldx, row_stride, g, mean, rstd, dres, ldres, work,
+                               work + (long)n_part * d, rows, d, n_part, S(stream)));
+  SAT_HIP(launch_colsum_partials(work, n_part, d, dg, S(stream)));
+  SAT_HIP(launch_colsum_partials(work + (long)n_part * d, n_part, d, db, S(stream)));
+  return SAT_OK;
+}
+
+extern "C" sat_status sat_op_attention_fwd(const void* q, const void* k, const void* v,
+                                           int64_t ldq, int64_t ldk, int64_t ldv, void* o,
+                                           int64_t ldo, float* lse, int32_t B, int32_t H,
+                                           int32_t Sq, int32_t dh, int32_t causal, float scale,
+                                           void* stream) {
+  SAT_CHECK_ARG(q && k && v && o && lse, "attention_fwd: null pointer");
+  SAT_CHECK_ARG(B >= 0 && H > 0 && Sq >= 0, "attention_fwd: bad sizes");
+  SAT_CHECK_ARG(attention_supports_dh(dh), "attention_fwd: head dim %d not in {16,32,64,80,128,256}", dh);
+  SAT_CHECK_ARG(ldq % 8 == 0 && ldk % 8 == 0 && ldv % 8 == 0 && ldq >= (int64_t)H * dh &&
+                    ldk >= (int64_t)H * dh && ldv >= (int64_t)H * dh && ldo >= (int64_t)H * dh,
+                "attention_fwd: leading dimensions must be multiples of 8 and >= H*dh");
+  AttnArgs a;
+  a.q = (const bf16*)q; a.k = (const bf16*)k; a.v = (const bf16*)v;
+  a.ldq = ldq; a.ldk = ldk; a.ldv = ldv;
+  a.o = (bf16*)o; a.ldo = ldo; a.lse = lse;
+  a.B = B; a.H = H; a.S = Sq; a.dh = dh; a.causal = causal; a.scale = scale;
+  SAT_HIP(launch_attention_fwd(a, S(stream)));
+  return SAT_OK;
+}
+
+extern "C" sat_status sat_op_attention_bwd(const void* q, const void* k, const void* v,
+                                           int64_t ldq, int64_t ldk, int64_t ldv, const void* o,
+                                           int64_t ldo, const float* lse, const void* dout,
+                                           int64_t lddo, float* delta, void* dq, void* dk,
+                                           void* dv, int64_t lddq, int64_t lddk, int64_t lddv,
+                                           int32_t B, int32_t H, int32_t Sq, int32_t dh,
+                                           int32_t causal, float scale, void* stream) {
+  SAT_CHECK_ARG(q && k && v && o && lse && dout && delta && dq && dk && dv,
+                "attention_bwd: null pointer");
+  SAT_CHECK_ARG(B >= 0 && H > 0 && Sq >= 0, "attention_bwd: bad sizes");
+  SAT_CHECK_ARG(attention_supports_dh(dh), "attention_bwd: head dim %d not in {16,32,64,80,128,256}", dh);
+  SAT_CHECK_ARG(ldq % 8 == 0 && ldk % 8 == 0 && ldv % 8 == 0 && lddo % 8 == 0,
+                "attention_bwd: leading dimensions must be multiples of 8");
+  AttnBwdArgs a;
+  a.f.q = (const bf16*)q; a.f.k = (const bf16*)k; a.f.v = (const bf16*)v;
+  a.f.ldq = ldq; a.f.ldk = ldk; a.f.ldv = ldv;
+  a.f.o = (bf16*)o; a.f.ldo = ldo; a.f.lse = (float*)lse;
+  a.f.B = B; a.f.H = H; a.f.S = Sq; a.f.dh = dh; a.f.causal = causal; a.f.scale = scale;
+  a.dout = (const bf16*)dout; a.lddo = lddo; a.delta = delta;
+  a.dq = (bf16*)dq; a.dk = (bf16*)dk; a.dv = (bf16*)dv;
+  a.lddq = lddq; a.lddk = lddk; a.lddv = lddv;
+  SAT_HIP(launch_attention_bwd(a, S(stream)));
+  return SAT_OK;
+}
+
+extern "C" sat_status sat_op_rotary(void* qk, int64_t ld, int32_t B, int32_t Sq, int32_t H,
+                                    int32_t dh, int32_t rd, int32_t inverse, void* stream) {
+  SAT_CHECK_ARG(qk != nullptr, "rotary: null pointer");
+  SAT_CHECK_ARG(rd >= 0 && rd % 2 == 0 && rd <= dh, "rotary: rotary dim %d must be even and <= %d", rd, dh);
+  SAT_CHECK_ARG(ld >= 2L * H * dh, "rotary: ld too small");
+  SAT_HIP(launch_rotary((bf16*)qk, ld, B, Sq, H, dh, rd, inverse, S(stream)));
+  return SAT_OK;
+}
+
+extern "C" sat_status sat_op_cross_entropy(const float* z, int64_t ldz, const int32_t* labels,
+                                           int32_t N, int32_t V, float* row_loss, void* dz,
+                                           int64_t lddz, float* inv_n, void* stream) {
+  SAT_CHECK_ARG(z && labels && row_loss && dz && inv_n, "cross_entropy: null pointer");
+  SAT_CHECK_ARG(N >= 0 && V > 0 && ldz >= V && lddz >= V, "cross_entropy: bad sizes");
+  SAT_HIP(launch_count_valid(labels, N, inv_n, S(stream)));
+  SAT_HIP(launch_xent(z, ldz, labels, N, V, row_loss, (bf16*)dz, lddz, inv_n, S(stream)));
+  return SAT_OK;
+}
+
+extern "C" sat_status sat_op_adamw(float* p, const float* g, float* m, float* v, void* shadow,
+                                   int64_t n, double lr, double beta1, double beta2, double eps,
+                                   double wd, int64_t t, void* stream) {
+  SAT_CHECK_ARG(p && g && m && v, "adamw: null pointer");
+  SAT_CHECK_ARG(n >= 0 && t >= 1, "adamw: n >= 0 and t >= 1 required");
+  SAT_HIP(launch_adamw(p, g, m, v, (bf16*)shadow, n, adamw_consts(lr, beta1, beta2, eps, wd, t),
+                       S(stream)));
+  return SAT_OK;
+}
+
+extern "C" sat_status sat_op_embed_fwd(const int32_t* tok, const float* wte, const float* wpe,
+                                       float* h, int32_t T, int32_t Sq, int32_t d, int32_t V,
+                                       void* stream) {
+  SAT_CHECK_ARG(tok && wte && h, "embed_fwd: null pointer");
+  SAT_CHECK_ARG(T >= 0 && Sq > 0 && d > 0 && d % 4 == 0 && V > 0, "embed_fwd: bad sizes");
+  SAT_HIP(launch_embed_fwd(tok, wte, wpe, h, T, Sq, d, V, S(stream)));
+  return SAT_OK;
+}
+
+extern "C" sat_status sat_op_embed_bwd(const int32_t* tok, const float* dh, float* dwte,
+                                       int32_t T, int32_t d, int32_t V, int32_t* work,
+                                       void* stream) {
+  SAT_CHECK_ARG(tok && dh && dwte && work, "embed_bwd: null pointer");
+  SAT_CHECK_ARG(T > 0 && T <= 16384 && d > 0 && d % 4 == 0 && V > 0 && V < 65536,
+                "embed_bwd: needs 0 < T <= 16384, d %% 4 == 0, 0 < V < 65536");
+  SAT_HIP(launch_embed_bwd(tok, dh, dwte, T, d, V, work, S(stream)));
+  return SAT_OK;
+}
+
+extern "C" sat_status sat_op_colsum(const float* X, int64_t ldx, int32_t rows, int32_t cols,
+                                    float* out, float* work, void* stream) {
+  SAT_CHECK_ARG(X && out && work, "colsum: null pointer");
+  SAT_CHECK_ARG(rows > 0 && cols >= 0 && ldx >= cols, "colsum: bad sizes");
+  int n_part = rows < 256 ? rows : 256;
+  SAT_HIP(launch_colsum_f32(X, ldx, rows, cols, work, n_part, out, S(stream)));
+  return SAT_OK;
+}

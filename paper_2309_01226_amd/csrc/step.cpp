@@ -1,0 +1,387 @@
+// Launch sequence of one fine-tuning step on the model's stream:
+// embeddings -> blocks (LN, QKV, rotary, attention, out-projection, LN, MLP)
+// -> final LN -> head -> cross-entropy, then the backward pass from the head
+// down to block k (no work at all below it), then AdamW on the trainable
+// suffix of the parameter arena.
+#include <math.h>
+#include <string.h>
+
+#include "abi_common.h"
+#include "kernels.h"
+#include "model.h"
+
+namespace {
+
+enum { TK_OFF = 0, TK_QKV_FWD = 1, TK_ALL_GEMM = 2, TK_ADAMW = 3, TK_ATTN_FWD = 4, TK_ATTN_BWD = 5 };
+
+struct Timed {
+  sat_model* M;
+  TimingRec* rec = nullptr;
+  Timed(sat_model* m, int kind, double work) : M(m) {
+    if (m->timing_kind == TK_OFF) return;
+    bool match = (m->timing_kind == kind) ||
+                 (m->timing_kind == TK_ALL_GEMM && (kind == TK_QKV_FWD || kind == TK_ALL_GEMM));
+    if (!match || m->timing_used >= m->timing.size()) return;
+    rec = &m->timing[m->timing_used++];
+    rec->flops = work;
+    hipEventRecord(rec->e0, m->stream);
+  }
+  ~Timed() {
+    if (rec) hipEventRecord(rec->e1, M->stream);
+  }
+};
+
+GemmArgs gargs(const bf16* A, long lda, const bf16* B, long ldb, int Mr, int N, int K, void* out,
+               long ldo) {
+  GemmArgs a;
+  memset(&a, 0, sizeof a);
+  a.A = A;
+  a.lda = lda;
+  a.B = B;
+  a.ldb = ldb;
+  a.M = Mr;
+  a.N = N;
+  a.K = K;
+  a.out = out;
+  a.ldo = ldo;
+  a.ldr = ldo;
+  return a;
+}
+
+sat_status gemm(sat_model* M, const GemmArgs& a, int alay, int blay, int epi,
+                int tk = TK_ALL_GEMM) {
+  Timed t(M, tk, 2.0 * a.M * a.N * (double)a.K);
+  SAT_HIP(launch_gemm(a, alay, blay, epi, M->stream));
+  return SAT_OK;
+}
+
+#define TRY(x)                        \
+  do {                                \
+    sat_status st_ = (x);             \
+    if (st_ != SAT_OK) return st_;    \
+  } while (0)
+
+struct PIdx {
+  const sat_model* M;
+  int base;
+  const ParamDesc& p(int i) const { return M->params[base + i]; }
+};
+
+// Parameter accessors by table index.
+inline const float* master(const sat_model* M, int i) { return M->master + M->params[i].off; }
+inline const bf16* shadow(const sat_model* M, int i) { return M->shadow + M->params[i].off; }
+inline float* grad(sat_model* M, int i) { return M->grad + M->params[i].off; }
+
+// Index of the first parameter of block l and of the head group.
+int embed_count(const sat_model* M) {
+  if (M->D.arch == SAT_VIT) return 4;
+  return M->D.arch == SAT_GPT2 ? 2 : 1;
+}
+int per_block(const sat_model* M) { return M->D.arch == SAT_GPTJ ? 8 : 12; }
+int block_base(const sat_model* M, int l) { return embed_count(M) + l * per_block(M); }
+int head_base(const sat_model* M) { return embed_count(M) + M->D.L * per_block(M); }
+
+// Block parameter slots (GPT-2 / ViT order; GPT-J uses its own).
+enum { B_LN1G = 0, B_LN1B, B_QKVW, B_QKVB, B_PROJW, B_PROJB, B_LN2G, B_LN2B, B_FC1W, B_FC1B, B_FC2W, B_FC2B };
+enum { J_LN1G = 0, J_LN1B, J_QKVW, J_FC1W, J_FC1B, J_PROJW, J_FC2W, J_FC2B };
+
+}  // namespace
+
+const LayerActs& sat_layer_acts(const sat_model* M, int l) {
+  const int k = M->D.k;
+  return (l < k) ? M->acts[0] : M->acts[l - k + (k > 0 ? 1 : 0)];
+}
+
+sat_status sat_run_init(sat_model* M) {
+  const size_t NP = M->n_param_elems;
+  hipStream_t s = M->stream;
+  SAT_HIP(launch_zero(M->master, NP * 4, s));
+  SAT_HIP(launch_zero(M->shadow, ((NP * 2 + 3) / 4) * 4, s));
+  SAT_HIP(launch_zero(M->grad, NP * 4, s));
+  SAT_HIP(launch_zero(M->mom, NP * 4, s));
+  SAT_HIP(launch_zero(M->vel, NP * 4, s));
+  for (size_t i = 0; i < M->params.size(); ++i) {
+    const ParamDesc& p = M->params[i];
+    long n = p.rows * p.cols;
+    float* dst = M->master + p.off;
+    bf16* sh = M->shadow + p.off;
+    if (p.kind == 0)
+      SAT_HIP(launch_init_normal(dst, sh, n, M->cfg.seed, (uint32_t)i, M->cfg.init_std, s));
+    else
+      SAT_HIP(launch_fill(dst, sh, n, p.kind == 2 ? 1.f : 0.f, s));
+  }
+  return SAT_OK;
+}
+
+sat_status sat_run_forward(sat_model* M, const void* inputs, const int32_t* labels) {
+  const Dims& D = M->D;
+  hipStream_t s = M->stream;
+  const int T = D.T, d = D.d, m = D.m;
+  const float eps = M->cfg.ln_eps;
+  const int gelu_erf = D.arch == SAT_VIT ? 1 : 0;
+  const bool gptj = D.arch == SAT_GPTJ;
+
+  // ---- embeddings
+  if (D.arch == SAT_VIT) {
+    SAT_HIP(launch_patchify((const float*)inputs, M->patches, D.B, M->cfg.channels,
+                            M->cfg.img_size, M->cfg.patch, s));
+    GemmArgs a = gargs(M->patches, D.pd, shadow(M, 0), D.pd, D.B * D.np, d, D.pd, M->zpatch, d);
+    a.bias = master(M, 1);
+    TRY(gemm(M, a, LAY_K, LAY_K, EPI_F32));
+    SAT_HIP(launch_vit_assemble(M->zpatch, master(M, 2), master(M, 3), M->h_in[0], D.B, D.np, d, s));
+  } else {
+    const float* wpe = (D.arch == SAT_GPT2) ? master(M, 1) : nullptr;
+    SAT_HIP(launch_embed_fwd((const int32_t*)inputs, master(M, 0), wpe, M->h_in[0], T, D.S, d,
+                             D.V, s));
+  }
+
+  // ---- blocks
+  for (int l = 0; l < D.L; ++l) {
+    const LayerActs& A = sat_layer_acts(M, l);
+    const int pb = block_base(M, l);
+    SAT_HIP(launch_layernorm_fwd(M->h_in[l], d, 1, master(M, pb + 0), master(M, pb + 1), A.a, d,
+                                 A.mean1, A.rstd1, T, d, eps, s));
+    if (gptj) {
+      // fused q | k | v | u = a [W_qkv; W_fc1]^T (+ fc1 bias on u), g = GELU(u)
+      GemmArgs a = gargs(A.a, d, shadow(M, pb + J_QKVW), d, T, D.qkv_ld, d, A.qkv, D.qkv_ld);
+      a.bias = master(M, pb + J_FC1B);
+      a.bias_col0 = 3 * d;
+      a.out2 = A.g;
+      a.ldo2 = m;
+      a.gelu_col0 = 3 * d;
+      a.gelu_erf = 0;
+      TRY(gemm(M, a, LAY_K, LAY_K, EPI_BF16, TK_QKV_FWD));
+      SAT_HIP(launch_rotary(A.qkv, D.qkv_ld, D.B, D.S, D.H, D.dh, D.rd, 0, s));
+    } else {
+      GemmArgs a = gargs(A.a, d, shadow(M, pb + B_QKVW), d, T, 3 * d, d, A.qkv, 3 * d);
+      a.bias = master(M, pb + B_QKVB);
+      TRY(gemm(M, a, LAY_K, LAY_K, EPI_BF16, TK_QKV_FWD));
+    }
+    {
+      AttnArgs at;
+      at.q = A.qkv;
+      at.k = A.qkv + d;
+      at.v = A.qkv + 2 * d;
+      at.ldq = at.ldk = at.ldv = D.qkv_ld;
+      at.o = A.o;
+      at.ldo = d;
+      at.lse = A.lse;
+      at.B = D.B;
+      at.H = D.H;
+      at.S = D.S;
+      at.dh = D.dh;
+      at.causal = D.arch != SAT_VIT;
+      at.scale = 1.f / sqrtf((float)D.dh);
+      Timed tm(M, TK_ATTN_FWD, 4.0 * D.B * D.H * (double)D.S * D.S * D.dh * (at.causal ? 0.5 : 1.0));
+      SAT_HIP(launch_attention_fwd(at, s));
+    }
+    if (gptj) {
+      GemmArgs a = gargs(A.o, d, shadow(M, pb + J_PROJW), d, T, d, d, M->h_in[l + 1], d);
+      a.resid = M->h_in[l];
+      TRY(gemm(M, a, LAY_K, LAY_K, EPI_RESID_F32));
+      GemmArgs b = gargs(A.g, m, shadow(M, pb + J_FC2W), m, T, d, m, M->h_in[l + 1], d);
+      b.resid = M->h_in[l + 1];
+      b.bias = master(M, pb + J_FC2B);
+      TRY(gemm(M, b, LAY_K, LAY_K, EPI_RESID_F32));
+    } else {
+      GemmArgs a = gargs(A.o, d, shadow(M, pb + B_PROJW), d, T, d, d, A.h_mid, d);
+      a.resid = M->h_in[l];
+      a.bias = master(M, pb + B_PROJB);
+      TRY(gemm(M, a, LAY_K, LAY_K, EPI_RESID_F32));
+      SAT_HIP(launch_layernorm_fwd(A.h_mid, d, 1, master(M, pb + B_LN2G), master(M, pb + B_LN2B),
+                                   A.c, d, A.mean2, A.rstd2, T, d, eps, s));
+      GemmArgs b = gargs(A.c, d, shadow(M, pb + B_FC1W), d, T, m, d, A.u, m);
+      b.bias = master(M, pb + B_FC1B);
+      b.out2 = A.g;
+      b.ldo2 = m;
+      b.gelu_col0 = 0;
+      b.gelu_erf = gelu_erf;
+      TRY(gemm(M, b, LAY_K, LAY_K, EPI_BF16));
+      GemmArgs c = gargs(A.g, m, shadow(M, pb + B_FC2W), m, T, d, m, M->h_in[l + 1], d);
+      c.resid = A.h_mid;
+      c.bias = master(M, pb + B_FC2B);
+      TRY(gemm(M, c, LAY_K, LAY_K, EPI_RESID_F32));
+    }
+  }
+
+  // ---- final LN, head, cross-entropy
+  const int hb = head_base(M);
+  const int R = D.rows_head;
+  const long rstride = (D.arch == SAT_VIT) ? D.S : 1;
+  SAT_HIP(launch_layernorm_fwd(M->h_in[D.L], d, rstride, master(M, hb + 0), master(M, hb + 1),
+                               M->f, d, M->meanf, M->rstdf, R, d, eps, s));
+  GemmArgs a = gargs(M->f, d, shadow(M, hb + 2), d, R, D.V, d, M->logits, D.Vp);
+  if (D.arch != SAT_GPT2) a.bias = master(M, hb + 3);
+  TRY(gemm(M, a, LAY_K, LAY_K, EPI_F32));
+  SAT_HIP(launch_count_valid(labels, R, M->scal + 1, s));
+  SAT_HIP(launch_xent(M->logits, D.Vp, labels, R, D.V, M->row_loss, M->dz, D.Vp, M->scal + 1, s));
+  SAT_HIP(launch_loss_finalize(M->row_loss, R, M->scal + 1, M->scal, s));
+  return SAT_OK;
+}
+
+static sat_status ln_bwd(sat_model* M, const float* dy, const float* x, long row_stride,
+                         int gidx, const float* mean, const float* rstd, int rows) {
+  const int d = M->D.d;
+  const int np_ = rows < 256 ? rows : 256;
+  float* pg = M->part;
+  float* pbb = M->part + (size_t)np_ * d;
+  SAT_HIP(launch_layernorm_bwd(dy, d, x, d, row_stride, master(M, gidx), mean, rstd, M->dh, d, pg,
+                               pbb, rows, d, np_, M->stream));
+  SAT_HIP(launch_colsum_partials(pg, np_, d, grad(M, gidx), M->stream));
+  SAT_HIP(launch_colsum_partials(pbb, np_, d, grad(M, gidx + 1), M->stream));
+  return SAT_OK;
+}
+
+sat_status sat_run_backward(sat_model* M, const void* inputs) {
+  const Dims& D = M->D;
+  hipStream_t s = M->stream;
+  const int T = D.T, d = D.d, m = D.m;
+  const int gelu_erf = D.arch == SAT_VIT ? 1 : 0;
+  const bool gptj = D.arch == SAT_GPTJ;
+  const int hb = head_base(M);
+  const int R = D.rows_head;
+  const int npT = M->n_part;
+
+  // ---- head
+  {
+    GemmArgs w = gargs(M->dz, D.Vp, M->f, d, D.V, d, R, grad(M, hb + 2), d);
+    TRY(gemm(M, w, LAY_MN, LAY_MN, EPI_F32));
+    if (D.arch != SAT_GPT2)
+      SAT_HIP(launch_colsum_bf16(M->dz, D.Vp, R, D.V, M->part, R < 256 ? R : 256,
+                                 grad(M, hb + 3), s));
+    // K = Vp: the padding columns of dz are zero and the parameter arena has a
+    // zero tail, so the extra products vanish and the 16-byte path applies.
+    GemmArgs g = gargs(M->dz, D.Vp, shadow(M, hb + 2), d, R, d, D.Vp, M->dA, d);
+    TRY(gemm(M, g, LAY_K, LAY_MN, EPI_F32));
+    SAT_HIP(launch_zero(M->dh, (long)T * d * 4, s));
+    const long rstride = (D.arch == SAT_VIT) ? D.S : 1;
+    // LN_f backward writes rows r * rstride of dh (CLS rows for ViT)
+    const int np_ = R < 256 ? R : 256;
+    float* pg = M->part;
+    float* pbb = M->part + (size_t)np_ * d;
+    SAT_HIP(launch_layernorm_bwd(M->dA, d, M->h_in[D.L], d, rstride, master(M, hb + 0), M->meanf,
+                                 M->rstdf, M->dh, d, pg, pbb, R, d, np_, s));
+    SAT_HIP(launch_colsum_partials(pg, np_, d, grad(M, hb + 0), s));
+    SAT_HIP(launch_colsum_partials(pbb, np_, d, grad(M, hb + 1), s));
+  }
+
+  // ---- blocks L-1 .. k
+  for (int l = D.L - 1; l >= D.k; --l) {
+    const LayerActs& A = sat_layer_acts(M, l);
+    const int pb = block_base(M, l);
+    AttnBwdArgs ab;
+    ab.f.q = A.qkv;
+    ab.f.k = A.qkv + d;
+    ab.f.v = A.qkv + 2 * d;
+    ab.f.ldq = ab.f.ldk = ab.f.ldv = D.qkv_ld;
+    ab.f.o = A.o;
+    ab.f.ldo = d;
+    ab.f.lse = A.lse;
+    ab.f.B = D.B;
+    ab.f.H = D.H;
+    ab.f.S = D.S;
+    ab.f.dh = D.dh;
+    ab.f.causal = D.arch != SAT_VIT;
+    ab.f.scale = 1.f / sqrtf((float)D.dh);
+    ab.dout = M->dout;
+    ab.lddo = d;
+    ab.delta = M->delta;
+    ab.dq = M->dqkv;
+    ab.dk = M->dqkv + d;
+    ab.dv = M->dqkv + 2 * d;
+    ab.lddq = ab.lddk = ab.lddv = D.qkv_ld;
+    const double attn_bwd_flops =
+        8.0 * D.B * D.H * (double)D.S * D.S * D.dh * (ab.f.causal ? 0.5 : 1.0);
+
+    if (gptj) {
+      SAT_HIP(launch_f32_to_bf16(M->dh, d, M->dh_bf, d, T, d, s));
+      GemmArgs w2 = gargs(M->dh_bf, d, A.g, m, d, m, T, grad(M, pb + J_FC2W), m);
+      TRY(gemm(M, w2, LAY_MN, LAY_MN, EPI_F32));
+      SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + J_FC2B), s));
+      GemmArgs du = gargs(M->dh_bf, d, shadow(M, pb + J_FC2W), m, T, m, d, M->dqkv + 3 * d, D.qkv_ld);
+      du.aux = A.qkv + 3 * d;
+      du.ldaux = D.qkv_ld;
+      du.gelu_erf = 0;
+      TRY(gemm(M, du, LAY_K, LAY_MN, EPI_DGELU_BF16));
+      GemmArgs wo = gargs(M->dh_bf, d, A.o, d, d, d, T, grad(M, pb + J_PROJW), d);
+      TRY(gemm(M, wo, LAY_MN, LAY_MN, EPI_F32));
+      GemmArgs go = gargs(M->dh_bf, d, shadow(M, pb + J_PROJW), d, T, d, d, M->dout, d);
+      TRY(gemm(M, go, LAY_K, LAY_MN, EPI_BF16));
+      {
+        Timed tm(M, TK_ATTN_BWD, attn_bwd_flops);
+        SAT_HIP(launch_attention_bwd(ab, s));
+      }
+      SAT_HIP(launch_rotary(M->dqkv, D.qkv_ld, D.B, D.S, D.H, D.dh, D.rd, 1, s));
+      GemmArgs wq = gargs(M->dqkv, D.qkv_ld, A.a, d, D.qkv_ld, d, T, grad(M, pb + J_QKVW), d);
+      TRY(gemm(M, wq, LAY_MN, LAY_MN, EPI_F32));
+      SAT_HIP(launch_colsum_bf16(M->dqkv + 3 * d, D.qkv_ld, T, m, M->part, npT,
+                                 grad(M, pb + J_FC1B), s));
+      GemmArgs ga = gargs(M->dqkv, D.qkv_ld, shadow(M, pb + J_QKVW), d, T, d, D.qkv_ld, M->dA, d);
+      TRY(gemm(M, ga, LAY_K, LAY_MN, EPI_F32));
+      TRY(ln_bwd(M, M->dA, M->h_in[l], 1, pb + J_LN1G, A.mean1, A.rstd1, T));
+    } else {
+      SAT_HIP(launch_f32_to_bf16(M->dh, d, M->dh_bf, d, T, d, s));
+      GemmArgs w2 = gargs(M->dh_bf, d, A.g, m, d, m, T, grad(M, pb + B_FC2W), m);
+      TRY(gemm(M, w2, LAY_MN, LAY_MN, EPI_F32));
+      SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + B_FC2B), s));
+      GemmArgs du = gargs(M->dh_bf, d, shadow(M, pb + B_FC2W), m, T, m, d, M->du, m);
+      du.aux = A.u;
+      du.ldaux = m;
+      du.gelu_erf = gelu_erf;
+      TRY(gemm(M, du, LAY_K, LAY_MN, EPI_DGELU_BF16));
+      GemmArgs w1 = gargs(M->du, m, A.c, d, m, d, T, grad(M, pb + B_FC1W), d);
+      TRY(gemm(M, w1, LAY_MN, LAY_MN, EPI_F32));
+      SAT_HIP(launch_colsum_bf16(M->du, m, T, m, M->part, npT, grad(M, pb + B_FC1B), s));
+      GemmArgs gc = gargs(M->du, m, shadow(M, pb + B_FC1W), d, T, d, m, M->dA, d);
+      TRY(gemm(M, gc, LAY_K, LAY_MN, EPI_F32));
+      TRY(ln_bwd(M, M->dA, A.h_mid, 1, pb + B_LN2G, A.mean2, A.rstd2, T));
+      SAT_HIP(launch_f32_to_bf16(M->dh, d, M->dh_bf, d, T, d, s));
+      GemmArgs wo = gargs(M->dh_bf, d, A.o, d, d, d, T, grad(M, pb + B_PROJW), d);
+      TRY(gemm(M, wo, LAY_MN, LAY_MN, EPI_F32));
+      SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + B_PROJB), s));
+      GemmArgs go = gargs(M->dh_bf, d, shadow(M, pb + B_PROJW), d, T, d, d, M->dout, d);
+      TRY(gemm(M, go, LAY_K, LAY_MN, EPI_BF16));
+      {
+        Timed tm(M, TK_ATTN_BWD, attn_bwd_flops);
+        SAT_HIP(launch_attention_bwd(ab, s));
+      }
+      GemmArgs wq = gargs(M->dqkv, 3 * d, A.a, d, 3 * d, d, T, grad(M, pb + B_QKVW), d);
+      TRY(gemm(M, wq, LAY_MN, LAY_MN, EPI_F32));
+      SAT_HIP(launch_colsum_bf16(M->dqkv, 3 * d, T, 3 * d, M->part, npT, grad(M, pb + B_QKVB), s));
+      GemmArgs ga = gargs(M->dqkv, 3 * d, shadow(M, pb + B_QKVW), d, T, d, 3 * d, M->dA, d);
+      TRY(gemm(M, ga, LAY_K, LAY_MN, EPI_F32));
+      TRY(ln_bwd(M, M->dA, M->h_in[l], 1, pb + B_LN1G, A.mean1, A.rstd1, T));
+    }
+  }
+
+  // ---- embeddings (only when nothing is frozen)
+  if (D.k == 0) {
+    if (D.arch == SAT_VIT) {
+      SAT_HIP(launch_sum_rows_batched(M->dh, grad(M, 3), D.B, D.S, d, s));
+      SAT_HIP(hipMemcpyAsync(grad(M, 2), grad(M, 3), (size_t)d * 4, hipMemcpyDeviceToDevice, s));
+      SAT_HIP(launch_vit_patch_grad(M->dh, M->dzpatch, D.B, D.np, d, s));
+      GemmArgs wp = gargs(M->dzpatch, d, M->patches, D.pd, d, D.pd, D.B * D.np, grad(M, 0), D.pd);
+      TRY(gemm(M, wp, LAY_MN, LAY_MN, EPI_F32));
+      int rows = D.B * D.np;
+      SAT_HIP(launch_colsum_bf16(M->dzpatch, d, rows, d, M->part, rows < 256 ? rows : 256,
+                                 grad(M, 1), s));
+    } else {
+      SAT_HIP(launch_embed_bwd((const int32_t*)inputs, M->dh, grad(M, 0), T, d, D.V, M->sortbuf, s));
+      if (D.arch == SAT_GPT2) SAT_HIP(launch_sum_rows_batched(M->dh, grad(M, 1), D.B, D.S, d, s));
+    }
+  }
+  return SAT_OK;
+}
+
+sat_status sat_run_adamw(sat_model* M) {
+  M->t += 1;
+  const sat_config& c = M->cfg;
+  size_t off = M->train_off;
+  long n = (long)(M->n_param_elems - off);
+  Timed tm(M, TK_ADAMW, 30.0 * n);
+  SAT_HIP(launch_adamw(M->master + off, M->grad + off, M->mom + off, M->vel + off,
+                       M->shadow + off, n,
+                       adamw_consts(c.lr, c.beta1, c.beta2, c.eps, c.weight_decay, M->t),
+                       M->stream));
+  return SAT_OK;
+}

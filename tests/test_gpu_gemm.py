@@ -1,0 +1,90 @@
+"""GEMM kernel parity against the float64 matmul of the same bf16 operands,
+over all operand layouts and epilogues, at shapes that span several tiles with
+ragged edges, and the unaligned (scalar-load) path."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import ops as O
+from tests.gpu_util import bf16_round, flush, host, rel, to_dev_bf16, to_dev_f32
+
+pytestmark = pytest.mark.gpu
+
+
+def _operands(rng, M, N, K, a_layout, b_layout):
+    A = bf16_round(rng.normal(size=(M, K)))
+    B = bf16_round(rng.normal(size=(N, K)))
+    Ad = to_dev_bf16(A if a_layout == 0 else A.T.copy())
+    Bd = to_dev_bf16(B if b_layout == 0 else B.T.copy())
+    lda = K if a_layout == 0 else M
+    ldb = K if b_layout == 0 else N
+    return A, B, Ad, Bd, lda, ldb
+
+
+SHAPES = [(64, 64, 64), (300, 200, 136), (513, 257, 520), (256, 128, 64), (8, 8, 8), (1000, 40, 16)]
+
+
+@pytest.mark.parametrize("a_layout,b_layout", [(0, 0), (0, 1), (1, 1), (1, 0)])
+@pytest.mark.parametrize("M,N,K", SHAPES)
+def test_gemm_f32_layouts(a_layout, b_layout, M, N, K):
+    from paper_2309_01226_amd import ops
+    flush(f"gemm f32 lay=({a_layout},{b_layout}) M={M} N={N} K={K}")
+    rng = np.random.default_rng(M * 7 + N * 3 + K)
+    A, B, Ad, Bd, lda, ldb = _operands(rng, M, N, K, a_layout, b_layout)
+    bias = rng.normal(size=N)
+    out = torch.empty(M, N, device="cuda", dtype=torch.float32)
+    ops.gemm(Ad, Bd, M, N, K, out, lda=lda, ldb=ldb, a_layout=a_layout, b_layout=b_layout,
+             bias=to_dev_f32(bias))
+    torch.cuda.synchronize()
+    ref = O.gemm(A, B) + bias
+    assert rel(host(out), ref) < 2e-6
+
+
+@pytest.mark.parametrize("M,N,K", [(300, 200, 100), (77, 45, 588), (129, 65, 37)])
+def test_gemm_unaligned_scalar_path(M, N, K):
+    from paper_2309_01226_amd import ops
+    flush(f"gemm unaligned M={M} N={N} K={K}")
+    rng = np.random.default_rng(5)
+    A, B, Ad, Bd, lda, ldb = _operands(rng, M, N, K, 0, 0)
+    out = torch.empty(M, N, device="cuda", dtype=torch.float32)
+    ops.gemm(Ad, Bd, M, N, K, out, lda=lda, ldb=ldb)
+    torch.cuda.synchronize()
+    assert rel(host(out), O.gemm(A, B)) < 2e-6
+
+
+@pytest.mark.parametrize("erf_form", [0, 1])
+def test_gemm_epilogues(erf_form):
+    from paper_2309_01226_amd import ops
+    M, N, K = 390, 272, 200
+    flush(f"gemm epilogues erf={erf_form}")
+    rng = np.random.default_rng(11)
+    A, B, Ad, Bd, lda, ldb = _operands(rng, M, N, K, 0, 0)
+    C = O.gemm(A, B)
+    bias = rng.normal(size=N - 40)
+    # residual add into fp32, resid aliasing out
+    R = rng.normal(size=(M, N))
+    out = to_dev_f32(R)
+    ops.gemm(Ad, Bd, M, N, K, out, lda=lda, ldb=ldb, epilogue=1, resid=out,
+             bias=to_dev_f32(bias), bias_col0=40)
+    torch.cuda.synchronize()
+    ref = R + C
+    ref[:, 40:] += bias
+    assert rel(host(out), ref) < 2e-6
+    # bf16 store with bias from column 40 and GELU of columns >= 100 into out2
+    o1 = torch.empty(M, N, device="cuda", dtype=torch.bfloat16)
+    o2 = torch.empty(M, N - 100, device="cuda", dtype=torch.bfloat16)
+    ops.gemm(Ad, Bd, M, N, K, o1, lda=lda, ldb=ldb, epilogue=2, bias=to_dev_f32(bias),
+             bias_col0=40, out2=o2, ldo2=N - 100, gelu_col0=100, gelu_erf=erf_form)
+    torch.cuda.synchronize()
+    pre = C.copy()
+    pre[:, 40:] += bias
+    assert rel(host(o1), pre) < 4e-3
+    assert rel(host(o2), O.gelu(pre[:, 100:], erf_form)) < 4e-3
+    # GELU-backward epilogue
+    U = bf16_round(rng.normal(size=(M, N)))
+    o3 = torch.empty(M, N, device="cuda", dtype=torch.bfloat16)
+    ops.gemm(Ad, Bd, M, N, K, o3, lda=lda, ldb=ldb, epilogue=3, aux=to_dev_bf16(U), ldaux=N,
+             gelu_erf=erf_form)
+    torch.cuda.synchronize()
+    assert rel(host(o3), C * O.gelu_grad(U, erf_form)) < 4e-3
