@@ -1,0 +1,257 @@
+#!/usr/bin/env python3
+"""Throughput of one fine-tuning step on one MI355X, as one JSON line.
+
+Default workload: the GPT-J-shaped step (28 layers, d 4096, 16 heads of 256
+with rotary on 64 dims, parallel attention + MLP block, MLP 16384, vocab
+50400, seq 2048, batch 2; bf16 compute, fp32 master weights, AdamW lr 1e-5,
+nothing frozen) on seeded uniform-random tokens that stand in for WikiText-2.
+A step is forward + backward + AdamW over all 6.05 B parameters; inputs are
+resident in HBM before the timed region.
+
+Reported beside the throughput:
+  roofline      the dominant kernel (the fused QKV + fc1 forward GEMM,
+                4096 x 28672 x 4096) timed with HIP events on the model's
+                stream around each of its launches inside the timed region;
+                achieved = algorithmic FLOPs per launch / mean launch time.
+                traffic = HBM bytes per launch from rocprofv3 FETCH_SIZE /
+                WRITE_SIZE counters, read from profiles/ when they were taken
+                on the current GEMM source (else null).
+  cpu_baseline  the float64 oracle timed on this host on a bounded sample
+                (one GPT-J-shaped block plus embedding and head, batch 1, 512
+                tokens; AdamW over that block's tensors), scaled to the full
+                step by algorithmic FLOPs (forward + backward) and by
+                parameter count (AdamW).
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 2.4 GHz x 4096 dense bf16 FLOP/clk/CU (published: 2.5 PF)
+PEAK_HBM_GBS = 8000.0
+METRIC = "training tokens/sec + % bf16 MFMA peak, GPT-J-shaped step, 1 MI355X"
+
+WORKLOADS = {
+    "gptj": "GPT-J-shaped fine-tuning step: 28 layers, d_model 4096, 16 heads (dh 256, rotary 64), "
+            "parallel attn+MLP, MLP 16384, vocab 50400, seq 2048, batch 2, AdamW on all 6.05B params",
+    "gpt2s": "GPT-2-small-shaped fine-tuning step: 12 layers, d_model 768, 12 heads, MLP 3072, "
+             "vocab 50257, seq 1024, batch 8, AdamW on all params",
+    "vith": "ViT-H/14-shaped fine-tuning step: 32 layers, d_model 1280, 16 heads, MLP 5120, "
+            "224x224x3 images, 257 tokens, 1000 classes, batch 64, AdamW on all params",
+    "gpt2m": "GPT-2-medium-shaped fine-tuning step: 24 layers, d_model 1024, 16 heads, MLP 4096, "
+             "vocab 50257, seq 512, batch 8",
+    "tiny": "tiny GPT-2-style decoder: 2 layers, d_model 64, 4 heads, MLP 256, vocab 512, seq 32, batch 2",
+}
+
+
+def step_flops(kw):
+    """Algorithmic FLOPs of one step (same formula as the library's
+    sat_model_stats): 2 FLOPs per multiply-add of every forward product, twice
+    that again for the input- and weight-gradient products of blocks >= k and
+    the head, causal attention counted as half the square."""
+    d, m, L, k = kw["d_model"], kw["d_mlp"], kw["n_layers"], kw.get("frozen_layers", 0)
+    dh = d // kw["n_heads"]
+    if kw["arch"] == "vit":
+        g = kw["img_size"] // kw["patch"]
+        S, npch, pd = g * g + 1, g * g, kw.get("channels", 3) * kw["patch"] ** 2
+    else:
+        S, npch, pd = kw["seq_len"], 0, 0
+    B = kw["batch"]
+    T = B * S
+    gemm = 2.0 * T * (4 * d * d + 2 * d * m)
+    attn = 4.0 * B * kw["n_heads"] * S * S * dh * (1.0 if kw["arch"] == "vit" else 0.5)
+    f = L * (gemm + attn) + (L - k) * 2.0 * (gemm + attn)
+    rows = B if kw["arch"] == "vit" else T
+    f += 3.0 * 2.0 * rows * d * kw["vocab"]
+    if kw["arch"] == "vit":
+        pe = 2.0 * B * npch * pd * d
+        f += pe + (pe if k == 0 else 0.0)
+    return f
+
+
+def n_params(kw):
+    import oracle
+    cfg = oracle.Config(**{k: v for k, v in kw.items() if k in oracle.Config.__dataclass_fields__})
+    return sum(int(__import__("numpy").prod(s)) for _, s, _ in oracle.param_spec(cfg))
+
+
+def cpu_baseline(kw, seed):
+    """Oracle fwd+bwd and AdamW on a bounded sample of the same workload."""
+    import numpy as np
+
+    import oracle
+    from paper_2309_01226_amd.inputs import batch_for
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count()
+    sample = dict(kw, n_layers=1, frozen_layers=0)
+    if kw["arch"] == "vit":
+        sample["batch"] = 4
+    else:
+        sample.update(batch=1, seq_len=min(512, kw["seq_len"]))
+    fields = oracle.Config.__dataclass_fields__
+    cfg = oracle.Config(**{k: v for k, v in sample.items() if k in fields})
+    rng = np.random.default_rng(seed)
+    P = oracle.init_params(cfg, rng)
+    x, y = batch_for(sample, seed=seed, step=0)
+    t0 = time.perf_counter()
+    loss, cache = oracle.forward(cfg, P, x, y)
+    G = oracle.backward(cfg, P, cache)
+    t_fb = time.perf_counter() - t0
+    del cache
+    # AdamW timed on the block's tensors only (bounded work), scaled by count
+    t0 = time.perf_counter()
+    p_s = 0
+    for n in G:
+        if not n.startswith("h0."):
+            continue
+        z = np.zeros_like(P[n])
+        oracle.adamw_update(cfg, P[n], G[n], z, z, 1)
+        p_s += P[n].size
+    t_opt = time.perf_counter() - t0
+    f_s, f_full = step_flops(sample), step_flops(kw)
+    p_full = n_params(kw)
+    est = t_fb * f_full / f_s + t_opt * p_full / p_s
+    rows = kw["batch"] * (kw["seq_len"] if kw["arch"] != "vit" else 1)
+    if kw["arch"] == "vit":
+        rows = kw["batch"] * ((kw["img_size"] // kw["patch"]) ** 2 + 1)
+    srows = sample["batch"] * (sample.get("seq_len", 0) if kw["arch"] != "vit" else
+                               (kw["img_size"] // kw["patch"]) ** 2 + 1)
+    return {
+        "value": rows / est,
+        "unit": "tokens/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"float64 numpy oracle, one block of the same shapes with batch {sample['batch']} x "
+                   f"{srows // sample['batch']} tokens ({srows} tokens) plus the full embedding/head: "
+                   f"fwd+bwd {t_fb:.2f} s scaled by FLOPs x{f_full / f_s:.1f}; AdamW over the block's "
+                   f"{p_s / 1e6:.0f} M params {t_opt:.2f} s scaled by params x{p_full / p_s:.1f}; "
+                   f"estimated full step {est:.1f} s"),
+        "sample_seconds": round(t_fb + t_opt, 2),
+    }
+
+
+def traffic_from_profiles():
+    """HBM bytes per launch of the dominant GEMM from the committed counter
+    summary, if it was taken on the current GEMM source."""
+    path = os.path.join(ROOT, "profiles", "gemm_qkv_fc1_fwd_gptj_counters.json")
+    src = os.path.join(ROOT, "paper_2309_01226_amd", "csrc", "gemm.hip")
+    try:
+        rec = json.load(open(path))
+        cur = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        if rec.get("gemm_source_sha256") != cur:
+            return None
+        return rec.get("hbm_bytes_per_launch")
+    except Exception:
+        return None
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="gptj", choices=sorted(WORKLOADS))
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path; run it with "
+              "--gpus 1 (the default).", file=sys.stderr, flush=True)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2309_01226_amd.configs import preset
+    from paper_2309_01226_amd.model import TIMING, Model, device_batch
+
+    kw = preset(args.config)
+    torch.cuda.set_device(0)
+    m = Model(kw)
+    n_all, n_train, flops = m.stats()
+    assert abs(flops - step_flops(kw)) <= 1e-9 * flops, (flops, step_flops(kw))
+    K, W = args.steps, args.warmup
+    batches = [device_batch(kw, seed=args.seed, step=t) for t in range(W + K)]
+    tokens = m.rows() if kw["arch"] != "vit" else m.rows()
+    for t in range(W):
+        m.train_step(*batches[t], sync=False)
+    torch.cuda.synchronize()
+    per_step = kw["n_layers"]
+    m.set_timing(TIMING["qkv_fwd_gemm"], per_step * K + 8)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(K):
+        m.train_step(*batches[W + t], sync=False)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    q_ms, q_n, q_fl = m.timing_read()
+
+    # diagnostics outside the timed region: one step per kernel class
+    diag = {}
+    for name in ("adamw", "all_gemm", "attn_fwd", "attn_bwd"):
+        m.set_timing(TIMING[name], 4096)
+        m.train_step(*batches[0], sync=False)
+        diag[name] = m.timing_read()
+    m.set_timing(0, 0)
+    loss = m.train_step(*batches[0])
+
+    ms_step = dt / K * 1e3
+    step_tflops = flops / (dt / K) / 1e12
+    adamw_ms = diag["adamw"][0]
+    out = {
+        "metric": METRIC,
+        "value": tokens * K / dt,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": WORKLOADS[args.config], "name": args.config,
+                   "global_batch": kw["batch"], "seq_len": m.rows() // kw["batch"],
+                   "tokens_per_step": tokens, "params": n_all, "trainable_params": n_train,
+                   "frozen_layers": kw.get("frozen_layers", 0)},
+        "step_tflop": flops / 1e12,
+        "achieved_tflops": step_tflops,
+        "mfu_step": step_tflops / PEAK_BF16_TFLOPS,
+        "mfu_fwd_bwd": flops / ((dt / K) - adamw_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+        "adamw": {"ms": adamw_ms, "gbs": diag["adamw"][2] / (adamw_ms * 1e-3) / 1e9 if adamw_ms else None,
+                  "frac_hbm": (diag["adamw"][2] / (adamw_ms * 1e-3) / 1e9 / PEAK_HBM_GBS) if adamw_ms else None},
+        "all_gemm": {"ms": diag["all_gemm"][0], "launches": diag["all_gemm"][1],
+                     "tflops": diag["all_gemm"][2] / (diag["all_gemm"][0] * 1e-3) / 1e12},
+        "attention": {"fwd_ms": diag["attn_fwd"][0], "bwd_ms": diag["attn_bwd"][0],
+                      "fwd_tflops": diag["attn_fwd"][2] / max(diag["attn_fwd"][0], 1e-9) / 1e9,
+                      "bwd_tflops": diag["attn_bwd"][2] / max(diag["attn_bwd"][0], 1e-9) / 1e9},
+        "loss_after": loss,
+    }
+    if q_n:
+        achieved = q_fl / q_n / (q_ms / q_n * 1e-3) / 1e12
+        out["roofline"] = {
+            "kernel": "gemm_kernel<A K-major, B K-major, bf16 epilogue>: fused QKV + fc1 forward "
+                      f"({m.rows()} x {3 * kw['d_model'] + kw['d_mlp'] if kw['arch'] == 'gptj' else 3 * kw['d_model']}"
+                      f" x {kw['d_model']})",
+            "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic_from_profiles(),
+            "launches": q_n, "avg_ms": q_ms / q_n, "flop_per_launch": q_fl / q_n,
+        }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(kw, args.seed)
+    m.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
