@@ -38,14 +38,17 @@ __device__ __forceinline__ double wave_sum_d(double v) {
 }
 
 // GELU, tanh approximation and exact erf form, and their derivatives.
+// tanh(y) is evaluated as 1 - 2 / (exp(2y) + 1), which saturates correctly at
+// both ends (exp overflow gives 1, underflow gives -1).
+__device__ __forceinline__ float tanh_fast(float y) { return 1.f - 2.f / (__expf(2.f * y) + 1.f); }
 __device__ __forceinline__ float gelu_tanh_f(float x) {
   const float c = 0.7978845608028654f, a = 0.044715f;
-  float t = tanhf(c * (x + a * x * x * x));
+  float t = tanh_fast(c * (x + a * x * x * x));
   return 0.5f * x * (1.f + t);
 }
 __device__ __forceinline__ float gelu_tanh_grad_f(float x) {
   const float c = 0.7978845608028654f, a = 0.044715f;
-  float t = tanhf(c * (x + a * x * x * x));
+  float t = tanh_fast(c * (x + a * x * x * x));
   return 0.5f * (1.f + t) + 0.5f * x * (1.f - t * t) * c * (1.f + 3.f * a * x * x);
 }
 __device__ __forceinline__ float gelu_erf_f(float x) {
@@ -61,6 +64,14 @@ __device__ __forceinline__ float gelu_f(float x, int erf_form) {
 }
 __device__ __forceinline__ float gelu_grad_f(float x, int erf_form) {
   return erf_form ? gelu_erf_grad_f(x) : gelu_tanh_grad_f(x);
+}
+template <int ERF>
+__device__ __forceinline__ float gelu_t(float x) {
+  return ERF ? gelu_erf_f(x) : gelu_tanh_f(x);
+}
+template <int ERF>
+__device__ __forceinline__ float gelu_grad_t(float x) {
+  return ERF ? gelu_erf_grad_f(x) : gelu_tanh_grad_f(x);
 }
 
 static inline int sat_cdiv(long a, long b) { return (int)((a + b - 1) / b); }

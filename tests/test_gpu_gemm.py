@@ -88,3 +88,26 @@ def test_gemm_epilogues(erf_form):
              gelu_erf=erf_form)
     torch.cuda.synchronize()
     assert rel(host(o3), C * O.gelu_grad(U, erf_form)) < 4e-3
+
+
+@pytest.mark.parametrize("a_layout,b_layout", [(0, 0), (0, 1), (1, 1), (1, 0)])
+@pytest.mark.parametrize("epi", [0, 2])
+def test_gemm_large_tiles_sampled(a_layout, b_layout, epi):
+    """Shapes large enough for the 256 x 256 tile path (>= 256 tiles), with a
+    ragged M and a K tail; checked on 300 sampled rows against float64."""
+    from paper_2309_01226_amd import ops
+    M, N, K = 4100, 4096, 584
+    flush(f"gemm large lay=({a_layout},{b_layout}) epi={epi}")
+    rng = np.random.default_rng(17 + a_layout + 2 * b_layout)
+    A, B, Ad, Bd, lda, ldb = _operands(rng, M, N, K, a_layout, b_layout)
+    bias = rng.normal(size=N)
+    dt = torch.float32 if epi == 0 else torch.bfloat16
+    out = torch.empty(M, N, device="cuda", dtype=dt)
+    ops.gemm(Ad, Bd, M, N, K, out, lda=lda, ldb=ldb, a_layout=a_layout, b_layout=b_layout,
+             epilogue=epi, bias=to_dev_f32(bias))
+    torch.cuda.synchronize()
+    rows = np.sort(rng.choice(M, size=300, replace=False))
+    rows[-1] = M - 1
+    ref = O.gemm(A[rows], B) + bias
+    got = host(out)[rows]
+    assert rel(got, ref) < (2e-6 if epi == 0 else 4e-3)
