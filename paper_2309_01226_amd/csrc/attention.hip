@@ -229,6 +229,253 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   }
 }
 
+// ================================================================ forward, pipelined
+// For head dims 64, 128 and 256: 64-key blocks in two LDS stages.  K rows go
+// HBM -> LDS with buffer_load ... lds into a swizzled layout (16-byte chunk c
+// of row r at position c ^ swz(r), conflict-free for the 16 lanes a 128-bit
+// read serves); V is loaded one block ahead into registers and stored
+// transposed (V^T, keys contiguous).  The copies of block j + 1 are in flight
+// while block j is computed.
+
+#define LDS_PTR(p) ((void __attribute__((address_space(3)))*)(p))
+constexpr uint32_t OOB = 0x80000000u;
+constexpr int FBKV = 64;  // keys per block
+
+template <int DH>
+struct KTile {  // K block in LDS: FBKV rows of DH bf16
+  static constexpr int CPR = DH / 8;  // 16-byte chunks per row
+  __device__ __forceinline__ static int swz(int row) { return CPR >= 16 ? (row & 15) : ((row >> 1) & 7); }
+  __device__ __forceinline__ static int off(int row, int chunk) {
+    return row * DH + ((chunk ^ swz(row)) << 3);
+  }
+  // DMA of rows [0, FBKV) of the block starting at key kv0 (rows >= nvalid read 0)
+  __device__ __forceinline__ static void copy(__amdgpu_buffer_rsrc_t rs, long ld, int nvalid,
+                                              bf16* __restrict__ S, int wave) {
+    const int lane = threadIdx.x & 63;
+    constexpr int NI = FBKV * CPR / 64 / 4;  // instructions per wave
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int q = (i * 4 + wave) * 64 + lane;
+      const int row = q / CPR, pos = q % CPR;
+      const int c = pos ^ swz(row);
+      const uint32_t o = row < nvalid ? (uint32_t)(((long)row * ld + c * 8) * 2) : OOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, LDS_PTR(S + (i * 4 + wave) * 512), 16, o, 0, 0, 0);
+    }
+  }
+};
+
+template <int DH>
+struct VtTile {  // V^T block in LDS: DH rows (head dims) of FBKV keys
+  static constexpr int KB = FBKV / 8;       // key blocks of 8
+  static constexpr int NB = KB * (DH / 8);  // 8 x 8 blocks
+  static constexpr int NPT = (NB + NT - 1) / NT;
+  __device__ __forceinline__ static int swz(int row) { return (row >> 1) & 7; }
+  __device__ __forceinline__ static int off(int row, int chunk) {
+    return row * FBKV + ((chunk ^ swz(row)) << 3);
+  }
+  __device__ __forceinline__ static int loads(int wave) {
+    int n = 0;
+#pragma unroll
+    for (int j = 0; j < NPT; ++j)
+      if (wave * 64 + j * NT < NB) n += 8;
+    return n;
+  }
+  // 8 keys x 8 dims per block; block b = key block b / (DH/8), dim block b % (DH/8)
+  __device__ __forceinline__ static void load(__amdgpu_buffer_rsrc_t rs, long ld, int nvalid,
+                                              u32x4* regs) {
+#pragma unroll
+    for (int j = 0; j < NPT; ++j) {
+      const int b = threadIdx.x + j * NT;
+      if (b >= NB) break;
+      const int kb = b / (DH / 8), db = b % (DH / 8);
+#pragma unroll
+      for (int kk = 0; kk < 8; ++kk) {
+        const int key = kb * 8 + kk;
+        const uint32_t o = key < nvalid ? (uint32_t)(((long)key * ld + db * 8) * 2) : OOB;
+        regs[8 * j + kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, o, 0, 0));
+      }
+    }
+  }
+  __device__ __forceinline__ static void store(bf16* __restrict__ S, const u32x4* regs) {
+#pragma unroll
+    for (int j = 0; j < NPT; ++j) {
+      const int b = threadIdx.x + j * NT;
+      if (b >= NB) break;
+      const int kb = b / (DH / 8), db = b % (DH / 8);
+      const u32x4* x = regs + 8 * j;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        u32x4 lo, hi;
+#pragma unroll
+        for (int w2 = 0; w2 < 4; ++w2) {
+          uint32_t a0 = x[2 * w2][w], a1 = x[2 * w2 + 1][w];
+          lo[w2] = __builtin_amdgcn_perm(a1, a0, 0x05040100u);
+          hi[w2] = __builtin_amdgcn_perm(a1, a0, 0x07060302u);
+        }
+        *reinterpret_cast<u32x4*>(S + off(db * 8 + 2 * w, kb)) = lo;
+        *reinterpret_cast<u32x4*>(S + off(db * 8 + 2 * w + 1, kb)) = hi;
+      }
+    }
+  }
+};
+
+template <int VM>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4));
+}
+__device__ __forceinline__ void cta_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_sched_barrier(0);
+}
+// wait until at most `n` (0, 8 or 16) vector loads of this wave are in flight
+__device__ __forceinline__ void wait_loads_upto(int n) {
+  if (n >= 16) wait_vm_lgkm0<16>();
+  else if (n >= 8) wait_vm_lgkm0<8>();
+  else wait_vm_lgkm0<0>();
+}
+
+// One forward block: S^T = K Q^T, online softmax, O^T += V^T P^T.  `kt` and
+// `vt` are the resident stage; `nxt` receives the copies of the next block.
+template <int DH>
+__device__ __forceinline__ void fwd_block(const bf16* __restrict__ kt, const bf16* __restrict__ vt,
+                                          bf16* __restrict__ nxt, bool copy_next,
+                                          __amdgpu_buffer_rsrc_t rsK, long ldk, int nvalid_next,
+                                          const bf16x8 (&qf)[DH / 16], floatx16 (&o)[DH / 32],
+                                          float& m, float& l, int kv0, int q, int S, int causal,
+                                          float sc, bool active, int wave, int lane) {
+  if (copy_next) KTile<DH>::copy(rsK, ldk, nvalid_next, nxt, wave);
+  if (!active) return;
+  const int g = lane >> 5;
+  floatx16 s[FBKV / 32];
+#pragma unroll
+  for (int t = 0; t < FBKV / 32; ++t) {
+    s[t] = zero16();
+    const int row = t * 32 + (lane & 31);
+#pragma unroll
+    for (int c = 0; c < DH / 16; ++c)
+      s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+          *reinterpret_cast<const bf16x8*>(kt + KTile<DH>::off(row, 2 * c + g)), qf[c], s[t], 0, 0, 0);
+  }
+  float mloc = -INFINITY;
+#pragma unroll
+  for (int t = 0; t < FBKV / 32; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int key = kv0 + t * 32 + acc_row(r, g);
+      float x = s[t][r] * sc;
+      if (key >= S || (causal && key > q)) x = -INFINITY;
+      s[t][r] = x;
+      mloc = fmaxf(mloc, x);
+    }
+  mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+  const float mnew = fmaxf(m, mloc);
+  const float alpha = (mnew == -INFINITY) ? 1.f : exp2f(m - mnew);
+  float lsum = 0.f;
+#pragma unroll
+  for (int t = 0; t < FBKV / 32; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float pr = (mnew == -INFINITY) ? 0.f : exp2f(s[t][r] - mnew);
+      s[t][r] = pr;
+      lsum += pr;
+    }
+  lsum += __shfl_xor(lsum, 32, 64);
+  l = l * alpha + lsum;
+  m = mnew;
+#pragma unroll
+  for (int ot = 0; ot < DH / 32; ++ot)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[ot][r] *= alpha;
+#pragma unroll
+  for (int t = 0; t < FBKV / 32; ++t)
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const bf16x8 pb = acc_to_bf16(s[t], hh);
+      const int c0 = (t * 32 + hh * 16) / 8;  // first 8-key chunk of this 16-key step
+#pragma unroll
+      for (int ot = 0; ot < DH / 32; ++ot) {
+        const int row = ot * 32 + (lane & 31);
+        const bf16x4 a0 = *reinterpret_cast<const bf16x4*>(vt + VtTile<DH>::off(row, c0) + 4 * g);
+        const bf16x4 a1 = *reinterpret_cast<const bf16x4*>(vt + VtTile<DH>::off(row, c0 + 1) + 4 * g);
+        bf16x8 av;
+        av[0] = a0[0]; av[1] = a0[1]; av[2] = a0[2]; av[3] = a0[3];
+        av[4] = a1[0]; av[5] = a1[1]; av[6] = a1[2]; av[7] = a1[3];
+        o[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb, o[ot], 0, 0, 0);
+      }
+    }
+}
+
+template <int DH>
+__global__ __launch_bounds__(NT) void attn_fwd_fast(AttnArgs a) {
+  constexpr int KSZ = FBKV * DH, VSZ = DH * FBKV, STG = KSZ + VSZ;
+  __shared__ __attribute__((aligned(1024))) bf16 smem[2 * STG];
+  const int S = a.S;
+  const int nqb = (S + WG_ROWS - 1) / WG_ROWS;
+  const int qb = block_index(nqb, a.causal);
+  const int bh = blockIdx.y, b = bh / a.H, h = bh % a.H;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane >> 5;
+  const int q0 = qb * WG_ROWS;
+  const int q = q0 + wave * WROWS + (lane & 31);
+  const bf16* Qb = a.q + (long)b * S * a.ldq + (long)h * DH;
+  const bf16* Kb = a.k + (long)b * S * a.ldk + (long)h * DH;
+  const bf16* Vb = a.v + (long)b * S * a.ldv + (long)h * DH;
+
+  bf16x8 qf[DH / 16];
+  load_row_operand<DH>(Qb, a.ldq, q, S, g, qf);
+  floatx16 o[DH / 32];
+#pragma unroll
+  for (int t = 0; t < DH / 32; ++t) o[t] = zero16();
+  float m = -INFINITY, l = 0.f;
+  const float sc = a.scale * LOG2E;
+  const int wave_qmax = q0 + wave * WROWS + WROWS - 1;
+  const int kv_end = a.causal ? min(S, q0 + WG_ROWS) : S;
+  const int nblk = (kv_end + FBKV - 1) / FBKV;
+  const int nvl = VtTile<DH>::loads(wave);
+  auto rsrc = [&](const bf16* base, int kv0, long ld) {
+    return __builtin_amdgcn_make_buffer_rsrc((void*)(base + (long)kv0 * ld), (short)0, 0x7FFFFFFF,
+                                             0x00020000);
+  };
+
+  // prologue: block 0 resident in stage 0, V of block 1 requested
+  u32x4 vr[8 * VtTile<DH>::NPT];
+  KTile<DH>::copy(rsrc(Kb, 0, a.ldk), a.ldk, S, smem, wave);
+  VtTile<DH>::load(rsrc(Vb, 0, a.ldv), a.ldv, S, vr);
+  VtTile<DH>::store(smem + KSZ, vr);
+  if (nblk > 1) VtTile<DH>::load(rsrc(Vb, FBKV, a.ldv), a.ldv, S - FBKV, vr);
+  wait_loads_upto(nblk > 1 ? nvl : 0);
+  cta_barrier();
+
+  for (int j = 0; j < nblk; ++j) {
+    const int kv0 = j * FBKV;
+    bf16* cur = smem + (j & 1) * STG;
+    bf16* nxt = smem + ((j + 1) & 1) * STG;
+    const bool next = j + 1 < nblk;
+    fwd_block<DH>(cur, cur + KSZ, nxt, next, rsrc(Kb, kv0 + FBKV, a.ldk), a.ldk, S - kv0 - FBKV,
+                  qf, o, m, l, kv0, q, S, a.causal, sc, !(a.causal && kv0 > wave_qmax), wave, lane);
+    if (next) {
+      VtTile<DH>::store(nxt + KSZ, vr);
+      if (j + 2 < nblk) VtTile<DH>::load(rsrc(Vb, kv0 + 2 * FBKV, a.ldv), a.ldv, S - kv0 - 2 * FBKV, vr);
+      wait_loads_upto(j + 2 < nblk ? nvl : 0);
+      cta_barrier();
+    }
+  }
+  if (q < S) {
+    const float inv = (l > 0.f) ? 1.f / l : 0.f;
+    bf16* Ob = a.o + ((long)b * S + q) * a.ldo + (long)h * DH;
+#pragma unroll
+    for (int ot = 0; ot < DH / 32; ++ot)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) Ob[ot * 32 + acc_row(r, g)] = f2bf(o[ot][r] * inv);
+    if (g == 0) a.lse[((long)b * a.H + h) * S + q] = (m + log2f(l)) * LN2;
+  }
+}
+
 // ================================================================ backward
 // delta[b, h, s] = sum_j dO[s, j] * O[s, j]; one wave per (b, s, h).
 __global__ __launch_bounds__(256) void attn_delta_kernel(AttnBwdArgs a) {
@@ -446,7 +693,11 @@ struct AttnCfg {
 template <int DH>
 hipError_t fwd_launch(const AttnArgs& a, hipStream_t s) {
   dim3 grid((a.S + WG_ROWS - 1) / WG_ROWS, a.B * a.H);
-  hipLaunchKernelGGL((attn_fwd_kernel<DH, AttnCfg<DH>::BKV>), grid, dim3(NT), 0, s, a);
+  if (DH == 64 || DH == 128 || DH == 256)
+    hipLaunchKernelGGL((attn_fwd_fast<(DH == 64 || DH == 128 || DH == 256) ? DH : 64>), grid,
+                       dim3(NT), 0, s, a);
+  else
+    hipLaunchKernelGGL((attn_fwd_kernel<DH, AttnCfg<DH>::BKV>), grid, dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 
