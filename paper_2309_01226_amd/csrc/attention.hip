@@ -241,6 +241,70 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
 constexpr uint32_t OOB = 0x80000000u;
 constexpr int FBKV = 64;  // keys per block
 
+template <int ROWS, int DH>
+struct RowTile {  // ROWS rows of DH bf16 in LDS, swizzled 16-byte chunks, filled by DMA
+  static constexpr int CPR = DH / 8;
+  __device__ __forceinline__ static int swz(int row) { return CPR >= 16 ? (row & 15) : ((row >> 1) & 7); }
+  __device__ __forceinline__ static int off(int row, int chunk) {
+    return row * DH + ((chunk ^ swz(row)) << 3);
+  }
+  static constexpr int NI = ROWS * CPR / 64 / 4;  // DMA instructions per wave
+  static_assert(ROWS * CPR % 256 == 0, "tile must be a whole number of 1 KB wave copies");
+  __device__ __forceinline__ static void copy(__amdgpu_buffer_rsrc_t rs, long ld, int nvalid,
+                                              bf16* __restrict__ S, int wave) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int q = (i * 4 + wave) * 64 + lane;
+      const int row = q / CPR, pos = q % CPR;
+      const int c = pos ^ swz(row);
+      const uint32_t o = row < nvalid ? (uint32_t)(((long)row * ld + c * 8) * 2) : OOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, LDS_PTR(S + (i * 4 + wave) * 512), 16, o, 0, 0, 0);
+    }
+  }
+};
+
+// Transposed tile: DH rows (head dims) x ROWS columns (keys or queries) in
+// LDS, pitch ROWS + 4 (for 32 columns: 72-byte rows, so the 8-byte operand
+// reads of 32 consecutive rows hit distinct banks).  Built from ROWS x DH
+// row-major data in 4 x 8 pieces: a thread loads 4 rows x 8 columns (four
+// 16-byte loads) and writes 8 transposed rows of 4 values.
+template <int ROWS, int DH>
+struct TransTile {
+  static constexpr int PITCH = ROWS + 4;
+  static constexpr int SIZE = DH * PITCH;
+  static constexpr int NP = (ROWS / 4) * (DH / 8);  // pieces
+  __device__ __forceinline__ static void load(__amdgpu_buffer_rsrc_t rs, long ld, int nvalid, int p,
+                                              u32x4* regs) {
+    const int rq = p / (DH / 8), db = p % (DH / 8);
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const int r = rq * 4 + kk;
+      const uint32_t o = r < nvalid ? (uint32_t)(((long)r * ld + db * 8) * 2) : OOB;
+      regs[kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, o, 0, 0));
+    }
+  }
+  __device__ __forceinline__ static void store(bf16* __restrict__ S, int p, const u32x4* x) {
+    const int rq = p / (DH / 8), db = p % (DH / 8);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      u32x2 lo, hi;
+#pragma unroll
+      for (int w2 = 0; w2 < 2; ++w2) {
+        const uint32_t a0 = x[2 * w2][w], a1 = x[2 * w2 + 1][w];
+        lo[w2] = __builtin_amdgcn_perm(a1, a0, 0x05040100u);
+        hi[w2] = __builtin_amdgcn_perm(a1, a0, 0x07060302u);
+      }
+      *reinterpret_cast<u32x2*>(S + (db * 8 + 2 * w) * PITCH + rq * 4) = lo;
+      *reinterpret_cast<u32x2*>(S + (db * 8 + 2 * w + 1) * PITCH + rq * 4) = hi;
+    }
+  }
+  // MFMA operand of row `row` in the accumulator permutation (lds8_perm)
+  __device__ __forceinline__ static bf16x8 read_perm(const bf16* __restrict__ S, int row, int base, int g) {
+    return lds8_perm(S + row * PITCH, base, g);
+  }
+};
+
 template <int DH>
 struct KTile {  // K block in LDS: FBKV rows of DH bf16
   static constexpr int CPR = DH / 8;  // 16-byte chunks per row
@@ -331,10 +395,17 @@ __device__ __forceinline__ void cta_barrier() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
   __builtin_amdgcn_sched_barrier(0);
 }
-// wait until at most `n` (0, 8 or 16) vector loads of this wave are in flight
+// Wait until at most n' vector loads of this wave are in flight (and all LDS
+// operations are done), n' the largest of {0, 2, 4, 6, 8, 10, 12, 16} not
+// above `n` (wave-uniform).
 __device__ __forceinline__ void wait_loads_upto(int n) {
   if (n >= 16) wait_vm_lgkm0<16>();
+  else if (n >= 12) wait_vm_lgkm0<12>();
+  else if (n >= 10) wait_vm_lgkm0<10>();
   else if (n >= 8) wait_vm_lgkm0<8>();
+  else if (n >= 6) wait_vm_lgkm0<6>();
+  else if (n >= 4) wait_vm_lgkm0<4>();
+  else if (n >= 2) wait_vm_lgkm0<2>();
   else wait_vm_lgkm0<0>();
 }
 
@@ -682,6 +753,447 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnBwdArgs a) {
   }
 }
 
+// ================================================================ backward, pipelined
+// Both kernels loop over 32-row blocks of the other operand in two LDS
+// stages: the rows arrive by direct HBM-to-LDS copies issued at the start of
+// the previous block, the transposed tiles through registers loaded two
+// blocks ahead; one barrier per block.
+constexpr int BQB = 32;  // query rows per block (dK/dV kernels)
+constexpr int BKB = 32;  // key rows per block (dQ kernel)
+
+__device__ __forceinline__ void wait_lgkm0() {
+  __builtin_amdgcn_s_waitcnt(0xF | (3 << 14) | (7 << 4));  // lgkmcnt(0), vmcnt and expcnt untouched
+}
+
+// dK/dV stage: Q rows, dO rows, Q^T, dO^T, lse * log2(e) and delta of 32 queries.
+template <int DH>
+struct KVStage {
+  using RT = RowTile<BQB, DH>;
+  using TT = TransTile<BQB, DH>;
+  static constexpr int RQ = BQB * DH;
+  static constexpr int SIZE = 2 * RQ + 2 * TT::SIZE + 2 * 2 * BQB;  // in bf16 units
+  __device__ __forceinline__ static const bf16* rows(const bf16* st, int which) { return st + which * RQ; }
+  __device__ __forceinline__ static const bf16* trans(const bf16* st, int which) {
+    return st + 2 * RQ + which * TT::SIZE;
+  }
+  __device__ __forceinline__ static const float* lse(const bf16* st) {
+    return reinterpret_cast<const float*>(st + 2 * RQ + 2 * TT::SIZE);
+  }
+};
+
+// Register-staged half of a stage: the transposed pieces a thread loads for
+// block q0 (Q^T pieces first, then dO^T), plus lse and delta on 32 threads.
+template <int DH, int NTH>
+struct KVTrans {
+  using S = KVStage<DH>;
+  using TT = typename S::TT;
+  static constexpr int PER = (2 * TT::NP + NTH - 1) / NTH;
+  u32x4 r[4 * PER];
+  float lse = 0.f, dlt = 0.f;
+  __device__ __forceinline__ static int loads(int wave) {  // vector loads per wave and call
+    int n = 0;
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+      if (wave * 64 + j * NTH < 2 * TT::NP) n += 4;
+    return wave == 0 ? n + 2 : n;
+  }
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rsQ, __amdgpu_buffer_rsrc_t rsO, long ldq,
+                                       long ldo, int nvalid, const float* lse_g, const float* dlt_g) {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int p = tid + j * NTH;
+      if (p < TT::NP) TT::load(rsQ, ldq, nvalid, p, r + 4 * j);
+      else if (p < 2 * TT::NP) TT::load(rsO, ldo, nvalid, p - TT::NP, r + 4 * j);
+    }
+    if (tid < BQB) {
+      lse = tid < nvalid ? lse_g[tid] * LOG2E : 0.f;
+      dlt = tid < nvalid ? dlt_g[tid] : 0.f;
+    }
+  }
+  __device__ __forceinline__ void store(bf16* __restrict__ st) const {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int p = tid + j * NTH;
+      if (p < TT::NP) TT::store(st + 2 * S::RQ, p, r + 4 * j);
+      else if (p < 2 * TT::NP) TT::store(st + 2 * S::RQ + TT::SIZE, p - TT::NP, r + 4 * j);
+    }
+    if (tid < BQB) {
+      float* f = reinterpret_cast<float*>(st + 2 * S::RQ + 2 * TT::SIZE);
+      f[tid] = lse;
+      f[BQB + tid] = dlt;
+    }
+  }
+};
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const bf16* base, int r0, long ld) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)(base + (long)r0 * ld), (short)0, 0x7FFFFFFF, 0x00020000);
+}
+
+// One query block of the dK/dV kernel for a wave owning 32 keys (full head
+// dim): S = Q K^T and dP = dO V^T, P = exp(S - lse), dS = P (dP - delta),
+// dV^T += dO^T P, dK^T += Q^T dS.
+template <int DH>
+__device__ __forceinline__ void kv_block(const bf16* __restrict__ cur, bf16* __restrict__ nxt, bool copy_next,
+                                         __amdgpu_buffer_rsrc_t rsQ, __amdgpu_buffer_rsrc_t rsO, long ldq,
+                                         long ldo, int nvalid_next, const bf16x8 (&kf)[DH / 16],
+                                         const bf16x8 (&vf)[DH / 16], floatx16 (&dk)[DH / 32],
+                                         floatx16 (&dv)[DH / 32], int qs0, int key, int S, int causal,
+                                         float sc, bool active, int wave, int lane) {
+  using SG = KVStage<DH>;
+  using TT = typename SG::TT;
+  using RT = typename SG::RT;
+  if (copy_next) {
+    RT::copy(rsQ, ldq, nvalid_next, nxt, wave);
+    RT::copy(rsO, ldo, nvalid_next, nxt + SG::RQ, wave);
+  }
+  if (!active) return;
+  const int g = lane >> 5, row = lane & 31;
+  const bf16* Qs = SG::rows(cur, 0);
+  const bf16* dOs = SG::rows(cur, 1);
+  const float* ls = SG::lse(cur);
+  floatx16 sv = zero16(), dp = zero16();
+#pragma unroll
+  for (int c = 0; c < DH / 16; ++c) {
+    sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(Qs + RT::off(row, 2 * c + g)),
+                                                 kf[c], sv, 0, 0, 0);
+    dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(dOs + RT::off(row, 2 * c + g)),
+                                                 vf[c], dp, 0, 0, 0);
+  }
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int qi = acc_row(r, g);
+    const int qq = qs0 + qi;
+    const bool ok = qq < S && key < S && !(causal && key > qq);
+    const float pr = ok ? exp2f(sv[r] * sc - ls[qi]) : 0.f;
+    sv[r] = pr;
+    dp[r] = pr * (dp[r] - ls[BQB + qi]);
+  }
+  const bf16* QT = SG::trans(cur, 0);
+  const bf16* dOT = SG::trans(cur, 1);
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const bf16x8 pb = acc_to_bf16(sv, hh);
+    const bf16x8 db = acc_to_bf16(dp, hh);
+#pragma unroll
+    for (int ot = 0; ot < DH / 32; ++ot) {
+      const int tr = ot * 32 + row;
+      dv[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(TT::read_perm(dOT, tr, hh * 16, g), pb, dv[ot], 0, 0, 0);
+      dk[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(TT::read_perm(QT, tr, hh * 16, g), db, dk[ot], 0, 0, 0);
+    }
+  }
+}
+
+// Paired variant for large head dims: the two waves of a pair own the same
+// 32 keys; role 0 holds K, forms P and accumulates dV^T, role 1 holds V,
+// forms dP, takes P from its partner through LDS and accumulates dK^T.  Each
+// wave then needs one row operand and one accumulator set, and no product is
+// computed twice.
+template <int DH>
+__device__ __forceinline__ void kv_pair_block(const bf16* __restrict__ cur, bf16* __restrict__ nxt,
+                                              float* __restrict__ xw, bool copy_next,
+                                              __amdgpu_buffer_rsrc_t rsQ, __amdgpu_buffer_rsrc_t rsO,
+                                              long ldq, long ldo, int nvalid_next,
+                                              const bf16x8 (&rf)[DH / 16], floatx16 (&acc)[DH / 32],
+                                              int qs0, int key, int S, int causal, float sc, bool active,
+                                              int role, int wave, int lane) {
+  using SG = KVStage<DH>;
+  using TT = typename SG::TT;
+  using RT = typename SG::RT;
+  if (copy_next) {
+    RT::copy(rsQ, ldq, nvalid_next, nxt, wave);
+    RT::copy(rsO, ldo, nvalid_next, nxt + SG::RQ, wave);
+  }
+  const int g = lane >> 5, row = lane & 31;
+  const float* ls = SG::lse(cur);
+  floatx16 x = zero16();
+  if (active) {
+    const bf16* rs = SG::rows(cur, role);  // Q rows (role 0) or dO rows (role 1)
+#pragma unroll
+    for (int c = 0; c < DH / 16; ++c)
+      x = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(rs + RT::off(row, 2 * c + g)),
+                                                  rf[c], x, 0, 0, 0);
+    if (role == 0) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int qi = acc_row(r, g);
+        const int qq = qs0 + qi;
+        const bool ok = qq < S && key < S && !(causal && key > qq);
+        const float pr = ok ? exp2f(x[r] * sc - ls[qi]) : 0.f;
+        x[r] = pr;
+        xw[r * 64 + lane] = pr;
+      }
+    }
+  }
+  wait_lgkm0();
+  cta_barrier();
+  if (!active) return;
+  if (role == 1) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) x[r] = xw[r * 64 + lane] * (x[r] - ls[BQB + acc_row(r, g)]);
+  }
+  const bf16* T = SG::trans(cur, 1 - role);  // dO^T (role 0) or Q^T (role 1)
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const bf16x8 xb = acc_to_bf16(x, hh);
+#pragma unroll
+    for (int ot = 0; ot < DH / 32; ++ot)
+      acc[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(TT::read_perm(T, ot * 32 + row, hh * 16, g), xb, acc[ot],
+                                                        0, 0, 0);
+  }
+}
+
+template <int DH, bool PAIR>
+__global__ __launch_bounds__(NT) void attn_bwd_dkdv_fast(AttnBwdArgs a) {
+  using SG = KVStage<DH>;
+  using RT = typename SG::RT;
+  using TR = KVTrans<DH, NT>;
+  constexpr int KPW = PAIR ? WG_ROWS / 2 : WG_ROWS;  // keys per workgroup
+  constexpr int XB = PAIR ? 2 * 16 * 64 * 2 : 0;     // P exchange (fp32) of two pairs, bf16 units
+  __shared__ __attribute__((aligned(1024))) bf16 smem[2 * SG::SIZE + XB];
+  const int S = a.f.S;
+  const int bh = blockIdx.y, b = bh / a.f.H, h = bh % a.f.H;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane >> 5;
+  const int grp = PAIR ? (wave >> 1) : wave, role = PAIR ? (wave & 1) : 0;
+  const int k0 = blockIdx.x * KPW;
+  const int kmin = k0 + grp * WROWS;
+  const int key = kmin + (lane & 31);
+  const long hs = ((long)b * a.f.H + h) * S;
+  const bf16* Qb = a.f.q + (long)b * S * a.f.ldq + (long)h * DH;
+  const bf16* Kb = a.f.k + (long)b * S * a.f.ldk + (long)h * DH;
+  const bf16* Vb = a.f.v + (long)b * S * a.f.ldv + (long)h * DH;
+  const bf16* dOb = a.dout + (long)b * S * a.lddo + (long)h * DH;
+  const float* lse_g = a.f.lse + hs;
+  const float* dlt_g = a.delta + hs;
+
+  constexpr int NACC = PAIR ? 1 : 2;
+  bf16x8 rf[NACC][DH / 16];
+  floatx16 acc[NACC][DH / 32];
+  if (PAIR) {
+    load_row_operand<DH>(role ? Vb : Kb, role ? a.f.ldv : a.f.ldk, key, S, g, rf[0]);
+  } else {
+    load_row_operand<DH>(Kb, a.f.ldk, key, S, g, rf[0]);
+    load_row_operand<DH>(Vb, a.f.ldv, key, S, g, rf[NACC - 1]);
+  }
+#pragma unroll
+  for (int i = 0; i < NACC; ++i)
+#pragma unroll
+    for (int t = 0; t < DH / 32; ++t) acc[i][t] = zero16();
+  const float sc = a.f.scale * LOG2E;
+  const int q_start = a.f.causal ? k0 : 0;
+  const int nqb = (S - q_start + BQB - 1) / BQB;
+  const int nld = TR::loads(wave);
+  TR tr;
+
+  // prologue: block 0 resident in stage 0, transposes of block 1 in registers
+  RT::copy(rows_rsrc(Qb, q_start, a.f.ldq), a.f.ldq, S - q_start, smem, wave);
+  RT::copy(rows_rsrc(dOb, q_start, a.lddo), a.lddo, S - q_start, smem + SG::RQ, wave);
+  tr.load(rows_rsrc(Qb, q_start, a.f.ldq), rows_rsrc(dOb, q_start, a.lddo), a.f.ldq, a.lddo, S - q_start,
+          lse_g + q_start, dlt_g + q_start);
+  wait_vm_lgkm0<0>();
+  tr.store(smem);
+  if (nqb > 1)
+    tr.load(rows_rsrc(Qb, q_start + BQB, a.f.ldq), rows_rsrc(dOb, q_start + BQB, a.lddo), a.f.ldq, a.lddo,
+            S - q_start - BQB, lse_g + q_start + BQB, dlt_g + q_start + BQB);
+  wait_loads_upto(nqb > 1 ? nld : 0);
+  cta_barrier();
+
+  for (int j = 0; j < nqb; ++j) {
+    const int qs0 = q_start + j * BQB;
+    bf16* cur = smem + (j & 1) * SG::SIZE;
+    bf16* nxt = smem + ((j + 1) & 1) * SG::SIZE;
+    const bool next = j + 1 < nqb;
+    const bool active = !(a.f.causal && qs0 + BQB - 1 < kmin);
+    const auto rq = rows_rsrc(Qb, qs0 + BQB, a.f.ldq);
+    const auto ro = rows_rsrc(dOb, qs0 + BQB, a.lddo);
+    if constexpr (PAIR)
+      kv_pair_block<DH>(cur, nxt, reinterpret_cast<float*>(smem + 2 * SG::SIZE) + grp * 16 * 64, next, rq, ro,
+                        a.f.ldq, a.lddo, S - qs0 - BQB, rf[0], acc[0], qs0, key, S, a.f.causal, sc, active,
+                        role, wave, lane);
+    else
+      kv_block<DH>(cur, nxt, next, rq, ro, a.f.ldq, a.lddo, S - qs0 - BQB, rf[0], rf[NACC - 1], acc[0],
+                   acc[NACC - 1], qs0, key, S, a.f.causal, sc, active, wave, lane);
+    if (next) {
+      tr.store(nxt);
+      if (j + 2 < nqb)
+        tr.load(rows_rsrc(Qb, qs0 + 2 * BQB, a.f.ldq), rows_rsrc(dOb, qs0 + 2 * BQB, a.lddo), a.f.ldq, a.lddo,
+                S - qs0 - 2 * BQB, lse_g + qs0 + 2 * BQB, dlt_g + qs0 + 2 * BQB);
+      wait_loads_upto(j + 2 < nqb ? nld : 0);
+      cta_barrier();
+    }
+  }
+  if (key < S) {
+    bf16* ok_ = a.dk + ((long)b * S + key) * a.lddk + (long)h * DH;
+    bf16* ov = a.dv + ((long)b * S + key) * a.lddv + (long)h * DH;
+    // PAIR: role 0 holds dV^T, role 1 dK^T; otherwise acc[0] = dK^T, acc[1] = dV^T
+#pragma unroll
+    for (int i = 0; i < NACC; ++i) {
+      const bool is_k = PAIR ? role == 1 : i == 0;
+      bf16* o = is_k ? ok_ : ov;
+      const float f = is_k ? a.f.scale : 1.f;
+#pragma unroll
+      for (int ot = 0; ot < DH / 32; ++ot)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[ot * 32 + acc_row(r, g)] = f2bf(acc[i][ot][r] * f);
+    }
+  }
+}
+
+// dQ stage: K rows, V rows, K^T of 32 keys.
+template <int DH>
+struct QStage {
+  using RT = RowTile<BKB, DH>;
+  using TT = TransTile<BKB, DH>;
+  static constexpr int RK = BKB * DH;
+  static constexpr int SIZE = 2 * RK + TT::SIZE;
+};
+
+template <int DH, int NTH>
+struct QTrans {
+  using TT = TransTile<BKB, DH>;
+  static constexpr int PER = (TT::NP + NTH - 1) / NTH;
+  u32x4 r[4 * PER];
+  __device__ __forceinline__ static int loads(int wave) {
+    int n = 0;
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+      if (wave * 64 + j * NTH < TT::NP) n += 4;
+    return n;
+  }
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rsK, long ldk, int nvalid) {
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int p = threadIdx.x + j * NTH;
+      if (p < TT::NP) TT::load(rsK, ldk, nvalid, p, r + 4 * j);
+    }
+  }
+  __device__ __forceinline__ void store(bf16* __restrict__ st) const {
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int p = threadIdx.x + j * NTH;
+      if (p < TT::NP) TT::store(st + 2 * QStage<DH>::RK, p, r + 4 * j);
+    }
+  }
+};
+
+// One key block of the dQ kernel: S^T = K Q^T, dP^T = V dO^T,
+// dS^T = P^T (dP^T - delta), dQ^T += K^T dS^T.
+template <int DH>
+__device__ __forceinline__ void q_block(const bf16* __restrict__ cur, bf16* __restrict__ nxt, bool copy_next,
+                                        __amdgpu_buffer_rsrc_t rsK, __amdgpu_buffer_rsrc_t rsV, long ldk,
+                                        long ldv, int nvalid_next, const bf16x8 (&qf)[DH / 16],
+                                        const bf16x8 (&df)[DH / 16], floatx16 (&dq)[DH / 32], int kv0, int q,
+                                        int S, int causal, float sc, float lse2, float dlt, bool active,
+                                        int wave, int lane) {
+  using SG = QStage<DH>;
+  using TT = typename SG::TT;
+  using RT = typename SG::RT;
+  if (copy_next) {
+    RT::copy(rsK, ldk, nvalid_next, nxt, wave);
+    RT::copy(rsV, ldv, nvalid_next, nxt + SG::RK, wave);
+  }
+  if (!active) return;
+  const int g = lane >> 5, row = lane & 31;
+  const bf16* Ks = cur;
+  const bf16* Vs = cur + SG::RK;
+  floatx16 sv = zero16(), dp = zero16();
+#pragma unroll
+  for (int c = 0; c < DH / 16; ++c) {
+    sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(Ks + RT::off(row, 2 * c + g)),
+                                                 qf[c], sv, 0, 0, 0);
+    dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(Vs + RT::off(row, 2 * c + g)),
+                                                 df[c], dp, 0, 0, 0);
+  }
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int kk = kv0 + acc_row(r, g);
+    const bool ok = kk < S && q < S && !(causal && kk > q);
+    const float pr = ok ? exp2f(sv[r] * sc - lse2) : 0.f;
+    sv[r] = pr * (dp[r] - dlt);
+  }
+  const bf16* KT = cur + 2 * SG::RK;
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const bf16x8 db = acc_to_bf16(sv, hh);
+#pragma unroll
+    for (int ot = 0; ot < DH / 32; ++ot)
+      dq[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(TT::read_perm(KT, ot * 32 + row, hh * 16, g), db, dq[ot], 0,
+                                                       0, 0);
+  }
+}
+
+template <int DH>
+__global__ __launch_bounds__(NT) void attn_bwd_dq_fast(AttnBwdArgs a) {
+  using SG = QStage<DH>;
+  using RT = typename SG::RT;
+  using TR = QTrans<DH, NT>;
+  __shared__ __attribute__((aligned(1024))) bf16 smem[2 * SG::SIZE];
+  const int S = a.f.S;
+  const int nqb = (S + WG_ROWS - 1) / WG_ROWS;
+  const int qb = block_index(nqb, a.f.causal);
+  const int bh = blockIdx.y, b = bh / a.f.H, h = bh % a.f.H;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane >> 5;
+  const int q0 = qb * WG_ROWS;
+  const int q = q0 + wave * WROWS + (lane & 31);
+  const long hs = ((long)b * a.f.H + h) * S;
+  const bf16* Qb = a.f.q + (long)b * S * a.f.ldq + (long)h * DH;
+  const bf16* Kb = a.f.k + (long)b * S * a.f.ldk + (long)h * DH;
+  const bf16* Vb = a.f.v + (long)b * S * a.f.ldv + (long)h * DH;
+  const bf16* dOb = a.dout + (long)b * S * a.lddo + (long)h * DH;
+
+  bf16x8 qf[DH / 16], df[DH / 16];
+  load_row_operand<DH>(Qb, a.f.ldq, q, S, g, qf);
+  load_row_operand<DH>(dOb, a.lddo, q, S, g, df);
+  const float sc = a.f.scale * LOG2E;
+  const float lse2 = (q < S) ? a.f.lse[hs + q] * LOG2E : 0.f;
+  const float dlt = (q < S) ? a.delta[hs + q] : 0.f;
+  floatx16 dq[DH / 32];
+#pragma unroll
+  for (int t = 0; t < DH / 32; ++t) dq[t] = zero16();
+  const int wave_qmax = q0 + wave * WROWS + WROWS - 1;
+  const int kv_end = a.f.causal ? min(S, q0 + WG_ROWS) : S;
+  const int nkb = (kv_end + BKB - 1) / BKB;
+  const int nld = TR::loads(wave);
+  TR tr;
+
+  RT::copy(rows_rsrc(Kb, 0, a.f.ldk), a.f.ldk, S, smem, wave);
+  RT::copy(rows_rsrc(Vb, 0, a.f.ldv), a.f.ldv, S, smem + SG::RK, wave);
+  tr.load(rows_rsrc(Kb, 0, a.f.ldk), a.f.ldk, S);
+  wait_vm_lgkm0<0>();
+  tr.store(smem);
+  if (nkb > 1) tr.load(rows_rsrc(Kb, BKB, a.f.ldk), a.f.ldk, S - BKB);
+  wait_loads_upto(nkb > 1 ? nld : 0);
+  cta_barrier();
+
+  for (int j = 0; j < nkb; ++j) {
+    const int kv0 = j * BKB;
+    bf16* cur = smem + (j & 1) * SG::SIZE;
+    bf16* nxt = smem + ((j + 1) & 1) * SG::SIZE;
+    const bool next = j + 1 < nkb;
+    q_block<DH>(cur, nxt, next, rows_rsrc(Kb, kv0 + BKB, a.f.ldk), rows_rsrc(Vb, kv0 + BKB, a.f.ldv), a.f.ldk,
+                a.f.ldv, S - kv0 - BKB, qf, df, dq, kv0, q, S, a.f.causal, sc, lse2, dlt,
+                !(a.f.causal && kv0 > wave_qmax), wave, lane);
+    if (next) {
+      tr.store(nxt);
+      if (j + 2 < nkb) tr.load(rows_rsrc(Kb, kv0 + 2 * BKB, a.f.ldk), a.f.ldk, S - kv0 - 2 * BKB);
+      wait_loads_upto(j + 2 < nkb ? nld : 0);
+      cta_barrier();
+    }
+  }
+  if (q < S) {
+    bf16* out = a.dq + ((long)b * S + q) * a.lddq + (long)h * DH;
+#pragma unroll
+    for (int ot = 0; ot < DH / 32; ++ot)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) out[ot * 32 + acc_row(r, g)] = f2bf(dq[ot][r] * a.f.scale);
+  }
+}
+
 template <int DH>
 struct AttnCfg {
   static constexpr int BKV = (DH >= 256) ? 32 : 64;
@@ -708,6 +1220,18 @@ hipError_t bwd_launch(const AttnBwdArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(attn_delta_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (DH == 64 || DH == 128 || DH == 256) {
+    constexpr int D = (DH == 64 || DH == 128 || DH == 256) ? DH : 64;
+    constexpr bool PAIR = D == 256;
+    constexpr int KPW = PAIR ? WG_ROWS / 2 : WG_ROWS;
+    dim3 gkv((a.f.S + KPW - 1) / KPW, a.f.B * a.f.H);
+    hipLaunchKernelGGL((attn_bwd_dkdv_fast<D, PAIR>), gkv, dim3(NT), 0, s, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    dim3 gq((a.f.S + WG_ROWS - 1) / WG_ROWS, a.f.B * a.f.H);
+    hipLaunchKernelGGL((attn_bwd_dq_fast<D>), gq, dim3(NT), 0, s, a);
+    return hipGetLastError();
+  }
   dim3 grid((a.f.S + WG_ROWS - 1) / WG_ROWS, a.f.B * a.f.H, C::NSLICE);
   hipLaunchKernelGGL((attn_bwd_dkdv_kernel<DH, C::DHS, C::BQ>), grid, dim3(NT), 0, s, a);
   e = hipGetLastError();

@@ -80,7 +80,10 @@ def _merge(x):
 
 
 ATTN = [(2, 3, 100, 16, True), (1, 2, 257, 80, False), (2, 2, 300, 64, True), (1, 2, 160, 256, True),
-        (1, 1, 1, 64, True), (1, 2, 129, 128, False), (2, 1, 70, 32, False)]
+        (1, 1, 1, 64, True), (1, 2, 129, 128, False), (2, 1, 70, 32, False),
+        # pipelined kernels: several 32-row blocks, ragged tails, both masks
+        (2, 1, 520, 256, True), (1, 2, 97, 256, False), (1, 1, 5, 256, True), (2, 2, 333, 128, True),
+        (1, 3, 200, 64, False), (1, 1, 31, 128, True)]
 
 
 @pytest.mark.parametrize("B,H,S,dh,causal", ATTN)
