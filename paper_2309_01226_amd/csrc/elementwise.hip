@@ -263,28 +263,69 @@ __device__ __forceinline__ void adamw_one(float& p, float g, float& m, float& v,
   p = p - c.step * m / (sqrtf(v) / c.bc2s + c.eps);
 }
 
+__device__ __forceinline__ void adamw_four(floatx4& p, floatx4 g, floatx4& m, floatx4& v,
+                                           const AdamWConsts& c) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    float pe = p[e], me = m[e], ve = v[e];
+    adamw_one(pe, g[e], me, ve, c);
+    p[e] = pe;
+    m[e] = me;
+    v[e] = ve;
+  }
+}
+
+// Grid-stride over float4 groups, two groups per iteration with all eight
+// loads issued first.  Every byte is touched once per step, so loads and
+// stores are non-temporal (they stream past the caches).
 __global__ __launch_bounds__(256) void adamw_kernel(float* __restrict__ p,
                                                     const float* __restrict__ g,
                                                     float* __restrict__ m, float* __restrict__ v,
                                                     bf16* __restrict__ shadow, long n4, long n,
                                                     AdamWConsts c) {
   const long stride = (long)gridDim.x * blockDim.x;
-  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
-    float4 pp = reinterpret_cast<float4*>(p)[i];
-    float4 gg = reinterpret_cast<const float4*>(g)[i];
-    float4 mm = reinterpret_cast<float4*>(m)[i];
-    float4 vv = reinterpret_cast<float4*>(v)[i];
-    adamw_one(pp.x, gg.x, mm.x, vv.x, c);
-    adamw_one(pp.y, gg.y, mm.y, vv.y, c);
-    adamw_one(pp.z, gg.z, mm.z, vv.z, c);
-    adamw_one(pp.w, gg.w, mm.w, vv.w, c);
-    reinterpret_cast<float4*>(p)[i] = pp;
-    reinterpret_cast<float4*>(m)[i] = mm;
-    reinterpret_cast<float4*>(v)[i] = vv;
+  floatx4* P = reinterpret_cast<floatx4*>(p);
+  const floatx4* G = reinterpret_cast<const floatx4*>(g);
+  floatx4* Mo = reinterpret_cast<floatx4*>(m);
+  floatx4* Vo = reinterpret_cast<floatx4*>(v);
+  bf16x4* Sh = reinterpret_cast<bf16x4*>(shadow);
+  long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  for (; i + stride < n4; i += 2 * stride) {
+    floatx4 pp[2], gg[2], mm[2], vv[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const long j = i + u * stride;
+      pp[u] = __builtin_nontemporal_load(P + j);
+      gg[u] = __builtin_nontemporal_load(G + j);
+      mm[u] = __builtin_nontemporal_load(Mo + j);
+      vv[u] = __builtin_nontemporal_load(Vo + j);
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const long j = i + u * stride;
+      adamw_four(pp[u], gg[u], mm[u], vv[u], c);
+      __builtin_nontemporal_store(pp[u], P + j);
+      __builtin_nontemporal_store(mm[u], Mo + j);
+      __builtin_nontemporal_store(vv[u], Vo + j);
+      if (shadow != nullptr) {
+        bf16x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = f2bf(pp[u][e]);
+        __builtin_nontemporal_store(o, Sh + j);
+      }
+    }
+  }
+  for (; i < n4; i += stride) {
+    floatx4 pp = P[i], mm = Mo[i], vv = Vo[i];
+    adamw_four(pp, G[i], mm, vv, c);
+    P[i] = pp;
+    Mo[i] = mm;
+    Vo[i] = vv;
     if (shadow != nullptr) {
       bf16x4 o;
-      o[0] = f2bf(pp.x); o[1] = f2bf(pp.y); o[2] = f2bf(pp.z); o[3] = f2bf(pp.w);
-      reinterpret_cast<bf16x4*>(shadow)[i] = o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = f2bf(pp[e]);
+      Sh[i] = o;
     }
   }
   // scalar tail (n not a multiple of 4, or unaligned pointers)

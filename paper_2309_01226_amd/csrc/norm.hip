@@ -3,9 +3,10 @@
 // One wavefront owns one row (rows up to 8192 wide stay in registers as
 // float4 chunks, 256 columns per chunk); mean and variance are two-pass
 // wave reductions over the register copy, so x is read from HBM once.
-// Gain / shift gradients are reduced without atomics: each wave accumulates
-// the columns of a fixed, strided set of rows into a partial row, and a second
-// kernel sums the partial rows in a fixed order (bitwise reproducible).
+// Gain / shift gradients are reduced without atomics: each workgroup of the
+// backward accumulates the columns of a fixed block of rows into a partial
+// row, and a second kernel sums the partial rows in a fixed order (bitwise
+// reproducible).
 #include "common.h"
 #include "kernels.h"
 
@@ -65,93 +66,157 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x
   }
 }
 
-// Each wave handles rows w, w + n_part, w + 2 n_part, ... (w = global wave id
-// < n_part) and keeps per-column partial sums of dy * xhat and dy in registers.
-// A row is read twice (row statistics, then dx); the second read hits cache.
-template <int NC>
+// Backward: workgroup p owns rows [p * rpb, (p + 1) * rpb); each thread owns
+// the columns (j * 256 + tid) * 4 .. +3 and keeps their dg / db partial sums
+// in registers, so the workgroup writes one partial row per tensor and needs
+// no cross-wave reduction of the columns.  Two rows are processed per
+// iteration; their two row sums go through LDS (fixed order: lane tree, then
+// waves 0..3), one barrier per iteration.  dy and x are read once.
+template <int NC4>
 __global__ __launch_bounds__(256) void ln_bwd_kernel(
     const float* __restrict__ dy, long lddy, const float* __restrict__ x, long ldx,
     long row_stride, const float* __restrict__ g, const float* __restrict__ mean,
     const float* __restrict__ rstd, float* __restrict__ dres, long ldres,
-    float* __restrict__ part_g, float* __restrict__ part_b, int rows, int d, int n_part) {
-  const int lane = threadIdx.x & 63;
-  const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (w >= n_part) return;
-  float4 pg[NC], pb[NC];
+    float* __restrict__ part_g, float* __restrict__ part_b, int rows, int d, int rpb) {
+  __shared__ float red[2][4][4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r0 = blockIdx.x * rpb, r1 = min(rows, r0 + rpb);
+  float4 gg[NC4], pg[NC4], pb[NC4];
 #pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    pg[c] = make_float4(0.f, 0.f, 0.f, 0.f);
-    pb[c] = pg[c];
+  for (int j = 0; j < NC4; ++j) {
+    const int col = (j * 256 + tid) * 4;
+    gg[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (col < d) gg[j] = *reinterpret_cast<const float4*>(g + col);
+    pg[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+    pb[j] = pg[j];
   }
-  for (int row = w; row < rows; row += n_part) {
-    const float* dyr = dy + (long)row * lddy;
-    const float* xr = x + (long)row * row_stride * ldx;
-    float* dr = dres + (long)row * row_stride * ldres;
-    const float mu = mean[row], rs = rstd[row];
-    float s1 = 0.f, s2 = 0.f;
+  int it = 0;
+  for (int row = r0; row < r1; row += 2, ++it) {
+    const bool two = row + 1 < r1;
+    float4 dv[2][NC4], xh[2][NC4];
+    float mu[2], rs[2], s[2][2];
 #pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      int col = (c * 64 + lane) * 4;
-      if (col < d) {
-        float4 dv = *reinterpret_cast<const float4*>(dyr + col);
-        float4 xv = *reinterpret_cast<const float4*>(xr + col);
-        float4 gg = *reinterpret_cast<const float4*>(g + col);
-        float4 xh = make_float4((xv.x - mu) * rs, (xv.y - mu) * rs, (xv.z - mu) * rs, (xv.w - mu) * rs);
-        float4 gy = make_float4(dv.x * gg.x, dv.y * gg.y, dv.z * gg.z, dv.w * gg.w);
-        pg[c].x += dv.x * xh.x; pg[c].y += dv.y * xh.y;
-        pg[c].z += dv.z * xh.z; pg[c].w += dv.w * xh.w;
-        pb[c].x += dv.x; pb[c].y += dv.y; pb[c].z += dv.z; pb[c].w += dv.w;
-        s1 += gy.x + gy.y + gy.z + gy.w;
-        s2 += gy.x * xh.x + gy.y * xh.y + gy.z * xh.z + gy.w * xh.w;
+    for (int q = 0; q < 2; ++q) {
+      const int rr = two ? row + q : row;  // a lone last row is processed twice, counted once
+      mu[q] = mean[rr];
+      rs[q] = rstd[rr];
+      const float* dyr = dy + (long)rr * lddy;
+      const float* xr = x + (long)rr * row_stride * ldx;
+      s[q][0] = s[q][1] = 0.f;
+#pragma unroll
+      for (int j = 0; j < NC4; ++j) {
+        const int col = (j * 256 + tid) * 4;
+        float4 xv = make_float4(0.f, 0.f, 0.f, 0.f);
+        dv[q][j] = xv;
+        if (col < d) {
+          dv[q][j] = *reinterpret_cast<const float4*>(dyr + col);
+          xv = *reinterpret_cast<const float4*>(xr + col);
+        }
+        float4 h = make_float4((xv.x - mu[q]) * rs[q], (xv.y - mu[q]) * rs[q], (xv.z - mu[q]) * rs[q],
+                               (xv.w - mu[q]) * rs[q]);
+        if (col >= d) h = make_float4(0.f, 0.f, 0.f, 0.f);
+        xh[q][j] = h;
+        const float4 v = dv[q][j];
+        const float4 gy = make_float4(v.x * gg[j].x, v.y * gg[j].y, v.z * gg[j].z, v.w * gg[j].w);
+        s[q][0] += gy.x + gy.y + gy.z + gy.w;
+        s[q][1] += gy.x * h.x + gy.y * h.y + gy.z * h.z + gy.w * h.w;
       }
     }
-    const float m1 = wave_sum(s1) / d, m2 = wave_sum(s2) / d;
 #pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      int col = (c * 64 + lane) * 4;
-      if (col < d) {
-        float4 dv = *reinterpret_cast<const float4*>(dyr + col);
-        float4 xv = *reinterpret_cast<const float4*>(xr + col);
-        float4 gg = *reinterpret_cast<const float4*>(g + col);
-        float4 o = *reinterpret_cast<float4*>(dr + col);
-        o.x += rs * (dv.x * gg.x - m1 - (xv.x - mu) * rs * m2);
-        o.y += rs * (dv.y * gg.y - m1 - (xv.y - mu) * rs * m2);
-        o.z += rs * (dv.z * gg.z - m1 - (xv.z - mu) * rs * m2);
-        o.w += rs * (dv.w * gg.w - m1 - (xv.w - mu) * rs * m2);
-        *reinterpret_cast<float4*>(dr + col) = o;
+    for (int q = 0; q < 2; ++q) {
+      const float a0 = wave_sum(s[q][0]), a1 = wave_sum(s[q][1]);
+      if (lane == 0) {
+        red[it & 1][wave][2 * q] = a0;
+        red[it & 1][wave][2 * q + 1] = a1;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      if (q == 1 && !two) continue;
+      const int rr = row + q;
+      float t0 = red[it & 1][0][2 * q], t1 = red[it & 1][0][2 * q + 1];
+#pragma unroll
+      for (int w = 1; w < 4; ++w) {
+        t0 += red[it & 1][w][2 * q];
+        t1 += red[it & 1][w][2 * q + 1];
+      }
+      const float m1 = t0 / d, m2 = t1 / d;
+      float* dr = dres + (long)rr * row_stride * ldres;
+#pragma unroll
+      for (int j = 0; j < NC4; ++j) {
+        const int col = (j * 256 + tid) * 4;
+        if (col < d) {
+          const float4 v = dv[q][j], h = xh[q][j];
+          float4 o = *reinterpret_cast<float4*>(dr + col);
+          o.x += rs[q] * (v.x * gg[j].x - m1 - h.x * m2);
+          o.y += rs[q] * (v.y * gg[j].y - m1 - h.y * m2);
+          o.z += rs[q] * (v.z * gg[j].z - m1 - h.z * m2);
+          o.w += rs[q] * (v.w * gg[j].w - m1 - h.w * m2);
+          *reinterpret_cast<float4*>(dr + col) = o;
+          pg[j].x += v.x * h.x; pg[j].y += v.y * h.y; pg[j].z += v.z * h.z; pg[j].w += v.w * h.w;
+          pb[j].x += v.x; pb[j].y += v.y; pb[j].z += v.z; pb[j].w += v.w;
+        }
       }
     }
   }
 #pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    int col = (c * 64 + lane) * 4;
+  for (int j = 0; j < NC4; ++j) {
+    const int col = (j * 256 + tid) * 4;
     if (col < d) {
-      *reinterpret_cast<float4*>(part_g + (long)w * d + col) = pg[c];
-      *reinterpret_cast<float4*>(part_b + (long)w * d + col) = pb[c];
+      *reinterpret_cast<float4*>(part_g + (long)blockIdx.x * d + col) = pg[j];
+      *reinterpret_cast<float4*>(part_b + (long)blockIdx.x * d + col) = pb[j];
     }
   }
 }
 
-__global__ void colsum_partials_kernel(const float* __restrict__ part, int n_part, int d,
-                                       float* __restrict__ out) {
-  int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= d) return;
+// out[c] = sum_p part[p, c] in a fixed order: wave w sums p = w, w + 8, ...,
+// then the eight wave sums are added in order.  64 columns per workgroup.
+__global__ __launch_bounds__(512) void colsum_partials_kernel(const float* __restrict__ part, int n_part,
+                                                              int d, float* __restrict__ out) {
+  __shared__ float red[8][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + lane;
   float s = 0.f;
-  for (int p = 0; p < n_part; ++p) s += part[(long)p * d + c];
-  out[c] = s;
+  if (c < d)
+    for (int p = w; p < n_part; p += 8) s += part[(long)p * d + c];
+  red[w][lane] = s;
+  __syncthreads();
+  if (w == 0 && c < d) {
+    float t = red[0][lane];
+#pragma unroll
+    for (int k = 1; k < 8; ++k) t += red[k][lane];
+    out[c] = t;
+  }
 }
 
-// Block p sums rows [p * rpp, min(rows, (p+1) * rpp)) of every column.
-template <typename T>
+// Block (x, p) sums rows [p * rpp, min(rows, (p+1) * rpp)) of columns
+// [x * 256 * V, (x + 1) * 256 * V), V consecutive columns per thread (one
+// 16-byte load per row when VEC, else V = 1).
+template <typename T, bool VEC>
 __global__ __launch_bounds__(256) void colsum_pass1(const T* __restrict__ X, long ldx, int rows,
                                                     int cols, int rpp, float* __restrict__ part) {
+  constexpr int V = VEC ? 16 / (int)sizeof(T) : 1;
   const int p = blockIdx.y;
-  const int c = blockIdx.x * 256 + threadIdx.x;
+  const int c = (blockIdx.x * 256 + threadIdx.x) * V;
   if (c >= cols) return;
   const int r0 = p * rpp, r1 = min(rows, r0 + rpp);
-  float s = 0.f;
-  for (int r = r0; r < r1; ++r) s += (float)X[(long)r * ldx + c];
-  part[(long)p * cols + c] = s;
+  float s[V];
+#pragma unroll
+  for (int v = 0; v < V; ++v) s[v] = 0.f;
+  for (int r = r0; r < r1; ++r) {
+    const T* src = X + (long)r * ldx + c;
+    if constexpr (VEC) {
+      u32x4 raw = *reinterpret_cast<const u32x4*>(src);
+      const T* e = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+      for (int v = 0; v < V; ++v) s[v] += (float)e[v];
+    } else {
+      s[0] += (float)src[0];
+    }
+  }
+#pragma unroll
+  for (int v = 0; v < V; ++v) part[(long)p * cols + c + v] = s[v];
 }
 
 template <int NC>
@@ -163,13 +228,15 @@ hipError_t ln_fwd_launch(const float* x, long ldx, long rs, const float* g, cons
   return hipGetLastError();
 }
 
-template <int NC>
+template <int NC4>
 hipError_t ln_bwd_launch(const float* dy, long lddy, const float* x, long ldx, long rs,
                          const float* g, const float* mean, const float* rstd, float* dres,
                          long ldres, float* pg, float* pb, int rows, int d, int n_part,
                          hipStream_t s) {
-  hipLaunchKernelGGL(ln_bwd_kernel<NC>, dim3(sat_cdiv(n_part, 4)), dim3(256), 0, s, dy, lddy, x,
-                     ldx, rs, g, mean, rstd, dres, ldres, pg, pb, rows, d, n_part);
+  // exactly n_part workgroups, so every partial row is written (zeros past the last row)
+  const int rpb = sat_cdiv(rows, n_part);
+  hipLaunchKernelGGL(ln_bwd_kernel<NC4>, dim3(n_part), dim3(256), 0, s, dy, lddy, x,
+                     ldx, rs, g, mean, rstd, dres, ldres, pg, pb, rows, d, rpb);
   return hipGetLastError();
 }
 
@@ -198,21 +265,19 @@ hipError_t launch_layernorm_bwd(const float* dy, long lddy, const float* x, long
   if (d % 4 != 0 || d > 64 * 4 * 16 || lddy % 4 != 0 || ldx % 4 != 0 || ldres % 4 != 0 ||
       n_part <= 0)
     return hipErrorInvalidValue;
-  int nc = sat_cdiv(d, 256);
+  const int nc = sat_cdiv(d, 1024);
 #define LNB(NC) ln_bwd_launch<NC>(dy, lddy, x, ldx, row_stride, g, mean, rstd, dres, ldres, part_g, part_b, rows, d, n_part, s)
   if (nc <= 1) return LNB(1);
   if (nc <= 2) return LNB(2);
-  if (nc <= 4) return LNB(4);
-  if (nc <= 8) return LNB(8);
-  return LNB(16);
+  return LNB(4);
 #undef LNB
 }
 
 hipError_t launch_colsum_partials(const float* part, int n_part, int d, float* out,
                                   hipStream_t s) {
   if (d <= 0) return hipSuccess;
-  hipLaunchKernelGGL(colsum_partials_kernel, dim3(sat_cdiv(d, 256)), dim3(256), 0, s, part,
-                     n_part, d, out);
+  hipLaunchKernelGGL(colsum_partials_kernel, dim3(sat_cdiv(d, 64)), dim3(512), 0, s, part, n_part, d,
+                     out);
   return hipGetLastError();
 }
 
@@ -221,10 +286,16 @@ static hipError_t colsum_any(const T* X, long ldx, int rows, int cols, float* pa
                              float* out, hipStream_t s) {
   if (cols <= 0) return hipSuccess;
   if (rows <= 0 || n_part <= 0) return hipErrorInvalidValue;
-  int rpp = sat_cdiv(rows, n_part);
-  int np = sat_cdiv(rows, rpp);
-  hipLaunchKernelGGL(colsum_pass1<T>, dim3(sat_cdiv(cols, 256), np), dim3(256), 0, s, X, ldx,
-                     rows, cols, rpp, part);
+  const int rpp = sat_cdiv(rows, n_part);
+  const int np = sat_cdiv(rows, rpp);
+  constexpr int V = 16 / (int)sizeof(T);
+  const bool vec = cols % V == 0 && ldx % V == 0 && reinterpret_cast<uintptr_t>(X) % 16 == 0;
+  if (vec)
+    hipLaunchKernelGGL((colsum_pass1<T, true>), dim3(sat_cdiv(cols, 256 * V), np), dim3(256), 0, s, X,
+                       ldx, rows, cols, rpp, part);
+  else
+    hipLaunchKernelGGL((colsum_pass1<T, false>), dim3(sat_cdiv(cols, 256), np), dim3(256), 0, s, X, ldx,
+                       rows, cols, rpp, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_colsum_partials(part, np, cols, out, s);
