@@ -639,6 +639,7 @@ inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 
 hipError_t launch_gemm(const GemmArgs& a, int alay, int blay, int epi, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   if (a.K <= 0) return hipErrorInvalidValue;
+  if (gemm256_eligible(a, alay, blay, epi)) return launch_gemm256(a, alay, blay, epi, s);
   // 16-byte loads need aligned rows.  Along K a partial vector would mix in
   // values past K, so K must be a multiple of 8; along M / N a partial vector
   // only feeds output rows / columns that are never stored, so it suffices that

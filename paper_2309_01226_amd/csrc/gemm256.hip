@@ -1,0 +1,456 @@
+// bf16 MFMA GEMM for large, aligned problems: 256 x 256 output tiles,
+// K-tiles of 64, two LDS stages.
+//
+//   C[m, n] = sum_k A(m, k) B(n, k), bf16 operands, fp32 accumulation, with
+//   the same fused epilogues as the general kernel in gemm.hip.
+//
+// What bounds it on MI355X (measured with single-purpose variants of this
+// kernel): the L2 -> LDS copy stream, not the matrix cores.  One 256 x 256
+// tile needs 32 bytes per clock per CU at full MFMA rate, and a CU's copy
+// throughput is set by the number of 128-byte cache lines it requests, not by
+// bytes: rows copied in 64-byte pieces (K-tiles of 32) deliver about half of
+// what full-line pieces do.  So K-tiles are 64 deep (a K-contiguous row of the
+// tile is exactly one line), which leaves room for two stages in the 160 KB of
+// LDS; the copies of tile k + 2 are issued as soon as every wave has finished
+// reading tile k.  (A four-stage, 32-deep variant of the same loop is kept
+// selectable at compile time: it hides more latency but is line-bound.)
+//
+// Layout of one stage: the A tile, then the B tile.
+//  * K-contiguous operand (rows = m or n): [256 rows][64 k], 128 B per row;
+//    the eight 16-byte chunks of row r are XOR-swizzled with (r >> 1) & 7,
+//    which keeps the fragment reads (16 lanes = 16 consecutive rows at one
+//    chunk) free of bank conflicts.
+//  * M/N-contiguous operand (k rows, m or n contiguous): [64 k][256], 512 B
+//    per k-row; the 32 chunks of k-row k are XOR-swizzled with
+//    {0, 4, 10, 14}[k & 3].  Fragments are read with ds_read_b64_tr_b16, the
+//    CDNA4 transposing LDS read: a 16-lane group reads a 4 (k) x 16 (n) block,
+//    lane 4e + q supplying the address of k-row e, columns 4q .. 4q + 3, and
+//    lane o receives column o, k-rows 0..3.  Two such reads give the eight
+//    consecutive k of a 32 x 32 x 16 MFMA operand.
+//  * Both layouts go HBM -> LDS with buffer_load ... lds (16 bytes per lane,
+//    1 KB per instruction, no VGPR staging).  Rows past M / N and k past K get
+//    an out-of-range buffer offset and read as zeros.
+//
+// Main loop per K-tile (four k-steps of 16), per wave (128 x 128 sub-tile,
+// 4 x 4 MFMA 32x32x16 accumulators in AGPRs): the MFMAs of each k-step are
+// interleaved with the fragment reads of the next; before the last k-step,
+// wait for this wave's copies of the next tile and for its reads; barrier;
+// copies of tile k + 2 into the stage just released and the fragment reads of
+// the next tile's first k-step, interleaved with the last k-step's MFMAs.
+//
+// Epilogue: each wave stages one 32-row slab of its sub-tile in its own LDS
+// region and stores 4 consecutive columns per lane (16-byte fp32 or 8-byte
+// bf16 vectors), so no workgroup barrier is needed between slabs.
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr int BT = 256;               // tile rows and columns
+constexpr int NT = 256;               // 4 wavefronts, 2 x 2
+constexpr uint32_t OOB = 0x80000000u; // buffer offset past num_records: reads zero
+constexpr int EP = 136;               // fp32 pitch of an epilogue staging row
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+// K-layout swizzle: BK = 32 (four chunks per row) or BK = 64 (eight chunks);
+// the BK = 64 form measured free of bank conflicts for the fragment reads
+template <int BK>
+__device__ __forceinline__ int swz_k(int row) {
+  return BK == 32 ? (((row >> 1) ^ (row >> 3)) & 3) : ((row >> 1) & 7);
+}
+__device__ __forceinline__ int swz_mn(int k) { return (0xEA40 >> ((k & 3) << 2)) & 15; }
+
+__device__ __forceinline__ lds_void* lds(const bf16* p) { return (lds_void*)(const_cast<bf16*>(p)); }
+
+// s_waitcnt vmcnt(VM) lgkmcnt(0)
+template <int VM>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4));
+}
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+
+__device__ __forceinline__ void cta_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// Copies of one operand tile: 16 instructions of 1 KB, four per wave.
+// Instruction j = 4 i + wave fills LDS bytes [1024 j, 1024 j + 1024) of the
+// tile; lane L writes the 16 bytes at 1024 j + 16 L.  A copy whose k lies at or
+// past K (the K tail, and the tiles past the last one that the steady-state
+// loop issues to keep its wait counts constant) reads zeros and touches no
+// memory.
+template <int LAY, int BK>
+struct Loader {
+  static constexpr int CPR = BK / 8;                       // 16-byte chunks per K-layout row
+  static constexpr int NI = (BT * BK * 2 / 1024) / 4;      // copy instructions per wave
+  uint32_t off[NI];  // byte offsets relative to (tile row 0, k0)
+  int kof[NI];       // k of this lane's chunk relative to k0
+  __device__ __forceinline__ void init(long ld, int nrows, int wave) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int j = 4 * i + wave;
+      if (LAY == LAY_K) {
+        const int row = (64 / CPR) * j + lane / CPR;
+        const int c = (lane % CPR) ^ swz_k<BK>(row);
+        off[i] = row < nrows ? (uint32_t)(((long)row * ld + 8 * c) * 2) : OOB;
+        kof[i] = 8 * c;
+      } else {
+        const int kr = 2 * j + (lane >> 5);
+        const int c = (lane & 31) ^ swz_mn(kr);
+        off[i] = 8 * c < nrows ? (uint32_t)(((long)kr * ld + 8 * c) * 2) : OOB;
+        kof[i] = kr;
+      }
+    }
+  }
+  __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, int k0, int K, long ld,
+                                        bf16* dst, int wave) const {
+    const uint32_t soff = LAY == LAY_K ? (uint32_t)(k0 * 2) : (uint32_t)((long)k0 * ld * 2);
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const uint32_t o = (k0 + kof[i] < K) ? off[i] : OOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds(dst + (4 * i + wave) * 512), 16, o, soff,
+                                               0, 0);
+    }
+  }
+};
+
+// Fragment addressing of one operand inside a stage, for the wave's 128-row
+// (or column) half `w0` (0 or 128).  frag(sub, ks) is the 32 x 16 MFMA operand
+// of rows w0 + 32 sub .. + 31, k = 16 ks .. + 15.
+template <int LAY, int BK>
+struct Frags {
+  static constexpr int KS = BK / 16;
+  int o[LAY == LAY_K ? KS : 8];  // element offsets: K layout o[ks]; MN layout o[2 sub + h]
+  __device__ __forceinline__ void init(int w0) {
+    const int lane = threadIdx.x & 63;
+    if (LAY == LAY_K) {
+      const int r = lane & 31;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        o[ks] = (w0 + r) * BK + 8 * ((2 * ks + (lane >> 5)) ^ swz_k<BK>(r));
+    } else {
+      const int G = lane >> 4, l = lane & 15;
+      const int sm = swz_mn(l >> 2);
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int kr = 8 * (G >> 1) + 4 * h + (l >> 2);
+          const int c = (w0 >> 3) + 4 * sub + 2 * (G & 1) + ((l >> 1) & 1);
+          o[2 * sub + h] = kr * BT + 8 * (c ^ sm) + 4 * (l & 1);
+        }
+    }
+  }
+  __device__ __forceinline__ bf16x8 read(const bf16* tile, int sub, int ks) const {
+    if (LAY == LAY_K) {
+      return *reinterpret_cast<const bf16x8*>(tile + o[ks] + sub * 32 * BK);
+    } else {
+      const bf16* t = tile + ks * 16 * BT;
+      bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(t + o[2 * sub]));
+      bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(t + o[2 * sub + 1]));
+      return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+  }
+};
+
+template <int AL, int BL, int BK>
+__device__ __forceinline__ void read_step(bf16x8 (&fa)[4], bf16x8 (&fb)[4], const Frags<AL, BK>& FA,
+                                          const Frags<BL, BK>& FB, const bf16* stage, int ks) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) fa[i] = FA.read(stage, i, ks);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) fb[j] = FB.read(stage + BT * BK, j, ks);
+}
+
+__device__ __forceinline__ void mfma_step(floatx16 (&acc)[4][4], const bf16x8 (&fa)[4],
+                                          const bf16x8 (&fb)[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+}
+
+// Scheduling templates for one k-step of 16 MFMAs: one DS read after each of
+// the first ND MFMAs, and one copy after each of the first NV.
+template <int ND, int NV>
+__device__ __forceinline__ void interleave() {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if (i < NV) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    if (i < ND) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+}
+
+template <int EPI, int GE>
+__device__ __forceinline__ void store4(const GemmArgs& p, long row, int col, floatx4 x) {
+  const int N = p.N;
+  const long o = row * p.ldo + col;
+  if (col + 3 < N) {
+    if (EPI == EPI_F32) {
+      *reinterpret_cast<floatx4*>(reinterpret_cast<float*>(p.out) + o) = x;
+    } else if (EPI == EPI_RESID_F32) {
+      const floatx4 r = *reinterpret_cast<const floatx4*>(p.resid + row * p.ldr + col);
+      *reinterpret_cast<floatx4*>(reinterpret_cast<float*>(p.out) + o) = x + r;
+    } else if (EPI == EPI_BF16) {
+      bf16x4 y = {f2bf(x[0]), f2bf(x[1]), f2bf(x[2]), f2bf(x[3])};
+      *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(p.out) + o) = y;
+      if (p.out2 != nullptr && col >= p.gelu_col0) {
+        bf16x4 g = {f2bf(gelu_t<GE>(x[0])), f2bf(gelu_t<GE>(x[1])), f2bf(gelu_t<GE>(x[2])),
+                    f2bf(gelu_t<GE>(x[3]))};
+        *reinterpret_cast<bf16x4*>(p.out2 + row * p.ldo2 + (col - p.gelu_col0)) = g;
+      }
+    } else {
+      const bf16x4 u = *reinterpret_cast<const bf16x4*>(p.aux + row * p.ldaux + col);
+      bf16x4 y;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) y[e] = f2bf(x[e] * gelu_grad_t<GE>(bf2f(u[e])));
+      *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(p.out) + o) = y;
+    }
+    return;
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int c = col + e;
+    if (c >= N) break;
+    if (EPI == EPI_F32) {
+      reinterpret_cast<float*>(p.out)[o + e] = x[e];
+    } else if (EPI == EPI_RESID_F32) {
+      reinterpret_cast<float*>(p.out)[o + e] = p.resid[row * p.ldr + c] + x[e];
+    } else if (EPI == EPI_BF16) {
+      reinterpret_cast<bf16*>(p.out)[o + e] = f2bf(x[e]);
+      if (p.out2 != nullptr && c >= p.gelu_col0)
+        p.out2[row * p.ldo2 + (c - p.gelu_col0)] = f2bf(gelu_t<GE>(x[e]));
+    } else {
+      const float u = bf2f(p.aux[row * p.ldaux + c]);
+      reinterpret_cast<bf16*>(p.out)[o + e] = f2bf(x[e] * gelu_grad_t<GE>(u));
+    }
+  }
+}
+
+template <int EPI, int GE>
+__device__ __forceinline__ void epilogue(const GemmArgs& p, floatx16 (&acc)[4][4], float* stage,
+                                         int m0, int n0, int wave, int lane) {
+  const int wm = wave >> 1, wn = wave & 1;
+  float* st = stage + wave * 32 * EP;
+  const int cl = 4 * (lane & 31);
+  const int col = n0 + wn * 128 + cl;
+  floatx4 bias = {0.f, 0.f, 0.f, 0.f};
+  if (p.bias != nullptr) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (col + e < p.N && col + e >= p.bias_col0) bias[e] = p.bias[col + e - p.bias_col0];
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        st[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * EP + 32 * j + (lane & 31)] = acc[i][j][r];
+    const long rowbase = m0 + wm * 128 + 32 * i;
+    // fully unrolled only for the plain epilogues: the GELU forms would need
+    // more VGPRs than the AGPR-held accumulators leave free
+#pragma unroll(EPI == EPI_F32 || EPI == EPI_RESID_F32 ? 16 : 2)
+    for (int s = 0; s < 16; ++s) {
+      const int rl = 2 * s + (lane >> 5);
+      const long row = rowbase + rl;
+      floatx4 x = *reinterpret_cast<const floatx4*>(st + rl * EP + cl) + bias;
+      if (row < p.M) store4<EPI, GE>(p, row, col, x);
+    }
+  }
+}
+
+// BK: K-tile depth (32 or 64); NS: LDS stages (NS * BK * 1 KB <= 128 KB).
+template <int AL, int BL, int EPI, int GE, int BK, int NS>
+__global__ __launch_bounds__(NT, 1) void gemm256_kernel(GemmArgs p) {
+  constexpr int OPE = BT * BK;               // bf16 elements of one operand tile
+  constexpr int STE = 2 * OPE;               // bf16 elements of one stage
+  constexpr int KS = BK / 16;                // MFMA k-steps per K-tile
+  constexpr int CPT = Loader<AL, BK>::NI + Loader<BL, BK>::NI;  // copies per wave per tile
+  static_assert(NS * STE * 2 <= 131072 && KS % 2 == 0, "LDS budget / k-step parity");
+  __shared__ __attribute__((aligned(1024))) bf16 smem[NS * STE];
+
+  const int M = p.M, N = p.N, K = p.K;
+  const int tiles_m = (M + BT - 1) / BT, tiles_n = (N + BT - 1) / BT;
+  const int nwg = tiles_m * tiles_n;
+  // Workgroups are dealt round-robin over the 8 XCDs; renumber so that each
+  // XCD walks a contiguous range of the tile order, then order tiles in
+  // groups of 8 tile-rows so that the B tiles of a group stay in L2.
+  int bid = blockIdx.x;
+  if ((nwg & 7) == 0) bid = (bid & 7) * (nwg >> 3) + (bid >> 3);
+  constexpr int G = 8;
+  const int per_group = G * tiles_n;
+  const int group = bid / per_group;
+  const int first_m = group * G;
+  const int gsize = min(tiles_m - first_m, G);
+  const int in_g = bid - group * per_group;
+  const int m0 = (first_m + in_g % gsize) * BT, n0 = (in_g / gsize) * BT;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+
+  __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(p.A + (AL == LAY_K ? (long)m0 * p.lda : (long)m0)), (short)0, 0x7FFFFFFF, 0x00020000);
+  __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(p.B + (BL == LAY_K ? (long)n0 * p.ldb : (long)n0)), (short)0, 0x7FFFFFFF, 0x00020000);
+  Loader<AL, BK> la;
+  Loader<BL, BK> lb;
+  la.init(p.lda, M - m0, wave);
+  lb.init(p.ldb, N - n0, wave);
+  Frags<AL, BK> FA;
+  Frags<BL, BK> FB;
+  FA.init(wm * 128);
+  FB.init(wn * 128);
+
+  floatx16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  // Every iteration issues the copies of one tile (tiles past the last read
+  // zeros), so the wait counts are constants: once tile t + 1 is resident,
+  // tiles t + 2 .. t + NS - 1 may still be in flight.
+  const int nk = (K + BK - 1) / BK;
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    la.issue(rsA, s * BK, K, p.lda, smem + s * STE, wave);
+    lb.issue(rsB, s * BK, K, p.ldb, smem + s * STE + OPE, wave);
+  }
+  wait_vm_lgkm0<(NS - 1) * CPT>();  // tile 0 resident
+  cta_barrier();
+
+  constexpr int ND = (AL == LAY_K ? 4 : 8) + (BL == LAY_K ? 4 : 8);
+  bf16x8 f0a[4], f0b[4], f1a[4], f1b[4];
+  read_step(f0a, f0b, FA, FB, smem, 0);
+
+  for (int kt = 0; kt + 1 < nk; ++kt) {
+    bf16* cur = smem + (kt % NS) * STE;
+    const bf16* nxt = smem + ((kt + 1) % NS) * STE;
+#pragma unroll
+    for (int ks = 0; ks + 2 < KS; ks += 2) {
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_step(acc, f0a, f0b);
+      read_step(f1a, f1b, FA, FB, cur, ks + 1);
+      interleave<ND, 0>();
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_step(acc, f1a, f1b);
+      read_step(f0a, f0b, FA, FB, cur, ks + 2);
+      interleave<ND, 0>();
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(acc, f0a, f0b);
+    read_step(f1a, f1b, FA, FB, cur, KS - 1);
+    interleave<ND, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vm_lgkm0<(NS - 2) * CPT>();  // this wave's copies of tile kt + 1 and its reads of tile kt
+    cta_barrier();                    // ... and every other wave's: stage kt % NS is free
+    la.issue(rsA, (kt + NS) * BK, K, p.lda, cur, wave);
+    lb.issue(rsB, (kt + NS) * BK, K, p.ldb, cur + OPE, wave);
+    read_step(f0a, f0b, FA, FB, nxt, 0);
+    mfma_step(acc, f1a, f1b);
+    interleave<ND, CPT>();
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  {
+    const bf16* cur = smem + ((nk - 1) % NS) * STE;
+#pragma unroll
+    for (int ks = 0; ks + 2 < KS; ks += 2) {
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_step(acc, f0a, f0b);
+      read_step(f1a, f1b, FA, FB, cur, ks + 1);
+      interleave<ND, 0>();
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_step(acc, f1a, f1b);
+      read_step(f0a, f0b, FA, FB, cur, ks + 2);
+      interleave<ND, 0>();
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(acc, f0a, f0b);
+    read_step(f1a, f1b, FA, FB, cur, KS - 1);
+    interleave<ND, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(acc, f1a, f1b);
+  }
+  wait_vm_lgkm0<0>();  // the zero-filling copies past the last tile
+  __syncthreads();
+  epilogue<EPI, GE>(p, acc, reinterpret_cast<float*>(smem), m0, n0, wave, lane);
+}
+
+#ifndef SAT_GEMM256_BK
+#define SAT_GEMM256_BK 64
+#define SAT_GEMM256_NS 2
+#endif
+
+template <int AL, int BL, int EPI>
+hipError_t launch_e(const GemmArgs& a, hipStream_t s) {
+  dim3 grid((unsigned)(sat_cdiv(a.M, BT) * sat_cdiv(a.N, BT)));
+  if ((EPI == EPI_BF16 || EPI == EPI_DGELU_BF16) && a.gelu_erf)
+    hipLaunchKernelGGL((gemm256_kernel<AL, BL, EPI, 1, SAT_GEMM256_BK, SAT_GEMM256_NS>), grid, dim3(NT), 0, s, a);
+  else
+    hipLaunchKernelGGL((gemm256_kernel<AL, BL, EPI, 0, SAT_GEMM256_BK, SAT_GEMM256_NS>), grid, dim3(NT), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int AL, int BL>
+hipError_t launch_l(const GemmArgs& a, int epi, hipStream_t s) {
+  switch (epi) {
+    case EPI_F32: return launch_e<AL, BL, EPI_F32>(a, s);
+    case EPI_RESID_F32: return launch_e<AL, BL, EPI_RESID_F32>(a, s);
+    case EPI_BF16: return launch_e<AL, BL, EPI_BF16>(a, s);
+    case EPI_DGELU_BF16: return launch_e<AL, BL, EPI_DGELU_BF16>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+inline bool al(const void* p, int bytes) { return (reinterpret_cast<uintptr_t>(p) % bytes) == 0; }
+
+}  // namespace
+
+bool gemm256_eligible(const GemmArgs& a, int alay, int blay, int epi) {
+  if (a.M <= 0 || a.N <= 0 || a.K <= 0) return false;
+  // enough 256 x 256 tiles to give every CU one
+  if ((long)sat_cdiv(a.M, BT) * sat_cdiv(a.N, BT) < 256) return false;
+  auto r8 = [](long x) { return (x + 7) / 8 * 8; };
+  const long lim = 1L << 31;
+  // operands: 16-byte copies, 32-bit buffer offsets
+  if (!al(a.A, 16) || !al(a.B, 16) || a.lda % 8 || a.ldb % 8) return false;
+  if (alay == LAY_K ? (a.K % 8 || (long)BT * a.lda * 2 + 2L * a.K >= lim)
+                    : (a.lda < r8(a.M) || ((long)a.K + 256) * a.lda * 2 >= lim))
+    return false;
+  if (blay == LAY_K ? (a.K % 8 || (long)BT * a.ldb * 2 + 2L * a.K >= lim)
+                    : (a.ldb < r8(a.N) || ((long)a.K + 256) * a.ldb * 2 >= lim))
+    return false;
+  // epilogue: 4-column vectors
+  if (a.ldo % 4) return false;
+  if (epi == EPI_F32 || epi == EPI_RESID_F32) {
+    if (!al(a.out, 16)) return false;
+    if (epi == EPI_RESID_F32 && (!al(a.resid, 16) || a.ldr % 4)) return false;
+  } else {
+    if (!al(a.out, 8)) return false;
+    if (epi == EPI_BF16 && a.out2 != nullptr && (!al(a.out2, 8) || a.ldo2 % 4 || a.gelu_col0 % 4))
+      return false;
+    if (epi == EPI_DGELU_BF16 && (!al(a.aux, 8) || a.ldaux % 4)) return false;
+  }
+  return true;
+}
+
+hipError_t launch_gemm256(const GemmArgs& a, int alay, int blay, int epi, hipStream_t s) {
+  if (alay == LAY_K && blay == LAY_K) return launch_l<LAY_K, LAY_K>(a, epi, s);
+  if (alay == LAY_K && blay == LAY_MN) return launch_l<LAY_K, LAY_MN>(a, epi, s);
+  if (alay == LAY_MN && blay == LAY_K) return launch_l<LAY_MN, LAY_K>(a, epi, s);
+  return launch_l<LAY_MN, LAY_MN>(a, epi, s);
+}

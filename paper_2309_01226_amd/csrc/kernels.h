@@ -40,6 +40,10 @@ struct GemmArgs {
 };
 
 hipError_t launch_gemm(const GemmArgs& a, int alay, int blay, int epi, hipStream_t s);
+// The 256 x 256 four-stage kernel (gemm256.hip) for large aligned problems;
+// launch_gemm dispatches to it when gemm256_eligible holds.
+bool gemm256_eligible(const GemmArgs& a, int alay, int blay, int epi);
+hipError_t launch_gemm256(const GemmArgs& a, int alay, int blay, int epi, hipStream_t s);
 
 // ---------------------------------------------------------------- LayerNorm
 // y = (x - mean) * rstd * g + b over rows of length d; x fp32, y bf16.

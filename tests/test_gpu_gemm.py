@@ -91,23 +91,45 @@ def test_gemm_epilogues(erf_form):
 
 
 @pytest.mark.parametrize("a_layout,b_layout", [(0, 0), (0, 1), (1, 1), (1, 0)])
-@pytest.mark.parametrize("epi", [0, 2])
+@pytest.mark.parametrize("epi", [0, 1, 2, 3])
 def test_gemm_large_tiles_sampled(a_layout, b_layout, epi):
-    """Shapes large enough for the 256 x 256 tile path (>= 256 tiles), with a
-    ragged M and a K tail; checked on 300 sampled rows against float64."""
+    """Shapes large enough for the 256 x 256 four-stage path (>= 256 tiles),
+    with ragged M and N edges and a K tail, every epilogue; checked on 300
+    sampled rows (always including the last) against float64."""
     from paper_2309_01226_amd import ops
-    M, N, K = 4100, 4096, 584
+    M, N, K = 4100, 4104, 584
     flush(f"gemm large lay=({a_layout},{b_layout}) epi={epi}")
-    rng = np.random.default_rng(17 + a_layout + 2 * b_layout)
+    rng = np.random.default_rng(17 + a_layout + 2 * b_layout + 4 * epi)
     A, B, Ad, Bd, lda, ldb = _operands(rng, M, N, K, a_layout, b_layout)
-    bias = rng.normal(size=N)
-    dt = torch.float32 if epi == 0 else torch.bfloat16
-    out = torch.empty(M, N, device="cuda", dtype=dt)
-    ops.gemm(Ad, Bd, M, N, K, out, lda=lda, ldb=ldb, a_layout=a_layout, b_layout=b_layout,
-             epilogue=epi, bias=to_dev_f32(bias))
-    torch.cuda.synchronize()
-    rows = np.sort(rng.choice(M, size=300, replace=False))
-    rows[-1] = M - 1
-    ref = O.gemm(A[rows], B) + bias
-    got = host(out)[rows]
-    assert rel(got, ref) < (2e-6 if epi == 0 else 4e-3)
+    bias = rng.normal(size=N - 8)
+    rows = np.sort(rng.choice(M - 1, size=299, replace=False))
+    rows = np.append(rows, M - 1)
+    C = O.gemm(A[rows], B)
+    pre = C.copy()
+    pre[:, 8:] += bias
+    kw = dict(lda=lda, ldb=ldb, a_layout=a_layout, b_layout=b_layout, epilogue=epi)
+    if epi == 0:
+        out = torch.empty(M, N, device="cuda", dtype=torch.float32)
+        ops.gemm(Ad, Bd, M, N, K, out, bias=to_dev_f32(bias), bias_col0=8, **kw)
+        torch.cuda.synchronize()
+        assert rel(host(out)[rows], pre) < 2e-6
+    elif epi == 1:
+        R = rng.normal(size=(M, N)).astype(np.float32)
+        out = to_dev_f32(R)
+        ops.gemm(Ad, Bd, M, N, K, out, resid=out, bias=to_dev_f32(bias), bias_col0=8, **kw)
+        torch.cuda.synchronize()
+        assert rel(host(out)[rows], R[rows] + pre) < 2e-6
+    elif epi == 2:
+        o1 = torch.empty(M, N, device="cuda", dtype=torch.bfloat16)
+        o2 = torch.empty(M, N - 512, device="cuda", dtype=torch.bfloat16)
+        ops.gemm(Ad, Bd, M, N, K, o1, bias=to_dev_f32(bias), bias_col0=8, out2=o2, ldo2=N - 512,
+                 gelu_col0=512, **kw)
+        torch.cuda.synchronize()
+        assert rel(host(o1)[rows], pre) < 4e-3
+        assert rel(host(o2)[rows], O.gelu(pre[:, 512:], 0)) < 4e-3
+    else:
+        U = bf16_round(rng.normal(size=(M, N)))
+        o3 = torch.empty(M, N, device="cuda", dtype=torch.bfloat16)
+        ops.gemm(Ad, Bd, M, N, K, o3, aux=to_dev_bf16(U), ldaux=N, gelu_erf=1, **kw)
+        torch.cuda.synchronize()
+        assert rel(host(o3)[rows], C * O.gelu_grad(U[rows], 1)) < 4e-3
