@@ -14,7 +14,7 @@ CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libsaturn.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["gemm.hip", "gemm256.hip", "norm.hip", "elementwise.hip", "attention.hip", "ops_abi.cpp", "model.cpp",
+SOURCES = ["gemm.hip", "gemm256.hip", "norm.hip", "elementwise.hip", "attention.hip", "attn256.hip", "ops_abi.cpp", "model.cpp",
            "step.cpp", "abi.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -25,9 +25,16 @@ COMMON = [
 ]
 
 
+# Per-source code-generation options.  The 256-wide attention kernels keep
+# their O / dK / dV accumulators and the resident Q / K / V operands live for
+# the whole key loop; MFMA results in VGPRs avoid whole-accumulator copies
+# between the two register files on every iteration.
+EXTRA = {"attn256.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form"]}
+
+
 def _compile(src):
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC] + COMMON + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC] + COMMON + EXTRA.get(src, []) + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {src}\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

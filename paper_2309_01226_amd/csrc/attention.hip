@@ -1249,6 +1249,7 @@ bool ok16(const void* p, long ld) {
 hipError_t launch_attention_fwd(const AttnArgs& a, hipStream_t s) {
   if (a.B * a.H * a.S == 0) return hipSuccess;
   if (!ok16(a.q, a.ldq) || !ok16(a.k, a.ldk) || !ok16(a.v, a.ldv)) return hipErrorInvalidValue;
+  if (attn256_fwd_eligible(a)) return launch_attn256_fwd(a, s);
   switch (a.dh) {
     case 16: return fwd_launch<16>(a, s);
     case 32: return fwd_launch<32>(a, s);

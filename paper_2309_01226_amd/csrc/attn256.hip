@@ -1,0 +1,286 @@
+// Attention forward for 256-wide heads (GPT-J), causal or bidirectional:
+// O = softmax(scale * Q K^T + mask) V per head, plus the per-query natural-log
+// log-sum-exp that the backward pass recomputes P from.
+//
+// Layout (one workgroup = 4 waves x 32 queries of one (batch, head)):
+//  * The score tile is computed transposed, S^T = K Q^T, so every lane owns
+//    one query: its running max and sum are per-lane scalars, and its 16
+//    probabilities per 32-key tile already form the B operand of
+//    O^T += V^T P^T.  Q stays in registers for the whole key loop.
+//  * Per 64-key block, K and V arrive by direct HBM -> LDS copies (two
+//    stages; the copies of block j + 1 are issued as soon as block j - 1 is
+//    released).  K rows are read as 16-byte row fragments (chunk c of key row
+//    r stored at c ^ (r & 15)).  V stays key-major and is read with the CDNA4
+//    transposing LDS read ds_read_b64_tr_b16, which hands each lane four
+//    consecutive keys of one head dimension, in exactly the key order of the
+//    probabilities' accumulator layout (chunk c of key row r stored at
+//    c ^ {0, 4, 10, 14}[r & 3] so that the four key rows and the two 16-dim
+//    groups a pass serves fall on distinct banks).  No register transposes.
+//  * Online softmax in base 2 with a lazily refreshed maximum: the running
+//    max m is raised (and O, l rescaled) only when a new score exceeds it by
+//    more than 8, so the probabilities exp2(x - m) stay below 2^8 and the
+//    128 accumulator rescales are skipped on almost every block.  The result
+//    is exact: O and l always share the same m.
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr int DH = 256;
+constexpr int NT = 256;        // 4 waves
+constexpr int WQ = 32;         // queries per wave
+constexpr int QPB = 4 * WQ;    // queries per workgroup
+constexpr int KB = 64;         // keys per block
+constexpr int TILE = KB * DH;  // bf16 elements of one K or V block
+constexpr float LOG2E = 1.4426950408889634f;
+constexpr float LN2 = 0.6931471805599453f;
+constexpr float RESCALE_SLACK = 8.f;
+constexpr uint32_t OOB = 0x80000000u;
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+__device__ __forceinline__ lds_void* lds(const bf16* p) { return (lds_void*)(const_cast<bf16*>(p)); }
+
+__device__ __forceinline__ int swz_row(int r) { return r & 15; }
+__device__ __forceinline__ int swz_tr(int r) { return (0xEA40 >> ((r & 3) << 2)) & 15; }
+
+template <int VM>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4));
+}
+__device__ __forceinline__ void cta_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+__device__ __forceinline__ floatx16 zero16() {
+  floatx16 z;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) z[r] = 0.f;
+  return z;
+}
+// Row (within a 32 x 32 tile) held by accumulator register r of lane group g.
+__device__ __forceinline__ int acc_row(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
+
+// Copies of one 64-row block (K or V) of this (batch, head): 32 instructions
+// of 1 KB (two 512-byte rows each), eight per wave; rows >= nvalid read zero.
+// SWZ selects the row-fragment (0) or transposed-read (1) chunk swizzle.
+template <int SWZ>
+__device__ __forceinline__ void copy_block(__amdgpu_buffer_rsrc_t rs, long ld, int nvalid,
+                                           bf16* dst, int wave) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int j = 4 * i + wave;
+    const int row = 2 * j + (lane >> 5);
+    const int c = (lane & 31) ^ (SWZ ? swz_tr(row) : swz_row(row));
+    const uint32_t o = row < nvalid ? (uint32_t)(((long)row * ld + 8 * c) * 2) : OOB;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds(dst + j * 512), 16, o, 0, 0, 0);
+  }
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const bf16* base, int r0, long ld) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)(base + (long)r0 * ld), (short)0, 0x7FFFFFFF,
+                                           0x00020000);
+}
+
+// Max / sum over the two 32-lane halves (lanes l and l + 32 hold the same query).
+__device__ __forceinline__ float halves_max(float x) { return fmaxf(x, __shfl_xor(x, 32, 64)); }
+__device__ __forceinline__ float halves_sum(float x) { return x + __shfl_xor(x, 32, 64); }
+
+// Per-lane state of one wave: 32 queries, lane = query (two lanes per query).
+struct FwdState {
+  bf16x8 qf[DH / 16];   // Q operand: dims 16 c + 8 g .. + 7
+  floatx16 o[DH / 32];  // O^T accumulators: dims 32 ot + acc_row(r, g)
+  float m, l;           // running max (base 2, lazily raised) and sum
+  int kofs[8];          // K row-fragment offsets of k-steps 0..7 (+128 for 8..15)
+  int vofs[4];          // V^T transposed-read offsets of ot = 0..3 (+128 for 4..7)
+};
+
+// One 64-key block: S^T = K Q^T, masked (MASK) online softmax, O^T += V^T P^T.
+__device__ __forceinline__ void fwd_block(FwdState& st, const bf16* Ks, const bf16* Vs, float sc,
+                                          int kv0, int q, int S, int causal, int g) {
+  floatx16 s0 = zero16(), s1 = zero16();
+#pragma unroll
+  for (int c = 0; c < DH / 16; ++c) {
+    const int co = st.kofs[c & 7] + (c >> 3) * 128;
+    const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(Ks + co);
+    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(Ks + 32 * DH + co);
+    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, st.qf[c], s0, 0, 0, 0);
+    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, st.qf[c], s1, 0, 0, 0);
+  }
+  // keep at most two k-steps of K fragments in flight (register budget)
+  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+  for (int i = 0; i < 14; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  float x[32];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    x[r] = s0[r] * sc;
+    x[16 + r] = s1[r] * sc;
+  }
+  // keys past the end, or (causal) past the query, score -inf; lim = first key excluded
+  const int lim = min(S, causal ? q + 1 : S) - kv0 - 4 * g;
+#pragma unroll
+  for (int r = 0; r < 32; ++r) {
+    const int kr = 32 * (r >> 4) + 8 * ((r & 15) >> 2) + (r & 3);  // key - kv0 - 4 g
+    x[r] = kr < lim ? x[r] : -INFINITY;
+  }
+  float mloc = x[0];
+#pragma unroll
+  for (int r = 1; r < 32; ++r) mloc = fmaxf(mloc, x[r]);
+  mloc = halves_max(mloc);
+  // lazy max: raise m only when a score exceeds it by more than the slack
+  const bool raise = mloc > st.m + RESCALE_SLACK;
+  if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+    const float alpha = (raise && st.m != -INFINITY) ? __builtin_amdgcn_exp2f(st.m - mloc)
+                                                     : (raise ? 0.f : 1.f);
+    st.l *= alpha;
+#pragma unroll
+    for (int ot = 0; ot < DH / 32; ++ot)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) st.o[ot][r] *= alpha;
+    st.m = raise ? mloc : st.m;
+  }
+  const float mm = (st.m == -INFINITY) ? 0.f : st.m;  // all-masked rows: x = -inf gives p = 0
+  float lsum = 0.f;
+  bf16x8 pb[4];
+#pragma unroll
+  for (int r = 0; r < 32; ++r) {
+    const float pr = __builtin_amdgcn_exp2f(x[r] - mm);
+    lsum += pr;
+    pb[r >> 3][r & 7] = f2bf(pr);
+  }
+  st.l += halves_sum(lsum);
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {  // 16-key steps: keys 16 kk + {4g .. 4g+3, 8+4g .. 8+4g+3}
+    const bf16* vb = Vs + 16 * kk * DH;
+#pragma unroll
+    for (int ot = 0; ot < DH / 32; ++ot) {
+      const int vo = st.vofs[ot & 3] + (ot >> 2) * 128;
+      const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(vb + vo));
+      const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(vb + vo + 8 * DH));
+      const bf16x8 vf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      st.o[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[kk], st.o[ot], 0, 0, 0);
+    }
+  }
+  // two transposed reads per MFMA, two MFMAs of reads in flight
+  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+  for (int i = 0; i < 30; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+}
+
+__global__ __launch_bounds__(NT, 1) void attn256_fwd_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(1024))) bf16 smem[2 * 2 * TILE];  // 2 stages x (K, V)
+  const int S = a.S;
+  const int nqb = (S + QPB - 1) / QPB;
+  const int qb = a.causal ? (nqb - 1 - (int)blockIdx.x) : (int)blockIdx.x;  // heavy blocks first
+  const int bh = blockIdx.y, b = bh / a.H, h = bh % a.H;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane >> 5;
+  const int q0 = qb * QPB;
+  const int wq0 = q0 + wave * WQ;
+  const int q = wq0 + (lane & 31);
+  const bf16* Qb = a.q + (long)b * S * a.ldq + (long)h * DH;
+  const bf16* Kb = a.k + (long)b * S * a.ldk + (long)h * DH;
+  const bf16* Vb = a.v + (long)b * S * a.ldv + (long)h * DH;
+
+  FwdState st;
+  {
+    const __amdgpu_buffer_rsrc_t rq = rows_rsrc(Qb, wq0, a.ldq);
+    const int qr = lane & 31;
+    const uint32_t qo = wq0 + qr < S ? (uint32_t)(((long)qr * a.ldq + 8 * g) * 2) : OOB;
+#pragma unroll
+    for (int c = 0; c < DH / 16; ++c)
+      st.qf[c] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rq, qo, 32 * c, 0));
+  }
+#pragma unroll
+  for (int t = 0; t < DH / 32; ++t) st.o[t] = zero16();
+  st.m = -INFINITY;
+  st.l = 0.f;
+  // K fragment of k-step c for key row fr (+32 for the second tile): chunk
+  // 2c + g stored at (2c + g) ^ (fr & 15); k-steps 8..15 sit 16 chunks further.
+  const int fr = lane & 31;
+#pragma unroll
+  for (int c = 0; c < 8; ++c) st.kofs[c] = fr * DH + 8 * ((2 * c + g) ^ swz_row(fr));
+  // V^T operand: lane group G = lane / 16 reads keys 4 (G >> 1) + {0..3} (low
+  // half) and + 8 (high half) of head dims 32 ot + 16 (G & 1) + 0..15; lane
+  // 4e + q addresses key e, dims 4q .. 4q + 3.  ot = 4..7 sit 16 chunks further.
+  const int G = lane >> 4, ll = lane & 15;
+#pragma unroll
+  for (int ot = 0; ot < 4; ++ot) {
+    const int key = 4 * (G >> 1) + (ll >> 2);
+    const int c = 4 * ot + 2 * (G & 1) + ((ll >> 1) & 1);
+    st.vofs[ot] = key * DH + 8 * (c ^ swz_tr(key)) + 4 * (ll & 1);
+  }
+  const float sc = a.scale * LOG2E;
+  const int kv_end = a.causal ? min(S, q0 + QPB) : S;
+  const int nblk = (kv_end + KB - 1) / KB;
+
+  // prologue: block 0 in stage 0
+  copy_block<0>(rows_rsrc(Kb, 0, a.ldk), a.ldk, S, smem, wave);
+  copy_block<1>(rows_rsrc(Vb, 0, a.ldv), a.ldv, S, smem + TILE, wave);
+  wait_vm_lgkm0<0>();
+  cta_barrier();
+
+  for (int j = 0; j < nblk; ++j) {
+    const int kv0 = j * KB;
+    const bf16* Ks = smem + (j & 1) * 2 * TILE;
+    bf16* nxt = smem + ((j + 1) & 1) * 2 * TILE;
+    if (j + 1 < nblk) {
+      copy_block<0>(rows_rsrc(Kb, kv0 + KB, a.ldk), a.ldk, S - kv0 - KB, nxt, wave);
+      copy_block<1>(rows_rsrc(Vb, kv0 + KB, a.ldv), a.ldv, S - kv0 - KB, nxt + TILE, wave);
+    }
+    if (!(a.causal && kv0 > wq0 + WQ - 1)) {
+      fwd_block(st, Ks, Ks + TILE, sc, kv0, q, S, a.causal, g);
+    }
+    if (j + 1 < nblk) {
+      wait_vm_lgkm0<0>();
+      cta_barrier();
+    }
+  }
+  if (q < S) {
+    const float inv = (st.l > 0.f) ? 1.f / st.l : 0.f;
+    bf16* Ob = a.o + ((long)b * S + q) * a.ldo + (long)h * DH;
+#pragma unroll
+    for (int ot = 0; ot < DH / 32; ++ot)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        bf16x4 y;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) y[e] = f2bf(st.o[ot][4 * r4 + e] * inv);
+        *reinterpret_cast<bf16x4*>(Ob + 32 * ot + acc_row(4 * r4, g)) = y;
+      }
+    if (g == 0) a.lse[((long)b * a.H + h) * S + q] = (st.m + log2f(st.l)) * LN2;
+  }
+}
+
+}  // namespace
+
+bool attn256_fwd_eligible(const AttnArgs& a) {
+  auto ok = [](const void* p, long ld) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0 && ld % 8 == 0; };
+  return a.dh == DH && ok(a.q, a.ldq) && ok(a.k, a.ldk) && ok(a.v, a.ldv) &&
+         (reinterpret_cast<uintptr_t>(a.o) & 7) == 0 && a.ldo % 4 == 0 &&
+         (long)KB * a.ldk * 2 < (1L << 30) && (long)KB * a.ldv * 2 < (1L << 30);
+}
+
+hipError_t launch_attn256_fwd(const AttnArgs& a, hipStream_t s) {
+  dim3 grid((a.S + QPB - 1) / QPB, a.B * a.H);
+  hipLaunchKernelGGL(attn256_fwd_kernel, grid, dim3(NT), 0, s, a);
+  return hipGetLastError();
+}

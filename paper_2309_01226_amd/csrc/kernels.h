@@ -89,6 +89,9 @@ struct AttnBwdArgs {
   long lddq, lddk, lddv;
 };
 hipError_t launch_attention_fwd(const AttnArgs& a, hipStream_t s);
+// 256-wide heads (attn256.hip); launch_attention_fwd dispatches to it.
+bool attn256_fwd_eligible(const AttnArgs& a);
+hipError_t launch_attn256_fwd(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attention_bwd(const AttnBwdArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- elementwise
