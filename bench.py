@@ -48,6 +48,9 @@ WORKLOADS = {
     "gpt2m": "GPT-2-medium-shaped fine-tuning step: 24 layers, d_model 1024, 16 heads, MLP 4096, "
              "vocab 50257, seq 512, batch 8",
     "tiny": "tiny GPT-2-style decoder: 2 layers, d_model 64, 4 heads, MLP 256, vocab 512, seq 32, batch 2",
+    "grid": "model-selection grid: 8 GPT-2-medium-shaped decoders (24 layers, d_model 1024, 16 heads, "
+            "MLP 4096, vocab 50257, seq 512), lr {1e-5,3e-5,1e-4,3e-4} x batch {8,16}, bottom 12 blocks "
+            "frozen where (lr index + batch index) is odd, one HIP stream each, one shared seed",
 }
 
 
@@ -155,6 +158,64 @@ def traffic_from_profiles():
         return None
 
 
+def bench_grid(args):
+    """All grid members advance one step per round, each on its own stream;
+    the round is timed from the first enqueue to the last member's end."""
+    import torch
+
+    from paper_2309_01226_amd.configs import grid_members
+    from paper_2309_01226_amd.inputs import decoder_batch
+    from paper_2309_01226_amd.model import Model
+
+    torch.cuda.set_device(0)
+    kws = grid_members()
+    streams = [torch.cuda.Stream() for _ in kws]
+    models = [Model(kw, stream=st) for kw, st in zip(kws, streams)]
+    rows = max(kw["batch"] for kw in kws)
+    K, W = args.steps, args.warmup
+    batches = []
+    for t in range(W + K):
+        per = []
+        for kw in kws:
+            x, y = decoder_batch(kw["batch"], kw["seq_len"], kw["vocab"], seed=args.seed, step=t,
+                                 rows=rows)
+            per.append((torch.as_tensor(x).cuda(), torch.as_tensor(y).cuda()))
+        batches.append(per)
+    torch.cuda.synchronize()
+
+    def round_(t):
+        for m, (x, y) in zip(models, batches[t]):
+            m.train_step(x, y, sync=False)
+
+    for t in range(W):
+        round_(t)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(K):
+        round_(W + t)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    flops = sum(m.stats()[2] for m in models)
+    tokens = sum(kw["batch"] * kw["seq_len"] for kw in kws)
+    losses = [m.eval_loss(*batches[0][i]) for i, m in enumerate(models)]
+    out = {
+        "metric": "model-selection grid training tokens/sec, 8 GPT-2-medium-shaped members, 1 MI355X",
+        "value": tokens * K / dt, "unit": "tokens/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": dt / K * 1e3, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": WORKLOADS["grid"], "name": "grid", "tokens_per_round": tokens,
+                   "members": [{"lr": kw["lr"], "batch": kw["batch"], "frozen_layers": kw["frozen_layers"]}
+                               for kw in kws]},
+        "round_tflop": flops / 1e12,
+        "achieved_tflops": flops / (dt / K) / 1e12,
+        "mfu": flops / (dt / K) / 1e12 / PEAK_BF16_TFLOPS,
+        "loss_after": losses,
+    }
+    for m in models:
+        m.close()
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -168,6 +229,10 @@ def main():
         print("bench.py measures one GPU only: this build has no multi-GPU path; run it with "
               "--gpus 1 (the default).", file=sys.stderr, flush=True)
         sys.exit(2)
+
+    if args.config == "grid":
+        bench_grid(args)
+        return
 
     import torch
 
