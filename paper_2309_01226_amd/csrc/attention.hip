@@ -1224,9 +1224,13 @@ hipError_t bwd_launch(const AttnBwdArgs& a, hipStream_t s) {
     constexpr int D = (DH == 64 || DH == 128 || DH == 256) ? DH : 64;
     constexpr bool PAIR = D == 256;
     constexpr int KPW = PAIR ? WG_ROWS / 2 : WG_ROWS;
-    dim3 gkv((a.f.S + KPW - 1) / KPW, a.f.B * a.f.H);
-    hipLaunchKernelGGL((attn_bwd_dkdv_fast<D, PAIR>), gkv, dim3(NT), 0, s, a);
-    e = hipGetLastError();
+    if (D == 256 && attn256_bwd_eligible(a)) {
+      e = launch_attn256_bwd_dkdv(a, s);
+    } else {
+      dim3 gkv((a.f.S + KPW - 1) / KPW, a.f.B * a.f.H);
+      hipLaunchKernelGGL((attn_bwd_dkdv_fast<D, PAIR>), gkv, dim3(NT), 0, s, a);
+      e = hipGetLastError();
+    }
     if (e != hipSuccess) return e;
     dim3 gq((a.f.S + WG_ROWS - 1) / WG_ROWS, a.f.B * a.f.H);
     hipLaunchKernelGGL((attn_bwd_dq_fast<D>), gq, dim3(NT), 0, s, a);

@@ -49,6 +49,8 @@ __device__ __forceinline__ void wait_vm_lgkm0() {
   static_assert(VM >= 0 && VM < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4));
 }
+// s_waitcnt lgkmcnt(0) only (vector loads may stay in flight)
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xF | (3 << 14) | (7 << 4)); }
 __device__ __forceinline__ void cta_barrier() {
   __builtin_amdgcn_sched_barrier(0);
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
@@ -270,6 +272,204 @@ __global__ __launch_bounds__(NT, 1) void attn256_fwd_kernel(AttnArgs a) {
   }
 }
 
+
+// ================================================================ backward, dK and dV
+// Workgroup = 8 waves = 4 pairs; pair p owns keys k0 + 32 p .. + 31 of one
+// (batch, head) and loops over 32-query blocks.  Wave p (role A) holds K in
+// registers, forms P = exp2(S log2e - lse) from S = Q K^T and accumulates
+// dV^T += dO^T P; wave p + 4 (role B) holds V, forms dP = dO V^T, takes P from
+// its partner through LDS and accumulates dK^T += Q^T dS, dS = P (dP - delta).
+// Every SIMD hosts one wave of each role.  The Q and dO rows of a block are
+// copied HBM -> LDS once and read both as row fragments (S, dP) and, through
+// the transposing LDS read, as Q^T / dO^T (dK, dV); their chunk swizzle
+// c ^ (4 (r & 3) + ((r >> 2) & 3)) keeps both kinds of read free of bank
+// conflicts.  lse (times log2 e) and delta of the block travel with it.
+constexpr int BQ = 32;          // queries per block
+constexpr int KPW = 128;        // keys per workgroup
+constexpr int NT8 = 512;        // 8 waves
+constexpr int QT = BQ * DH;     // bf16 elements of one 32-row tile
+constexpr int STG_B = 2 * QT + 2 * 2 * BQ;  // Q rows, dO rows, lse2[32], delta[32] (fp32 as bf16 pairs)
+
+__device__ __forceinline__ int swz_dual(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+
+// 32 rows of 512 bytes: 16 copy instructions, two per wave of eight.
+__device__ __forceinline__ void copy_rows32(__amdgpu_buffer_rsrc_t rs, long ld, int nvalid, bf16* dst,
+                                            int wave) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int j = 8 * i + wave;
+    const int row = 2 * j + (lane >> 5);
+    const int c = (lane & 31) ^ swz_dual(row);
+    const uint32_t o = row < nvalid ? (uint32_t)(((long)row * ld + 8 * c) * 2) : OOB;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds(dst + j * 512), 16, o, 0, 0, 0);
+  }
+}
+
+// Row fragment (A operand, rows = tile rows, k = dims 16 c + 8 g .. + 7) of
+// row r of a dual-swizzled tile.
+__device__ __forceinline__ bf16x8 row_frag(const bf16* tile, int r, int c, int g) {
+  return *reinterpret_cast<const bf16x8*>(tile + r * DH + 8 * ((2 * c + g) ^ swz_dual(r)));
+}
+
+__global__ __launch_bounds__(NT8, 1) void attn256_bwd_dkdv_kernel(AttnBwdArgs a) {
+  __shared__ __attribute__((aligned(1024))) bf16 smem[2 * STG_B + 4 * 64 * 16 * 2];
+  float* xbuf = reinterpret_cast<float*>(smem + 2 * STG_B);  // P exchange: [pair][16][64 lanes]
+  const int S = a.f.S;
+  const int bh = blockIdx.y, b = bh / a.f.H, h = bh % a.f.H;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane >> 5;
+  const int pair = wave & 3, role = wave >> 2;
+  const int k0 = blockIdx.x * KPW;
+  const int kmin = k0 + pair * 32;
+  const int key = kmin + (lane & 31);
+  const long hs = ((long)b * a.f.H + h) * S;
+  const bf16* Qb = a.f.q + (long)b * S * a.f.ldq + (long)h * DH;
+  const bf16* Kb = a.f.k + (long)b * S * a.f.ldk + (long)h * DH;
+  const bf16* Vb = a.f.v + (long)b * S * a.f.ldv + (long)h * DH;
+  const bf16* dOb = a.dout + (long)b * S * a.lddo + (long)h * DH;
+  const float sc = a.f.scale * LOG2E;
+
+  // resident operand: K (role A) or V (role B) of this lane's key, dims 16 c + 8 g .. + 7
+  bf16x8 rf[DH / 16];
+  {
+    const bf16* base = role ? Vb : Kb;
+    const long ld = role ? a.f.ldv : a.f.ldk;
+    const __amdgpu_buffer_rsrc_t rk = rows_rsrc(base, kmin, ld);
+    const uint32_t ko = key < S ? (uint32_t)(((long)(lane & 31) * ld + 8 * g) * 2) : OOB;
+#pragma unroll
+    for (int c = 0; c < DH / 16; ++c)
+      rf[c] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, ko, 32 * c, 0));
+  }
+  floatx16 acc[DH / 32];  // dV^T (role A) or dK^T (role B): dims 32 ot + acc_row(r, g), key = lane
+#pragma unroll
+  for (int t = 0; t < DH / 32; ++t) acc[t] = zero16();
+  // transposed reads of a 32-row tile (Q^T or dO^T): lane group G reads rows
+  // 4 (G >> 1) + 8 hsel + {0..3} (+ 16 hh), dims 32 ot + 16 (G & 1) + 0..15
+  const int G = lane >> 4, ll = lane & 15;
+  int tofs[4];
+#pragma unroll
+  for (int ot = 0; ot < 4; ++ot) {
+    const int r = 4 * (G >> 1) + (ll >> 2);
+    const int c = 4 * ot + 2 * (G & 1) + ((ll >> 1) & 1);
+    tofs[ot] = r * DH + 8 * (c ^ swz_dual(r)) + 4 * (ll & 1);
+  }
+
+  const int q_start = a.f.causal ? k0 : 0;
+  const int nqb = (S - q_start + BQ - 1) / BQ;
+  float* xw = xbuf + pair * 16 * 64;
+  float lsd = 0.f;  // wave 0: lse2 (lanes 0..31) or delta (lanes 32..63) of the next block
+
+  auto stage_ptr = [&](int j) { return smem + (j & 1) * STG_B; };
+  auto fetch = [&](int j) {  // copies of block j; wave 0 also loads its lse / delta
+    const int qs = q_start + j * BQ;
+    bf16* st = stage_ptr(j);
+    copy_rows32(rows_rsrc(Qb, qs, a.f.ldq), a.f.ldq, S - qs, st, wave);
+    copy_rows32(rows_rsrc(dOb, qs, a.lddo), a.lddo, S - qs, st + QT, wave);
+    if (wave == 0) {
+      const int qi = qs + (lane & 31);
+      lsd = qi < S ? (g ? a.delta[hs + qi] : a.f.lse[hs + qi] * LOG2E) : 0.f;
+    }
+  };
+  auto publish = [&](int j) {  // wave 0 stores lse / delta of block j (after its loads landed)
+    if (wave == 0) reinterpret_cast<float*>(stage_ptr(j) + 2 * QT)[lane] = lsd;
+  };
+
+  fetch(0);
+  wait_vm_lgkm0<0>();
+  publish(0);
+  wait_vm_lgkm0<0>();
+  cta_barrier();
+
+  for (int j = 0; j < nqb; ++j) {
+    const int qs0 = q_start + j * BQ;
+    const bf16* st = stage_ptr(j);
+    const bf16* Qs = st;
+    const bf16* dOs = st + QT;
+    const float* lsd_s = reinterpret_cast<const float*>(st + 2 * QT);
+    if (j + 1 < nqb) fetch(j + 1);
+    const bool active = !(a.f.causal && qs0 + BQ - 1 < kmin);
+    // S = Q K^T (role A) or dP = dO V^T (role B): rows = queries, column = key
+    floatx16 x = zero16();
+    if (active) {
+      const bf16* rows = role ? dOs : Qs;
+#pragma unroll
+      for (int c = 0; c < DH / 16; ++c)
+        x = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(rows, lane & 31, c, g), rf[c], x, 0, 0, 0);
+      if (role == 0) {
+        // P = exp2(S log2e - lse2); zero for queries past S and (causal) keys past the query
+        const int lim_q = S - qs0 - 4 * g;            // rows r with acc_row < lim_q are valid
+        const int lim_k = key - qs0 - 4 * g;          // causal: need acc_row >= key - qs0
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const floatx4 l4 = *reinterpret_cast<const floatx4*>(lsd_s + 8 * i + 4 * g);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int rr = 8 * i + e;  // acc_row - 4 g
+            float pr = __builtin_amdgcn_exp2f(x[4 * i + e] * sc - l4[e]);
+            const bool ok = (rr < lim_q) & ((a.f.causal == 0) | (rr >= lim_k));
+            pr = ok ? pr : 0.f;
+            x[4 * i + e] = pr;
+            xw[(4 * i + e) * 64 + lane] = pr;
+          }
+        }
+      }
+    }
+    wait_lgkm0();
+    cta_barrier();  // P of every pair visible
+    if (active) {
+      if (role == 1) {
+        // dS = P (dP - delta)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const floatx4 d4 = *reinterpret_cast<const floatx4*>(lsd_s + BQ + 8 * i + 4 * g);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) x[4 * i + e] = xw[(4 * i + e) * 64 + lane] * (x[4 * i + e] - d4[e]);
+        }
+      }
+      // dV^T += dO^T P (role A) or dK^T += Q^T dS (role B)
+      const bf16* tt = role ? Qs : dOs;
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        bf16x8 xb;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) xb[e] = f2bf(x[8 * hh + e]);
+        const bf16* tb = tt + 16 * hh * DH;
+#pragma unroll
+        for (int ot = 0; ot < DH / 32; ++ot) {
+          // rows + 8 flip bit 1 of the row's swizzle group, i.e. chunk bit 1
+          const int to = tofs[ot & 3] + (ot >> 2) * 128;
+          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(tb + to));
+          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(tb + ((to ^ 16) + 8 * DH)));
+          acc[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7),
+                                                            xb, acc[ot], 0, 0, 0);
+        }
+      }
+    }
+    if (j + 1 < nqb) {
+      wait_vm_lgkm0<0>();
+      publish(j + 1);
+      wait_vm_lgkm0<0>();
+      cta_barrier();
+    }
+  }
+  if (key < S) {
+    bf16* out = role ? a.dk + ((long)b * S + key) * a.lddk + (long)h * DH
+                     : a.dv + ((long)b * S + key) * a.lddv + (long)h * DH;
+    const float f = role ? a.f.scale : 1.f;
+#pragma unroll
+    for (int ot = 0; ot < DH / 32; ++ot)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        bf16x4 y;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) y[e] = f2bf(acc[ot][4 * r4 + e] * f);
+        *reinterpret_cast<bf16x4*>(out + 32 * ot + acc_row(4 * r4, g)) = y;
+      }
+  }
+}
+
 }  // namespace
 
 bool attn256_fwd_eligible(const AttnArgs& a) {
@@ -277,6 +477,20 @@ bool attn256_fwd_eligible(const AttnArgs& a) {
   return a.dh == DH && ok(a.q, a.ldq) && ok(a.k, a.ldk) && ok(a.v, a.ldv) &&
          (reinterpret_cast<uintptr_t>(a.o) & 7) == 0 && a.ldo % 4 == 0 &&
          (long)KB * a.ldk * 2 < (1L << 30) && (long)KB * a.ldv * 2 < (1L << 30);
+}
+
+bool attn256_bwd_eligible(const AttnBwdArgs& a) {
+  auto ok = [](const void* p, long ld) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0 && ld % 8 == 0; };
+  auto ok8 = [](const void* p, long ld) { return (reinterpret_cast<uintptr_t>(p) & 7) == 0 && ld % 4 == 0; };
+  return attn256_fwd_eligible(a.f) && ok(a.dout, a.lddo) && ok8(a.dk, a.lddk) && ok8(a.dv, a.lddv) &&
+         (long)KPW * a.f.ldk * 2 < (1L << 30) && (long)KPW * a.f.ldv * 2 < (1L << 30) &&
+         (long)BQ * a.f.ldq * 2 < (1L << 30) && (long)BQ * a.lddo * 2 < (1L << 30);
+}
+
+hipError_t launch_attn256_bwd_dkdv(const AttnBwdArgs& a, hipStream_t s) {
+  dim3 grid((a.f.S + KPW - 1) / KPW, a.f.B * a.f.H);
+  hipLaunchKernelGGL(attn256_bwd_dkdv_kernel, grid, dim3(NT8), 0, s, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_attn256_fwd(const AttnArgs& a, hipStream_t s) {
