@@ -1232,6 +1232,7 @@ hipError_t bwd_launch(const AttnBwdArgs& a, hipStream_t s) {
       e = hipGetLastError();
     }
     if (e != hipSuccess) return e;
+    if (D == 256 && attn256_bwd_eligible(a)) return launch_attn256_bwd_dq(a, s);
     dim3 gq((a.f.S + WG_ROWS - 1) / WG_ROWS, a.f.B * a.f.H);
     hipLaunchKernelGGL((attn_bwd_dq_fast<D>), gq, dim3(NT), 0, s, a);
     return hipGetLastError();

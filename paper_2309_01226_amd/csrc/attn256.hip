@@ -470,6 +470,141 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dkdv_kernel(AttnBwdArgs a)
   }
 }
 
+
+// ================================================================ backward, dQ
+// Workgroup = 8 waves = 4 pairs; pair p owns queries q0 + 32 p .. + 31 of one
+// (batch, head) and loops over 32-key blocks.  Wave p (role A) holds Q and
+// forms P^T = exp2(S^T log2e - lse) from S^T = K Q^T; wave p + 4 (role B) holds
+// dO, forms dP^T = V dO^T, takes P^T from its partner through LDS and
+// accumulates dQ^T += K^T dS^T, dS^T = P^T (dP^T - delta).  Lanes own queries,
+// so lse and delta are per-lane scalars.  K rows are read as row fragments and
+// transposed (K^T) from the same dual-swizzled tile.
+constexpr int QPW = 128;   // queries per workgroup
+constexpr int STG_Q = 2 * QT;  // K rows, V rows of a 32-key block
+
+__global__ __launch_bounds__(NT8, 1) void attn256_bwd_dq_kernel(AttnBwdArgs a) {
+  __shared__ __attribute__((aligned(1024))) bf16 smem[2 * STG_Q + 4 * 64 * 16 * 2];
+  float* xbuf = reinterpret_cast<float*>(smem + 2 * STG_Q);
+  const int S = a.f.S;
+  const int nqb = (S + QPW - 1) / QPW;
+  const int qb = a.f.causal ? (nqb - 1 - (int)blockIdx.x) : (int)blockIdx.x;  // heavy blocks first
+  const int bh = blockIdx.y, b = bh / a.f.H, h = bh % a.f.H;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane >> 5;
+  const int pair = wave & 3, role = wave >> 2;
+  const int q0 = qb * QPW;
+  const int pq0 = q0 + pair * 32;
+  const int q = pq0 + (lane & 31);
+  const long hs = ((long)b * a.f.H + h) * S;
+  const bf16* Qb = a.f.q + (long)b * S * a.f.ldq + (long)h * DH;
+  const bf16* Kb = a.f.k + (long)b * S * a.f.ldk + (long)h * DH;
+  const bf16* Vb = a.f.v + (long)b * S * a.f.ldv + (long)h * DH;
+  const bf16* dOb = a.dout + (long)b * S * a.lddo + (long)h * DH;
+  const float sc = a.f.scale * LOG2E;
+
+  bf16x8 rf[DH / 16];  // Q (role A) or dO (role B) of this lane's query
+  {
+    const bf16* base = role ? dOb : Qb;
+    const long ld = role ? a.lddo : a.f.ldq;
+    const __amdgpu_buffer_rsrc_t rq = rows_rsrc(base, pq0, ld);
+    const uint32_t qo = q < S ? (uint32_t)(((long)(lane & 31) * ld + 8 * g) * 2) : OOB;
+#pragma unroll
+    for (int c = 0; c < DH / 16; ++c)
+      rf[c] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rq, qo, 32 * c, 0));
+  }
+  const float lsd = q < S ? (role ? a.delta[hs + q] : a.f.lse[hs + q] * LOG2E) : 0.f;
+  floatx16 acc[DH / 32];  // dQ^T (role B): dims 32 ot + acc_row(r, g), query = lane
+#pragma unroll
+  for (int t = 0; t < DH / 32; ++t) acc[t] = zero16();
+  const int G = lane >> 4, ll = lane & 15;
+  int tofs[4];
+#pragma unroll
+  for (int ot = 0; ot < 4; ++ot) {
+    const int r = 4 * (G >> 1) + (ll >> 2);
+    const int c = 4 * ot + 2 * (G & 1) + ((ll >> 1) & 1);
+    tofs[ot] = r * DH + 8 * (c ^ swz_dual(r)) + 4 * (ll & 1);
+  }
+
+  const int kv_end = a.f.causal ? min(S, q0 + QPW) : S;
+  const int nkb = (kv_end + BQ - 1) / BQ;
+  float* xw = xbuf + pair * 16 * 64;
+  auto stage_ptr = [&](int j) { return smem + (j & 1) * STG_Q; };
+  auto fetch = [&](int j) {
+    const int kv = j * BQ;
+    bf16* st = stage_ptr(j);
+    copy_rows32(rows_rsrc(Kb, kv, a.f.ldk), a.f.ldk, S - kv, st, wave);
+    copy_rows32(rows_rsrc(Vb, kv, a.f.ldv), a.f.ldv, S - kv, st + QT, wave);
+  };
+
+  fetch(0);
+  wait_vm_lgkm0<0>();
+  cta_barrier();
+
+  for (int j = 0; j < nkb; ++j) {
+    const int kv0 = j * BQ;
+    const bf16* Ks = stage_ptr(j);
+    const bf16* Vs = Ks + QT;
+    if (j + 1 < nkb) fetch(j + 1);
+    const bool active = !(a.f.causal && kv0 > pq0 + 31);
+    floatx16 x = zero16();
+    if (active) {
+      const bf16* rows = role ? Vs : Ks;
+#pragma unroll
+      for (int c = 0; c < DH / 16; ++c)
+        x = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(rows, lane & 31, c, g), rf[c], x, 0, 0, 0);
+      if (role == 0) {
+        // P^T = exp2(S^T log2e - lse2); zero for keys past S or (causal) past the query
+        const int lim = min(S, a.f.causal ? q + 1 : S) - kv0 - 4 * g;  // keys with acc_row < lim valid
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int kr = 8 * (r >> 2) + (r & 3);  // acc_row - 4 g
+          float pr = __builtin_amdgcn_exp2f(x[r] * sc - lsd);
+          pr = kr < lim ? pr : 0.f;
+          xw[r * 64 + lane] = pr;
+        }
+      }
+    }
+    wait_lgkm0();
+    cta_barrier();  // P^T of every pair visible
+    if (active && role == 1) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) x[r] = xw[r * 64 + lane] * (x[r] - lsd);
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        bf16x8 xb;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) xb[e] = f2bf(x[8 * hh + e]);
+        const bf16* tb = Ks + 16 * hh * DH;
+#pragma unroll
+        for (int ot = 0; ot < DH / 32; ++ot) {
+          const int to = tofs[ot & 3] + (ot >> 2) * 128;
+          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(tb + to));
+          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(tb + ((to ^ 16) + 8 * DH)));
+          acc[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7),
+                                                            xb, acc[ot], 0, 0, 0);
+        }
+      }
+    }
+    if (j + 1 < nkb) {
+      wait_vm_lgkm0<0>();
+      cta_barrier();
+    }
+  }
+  if (role == 1 && q < S) {
+    bf16* out = a.dq + ((long)b * S + q) * a.lddq + (long)h * DH;
+#pragma unroll
+    for (int ot = 0; ot < DH / 32; ++ot)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        bf16x4 y;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) y[e] = f2bf(acc[ot][4 * r4 + e] * a.f.scale);
+        *reinterpret_cast<bf16x4*>(out + 32 * ot + acc_row(4 * r4, g)) = y;
+      }
+  }
+}
+
 }  // namespace
 
 bool attn256_fwd_eligible(const AttnArgs& a) {
@@ -484,12 +619,19 @@ bool attn256_bwd_eligible(const AttnBwdArgs& a) {
   auto ok8 = [](const void* p, long ld) { return (reinterpret_cast<uintptr_t>(p) & 7) == 0 && ld % 4 == 0; };
   return attn256_fwd_eligible(a.f) && ok(a.dout, a.lddo) && ok8(a.dk, a.lddk) && ok8(a.dv, a.lddv) &&
          (long)KPW * a.f.ldk * 2 < (1L << 30) && (long)KPW * a.f.ldv * 2 < (1L << 30) &&
-         (long)BQ * a.f.ldq * 2 < (1L << 30) && (long)BQ * a.lddo * 2 < (1L << 30);
+         (long)QPW * a.f.ldq * 2 < (1L << 30) && (long)QPW * a.lddo * 2 < (1L << 30) &&
+         (reinterpret_cast<uintptr_t>(a.dq) & 7) == 0 && a.lddq % 4 == 0;
 }
 
 hipError_t launch_attn256_bwd_dkdv(const AttnBwdArgs& a, hipStream_t s) {
   dim3 grid((a.f.S + KPW - 1) / KPW, a.f.B * a.f.H);
   hipLaunchKernelGGL(attn256_bwd_dkdv_kernel, grid, dim3(NT8), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn256_bwd_dq(const AttnBwdArgs& a, hipStream_t s) {
+  dim3 grid((a.f.S + QPW - 1) / QPW, a.f.B * a.f.H);
+  hipLaunchKernelGGL(attn256_bwd_dq_kernel, grid, dim3(NT8), 0, s, a);
   return hipGetLastError();
 }
 

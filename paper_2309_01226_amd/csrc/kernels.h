@@ -93,10 +93,11 @@ hipError_t launch_attention_fwd(const AttnArgs& a, hipStream_t s);
 bool attn256_fwd_eligible(const AttnArgs& a);
 hipError_t launch_attn256_fwd(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attention_bwd(const AttnBwdArgs& a, hipStream_t s);
-// 256-wide heads (attn256.hip): the dK / dV kernel; launch_attention_bwd
-// dispatches to it after computing delta.
+// 256-wide heads (attn256.hip): the dK / dV and dQ kernels; launch_attention_bwd
+// dispatches to them after computing delta.
 bool attn256_bwd_eligible(const AttnBwdArgs& a);
 hipError_t launch_attn256_bwd_dkdv(const AttnBwdArgs& a, hipStream_t s);
+hipError_t launch_attn256_bwd_dq(const AttnBwdArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- elementwise
 // GPT-J rotary on interleaved pairs of the first rd dims of every q and k head,
