@@ -38,9 +38,12 @@ __device__ __forceinline__ double wave_sum_d(double v) {
 }
 
 // GELU, tanh approximation and exact erf form, and their derivatives.
-// tanh(y) is evaluated as 1 - 2 / (exp(2y) + 1), which saturates correctly at
+// tanh(y) is evaluated as 1 - 2 / (exp(2y) + 1) with the hardware base-2
+// exponential and reciprocal (about 1 ulp each), which saturates correctly at
 // both ends (exp overflow gives 1, underflow gives -1).
-__device__ __forceinline__ float tanh_fast(float y) { return 1.f - 2.f / (__expf(2.f * y) + 1.f); }
+__device__ __forceinline__ float tanh_fast(float y) {
+  return 1.f - 2.f * __builtin_amdgcn_rcpf(__builtin_amdgcn_exp2f(2.8853900817779268f * y) + 1.f);
+}
 __device__ __forceinline__ float gelu_tanh_f(float x) {
   const float c = 0.7978845608028654f, a = 0.044715f;
   float t = tanh_fast(c * (x + a * x * x * x));

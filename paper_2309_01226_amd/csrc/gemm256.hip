@@ -250,22 +250,70 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, floatx16 (&acc)[4][4
     for (int e = 0; e < 4; ++e)
       if (col + e < p.N && col + e >= p.bias_col0) bias[e] = p.bias[col + e - p.bias_col0];
   }
+  // Tiles wholly inside C (all but the ragged edge) take a branch-free path
+  // whose residual / pre-activation loads for a slab are all issued before the
+  // slab is staged, so their latency overlaps the LDS traffic.
+  const bool interior = m0 + BT <= p.M && n0 + BT <= p.N;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        st[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * EP + 32 * j + (lane & 31)] = acc[i][j][r];
     const long rowbase = m0 + wm * 128 + 32 * i;
-    // fully unrolled only for the plain epilogues: the GELU forms would need
-    // more VGPRs than the AGPR-held accumulators leave free
-#pragma unroll(EPI == EPI_F32 || EPI == EPI_RESID_F32 ? 16 : 2)
-    for (int s = 0; s < 16; ++s) {
-      const int rl = 2 * s + (lane >> 5);
-      const long row = rowbase + rl;
-      floatx4 x = *reinterpret_cast<const floatx4*>(st + rl * EP + cl) + bias;
-      if (row < p.M) store4<EPI, GE>(p, row, col, x);
+    if (interior) {
+      floatx4 rv[16];
+      bf16x4 uv[16];
+      if (EPI == EPI_RESID_F32) {
+#pragma unroll
+        for (int s = 0; s < 16; ++s)
+          rv[s] = *reinterpret_cast<const floatx4*>(p.resid + (rowbase + 2 * s + (lane >> 5)) * p.ldr + col);
+      }
+      if (EPI == EPI_DGELU_BF16) {
+#pragma unroll
+        for (int s = 0; s < 16; ++s)
+          uv[s] = *reinterpret_cast<const bf16x4*>(p.aux + (rowbase + 2 * s + (lane >> 5)) * p.ldaux + col);
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          st[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * EP + 32 * j + (lane & 31)] = acc[i][j][r];
+      const bool gel = EPI == EPI_BF16 && p.out2 != nullptr && col >= p.gelu_col0;
+#pragma unroll(EPI == EPI_BF16 ? 4 : 16)
+      for (int s = 0; s < 16; ++s) {
+        const int rl = 2 * s + (lane >> 5);
+        const long row = rowbase + rl;
+        const floatx4 x = *reinterpret_cast<const floatx4*>(st + rl * EP + cl) + bias;
+        const long o = row * p.ldo + col;
+        if (EPI == EPI_F32) {
+          *reinterpret_cast<floatx4*>(reinterpret_cast<float*>(p.out) + o) = x;
+        } else if (EPI == EPI_RESID_F32) {
+          *reinterpret_cast<floatx4*>(reinterpret_cast<float*>(p.out) + o) = x + rv[s];
+        } else if (EPI == EPI_BF16) {
+          bf16x4 y = {f2bf(x[0]), f2bf(x[1]), f2bf(x[2]), f2bf(x[3])};
+          *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(p.out) + o) = y;
+          if (gel) {
+            bf16x4 gv = {f2bf(gelu_t<GE>(x[0])), f2bf(gelu_t<GE>(x[1])), f2bf(gelu_t<GE>(x[2])),
+                         f2bf(gelu_t<GE>(x[3]))};
+            *reinterpret_cast<bf16x4*>(p.out2 + row * p.ldo2 + (col - p.gelu_col0)) = gv;
+          }
+        } else {
+          bf16x4 y;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) y[e] = f2bf(x[e] * gelu_grad_t<GE>(bf2f(uv[s][e])));
+          *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(p.out) + o) = y;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          st[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * EP + 32 * j + (lane & 31)] = acc[i][j][r];
+#pragma unroll 2
+      for (int s = 0; s < 16; ++s) {
+        const int rl = 2 * s + (lane >> 5);
+        const long row = rowbase + rl;
+        floatx4 x = *reinterpret_cast<const floatx4*>(st + rl * EP + cl) + bias;
+        if (row < p.M) store4<EPI, GE>(p, row, col, x);
+      }
     }
   }
 }
