@@ -14,12 +14,14 @@ Reported beside the throughput:
                 stream around each of its launches inside the timed region;
                 achieved = algorithmic FLOPs per launch / mean launch time.
                 traffic = HBM bytes per launch from rocprofv3 FETCH_SIZE /
-                WRITE_SIZE counters, read from profiles/ when they were taken
-                on the current GEMM source (else null).
+                WRITE_SIZE counters scaled by the same counters of a 1 GiB
+                device copy (bench.py --copy-calibration), read from
+                profiles/ when they were taken on the current GEMM source
+                (else null).
   cpu_baseline  the float64 oracle timed on this host on a bounded sample
-                (one GPT-J-shaped block plus embedding and head, batch 1, 512
-                tokens; AdamW over that block's tensors), scaled to the full
-                step by algorithmic FLOPs (forward + backward) and by
+                (one GPT-J-shaped block plus embedding and head, one sequence
+                of 2048 tokens; AdamW over that block's tensors), scaled to the
+                full step by algorithmic FLOPs (forward + backward) and by
                 parameter count (AdamW).
 """
 
@@ -100,7 +102,7 @@ def cpu_baseline(kw, seed):
     if kw["arch"] == "vit":
         sample["batch"] = 4
     else:
-        sample.update(batch=1, seq_len=min(512, kw["seq_len"]))
+        sample.update(batch=1)
     fields = oracle.Config.__dataclass_fields__
     cfg = oracle.Config(**{k: v for k, v in sample.items() if k in fields})
     rng = np.random.default_rng(seed)
@@ -145,17 +147,33 @@ def cpu_baseline(kw, seed):
 
 def traffic_from_profiles():
     """HBM bytes per launch of the dominant GEMM from the committed counter
-    summary, if it was taken on the current GEMM source."""
-    path = os.path.join(ROOT, "profiles", "gemm_qkv_fc1_fwd_gptj_counters.json")
-    src = os.path.join(ROOT, "paper_2309_01226_amd", "csrc", "gemm.hip")
+    summary, if it was taken on the current GEMM source (else None)."""
+    path = os.path.join(ROOT, "profiles", "gemm_qkv_fc1_fwd_gptj_traffic.txt")
+    src = os.path.join(ROOT, "paper_2309_01226_amd", "csrc", "gemm256.hip")
     try:
-        rec = json.load(open(path))
+        rec = {}
+        for line in open(path):
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                rec[k.strip()] = v.strip()
         cur = hashlib.sha256(open(src, "rb").read()).hexdigest()
         if rec.get("gemm_source_sha256") != cur:
             return None
-        return rec.get("hbm_bytes_per_launch")
+        return float(rec["hbm_bytes_per_launch"])
     except Exception:
         return None
+
+
+def copy_calibration(nbytes=1 << 30, reps=3):
+    """A plain device copy of known size, for scaling the FETCH_SIZE /
+    WRITE_SIZE counters of other kernels (run under rocprofv3 --pmc)."""
+    import torch
+    x = torch.ones(nbytes // 4, device="cuda", dtype=torch.float32)
+    y = torch.empty_like(x)
+    for _ in range(reps):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": nbytes, "reps": reps}), flush=True)
 
 
 def bench_grid(args):
@@ -224,7 +242,12 @@ def main():
     ap.add_argument("--config", default="gptj", choices=sorted(WORKLOADS))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 1 GiB device copy (counter calibration) and exit")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration()
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path; run it with "
               "--gpus 1 (the default).", file=sys.stderr, flush=True)
