@@ -237,6 +237,73 @@ __device__ __forceinline__ void store4(const GemmArgs& p, long row, int col, flo
   }
 }
 
+// bf16 epilogues of interior tiles with 16-byte aligned rows: each lane
+// stores 8 consecutive columns (one 16-byte store per output, half the store
+// instructions of the 4-column layout).  Same per-wave LDS slab staging.
+template <int EPI, int GE>
+__device__ __forceinline__ void epilogue_bf16_wide(const GemmArgs& p, floatx16 (&acc)[4][4],
+                                                   float* st, int m0, int n0, int wave, int lane) {
+  const int wm = wave >> 1, wn = wave & 1;
+  const int cl = 8 * (lane & 15);
+  const int col = n0 + wn * 128 + cl;
+  floatx4 b0 = {0.f, 0.f, 0.f, 0.f}, b1 = {0.f, 0.f, 0.f, 0.f};
+  if (p.bias != nullptr) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (col + e >= p.bias_col0) b0[e] = p.bias[col + e - p.bias_col0];
+      if (col + 4 + e >= p.bias_col0) b1[e] = p.bias[col + 4 + e - p.bias_col0];
+    }
+  }
+  const bool gel = EPI == EPI_BF16 && p.out2 != nullptr && col >= p.gelu_col0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const long rowbase = m0 + wm * 128 + 32 * i;
+    bf16x8 uv[8];
+    if (EPI == EPI_DGELU_BF16) {
+#pragma unroll
+      for (int s = 0; s < 8; ++s)
+        uv[s] = *reinterpret_cast<const bf16x8*>(p.aux + (rowbase + 4 * s + (lane >> 4)) * p.ldaux + col);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        st[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * EP + 32 * j + (lane & 31)] = acc[i][j][r];
+#pragma unroll(EPI == EPI_BF16 ? 2 : 8)
+    for (int s = 0; s < 8; ++s) {
+      const int rl = 4 * s + (lane >> 4);
+      const long row = rowbase + rl;
+      const floatx4 x0 = *reinterpret_cast<const floatx4*>(st + rl * EP + cl) + b0;
+      const floatx4 x1 = *reinterpret_cast<const floatx4*>(st + rl * EP + cl + 4) + b1;
+      bf16x8 y;
+      if (EPI == EPI_BF16) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          y[e] = f2bf(x0[e]);
+          y[4 + e] = f2bf(x1[e]);
+        }
+        *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(p.out) + row * p.ldo + col) = y;
+        if (gel) {
+          bf16x8 gv;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            gv[e] = f2bf(gelu_t<GE>(x0[e]));
+            gv[4 + e] = f2bf(gelu_t<GE>(x1[e]));
+          }
+          *reinterpret_cast<bf16x8*>(p.out2 + row * p.ldo2 + (col - p.gelu_col0)) = gv;
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          y[e] = f2bf(x0[e] * gelu_grad_t<GE>(bf2f(uv[s][e])));
+          y[4 + e] = f2bf(x1[e] * gelu_grad_t<GE>(bf2f(uv[s][4 + e])));
+        }
+        *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(p.out) + row * p.ldo + col) = y;
+      }
+    }
+  }
+}
+
 template <int EPI, int GE>
 __device__ __forceinline__ void epilogue(const GemmArgs& p, floatx16 (&acc)[4][4], float* stage,
                                          int m0, int n0, int wave, int lane) {
@@ -254,6 +321,17 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, floatx16 (&acc)[4][4
   // whose residual / pre-activation loads for a slab are all issued before the
   // slab is staged, so their latency overlaps the LDS traffic.
   const bool interior = m0 + BT <= p.M && n0 + BT <= p.N;
+  if (EPI == EPI_BF16 || EPI == EPI_DGELU_BF16) {
+    auto a16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
+    const bool wide = interior && a16(p.out) && p.ldo % 8 == 0 &&
+                      (EPI == EPI_BF16 ? (p.out2 == nullptr || (a16(p.out2) && p.ldo2 % 8 == 0 &&
+                                                                p.gelu_col0 % 8 == 0))
+                                       : (a16(p.aux) && p.ldaux % 8 == 0));
+    if (wide) {
+      epilogue_bf16_wide<EPI, GE>(p, acc, st, m0, n0, wave, lane);
+      return;
+    }
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const long rowbase = m0 + wm * 128 + 32 * i;
