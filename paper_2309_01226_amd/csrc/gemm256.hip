@@ -1,19 +1,28 @@
 // bf16 MFMA GEMM for large, aligned problems: 256 x 256 output tiles,
-// K-tiles of 64, two LDS stages.
+// K-tiles of 64.
 //
 //   C[m, n] = sum_k A(m, k) B(n, k), bf16 operands, fp32 accumulation, with
 //   the same fused epilogues as the general kernel in gemm.hip.
 //
 // What bounds it on MI355X (measured with single-purpose variants of this
-// kernel): the L2 -> LDS copy stream, not the matrix cores.  One 256 x 256
-// tile needs 32 bytes per clock per CU at full MFMA rate, and a CU's copy
-// throughput is set by the number of 128-byte cache lines it requests, not by
-// bytes: rows copied in 64-byte pieces (K-tiles of 32) deliver about half of
-// what full-line pieces do.  So K-tiles are 64 deep (a K-contiguous row of the
-// tile is exactly one line), which leaves room for two stages in the 160 KB of
-// LDS; the copies of tile k + 2 are issued as soon as every wave has finished
-// reading tile k.  (A four-stage, 32-deep variant of the same loop is kept
-// selectable at compile time: it hides more latency but is line-bound.)
+// kernel): the L2 -> LDS copy stream and, with an M/N-contiguous operand, the
+// LDS, not the matrix cores.  One 256 x 256 tile needs 32 bytes per clock per
+// CU at full MFMA rate, and a CU's copy throughput is set by the number of
+// 128-byte cache lines it requests, not by bytes: rows copied in 64-byte
+// pieces (K-tiles of 32) deliver about half of what full-line pieces do.  So
+// K-tiles are 64 deep (a K-contiguous row of the tile is exactly one line),
+// 64 KB per K-tile, and the 160 KB of LDS holds two and a half of them.
+//
+// Two schedules share the loop:
+//  * two stages (used when an operand is M/N-contiguous): the copies of tile
+//    k + 2 are issued as soon as every wave has finished reading tile k, all
+//    in the last k-step;
+//  * a ring of five single-operand slots (both operands K-contiguous): A of
+//    tile k + 2 is copied during the first k-steps of tile k, B of tile k + 2
+//    after the barrier.  Issuing all sixteen copies of a wave in one k-step
+//    fills the address unit's queue and stalls the MFMAs behind them in the
+//    in-order instruction stream (counter SQ_VMEM_TA_ADDR_FIFO_FULL); spread
+//    over the loop they cost about 10% less time on long-K problems.
 //
 // Layout of one stage: the A tile, then the B tile.
 //  * K-contiguous operand (rows = m or n): [256 rows][64 k], 128 B per row;
@@ -35,8 +44,9 @@
 // 4 x 4 MFMA 32x32x16 accumulators in AGPRs): the MFMAs of each k-step are
 // interleaved with the fragment reads of the next; before the last k-step,
 // wait for this wave's copies of the next tile and for its reads; barrier;
-// copies of tile k + 2 into the stage just released and the fragment reads of
-// the next tile's first k-step, interleaved with the last k-step's MFMAs.
+// the copies due after the barrier (all of tile k + 2, or its B) and the
+// fragment reads of the next tile's first k-step, interleaved with the last
+// k-step's MFMAs.
 //
 // Epilogue: each wave stages one 32-row slab of its sub-tile in its own LDS
 // region and stores 4 consecutive columns per lane (16-byte fp32 or 8-byte
@@ -110,11 +120,12 @@ struct Loader {
       }
     }
   }
+  template <int I0 = 0, int I1 = NI>
   __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, int k0, int K, long ld,
                                         bf16* dst, int wave) const {
     const uint32_t soff = LAY == LAY_K ? (uint32_t)(k0 * 2) : (uint32_t)((long)k0 * ld * 2);
 #pragma unroll
-    for (int i = 0; i < NI; ++i) {
+    for (int i = I0; i < I1; ++i) {
       const uint32_t o = (k0 + kof[i] < K) ? off[i] : OOB;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds(dst + (4 * i + wave) * 512), 16, o, soff,
                                                0, 0);
@@ -163,11 +174,12 @@ struct Frags {
 
 template <int AL, int BL, int BK>
 __device__ __forceinline__ void read_step(bf16x8 (&fa)[4], bf16x8 (&fb)[4], const Frags<AL, BK>& FA,
-                                          const Frags<BL, BK>& FB, const bf16* stage, int ks) {
+                                          const Frags<BL, BK>& FB, const bf16* sa, const bf16* sb,
+                                          int ks) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) fa[i] = FA.read(stage, i, ks);
+  for (int i = 0; i < 4; ++i) fa[i] = FA.read(sa, i, ks);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) fb[j] = FB.read(stage + BT * BK, j, ks);
+  for (int j = 0; j < 4; ++j) fb[j] = FB.read(sb, j, ks);
 }
 
 __device__ __forceinline__ void mfma_step(floatx16 (&acc)[4][4], const bf16x8 (&fa)[4],
@@ -396,15 +408,18 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, floatx16 (&acc)[4][4
   }
 }
 
-// BK: K-tile depth (32 or 64); NS: LDS stages (NS * BK * 1 KB <= 128 KB).
+// BK: K-tile depth (64; 32 for the stage schedule only); NS: LDS stages, or 5 for the ring.
 template <int AL, int BL, int EPI, int GE, int BK, int NS>
 __global__ __launch_bounds__(NT, 1) void gemm256_kernel(GemmArgs p) {
   constexpr int OPE = BT * BK;               // bf16 elements of one operand tile
-  constexpr int STE = 2 * OPE;               // bf16 elements of one stage
   constexpr int KS = BK / 16;                // MFMA k-steps per K-tile
-  constexpr int CPT = Loader<AL, BK>::NI + Loader<BL, BK>::NI;  // copies per wave per tile
-  static_assert(NS * STE * 2 <= 131072 && KS % 2 == 0, "LDS budget / k-step parity");
-  __shared__ __attribute__((aligned(1024))) bf16 smem[NS * STE];
+  constexpr int NI = Loader<AL, BK>::NI;     // copies per wave per operand tile
+  static_assert(Loader<BL, BK>::NI == NI, "both operands copy the same bytes");
+  // NS = 5 is the ring of five operand slots (two and a half stages)
+  constexpr int SLOTS = NS == 5 ? 5 : 2 * NS;
+  static_assert(SLOTS * OPE * 2 <= 163840 && KS % 2 == 0, "LDS budget / k-step parity");
+  static_assert((SLOTS - 2) * NI < 64, "vmcnt range");
+  __shared__ __attribute__((aligned(1024))) bf16 smem[SLOTS * OPE];
 
   const int M = p.M, N = p.N, K = p.K;
   const int tiles_m = (M + BT - 1) / BT, tiles_n = (N + BT - 1) / BT;
@@ -447,87 +462,163 @@ __global__ __launch_bounds__(NT, 1) void gemm256_kernel(GemmArgs p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // Every iteration issues the copies of one tile (tiles past the last read
-  // zeros), so the wait counts are constants: once tile t + 1 is resident,
-  // tiles t + 2 .. t + NS - 1 may still be in flight.
   const int nk = (K + BK - 1) / BK;
-#pragma unroll
-  for (int s = 0; s < NS; ++s) {
-    la.issue(rsA, s * BK, K, p.lda, smem + s * STE, wave);
-    lb.issue(rsB, s * BK, K, p.ldb, smem + s * STE + OPE, wave);
-  }
-  wait_vm_lgkm0<(NS - 1) * CPT>();  // tile 0 resident
-  cta_barrier();
-
   constexpr int ND = (AL == LAY_K ? 4 : 8) + (BL == LAY_K ? 4 : 8);
   bf16x8 f0a[4], f0b[4], f1a[4], f1b[4];
-  read_step(f0a, f0b, FA, FB, smem, 0);
+  if constexpr (SLOTS == 5) {
+    // Ring of five operand slots.  Operand tile u (A_t = 2t, B_t = 2t + 1)
+    // lives in slot u % 5.  While tile t is consumed, A_{t+2} is copied into
+    // the slot B_{t-1} left, spread over the first two k-steps; after the
+    // barrier that ends the reads of tile t, B_{t+2} goes into A_t's slot
+    // during the last k-step.  The copies of a K-tile are thus spread over
+    // most of the loop instead of arriving at the address unit in one burst,
+    // and the wait before the barrier still has a constant count (A_{t+2}).
+    static_assert(BK == 64 && NI % 2 == 0, "ring schedule");
+    la.issue(rsA, 0, K, p.lda, smem, wave);
+    lb.issue(rsB, 0, K, p.ldb, smem + OPE, wave);
+    la.issue(rsA, BK, K, p.lda, smem + 2 * OPE, wave);
+    lb.issue(rsB, BK, K, p.ldb, smem + 3 * OPE, wave);
+    wait_vm_lgkm0<2 * NI>();  // tile 0 resident
+    cta_barrier();
+    int ua = 0;  // slot of A_t; B_t is in the next slot, A_{t+2} goes to the previous one
+    read_step(f0a, f0b, FA, FB, smem, smem + OPE, 0);
+    for (int kt = 0; kt + 1 < nk; ++kt) {
+      bf16* ca = smem + ua * OPE;
+      bf16* cb = smem + (ua == 4 ? 0 : ua + 1) * OPE;
+      bf16* fr = smem + (ua == 0 ? 4 : ua - 1) * OPE;
+      const int un = ua >= 3 ? ua - 3 : ua + 2;
+      const bf16* na = smem + un * OPE;
+      const bf16* nb = smem + (un == 4 ? 0 : un + 1) * OPE;
+      const int k2 = (kt + 2) * BK;
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_step(acc, f0a, f0b);
+      read_step(f1a, f1b, FA, FB, ca, cb, 1);
+      la.template issue<0, NI / 2>(rsA, k2, K, p.lda, fr, wave);
+      interleave<ND, NI / 2>();
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_step(acc, f1a, f1b);
+      read_step(f0a, f0b, FA, FB, ca, cb, 2);
+      la.template issue<NI / 2, NI>(rsA, k2, K, p.lda, fr, wave);
+      interleave<ND, NI / 2>();
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_step(acc, f0a, f0b);
+      read_step(f1a, f1b, FA, FB, ca, cb, 3);
+      interleave<ND, 0>();
+      __builtin_amdgcn_sched_barrier(0);
+      wait_vm_lgkm0<NI>();  // this wave's copies of tile kt + 1 and its reads of tile kt
+      cta_barrier();         // ... and every other wave's: A_kt's slot is free
+      lb.issue(rsB, k2, K, p.ldb, ca, wave);
+      read_step(f0a, f0b, FA, FB, na, nb, 0);
+      mfma_step(acc, f1a, f1b);
+      interleave<ND, NI>();
+      __builtin_amdgcn_sched_barrier(0);
+      ua = un;
+    }
+    const bf16* ca = smem + ua * OPE;
+    const bf16* cb = smem + (ua == 4 ? 0 : ua + 1) * OPE;
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(acc, f0a, f0b);
+    read_step(f1a, f1b, FA, FB, ca, cb, 1);
+    interleave<ND, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(acc, f1a, f1b);
+    read_step(f0a, f0b, FA, FB, ca, cb, 2);
+    interleave<ND, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(acc, f0a, f0b);
+    read_step(f1a, f1b, FA, FB, ca, cb, 3);
+    interleave<ND, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(acc, f1a, f1b);
+  } else {
+    // Operand tiles are copied in the order A_0, B_0, A_1, B_1, ...; operand
+    // tile u goes to slot u % SLOTS.  After tile t has been consumed, its two
+    // slots take operand tiles 2t + SLOTS and 2t + SLOTS + 1, so the wait counts
+    // are constants: once tile t + 1 is resident, SLOTS - 4 operand tiles may
+    // still be in flight.  Operand tiles past the last K-tile read zeros.
+    auto issue = [&](int u, const bf16* dst) {  // u is odd exactly for B
+      if ((u & 1) == 0) la.issue(rsA, (u >> 1) * BK, K, p.lda, const_cast<bf16*>(dst), wave);
+      else lb.issue(rsB, (u >> 1) * BK, K, p.ldb, const_cast<bf16*>(dst), wave);
+    };
+  #pragma unroll
+    for (int u = 0; u < SLOTS; ++u) issue(u, smem + u * OPE);
+    wait_vm_lgkm0<(SLOTS - 2) * NI>();  // tile 0 resident
+    cta_barrier();
 
-  for (int kt = 0; kt + 1 < nk; ++kt) {
-    bf16* cur = smem + (kt % NS) * STE;
-    const bf16* nxt = smem + ((kt + 1) % NS) * STE;
-#pragma unroll
-    for (int ks = 0; ks + 2 < KS; ks += 2) {
+    int ua = 0;  // slot of the current tile's A (its B is in the next slot)
+    read_step(f0a, f0b, FA, FB, smem, smem + OPE, 0);
+
+    for (int kt = 0; kt + 1 < nk; ++kt) {
+      const bf16* ca = smem + ua * OPE;
+      const bf16* cb = smem + (ua + 1 == SLOTS ? 0 : ua + 1) * OPE;
+      const int un = ua + 2 >= SLOTS ? ua + 2 - SLOTS : ua + 2;
+      const bf16* na = smem + un * OPE;
+      const bf16* nb = smem + (un + 1 == SLOTS ? 0 : un + 1) * OPE;
+  #pragma unroll
+      for (int ks = 0; ks + 2 < KS; ks += 2) {
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_step(acc, f0a, f0b);
+        read_step(f1a, f1b, FA, FB, ca, cb, ks + 1);
+        interleave<ND, 0>();
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_step(acc, f1a, f1b);
+        read_step(f0a, f0b, FA, FB, ca, cb, ks + 2);
+        interleave<ND, 0>();
+      }
       __builtin_amdgcn_sched_barrier(0);
       mfma_step(acc, f0a, f0b);
-      read_step(f1a, f1b, FA, FB, cur, ks + 1);
+      read_step(f1a, f1b, FA, FB, ca, cb, KS - 1);
+      interleave<ND, 0>();
+      __builtin_amdgcn_sched_barrier(0);
+      wait_vm_lgkm0<(SLOTS - 4) * NI>();  // this wave's copies of tile kt + 1 and its reads of tile kt
+      cta_barrier();                       // ... and every other wave's: tile kt's slots are free
+      issue(2 * kt + SLOTS, ca);
+      issue(2 * kt + SLOTS + 1, cb);
+      read_step(f0a, f0b, FA, FB, na, nb, 0);
+      mfma_step(acc, f1a, f1b);
+      interleave<ND, 2 * NI>();
+      __builtin_amdgcn_sched_barrier(0);
+      ua = un;
+    }
+    {
+      const bf16* ca = smem + ua * OPE;
+      const bf16* cb = smem + (ua + 1 == SLOTS ? 0 : ua + 1) * OPE;
+  #pragma unroll
+      for (int ks = 0; ks + 2 < KS; ks += 2) {
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_step(acc, f0a, f0b);
+        read_step(f1a, f1b, FA, FB, ca, cb, ks + 1);
+        interleave<ND, 0>();
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_step(acc, f1a, f1b);
+        read_step(f0a, f0b, FA, FB, ca, cb, ks + 2);
+        interleave<ND, 0>();
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_step(acc, f0a, f0b);
+      read_step(f1a, f1b, FA, FB, ca, cb, KS - 1);
       interleave<ND, 0>();
       __builtin_amdgcn_sched_barrier(0);
       mfma_step(acc, f1a, f1b);
-      read_step(f0a, f0b, FA, FB, cur, ks + 2);
-      interleave<ND, 0>();
     }
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_step(acc, f0a, f0b);
-    read_step(f1a, f1b, FA, FB, cur, KS - 1);
-    interleave<ND, 0>();
-    __builtin_amdgcn_sched_barrier(0);
-    wait_vm_lgkm0<(NS - 2) * CPT>();  // this wave's copies of tile kt + 1 and its reads of tile kt
-    cta_barrier();                    // ... and every other wave's: stage kt % NS is free
-    la.issue(rsA, (kt + NS) * BK, K, p.lda, cur, wave);
-    lb.issue(rsB, (kt + NS) * BK, K, p.ldb, cur + OPE, wave);
-    read_step(f0a, f0b, FA, FB, nxt, 0);
-    mfma_step(acc, f1a, f1b);
-    interleave<ND, CPT>();
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  {
-    const bf16* cur = smem + ((nk - 1) % NS) * STE;
-#pragma unroll
-    for (int ks = 0; ks + 2 < KS; ks += 2) {
-      __builtin_amdgcn_sched_barrier(0);
-      mfma_step(acc, f0a, f0b);
-      read_step(f1a, f1b, FA, FB, cur, ks + 1);
-      interleave<ND, 0>();
-      __builtin_amdgcn_sched_barrier(0);
-      mfma_step(acc, f1a, f1b);
-      read_step(f0a, f0b, FA, FB, cur, ks + 2);
-      interleave<ND, 0>();
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_step(acc, f0a, f0b);
-    read_step(f1a, f1b, FA, FB, cur, KS - 1);
-    interleave<ND, 0>();
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_step(acc, f1a, f1b);
   }
   wait_vm_lgkm0<0>();  // the zero-filling copies past the last tile
   __syncthreads();
   epilogue<EPI, GE>(p, acc, reinterpret_cast<float*>(smem), m0, n0, wave, lane);
 }
 
-#ifndef SAT_GEMM256_BK
-#define SAT_GEMM256_BK 64
-#define SAT_GEMM256_NS 2
-#endif
-
+// Both operands K-contiguous: the five-slot ring with spread copies.  With an
+// M/N-contiguous operand the transposing fragment reads load the LDS more, and
+// copies arriving in one burst at the end of a K-tile measured faster: two
+// stages.
 template <int AL, int BL, int EPI>
 hipError_t launch_e(const GemmArgs& a, hipStream_t s) {
+  constexpr int NS = (AL == LAY_K && BL == LAY_K) ? 5 : 2;
   dim3 grid((unsigned)(sat_cdiv(a.M, BT) * sat_cdiv(a.N, BT)));
   if ((EPI == EPI_BF16 || EPI == EPI_DGELU_BF16) && a.gelu_erf)
-    hipLaunchKernelGGL((gemm256_kernel<AL, BL, EPI, 1, SAT_GEMM256_BK, SAT_GEMM256_NS>), grid, dim3(NT), 0, s, a);
+    hipLaunchKernelGGL((gemm256_kernel<AL, BL, EPI, 1, 64, NS>), grid, dim3(NT), 0, s, a);
   else
-    hipLaunchKernelGGL((gemm256_kernel<AL, BL, EPI, 0, SAT_GEMM256_BK, SAT_GEMM256_NS>), grid, dim3(NT), 0, s, a);
+    hipLaunchKernelGGL((gemm256_kernel<AL, BL, EPI, 0, 64, NS>), grid, dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 
