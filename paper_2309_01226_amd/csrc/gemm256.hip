@@ -5,40 +5,32 @@
 //   the same fused epilogues as the general kernel in gemm.hip.
 //
 // What bounds it on MI355X (measured with single-purpose variants of this
-// kernel): the L2 -> LDS copy stream and, with an M/N-contiguous operand, the
-// LDS, not the matrix cores.  One 256 x 256 tile needs 32 bytes per clock per
+// kernel): the L2 -> LDS copy stream and, for an M/N-contiguous operand, the
+// pass through registers that transposes it, not the matrix cores.  One 256 x 256 tile needs 32 bytes per clock per
 // CU at full MFMA rate, and a CU's copy throughput is set by the number of
 // 128-byte cache lines it requests, not by bytes: rows copied in 64-byte
 // pieces (K-tiles of 32) deliver about half of what full-line pieces do.  So
 // K-tiles are 64 deep (a K-contiguous row of the tile is exactly one line),
 // 64 KB per K-tile, and the 160 KB of LDS holds two and a half of them.
 //
-// Two schedules share the loop:
-//  * two stages (used when an operand is M/N-contiguous): the copies of tile
-//    k + 2 are issued as soon as every wave has finished reading tile k, all
-//    in the last k-step;
-//  * a ring of five single-operand slots (both operands K-contiguous): A of
-//    tile k + 2 is copied during the first k-steps of tile k, B of tile k + 2
-//    after the barrier.  Issuing all sixteen copies of a wave in one k-step
-//    fills the address unit's queue and stalls the MFMAs behind them in the
-//    in-order instruction stream (counter SQ_VMEM_TA_ADDR_FIFO_FULL); spread
-//    over the loop they cost about 10% less time on long-K problems.
+// Both operands K-contiguous (gemm256_kernel): a ring of five single-operand
+// slots.  A of tile k + 2 is copied during the first k-steps of tile k, B of
+// tile k + 2 after the barrier that ends the reads of tile k.  Issuing all
+// sixteen copies of a wave in one k-step fills the address unit's queue and
+// stalls the MFMAs behind them in the in-order instruction stream (counter
+// SQ_VMEM_TA_ADDR_FIFO_FULL); spread over the loop they cost about 10% less
+// time on long-K problems than a two-stage loop.
 //
-// Layout of one stage: the A tile, then the B tile.
-//  * K-contiguous operand (rows = m or n): [256 rows][64 k], 128 B per row;
-//    the eight 16-byte chunks of row r are XOR-swizzled with (r >> 1) & 7,
-//    which keeps the fragment reads (16 lanes = 16 consecutive rows at one
-//    chunk) free of bank conflicts.
-//  * M/N-contiguous operand (k rows, m or n contiguous): [64 k][256], 512 B
-//    per k-row; the 32 chunks of k-row k are XOR-swizzled with
-//    {0, 4, 10, 14}[k & 3].  Fragments are read with ds_read_b64_tr_b16, the
-//    CDNA4 transposing LDS read: a 16-lane group reads a 4 (k) x 16 (n) block,
-//    lane 4e + q supplying the address of k-row e, columns 4q .. 4q + 3, and
-//    lane o receives column o, k-rows 0..3.  Two such reads give the eight
-//    consecutive k of a 32 x 32 x 16 MFMA operand.
-//  * Both layouts go HBM -> LDS with buffer_load ... lds (16 bytes per lane,
-//    1 KB per instruction, no VGPR staging).  Rows past M / N and k past K get
-//    an out-of-range buffer offset and read as zeros.
+// Layout of an operand tile in LDS: [256 rows][64 k], 128 B per row; the
+// eight 16-byte chunks of row r are XOR-swizzled with (r >> 1) & 7, which
+// keeps the fragment reads (16 lanes = 16 consecutive rows at one chunk) free
+// of bank conflicts.  K-contiguous operands go HBM -> LDS with buffer_load
+// ... lds (16 bytes per lane, 1 KB per instruction, no VGPR staging).  Rows
+// past M / N and k past K get an out-of-range buffer offset and read as
+// zeros.  An M/N-contiguous operand (gemm256_rs_kernel) is loaded into
+// registers, transposed there and written in the same layout: the CDNA4
+// transposing LDS read (ds_read_b64_tr_b16) would spare the register pass,
+// but it costs more LDS time than the MFMAs leave (measured 10-30% slower).
 //
 // Main loop per K-tile (four k-steps of 16), per wave (128 x 128 sub-tile,
 // 4 x 4 MFMA 32x32x16 accumulators in AGPRs): the MFMAs of each k-step are
@@ -62,15 +54,9 @@ constexpr uint32_t OOB = 0x80000000u; // buffer offset past num_records: reads z
 constexpr int EP = 136;               // fp32 pitch of an epilogue staging row
 
 typedef __attribute__((address_space(3))) void lds_void;
-typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
-// K-layout swizzle: BK = 32 (four chunks per row) or BK = 64 (eight chunks);
-// the BK = 64 form measured free of bank conflicts for the fragment reads
-template <int BK>
-__device__ __forceinline__ int swz_k(int row) {
-  return BK == 32 ? (((row >> 1) ^ (row >> 3)) & 3) : ((row >> 1) & 7);
-}
-__device__ __forceinline__ int swz_mn(int k) { return (0xEA40 >> ((k & 3) << 2)) & 15; }
+// Chunk swizzle of the K-contiguous tile layout (eight 16-byte chunks per row)
+__device__ __forceinline__ int swz_k(int row) { return (row >> 1) & 7; }
 
 __device__ __forceinline__ lds_void* lds(const bf16* p) { return (lds_void*)(const_cast<bf16*>(p)); }
 
@@ -90,45 +76,38 @@ __device__ __forceinline__ void cta_barrier() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-// Copies of one operand tile: 16 instructions of 1 KB, four per wave.
-// Instruction j = 4 i + wave fills LDS bytes [1024 j, 1024 j + 1024) of the
-// tile; lane L writes the 16 bytes at 1024 j + 16 L.  A copy whose k lies at or
-// past K (the K tail, and the tiles past the last one that the steady-state
-// loop issues to keep its wait counts constant) reads zeros and touches no
-// memory.
-template <int LAY, int BK>
+constexpr int BK = 64;                // K-tile depth
+constexpr int OPE = BT * BK;          // bf16 elements of one operand tile
+
+// Copies of one K-contiguous operand tile: 32 instructions of 1 KB, eight per
+// wave.  Instruction j = 4 i + wave fills LDS bytes [1024 j, 1024 j + 1024) of
+// the tile (rows 8 j .. 8 j + 7); lane L writes the 16 bytes at 1024 j + 16 L.
+// A copy whose k lies at or past K (the K tail, and the tiles past the last
+// one that the steady-state loop issues to keep its wait counts constant)
+// reads zeros and touches no memory.
+
 struct Loader {
-  static constexpr int CPR = BK / 8;                       // 16-byte chunks per K-layout row
-  static constexpr int NI = (BT * BK * 2 / 1024) / 4;      // copy instructions per wave
+  static constexpr int NI = (BT * BK * 2 / 1024) / 4;  // copy instructions per wave
   uint32_t off[NI];  // byte offsets relative to (tile row 0, k0)
   int kof[NI];       // k of this lane's chunk relative to k0
   __device__ __forceinline__ void init(long ld, int nrows, int wave) {
     const int lane = threadIdx.x & 63;
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
-      const int j = 4 * i + wave;
-      if (LAY == LAY_K) {
-        const int row = (64 / CPR) * j + lane / CPR;
-        const int c = (lane % CPR) ^ swz_k<BK>(row);
-        off[i] = row < nrows ? (uint32_t)(((long)row * ld + 8 * c) * 2) : OOB;
-        kof[i] = 8 * c;
-      } else {
-        const int kr = 2 * j + (lane >> 5);
-        const int c = (lane & 31) ^ swz_mn(kr);
-        off[i] = 8 * c < nrows ? (uint32_t)(((long)kr * ld + 8 * c) * 2) : OOB;
-        kof[i] = kr;
-      }
+      const int row = 8 * (4 * i + wave) + lane / 8;
+      const int c = (lane % 8) ^ swz_k(row);
+      off[i] = row < nrows ? (uint32_t)(((long)row * ld + 8 * c) * 2) : OOB;
+      kof[i] = 8 * c;
     }
   }
   template <int I0 = 0, int I1 = NI>
-  __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, int k0, int K, long ld,
-                                        bf16* dst, int wave) const {
-    const uint32_t soff = LAY == LAY_K ? (uint32_t)(k0 * 2) : (uint32_t)((long)k0 * ld * 2);
+  __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, int k0, int K, bf16* dst,
+                                        int wave) const {
 #pragma unroll
     for (int i = I0; i < I1; ++i) {
       const uint32_t o = (k0 + kof[i] < K) ? off[i] : OOB;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds(dst + (4 * i + wave) * 512), 16, o, soff,
-                                               0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds(dst + (4 * i + wave) * 512), 16, o,
+                                               (uint32_t)(k0 * 2), 0, 0);
     }
   }
 };
@@ -136,46 +115,22 @@ struct Loader {
 // Fragment addressing of one operand inside a stage, for the wave's 128-row
 // (or column) half `w0` (0 or 128).  frag(sub, ks) is the 32 x 16 MFMA operand
 // of rows w0 + 32 sub .. + 31, k = 16 ks .. + 15.
-template <int LAY, int BK>
 struct Frags {
   static constexpr int KS = BK / 16;
-  int o[LAY == LAY_K ? KS : 8];  // element offsets: K layout o[ks]; MN layout o[2 sub + h]
+  int o[KS];  // element offsets of k-step ks
   __device__ __forceinline__ void init(int w0) {
     const int lane = threadIdx.x & 63;
-    if (LAY == LAY_K) {
-      const int r = lane & 31;
+    const int r = lane & 31;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        o[ks] = (w0 + r) * BK + 8 * ((2 * ks + (lane >> 5)) ^ swz_k<BK>(r));
-    } else {
-      const int G = lane >> 4, l = lane & 15;
-      const int sm = swz_mn(l >> 2);
-#pragma unroll
-      for (int sub = 0; sub < 4; ++sub)
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int kr = 8 * (G >> 1) + 4 * h + (l >> 2);
-          const int c = (w0 >> 3) + 4 * sub + 2 * (G & 1) + ((l >> 1) & 1);
-          o[2 * sub + h] = kr * BT + 8 * (c ^ sm) + 4 * (l & 1);
-        }
-    }
+    for (int ks = 0; ks < KS; ++ks) o[ks] = (w0 + r) * BK + 8 * ((2 * ks + (lane >> 5)) ^ swz_k(r));
   }
   __device__ __forceinline__ bf16x8 read(const bf16* tile, int sub, int ks) const {
-    if (LAY == LAY_K) {
-      return *reinterpret_cast<const bf16x8*>(tile + o[ks] + sub * 32 * BK);
-    } else {
-      const bf16* t = tile + ks * 16 * BT;
-      bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(t + o[2 * sub]));
-      bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(t + o[2 * sub + 1]));
-      return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-    }
+    return *reinterpret_cast<const bf16x8*>(tile + o[ks] + sub * 32 * BK);
   }
 };
 
-template <int AL, int BL, int BK>
-__device__ __forceinline__ void read_step(bf16x8 (&fa)[4], bf16x8 (&fb)[4], const Frags<AL, BK>& FA,
-                                          const Frags<BL, BK>& FB, const bf16* sa, const bf16* sb,
-                                          int ks) {
+__device__ __forceinline__ void read_step(bf16x8 (&fa)[4], bf16x8 (&fb)[4], const Frags& FA,
+                                          const Frags& FB, const bf16* sa, const bf16* sb, int ks) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) fa[i] = FA.read(sa, i, ks);
 #pragma unroll
@@ -408,25 +363,13 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, floatx16 (&acc)[4][4
   }
 }
 
-// BK: K-tile depth (64; 32 for the stage schedule only); NS: LDS stages, or 5 for the ring.
-template <int AL, int BL, int EPI, int GE, int BK, int NS>
-__global__ __launch_bounds__(NT, 1) void gemm256_kernel(GemmArgs p) {
-  constexpr int OPE = BT * BK;               // bf16 elements of one operand tile
-  constexpr int KS = BK / 16;                // MFMA k-steps per K-tile
-  constexpr int NI = Loader<AL, BK>::NI;     // copies per wave per operand tile
-  static_assert(Loader<BL, BK>::NI == NI, "both operands copy the same bytes");
-  // NS = 5 is the ring of five operand slots (two and a half stages)
-  constexpr int SLOTS = NS == 5 ? 5 : 2 * NS;
-  static_assert(SLOTS * OPE * 2 <= 163840 && KS % 2 == 0, "LDS budget / k-step parity");
-  static_assert((SLOTS - 2) * NI < 64, "vmcnt range");
-  __shared__ __attribute__((aligned(1024))) bf16 smem[SLOTS * OPE];
-
-  const int M = p.M, N = p.N, K = p.K;
+// Output tile of this workgroup.  Workgroups are dealt round-robin over the 8
+// XCDs; renumber so that each XCD walks a contiguous range of the tile order,
+// then order tiles in groups of 8 tile-rows so that the B tiles of a group
+// stay in L2.
+__device__ __forceinline__ void tile_origin(int M, int N, int& m0, int& n0) {
   const int tiles_m = (M + BT - 1) / BT, tiles_n = (N + BT - 1) / BT;
   const int nwg = tiles_m * tiles_n;
-  // Workgroups are dealt round-robin over the 8 XCDs; renumber so that each
-  // XCD walks a contiguous range of the tile order, then order tiles in
-  // groups of 8 tile-rows so that the B tiles of a group stay in L2.
   int bid = blockIdx.x;
   if ((nwg & 7) == 0) bid = (bid & 7) * (nwg >> 3) + (bid >> 3);
   constexpr int G = 8;
@@ -435,22 +378,33 @@ __global__ __launch_bounds__(NT, 1) void gemm256_kernel(GemmArgs p) {
   const int first_m = group * G;
   const int gsize = min(tiles_m - first_m, G);
   const int in_g = bid - group * per_group;
-  const int m0 = (first_m + in_g % gsize) * BT, n0 = (in_g / gsize) * BT;
+  m0 = (first_m + in_g % gsize) * BT;
+  n0 = (in_g / gsize) * BT;
+}
 
+// Both operands K-contiguous: the five-slot ring.
+template <int EPI, int GE>
+__global__ __launch_bounds__(NT, 1) void gemm256_kernel(GemmArgs p) {
+  constexpr int KS = BK / 16;                // MFMA k-steps per K-tile
+  constexpr int NI = Loader::NI;             // copies per wave per operand tile
+  static_assert(5 * OPE * 2 <= 163840 && KS == 4, "LDS budget / k-steps");
+  __shared__ __attribute__((aligned(1024))) bf16 smem[5 * OPE];
+
+  const int M = p.M, N = p.N, K = p.K;
+  int m0, n0;
+  tile_origin(M, N, m0, n0);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave >> 1, wn = wave & 1;
 
   __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(p.A + (AL == LAY_K ? (long)m0 * p.lda : (long)m0)), (short)0, 0x7FFFFFFF, 0x00020000);
+      (void*)(p.A + (long)m0 * p.lda), (short)0, 0x7FFFFFFF, 0x00020000);
   __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(p.B + (BL == LAY_K ? (long)n0 * p.ldb : (long)n0)), (short)0, 0x7FFFFFFF, 0x00020000);
-  Loader<AL, BK> la;
-  Loader<BL, BK> lb;
+      (void*)(p.B + (long)n0 * p.ldb), (short)0, 0x7FFFFFFF, 0x00020000);
+  Loader la, lb;
   la.init(p.lda, M - m0, wave);
   lb.init(p.ldb, N - n0, wave);
-  Frags<AL, BK> FA;
-  Frags<BL, BK> FB;
+  Frags FA, FB;
   FA.init(wm * 128);
   FB.init(wn * 128);
 
@@ -462,58 +416,56 @@ __global__ __launch_bounds__(NT, 1) void gemm256_kernel(GemmArgs p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+  // Ring of five operand slots.  Operand tile u (A_t = 2t, B_t = 2t + 1) lives
+  // in slot u % 5.  While tile t is consumed, A_{t+2} is copied into the slot
+  // B_{t-1} left, spread over the first two k-steps; after the barrier that
+  // ends the reads of tile t, B_{t+2} goes into A_t's slot during the last
+  // k-step.  The wait before the barrier has a constant count: only A_{t+2}
+  // may still be in flight.  Operand tiles past the last K-tile read zeros.
   const int nk = (K + BK - 1) / BK;
-  constexpr int ND = (AL == LAY_K ? 4 : 8) + (BL == LAY_K ? 4 : 8);
+  constexpr int ND = 8;
   bf16x8 f0a[4], f0b[4], f1a[4], f1b[4];
-  if constexpr (SLOTS == 5) {
-    // Ring of five operand slots.  Operand tile u (A_t = 2t, B_t = 2t + 1)
-    // lives in slot u % 5.  While tile t is consumed, A_{t+2} is copied into
-    // the slot B_{t-1} left, spread over the first two k-steps; after the
-    // barrier that ends the reads of tile t, B_{t+2} goes into A_t's slot
-    // during the last k-step.  The copies of a K-tile are thus spread over
-    // most of the loop instead of arriving at the address unit in one burst,
-    // and the wait before the barrier still has a constant count (A_{t+2}).
-    static_assert(BK == 64 && NI % 2 == 0, "ring schedule");
-    la.issue(rsA, 0, K, p.lda, smem, wave);
-    lb.issue(rsB, 0, K, p.ldb, smem + OPE, wave);
-    la.issue(rsA, BK, K, p.lda, smem + 2 * OPE, wave);
-    lb.issue(rsB, BK, K, p.ldb, smem + 3 * OPE, wave);
-    wait_vm_lgkm0<2 * NI>();  // tile 0 resident
-    cta_barrier();
-    int ua = 0;  // slot of A_t; B_t is in the next slot, A_{t+2} goes to the previous one
-    read_step(f0a, f0b, FA, FB, smem, smem + OPE, 0);
-    for (int kt = 0; kt + 1 < nk; ++kt) {
-      bf16* ca = smem + ua * OPE;
-      bf16* cb = smem + (ua == 4 ? 0 : ua + 1) * OPE;
-      bf16* fr = smem + (ua == 0 ? 4 : ua - 1) * OPE;
-      const int un = ua >= 3 ? ua - 3 : ua + 2;
-      const bf16* na = smem + un * OPE;
-      const bf16* nb = smem + (un == 4 ? 0 : un + 1) * OPE;
-      const int k2 = (kt + 2) * BK;
-      __builtin_amdgcn_sched_barrier(0);
-      mfma_step(acc, f0a, f0b);
-      read_step(f1a, f1b, FA, FB, ca, cb, 1);
-      la.template issue<0, NI / 2>(rsA, k2, K, p.lda, fr, wave);
-      interleave<ND, NI / 2>();
-      __builtin_amdgcn_sched_barrier(0);
-      mfma_step(acc, f1a, f1b);
-      read_step(f0a, f0b, FA, FB, ca, cb, 2);
-      la.template issue<NI / 2, NI>(rsA, k2, K, p.lda, fr, wave);
-      interleave<ND, NI / 2>();
-      __builtin_amdgcn_sched_barrier(0);
-      mfma_step(acc, f0a, f0b);
-      read_step(f1a, f1b, FA, FB, ca, cb, 3);
-      interleave<ND, 0>();
-      __builtin_amdgcn_sched_barrier(0);
-      wait_vm_lgkm0<NI>();  // this wave's copies of tile kt + 1 and its reads of tile kt
-      cta_barrier();         // ... and every other wave's: A_kt's slot is free
-      lb.issue(rsB, k2, K, p.ldb, ca, wave);
-      read_step(f0a, f0b, FA, FB, na, nb, 0);
-      mfma_step(acc, f1a, f1b);
-      interleave<ND, NI>();
-      __builtin_amdgcn_sched_barrier(0);
-      ua = un;
-    }
+  la.issue(rsA, 0, K, smem, wave);
+  lb.issue(rsB, 0, K, smem + OPE, wave);
+  la.issue(rsA, BK, K, smem + 2 * OPE, wave);
+  lb.issue(rsB, BK, K, smem + 3 * OPE, wave);
+  wait_vm_lgkm0<2 * NI>();  // tile 0 resident
+  cta_barrier();
+  int ua = 0;  // slot of A_t; B_t is in the next slot, A_{t+2} goes to the previous one
+  read_step(f0a, f0b, FA, FB, smem, smem + OPE, 0);
+  for (int kt = 0; kt + 1 < nk; ++kt) {
+    bf16* ca = smem + ua * OPE;
+    bf16* cb = smem + (ua == 4 ? 0 : ua + 1) * OPE;
+    bf16* fr = smem + (ua == 0 ? 4 : ua - 1) * OPE;
+    const int un = ua >= 3 ? ua - 3 : ua + 2;
+    const bf16* na = smem + un * OPE;
+    const bf16* nb = smem + (un == 4 ? 0 : un + 1) * OPE;
+    const int k2 = (kt + 2) * BK;
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(acc, f0a, f0b);
+    read_step(f1a, f1b, FA, FB, ca, cb, 1);
+    la.issue<0, NI / 2>(rsA, k2, K, fr, wave);
+    interleave<ND, NI / 2>();
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(acc, f1a, f1b);
+    read_step(f0a, f0b, FA, FB, ca, cb, 2);
+    la.issue<NI / 2, NI>(rsA, k2, K, fr, wave);
+    interleave<ND, NI / 2>();
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(acc, f0a, f0b);
+    read_step(f1a, f1b, FA, FB, ca, cb, 3);
+    interleave<ND, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vm_lgkm0<NI>();  // this wave's copies of tile kt + 1 and its reads of tile kt
+    cta_barrier();         // ... and every other wave's: A_kt's slot is free
+    lb.issue(rsB, k2, K, ca, wave);
+    read_step(f0a, f0b, FA, FB, na, nb, 0);
+    mfma_step(acc, f1a, f1b);
+    interleave<ND, NI>();
+    __builtin_amdgcn_sched_barrier(0);
+    ua = un;
+  }
+  {
     const bf16* ca = smem + ua * OPE;
     const bf16* cb = smem + (ua == 4 ? 0 : ua + 1) * OPE;
     __builtin_amdgcn_sched_barrier(0);
@@ -530,95 +482,226 @@ __global__ __launch_bounds__(NT, 1) void gemm256_kernel(GemmArgs p) {
     interleave<ND, 0>();
     __builtin_amdgcn_sched_barrier(0);
     mfma_step(acc, f1a, f1b);
-  } else {
-    // Operand tiles are copied in the order A_0, B_0, A_1, B_1, ...; operand
-    // tile u goes to slot u % SLOTS.  After tile t has been consumed, its two
-    // slots take operand tiles 2t + SLOTS and 2t + SLOTS + 1, so the wait counts
-    // are constants: once tile t + 1 is resident, SLOTS - 4 operand tiles may
-    // still be in flight.  Operand tiles past the last K-tile read zeros.
-    auto issue = [&](int u, const bf16* dst) {  // u is odd exactly for B
-      if ((u & 1) == 0) la.issue(rsA, (u >> 1) * BK, K, p.lda, const_cast<bf16*>(dst), wave);
-      else lb.issue(rsB, (u >> 1) * BK, K, p.ldb, const_cast<bf16*>(dst), wave);
-    };
-  #pragma unroll
-    for (int u = 0; u < SLOTS; ++u) issue(u, smem + u * OPE);
-    wait_vm_lgkm0<(SLOTS - 2) * NI>();  // tile 0 resident
-    cta_barrier();
-
-    int ua = 0;  // slot of the current tile's A (its B is in the next slot)
-    read_step(f0a, f0b, FA, FB, smem, smem + OPE, 0);
-
-    for (int kt = 0; kt + 1 < nk; ++kt) {
-      const bf16* ca = smem + ua * OPE;
-      const bf16* cb = smem + (ua + 1 == SLOTS ? 0 : ua + 1) * OPE;
-      const int un = ua + 2 >= SLOTS ? ua + 2 - SLOTS : ua + 2;
-      const bf16* na = smem + un * OPE;
-      const bf16* nb = smem + (un + 1 == SLOTS ? 0 : un + 1) * OPE;
-  #pragma unroll
-      for (int ks = 0; ks + 2 < KS; ks += 2) {
-        __builtin_amdgcn_sched_barrier(0);
-        mfma_step(acc, f0a, f0b);
-        read_step(f1a, f1b, FA, FB, ca, cb, ks + 1);
-        interleave<ND, 0>();
-        __builtin_amdgcn_sched_barrier(0);
-        mfma_step(acc, f1a, f1b);
-        read_step(f0a, f0b, FA, FB, ca, cb, ks + 2);
-        interleave<ND, 0>();
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      mfma_step(acc, f0a, f0b);
-      read_step(f1a, f1b, FA, FB, ca, cb, KS - 1);
-      interleave<ND, 0>();
-      __builtin_amdgcn_sched_barrier(0);
-      wait_vm_lgkm0<(SLOTS - 4) * NI>();  // this wave's copies of tile kt + 1 and its reads of tile kt
-      cta_barrier();                       // ... and every other wave's: tile kt's slots are free
-      issue(2 * kt + SLOTS, ca);
-      issue(2 * kt + SLOTS + 1, cb);
-      read_step(f0a, f0b, FA, FB, na, nb, 0);
-      mfma_step(acc, f1a, f1b);
-      interleave<ND, 2 * NI>();
-      __builtin_amdgcn_sched_barrier(0);
-      ua = un;
-    }
-    {
-      const bf16* ca = smem + ua * OPE;
-      const bf16* cb = smem + (ua + 1 == SLOTS ? 0 : ua + 1) * OPE;
-  #pragma unroll
-      for (int ks = 0; ks + 2 < KS; ks += 2) {
-        __builtin_amdgcn_sched_barrier(0);
-        mfma_step(acc, f0a, f0b);
-        read_step(f1a, f1b, FA, FB, ca, cb, ks + 1);
-        interleave<ND, 0>();
-        __builtin_amdgcn_sched_barrier(0);
-        mfma_step(acc, f1a, f1b);
-        read_step(f0a, f0b, FA, FB, ca, cb, ks + 2);
-        interleave<ND, 0>();
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      mfma_step(acc, f0a, f0b);
-      read_step(f1a, f1b, FA, FB, ca, cb, KS - 1);
-      interleave<ND, 0>();
-      __builtin_amdgcn_sched_barrier(0);
-      mfma_step(acc, f1a, f1b);
-    }
   }
   wait_vm_lgkm0<0>();  // the zero-filling copies past the last tile
   __syncthreads();
   epilogue<EPI, GE>(p, acc, reinterpret_cast<float*>(smem), m0, n0, wave, lane);
 }
 
-// Both operands K-contiguous: the five-slot ring with spread copies.  With an
-// M/N-contiguous operand the transposing fragment reads load the LDS more, and
-// copies arriving in one burst at the end of a K-tile measured faster: two
-// stages.
+// An M/N-contiguous operand tile (64 k-rows of 256 contiguous m or n) staged
+// through registers and written to LDS in the K-contiguous layout, so that
+// its fragments are read with plain 16-byte LDS reads like a K-contiguous
+// operand's (the transposing LDS read costs more LDS time than the MFMAs
+// leave).  Lane (c, g) loads the 8 x 8 block of k-rows 8g .. 8g + 7 and
+// columns 8c .. 8c + 7 (one 16-byte load per k-row), transposes it with byte
+// permutes and writes it as eight 16-byte pieces: row 8c + e, logical chunk g
+// (swizzled like the copied K-contiguous tiles).  Lane assignment:
+// c = 8 wave + 2 (lane >> 4) + ((lane >> 3) & 1), g = lane & 7, so that one
+// load instruction reads eight whole 128-byte lines (8 lanes per k-row), and
+// the 16 lanes of a quarter-wave write 16 different (chunk, row parity) bank
+// groups: of the two c in a quarter-wave, the odd one writes the two rows of
+// each pair in the opposite order.
+struct RegStage {
+  static constexpr int NL = 8;  // loads per lane per K-tile
+  uint32_t off;                 // byte offset of (k-row 8g, column 8c), or OOB past M / N
+  int kr;                       // 8g
+  uint32_t sel0, sel1;          // v_perm selectors of even / odd writes
+  uint32_t wa[4];               // LDS element offset of write 2s (write 2s + 1: ^ 64)
+  u32x4 r[8];                   // r[i]: k-row 8g + i, columns 8c .. 8c + 7
+  __device__ __forceinline__ void init(long ld, int nrows) {
+    const int t = threadIdx.x, lane = t & 63;
+    const int c = 8 * (t >> 6) + 2 * (lane >> 4) + ((lane >> 3) & 1), g = lane & 7;
+    const int cp = c & 1;
+    kr = 8 * g;
+    off = 8 * c < nrows ? (uint32_t)(((long)kr * ld + 8 * c) * 2) : OOB;
+    // element h of a pair of bf16 from k-rows 2t (low half) and 2t + 1 (high)
+    sel0 = cp ? 0x07060302u : 0x05040100u;  // writes 2s: element cp of dword s
+    sel1 = cp ? 0x05040100u : 0x07060302u;  // writes 2s + 1: element 1 - cp
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      wa[q] = (uint32_t)(512 * c + 128 * q + 64 * cp + 8 * (g ^ ((4 * cp + q) & 7)));
+  }
+  template <int I0 = 0, int I1 = NL>
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs, int k0, int K, long ld) {
+#pragma unroll
+    for (int i = I0; i < I1; ++i) {
+      const uint32_t o = (k0 + kr + i < K) ? off : OOB;
+      r[i] = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, o, (uint32_t)((long)(k0 + i) * ld * 2), 0));
+    }
+  }
+  __device__ __forceinline__ void store(bf16* tile) const {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int q = j >> 1;
+      const uint32_t sel = (j & 1) ? sel1 : sel0;
+      u32x4 v;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = __builtin_amdgcn_perm(r[2 * e + 1][q], r[2 * e][q], sel);
+      *reinterpret_cast<u32x4*>(tile + ((j & 1) ? (wa[q] ^ 64u) : wa[q])) = v;
+    }
+  }
+};
+
+// Scheduling template for one k-step of 16 MFMAs: after MFMA i, one DS read
+// if i < ND, one DS write if i < NW, one VMEM instruction if i < NV.
+template <int ND, int NW, int NV>
+__device__ __forceinline__ void interleave3() {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if (i < NV) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    if (i < NW) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+    if (i < ND) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+}
+
+// GEMM with at least one M/N-contiguous operand: those operands are staged
+// through registers (RegStage), a K-contiguous one is copied straight into
+// LDS; two LDS stages, both operands in the K-contiguous layout.  Per K-tile
+// kt, the staged operands of tile kt + 1 are written into the stage that tile
+// kt - 1 released, and the registers are then reloaded with tile kt + 2:
+//  * one staged operand: write in k-step 0, loads in k-step 1, and the copies
+//    of the other operand's tile kt + 2 after the barrier;
+//  * two: A written in k-step 0, B in k-step 1; A's loads over k-steps 0 - 1,
+//    B's over k-steps 2 - 3, so that the address unit sees four loads per
+//    k-step instead of sixteen at once.
+template <int AL, int BL, int EPI, int GE>
+__global__ __launch_bounds__(NT, 1) void gemm256_rs_kernel(GemmArgs p) {
+  constexpr bool RA = AL == LAY_MN, RB = BL == LAY_MN;
+  constexpr int NR = (RA ? 1 : 0) + (RB ? 1 : 0);
+  constexpr int NI = Loader::NI;  // copies per wave, or loads per lane, per operand tile
+  static_assert(NR >= 1 && NI == RegStage::NL, "staged operand count");
+  __shared__ __attribute__((aligned(1024))) bf16 smem[4 * OPE];
+
+  const int M = p.M, N = p.N, K = p.K;
+  int m0, n0;
+  tile_origin(M, N, m0, n0);
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(p.A + (RA ? (long)m0 : (long)m0 * p.lda)), (short)0, 0x7FFFFFFF, 0x00020000);
+  __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(p.B + (RB ? (long)n0 : (long)n0 * p.ldb)), (short)0, 0x7FFFFFFF, 0x00020000);
+  Loader la, lb;
+  RegStage ra, rb;
+  if constexpr (RA) ra.init(p.lda, M - m0); else la.init(p.lda, M - m0, wave);
+  if constexpr (RB) rb.init(p.ldb, N - n0); else lb.init(p.ldb, N - n0, wave);
+  Frags FA, FB;
+  FA.init(wm * 128);
+  FB.init(wn * 128);
+
+  floatx16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  auto copy = [&](int k0, bf16* st) {
+    if constexpr (!RA) la.issue(rsA, k0, K, st, wave);
+    if constexpr (!RB) lb.issue(rsB, k0, K, st + OPE, wave);
+  };
+  const int nk = (K + BK - 1) / BK;
+  // tile 0 and the registers of tile 1; the operations of tile 1 (NI per
+  // operand) are the last issued, so waiting down to 2 NI leaves tile 0 resident
+  if constexpr (RA) ra.load(rsA, 0, K, p.lda);
+  if constexpr (RB) rb.load(rsB, 0, K, p.ldb);
+  copy(0, smem);
+  if constexpr (RA) ra.store(smem);
+  if constexpr (RB) rb.store(smem + OPE);
+  if constexpr (RA) ra.load(rsA, BK, K, p.lda);
+  if constexpr (RB) rb.load(rsB, BK, K, p.ldb);
+  copy(BK, smem + 2 * OPE);
+  wait_vm_lgkm0<2 * NI>();
+  cta_barrier();
+
+  bf16x8 f0a[4], f0b[4], f1a[4], f1b[4];
+  read_step(f0a, f0b, FA, FB, smem, smem + OPE, 0);
+  for (int kt = 0; kt + 1 < nk; ++kt) {
+    bf16* cur = smem + (kt & 1) * 2 * OPE;
+    bf16* nxt = smem + ((kt + 1) & 1) * 2 * OPE;
+    const int k2 = (kt + 2) * BK;
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(acc, f0a, f0b);
+    read_step(f1a, f1b, FA, FB, cur, cur + OPE, 1);
+    if constexpr (NR == 2) {
+      ra.store(nxt);
+      ra.template load<0, NI / 2>(rsA, k2, K, p.lda);
+      interleave3<8, 8, NI / 2>();
+    } else {
+      if constexpr (RA) ra.store(nxt);
+      else rb.store(nxt + OPE);
+      interleave3<8, 8, 0>();
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(acc, f1a, f1b);
+    read_step(f0a, f0b, FA, FB, cur, cur + OPE, 2);
+    if constexpr (NR == 2) {
+      rb.store(nxt + OPE);
+      ra.template load<NI / 2, NI>(rsA, k2, K, p.lda);
+      interleave3<8, 8, NI / 2>();
+    } else {
+      if constexpr (RA) ra.load(rsA, k2, K, p.lda);
+      else rb.load(rsB, k2, K, p.ldb);
+      interleave3<8, 0, NI>();
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(acc, f0a, f0b);
+    read_step(f1a, f1b, FA, FB, cur, cur + OPE, 3);
+    if constexpr (NR == 2) {
+      rb.template load<0, NI / 2>(rsB, k2, K, p.ldb);
+      interleave3<8, 0, NI / 2>();
+    } else {
+      interleave3<8, 0, 0>();
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // this wave's copies of tile kt + 1 (issued before the register loads of
+    // tile kt + 2), its LDS writes and reads; then every other wave's
+    wait_vm_lgkm0<NR * NI>();
+    cta_barrier();
+    copy(k2, cur);
+    if constexpr (NR == 2) rb.template load<NI / 2, NI>(rsB, k2, K, p.ldb);
+    read_step(f0a, f0b, FA, FB, nxt, nxt + OPE, 0);
+    mfma_step(acc, f1a, f1b);
+    interleave3<8, 0, NR == 2 ? NI / 2 : NI>();
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  {
+    const bf16* cur = smem + ((nk - 1) & 1) * 2 * OPE;
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(acc, f0a, f0b);
+    read_step(f1a, f1b, FA, FB, cur, cur + OPE, 1);
+    interleave<8, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(acc, f1a, f1b);
+    read_step(f0a, f0b, FA, FB, cur, cur + OPE, 2);
+    interleave<8, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(acc, f0a, f0b);
+    read_step(f1a, f1b, FA, FB, cur, cur + OPE, 3);
+    interleave<8, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(acc, f1a, f1b);
+  }
+  wait_vm_lgkm0<0>();  // the register loads and copies past the last tile
+  __syncthreads();
+  epilogue<EPI, GE>(p, acc, reinterpret_cast<float*>(smem), m0, n0, wave, lane);
+}
+
 template <int AL, int BL, int EPI>
 hipError_t launch_e(const GemmArgs& a, hipStream_t s) {
-  constexpr int NS = (AL == LAY_K && BL == LAY_K) ? 5 : 2;
   dim3 grid((unsigned)(sat_cdiv(a.M, BT) * sat_cdiv(a.N, BT)));
-  if ((EPI == EPI_BF16 || EPI == EPI_DGELU_BF16) && a.gelu_erf)
-    hipLaunchKernelGGL((gemm256_kernel<AL, BL, EPI, 1, 64, NS>), grid, dim3(NT), 0, s, a);
-  else
-    hipLaunchKernelGGL((gemm256_kernel<AL, BL, EPI, 0, 64, NS>), grid, dim3(NT), 0, s, a);
+  const bool ge = (EPI == EPI_BF16 || EPI == EPI_DGELU_BF16) && a.gelu_erf;
+  if constexpr (AL == LAY_K && BL == LAY_K) {
+    if (ge) hipLaunchKernelGGL((gemm256_kernel<EPI, 1>), grid, dim3(NT), 0, s, a);
+    else hipLaunchKernelGGL((gemm256_kernel<EPI, 0>), grid, dim3(NT), 0, s, a);
+  } else {
+    if (ge) hipLaunchKernelGGL((gemm256_rs_kernel<AL, BL, EPI, 1>), grid, dim3(NT), 0, s, a);
+    else hipLaunchKernelGGL((gemm256_rs_kernel<AL, BL, EPI, 0>), grid, dim3(NT), 0, s, a);
+  }
   return hipGetLastError();
 }
 
