@@ -115,6 +115,15 @@ sat_status sat_op_embed_bwd(const int32_t* tok, const float* dh, float* dwte, in
 sat_status sat_op_colsum(const float* X, int64_t ldx, int32_t rows, int32_t cols, float* out,
                          float* work, void* stream);
 
+/* Transpose of a bf16 matrix: dst[c * ldd + r] = src[r * lds + c] for
+ * r < rows, c < cols.  rows, cols, lds and ldd are multiples of 8 with
+ * lds >= cols, ldd >= rows; both pointers device memory, 16-byte aligned
+ * (SAT_EINVAL otherwise).  The runtime keeps transposed bf16 copies of the
+ * weights for the input-gradient products dX = dY W (each a product over the
+ * contiguous index of both operands). */
+sat_status sat_op_transpose_bf16(const void* src, int64_t lds, void* dst, int64_t ldd,
+                                 int32_t rows, int32_t cols, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

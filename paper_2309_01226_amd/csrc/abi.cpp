@@ -210,6 +210,8 @@ extern "C" sat_status sat_param_write(sat_model* m, int32_t i, const float* host
   st = copy_h2d(m, m->master + p.off, host, (size_t)n * 4);
   if (st != SAT_OK) return st;
   SAT_HIP(launch_f32_to_bf16(m->master + p.off, n, m->shadow + p.off, n, 1, (int)n, m->stream));
+  st = sat_refresh_transposed(m, i);
+  if (st != SAT_OK) return st;
   return sync(m);
 }
 

@@ -122,6 +122,10 @@ hipError_t launch_vit_patch_grad(const float* dh, bf16* dz, int B, int np, int d
 // fp32 -> bf16 copy of a strided matrix (rows x cols)
 hipError_t launch_f32_to_bf16(const float* x, long ldx, bf16* y, long ldy, int rows, int cols,
                               hipStream_t s);
+// dst[c, r] = src[r, c], bf16; rows, cols, strides multiples of 8, 16-byte
+// aligned pointers (hipErrorInvalidValue otherwise).
+hipError_t launch_transpose_bf16(const bf16* src, long lds, bf16* dst, long ldd, int rows,
+                                int cols, hipStream_t s);
 // Cross-entropy fwd+bwd over fp32 logits [N, V]: per-row loss (0 for ignored
 // rows), dz = (softmax - onehot) * inv_n as bf16, count of valid rows.
 // inv_n: device pointer to 1 / (number of labels != -1).

@@ -3,8 +3,9 @@
 // fine-tuning step on the model's HIP stream.
 //
 // Arena (one per model, caller-provided or owned):
-//   fp32 master parameters | bf16 shadow | fp32 gradients | fp32 m | fp32 v |
-//   activations saved for backward | backward workspace.
+//   fp32 master parameters | bf16 shadow | bf16 transposed weights (trainable
+//   matrices of dX = dY W) | fp32 gradients | fp32 m | fp32 v | activations
+//   saved for backward | backward workspace.
 // Parameters run bottom to top (embeddings, blocks 0..L-1, final LN, head),
 // so the tensors frozen by k > 0 form a prefix and AdamW is a single flat
 // kernel over the trainable suffix; frozen gradients and moments are never
@@ -12,6 +13,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <algorithm>
 #include <string>
 #include <vector>
 
@@ -110,6 +112,9 @@ static void add_param(std::vector<ParamDesc>& P, size_t& off, const std::string&
   p.off = off;
   p.group = group;
   p.kind = kind;
+  p.trainable = false;
+  p.toff = SIZE_MAX;
+  p.trows = 0;
   P.push_back(p);
   off = align_up(off + (size_t)rows * cols, kAlignElems);
 }
@@ -160,6 +165,25 @@ void sat_build_params(const sat_config& c, const Dims& D, std::vector<ParamDesc>
   add_param(P, off, "head.w", D.V, d, D.L, 0);
   if (c.arch != SAT_GPT2) add_param(P, off, "head.b", D.V, 1, D.L, 1);
   for (auto& p : P) p.trainable = (p.group < 0) ? (D.k == 0) : (p.group >= D.k);
+  // Transposed copies for the input-gradient products of trainable blocks and
+  // of the head (B operand of dX = dY W, read along W's rows).
+  size_t toff = 0;
+  auto ends_with = [](const std::string& a, const char* b) {
+    const size_t n = strlen(b);
+    return a.size() >= n && a.compare(a.size() - n, n, b) == 0;
+  };
+  for (auto& p : P) {
+    if (!p.trainable || p.group < 0) continue;
+    long trows = 0;
+    if (ends_with(p.name, "attn.qkv.w")) trows = c.arch == SAT_GPTJ ? D.qkv_ld : p.rows;
+    else if (ends_with(p.name, "attn.proj.w") || ends_with(p.name, "mlp.fc2.w")) trows = p.rows;
+    else if (ends_with(p.name, "mlp.fc1.w") && c.arch != SAT_GPTJ) trows = p.rows;
+    else if (p.name == "head.w") trows = D.Vp;
+    if (trows == 0) continue;
+    p.toff = toff;
+    p.trows = trows;
+    toff = align_up(toff + (size_t)trows * p.cols, kAlignElems);
+  }
   // Zero tail: the head's input-gradient product reads up to 7 rows past the
   // last weight matrix when the vocabulary is not a multiple of 8.
   off = align_up(off + (size_t)8 * (d > m ? d : m), kAlignElems);
@@ -187,6 +211,10 @@ size_t carve(sat_model* M, char* base) {
   const size_t NP = M->n_param_elems;
   M->master = c.take<float>(NP);
   M->shadow = c.take<bf16>(NP);
+  size_t n_t = 0;
+  for (const auto& p : M->params)
+    if (p.toff != SIZE_MAX) n_t = std::max(n_t, p.toff + (size_t)p.trows * p.cols);
+  M->shadow_t = c.take<bf16>(n_t > 0 ? n_t : 8);
   M->grad = c.take<float>(NP);
   M->mom = c.take<float>(NP);
   M->vel = c.take<float>(NP);

@@ -27,6 +27,11 @@ struct ParamDesc {
   int group;       // -1 embeddings, l = block, L = final LN + head
   int kind;        // 0 normal init, 1 zeros, 2 ones
   bool trainable;
+  // Transposed bf16 copy [cols, trows] at this element offset of shadow_t
+  // (SIZE_MAX: none).  trows >= rows: the GPT-J q|k|v|fc1 weights are one
+  // [3d + m, d] matrix, the head's covers the padded vocabulary.
+  size_t toff;
+  long trows;
 };
 
 struct LayerActs {
@@ -65,6 +70,7 @@ struct sat_model {
   // parameter-sized sections
   float* master;
   bf16* shadow;
+  bf16* shadow_t;  // transposed copies of the trainable weights of dX = dY W
   float* grad;
   float* mom;
   float* vel;
@@ -110,5 +116,7 @@ sat_status sat_run_forward(sat_model* M, const void* inputs, const int32_t* labe
 sat_status sat_run_backward(sat_model* M, const void* inputs);
 sat_status sat_run_adamw(sat_model* M);
 sat_status sat_run_init(sat_model* M);
+// Rewrites shadow_t from shadow (all transposed weights, or parameter i only).
+sat_status sat_refresh_transposed(sat_model* M, int only = -1);
 
 const LayerActs& sat_layer_acts(const sat_model* M, int l);

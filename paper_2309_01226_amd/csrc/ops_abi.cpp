@@ -190,3 +190,15 @@ extern "C" sat_status sat_op_colsum(const float* X, int64_t ldx, int32_t rows, i
   SAT_HIP(launch_colsum_f32(X, ldx, rows, cols, work, n_part, out, S(stream)));
   return SAT_OK;
 }
+
+extern "C" sat_status sat_op_transpose_bf16(const void* src, int64_t lds, void* dst, int64_t ldd,
+                                            int32_t rows, int32_t cols, void* stream) {
+  SAT_CHECK_ARG(src && dst, "transpose: null pointer");
+  SAT_CHECK_ARG(rows >= 0 && cols >= 0 && rows % 8 == 0 && cols % 8 == 0,
+                "transpose: rows and cols must be multiples of 8");
+  SAT_CHECK_ARG(lds >= cols && ldd >= rows && lds % 8 == 0 && ldd % 8 == 0,
+                "transpose: strides must cover the matrix and be multiples of 8");
+  SAT_CHECK_ARG(((uintptr_t)src | (uintptr_t)dst) % 16 == 0, "transpose: pointers not 16-byte aligned");
+  SAT_HIP(launch_transpose_bf16((const bf16*)src, lds, (bf16*)dst, ldd, rows, cols, S(stream)));
+  return SAT_OK;
+}

@@ -71,6 +71,8 @@ struct PIdx {
 inline const float* master(const sat_model* M, int i) { return M->master + M->params[i].off; }
 inline const bf16* shadow(const sat_model* M, int i) { return M->shadow + M->params[i].off; }
 inline float* grad(sat_model* M, int i) { return M->grad + M->params[i].off; }
+// Transposed bf16 copy [cols, trows] of a weight (B operand of dX = dY W).
+inline const bf16* shadow_t(const sat_model* M, int i) { return M->shadow_t + M->params[i].toff; }
 
 // Index of the first parameter of block l and of the head group.
 int embed_count(const sat_model* M) {
@@ -110,7 +112,7 @@ sat_status sat_run_init(sat_model* M) {
     else
       SAT_HIP(launch_fill(dst, sh, n, p.kind == 2 ? 1.f : 0.f, s));
   }
-  return SAT_OK;
+  return sat_refresh_transposed(M);
 }
 
 sat_status sat_run_forward(sat_model* M, const void* inputs, const int32_t* labels) {
@@ -251,8 +253,8 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
                                  grad(M, hb + 3), s));
     // K = Vp: the padding columns of dz are zero and the parameter arena has a
     // zero tail, so the extra products vanish and the 16-byte path applies.
-    GemmArgs g = gargs(M->dz, D.Vp, shadow(M, hb + 2), d, R, d, D.Vp, M->dA, d);
-    TRY(gemm(M, g, LAY_K, LAY_MN, EPI_F32));
+    GemmArgs g = gargs(M->dz, D.Vp, shadow_t(M, hb + 2), D.Vp, R, d, D.Vp, M->dA, d);
+    TRY(gemm(M, g, LAY_K, LAY_K, EPI_F32));
     SAT_HIP(launch_zero(M->dh, (long)T * d * 4, s));
     const long rstride = (D.arch == SAT_VIT) ? D.S : 1;
     // LN_f backward writes rows r * rstride of dh (CLS rows for ViT)
@@ -298,15 +300,15 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
       GemmArgs w2 = gargs(M->dh_bf, d, A.g, m, d, m, T, grad(M, pb + J_FC2W), m);
       TRY(gemm(M, w2, LAY_MN, LAY_MN, EPI_F32));
       SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + J_FC2B), s));
-      GemmArgs du = gargs(M->dh_bf, d, shadow(M, pb + J_FC2W), m, T, m, d, M->dqkv + 3 * d, D.qkv_ld);
+      GemmArgs du = gargs(M->dh_bf, d, shadow_t(M, pb + J_FC2W), d, T, m, d, M->dqkv + 3 * d, D.qkv_ld);
       du.aux = A.qkv + 3 * d;
       du.ldaux = D.qkv_ld;
       du.gelu_erf = 0;
-      TRY(gemm(M, du, LAY_K, LAY_MN, EPI_DGELU_BF16));
+      TRY(gemm(M, du, LAY_K, LAY_K, EPI_DGELU_BF16));
       GemmArgs wo = gargs(M->dh_bf, d, A.o, d, d, d, T, grad(M, pb + J_PROJW), d);
       TRY(gemm(M, wo, LAY_MN, LAY_MN, EPI_F32));
-      GemmArgs go = gargs(M->dh_bf, d, shadow(M, pb + J_PROJW), d, T, d, d, M->dout, d);
-      TRY(gemm(M, go, LAY_K, LAY_MN, EPI_BF16));
+      GemmArgs go = gargs(M->dh_bf, d, shadow_t(M, pb + J_PROJW), d, T, d, d, M->dout, d);
+      TRY(gemm(M, go, LAY_K, LAY_K, EPI_BF16));
       {
         Timed tm(M, TK_ATTN_BWD, attn_bwd_flops);
         SAT_HIP(launch_attention_bwd(ab, s));
@@ -316,31 +318,32 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
       TRY(gemm(M, wq, LAY_MN, LAY_MN, EPI_F32));
       SAT_HIP(launch_colsum_bf16(M->dqkv + 3 * d, D.qkv_ld, T, m, M->part, npT,
                                  grad(M, pb + J_FC1B), s));
-      GemmArgs ga = gargs(M->dqkv, D.qkv_ld, shadow(M, pb + J_QKVW), d, T, d, D.qkv_ld, M->dA, d);
-      TRY(gemm(M, ga, LAY_K, LAY_MN, EPI_F32));
+      GemmArgs ga = gargs(M->dqkv, D.qkv_ld, shadow_t(M, pb + J_QKVW), D.qkv_ld, T, d, D.qkv_ld,
+                          M->dA, d);
+      TRY(gemm(M, ga, LAY_K, LAY_K, EPI_F32));
       TRY(ln_bwd(M, M->dA, M->h_in[l], 1, pb + J_LN1G, A.mean1, A.rstd1, T));
     } else {
       SAT_HIP(launch_f32_to_bf16(M->dh, d, M->dh_bf, d, T, d, s));
       GemmArgs w2 = gargs(M->dh_bf, d, A.g, m, d, m, T, grad(M, pb + B_FC2W), m);
       TRY(gemm(M, w2, LAY_MN, LAY_MN, EPI_F32));
       SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + B_FC2B), s));
-      GemmArgs du = gargs(M->dh_bf, d, shadow(M, pb + B_FC2W), m, T, m, d, M->du, m);
+      GemmArgs du = gargs(M->dh_bf, d, shadow_t(M, pb + B_FC2W), d, T, m, d, M->du, m);
       du.aux = A.u;
       du.ldaux = m;
       du.gelu_erf = gelu_erf;
-      TRY(gemm(M, du, LAY_K, LAY_MN, EPI_DGELU_BF16));
+      TRY(gemm(M, du, LAY_K, LAY_K, EPI_DGELU_BF16));
       GemmArgs w1 = gargs(M->du, m, A.c, d, m, d, T, grad(M, pb + B_FC1W), d);
       TRY(gemm(M, w1, LAY_MN, LAY_MN, EPI_F32));
       SAT_HIP(launch_colsum_bf16(M->du, m, T, m, M->part, npT, grad(M, pb + B_FC1B), s));
-      GemmArgs gc = gargs(M->du, m, shadow(M, pb + B_FC1W), d, T, d, m, M->dA, d);
-      TRY(gemm(M, gc, LAY_K, LAY_MN, EPI_F32));
+      GemmArgs gc = gargs(M->du, m, shadow_t(M, pb + B_FC1W), m, T, d, m, M->dA, d);
+      TRY(gemm(M, gc, LAY_K, LAY_K, EPI_F32));
       TRY(ln_bwd(M, M->dA, A.h_mid, 1, pb + B_LN2G, A.mean2, A.rstd2, T));
       SAT_HIP(launch_f32_to_bf16(M->dh, d, M->dh_bf, d, T, d, s));
       GemmArgs wo = gargs(M->dh_bf, d, A.o, d, d, d, T, grad(M, pb + B_PROJW), d);
       TRY(gemm(M, wo, LAY_MN, LAY_MN, EPI_F32));
       SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + B_PROJB), s));
-      GemmArgs go = gargs(M->dh_bf, d, shadow(M, pb + B_PROJW), d, T, d, d, M->dout, d);
-      TRY(gemm(M, go, LAY_K, LAY_MN, EPI_BF16));
+      GemmArgs go = gargs(M->dh_bf, d, shadow_t(M, pb + B_PROJW), d, T, d, d, M->dout, d);
+      TRY(gemm(M, go, LAY_K, LAY_K, EPI_BF16));
       {
         Timed tm(M, TK_ATTN_BWD, attn_bwd_flops);
         SAT_HIP(launch_attention_bwd(ab, s));
@@ -348,8 +351,8 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
       GemmArgs wq = gargs(M->dqkv, 3 * d, A.a, d, 3 * d, d, T, grad(M, pb + B_QKVW), d);
       TRY(gemm(M, wq, LAY_MN, LAY_MN, EPI_F32));
       SAT_HIP(launch_colsum_bf16(M->dqkv, 3 * d, T, 3 * d, M->part, npT, grad(M, pb + B_QKVB), s));
-      GemmArgs ga = gargs(M->dqkv, 3 * d, shadow(M, pb + B_QKVW), d, T, d, 3 * d, M->dA, d);
-      TRY(gemm(M, ga, LAY_K, LAY_MN, EPI_F32));
+      GemmArgs ga = gargs(M->dqkv, 3 * d, shadow_t(M, pb + B_QKVW), 3 * d, T, d, 3 * d, M->dA, d);
+      TRY(gemm(M, ga, LAY_K, LAY_K, EPI_F32));
       TRY(ln_bwd(M, M->dA, M->h_in[l], 1, pb + B_LN1G, A.mean1, A.rstd1, T));
     }
   }
@@ -373,15 +376,35 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
   return SAT_OK;
 }
 
+sat_status sat_refresh_transposed(sat_model* M, int only) {
+  for (size_t i = 0; i < M->params.size(); ++i) {
+    const ParamDesc& p = M->params[i];
+    if (p.toff == SIZE_MAX) continue;
+    if (only >= 0) {
+      // the block [off, off + trows * cols) may span several parameters
+      const ParamDesc& q = M->params[only];
+      if (q.off + (size_t)q.rows * q.cols <= p.off || q.off >= p.off + (size_t)p.trows * p.cols)
+        continue;
+    }
+    SAT_HIP(launch_transpose_bf16(M->shadow + p.off, p.cols, M->shadow_t + p.toff, p.trows,
+                                  (int)p.trows, (int)p.cols, M->stream));
+  }
+  return SAT_OK;
+}
+
 sat_status sat_run_adamw(sat_model* M) {
   M->t += 1;
   const sat_config& c = M->cfg;
   size_t off = M->train_off;
   long n = (long)(M->n_param_elems - off);
-  Timed tm(M, TK_ADAMW, 30.0 * n);
+  double nt = 0;
+  for (const auto& p : M->params)
+    if (p.toff != SIZE_MAX) nt += (double)p.trows * p.cols;
+  // bytes: AdamW 30 per element; each transposed weight element read and written as bf16
+  Timed tm(M, TK_ADAMW, 30.0 * n + 4.0 * nt);
   SAT_HIP(launch_adamw(M->master + off, M->grad + off, M->mom + off, M->vel + off,
                        M->shadow + off, n,
                        adamw_consts(c.lr, c.beta1, c.beta2, c.eps, c.weight_decay, M->t),
                        M->stream));
-  return SAT_OK;
+  return sat_refresh_transposed(M);
 }

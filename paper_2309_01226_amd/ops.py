@@ -131,3 +131,11 @@ def embed_bwd(tok, dh, dwte, T, d, V):
 def colsum(X, out, rows, cols, ldx=None):
     work = torch.empty(min(rows, 256) * max(cols, 1), device=X.device, dtype=torch.float32)
     _lib.call("sat_op_colsum", _p(X), ldx or cols, rows, cols, _p(out), _p(work), _stream())
+
+
+def transpose_bf16(src, dst, rows, cols, *, lds=None, ldd=None):
+    """dst[c, r] = src[r, c] (bf16, rows and cols multiples of 8)."""
+    _need(src, torch.bfloat16, "src")
+    _need(dst, torch.bfloat16, "dst")
+    _lib.call("sat_op_transpose_bf16", _p(src), lds or cols, _p(dst), ldd or rows, rows, cols,
+              _stream())

@@ -207,3 +207,29 @@ def test_colsum():
     ops().colsum(to_dev_f32(X), out, 1000, 333)
     torch.cuda.synchronize()
     assert rel(host(out), X.astype(np.float64).sum(axis=0)) < 1e-5
+
+
+# ------------------------------------------------------------------ transpose
+
+@pytest.mark.parametrize("rows,cols,pad_s,pad_d", [(8, 8, 0, 0), (136, 72, 8, 0), (256, 384, 0, 16),
+                                                   (1000, 24, 0, 0), (24, 1000, 8, 8)])
+def test_transpose_bf16(rows, cols, pad_s, pad_d):
+    flush(f"transpose rows={rows} cols={cols} pads={pad_s},{pad_d}")
+    g = torch.Generator().manual_seed(rows * 7 + cols)
+    lds, ldd = cols + pad_s, rows + pad_d
+    src = torch.randn(rows, lds, generator=g).to(torch.bfloat16).cuda()
+    # the padding columns of dst must be left as they were
+    dst = torch.full((cols, ldd), 7.0, dtype=torch.bfloat16).cuda()
+    ops().transpose_bf16(src, dst, rows, cols, lds=lds, ldd=ldd)
+    torch.cuda.synchronize()
+    s, d_ = src.cpu(), dst.cpu()
+    assert torch.equal(d_[:, :rows], s[:, :cols].t())
+    assert bool((d_[:, rows:] == 7.0).all())
+
+
+def test_transpose_bf16_rejects_ragged():
+    from paper_2309_01226_amd._lib import SatError
+    src = torch.zeros(12, 16, dtype=torch.bfloat16, device="cuda")
+    dst = torch.zeros(16, 16, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(SatError):
+        ops().transpose_bf16(src, dst, 12, 16)
