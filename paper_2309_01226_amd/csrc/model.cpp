@@ -270,6 +270,21 @@ size_t carve(sat_model* M, char* base) {
   M->dqkv = c.take<bf16>(T * D.qkv_ld);
   M->du = gptj ? nullptr : c.take<bf16>(T * m);
   M->dout = c.take<bf16>(T * d);
+  M->trans_blocks = T % 8 == 0;
+  M->trans_head = R % 8 == 0;
+  {
+    long na = 0, nb = 0;
+    if (M->trans_blocks) {
+      na = std::max(na, (long)std::max<long>(std::max<long>(d, D.qkv_ld), m) * T);
+      nb = std::max(nb, std::max(d, m) * T);
+    }
+    if (M->trans_head) {
+      na = std::max(na, (long)D.Vp * R);
+      nb = std::max(nb, d * R);
+    }
+    M->tA = na > 0 ? c.take<bf16>(na) : nullptr;
+    M->tB = nb > 0 ? c.take<bf16>(nb) : nullptr;
+  }
   M->delta = c.take<float>((size_t)D.B * D.H * D.S);
   M->n_part = (int)(T < 256 ? T : 256);
   long wide = D.qkv_ld > D.Vp ? D.qkv_ld : D.Vp;

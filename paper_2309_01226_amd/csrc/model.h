@@ -94,6 +94,13 @@ struct sat_model {
   bf16* dqkv;
   bf16* du;
   bf16* dout;
+  // Token-contiguous (transposed) copies of the operands of the weight-gradient
+  // products dW = dY^T X: tA holds dY^T, tB holds X^T (null when the token
+  // count is not a multiple of 8; those products then read the row-major copies).
+  bf16* tA;
+  bf16* tB;
+  bool trans_blocks;  // tA / tB serve the blocks (T % 8 == 0)
+  bool trans_head;    // ... and the head (rows_head % 8 == 0)
   float* delta;
   float* part;
   int n_part;

@@ -221,6 +221,23 @@ sat_status sat_run_forward(sat_model* M, const void* inputs, const int32_t* labe
   return SAT_OK;
 }
 
+// dW[Mr, N] = sum over the T rows of Y[t, m] X[t, n] (Y, X bf16 row-major).
+// With token-contiguous scratch (trans), both operands are first transposed
+// into it (ycols >= Mr: the transposed width of Y, a multiple of 8), so the
+// product reads K-contiguous operands; y_ready: tA already holds Y^T.
+static sat_status wgrad(sat_model* M, bool trans, bool y_ready, const bf16* Y, long ldy,
+                        int ycols, const bf16* X, long ldx, int Mr, int N, int T, float* out,
+                        long ldo) {
+  if (trans) {
+    if (!y_ready) SAT_HIP(launch_transpose_bf16(Y, ldy, M->tA, T, T, ycols, M->stream));
+    SAT_HIP(launch_transpose_bf16(X, ldx, M->tB, T, T, N, M->stream));
+    GemmArgs w = gargs(M->tA, T, M->tB, T, Mr, N, T, out, ldo);
+    return gemm(M, w, LAY_K, LAY_K, EPI_F32);
+  }
+  GemmArgs w = gargs(Y, ldy, X, ldx, Mr, N, T, out, ldo);
+  return gemm(M, w, LAY_MN, LAY_MN, EPI_F32);
+}
+
 static sat_status ln_bwd(sat_model* M, const float* dy, const float* x, long row_stride,
                          int gidx, const float* mean, const float* rstd, int rows) {
   const int d = M->D.d;
@@ -246,8 +263,7 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
 
   // ---- head
   {
-    GemmArgs w = gargs(M->dz, D.Vp, M->f, d, D.V, d, R, grad(M, hb + 2), d);
-    TRY(gemm(M, w, LAY_MN, LAY_MN, EPI_F32));
+    TRY(wgrad(M, M->trans_head, false, M->dz, D.Vp, D.Vp, M->f, d, D.V, d, R, grad(M, hb + 2), d));
     if (D.arch != SAT_GPT2)
       SAT_HIP(launch_colsum_bf16(M->dz, D.Vp, R, D.V, M->part, R < 256 ? R : 256,
                                  grad(M, hb + 3), s));
@@ -297,16 +313,15 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
 
     if (gptj) {
       SAT_HIP(launch_f32_to_bf16(M->dh, d, M->dh_bf, d, T, d, s));
-      GemmArgs w2 = gargs(M->dh_bf, d, A.g, m, d, m, T, grad(M, pb + J_FC2W), m);
-      TRY(gemm(M, w2, LAY_MN, LAY_MN, EPI_F32));
+      const bool tr = M->trans_blocks;
+      TRY(wgrad(M, tr, false, M->dh_bf, d, d, A.g, m, d, m, T, grad(M, pb + J_FC2W), m));
       SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + J_FC2B), s));
       GemmArgs du = gargs(M->dh_bf, d, shadow_t(M, pb + J_FC2W), d, T, m, d, M->dqkv + 3 * d, D.qkv_ld);
       du.aux = A.qkv + 3 * d;
       du.ldaux = D.qkv_ld;
       du.gelu_erf = 0;
       TRY(gemm(M, du, LAY_K, LAY_K, EPI_DGELU_BF16));
-      GemmArgs wo = gargs(M->dh_bf, d, A.o, d, d, d, T, grad(M, pb + J_PROJW), d);
-      TRY(gemm(M, wo, LAY_MN, LAY_MN, EPI_F32));
+      TRY(wgrad(M, tr, true, M->dh_bf, d, d, A.o, d, d, d, T, grad(M, pb + J_PROJW), d));
       GemmArgs go = gargs(M->dh_bf, d, shadow_t(M, pb + J_PROJW), d, T, d, d, M->dout, d);
       TRY(gemm(M, go, LAY_K, LAY_K, EPI_BF16));
       {
@@ -314,8 +329,8 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
         SAT_HIP(launch_attention_bwd(ab, s));
       }
       SAT_HIP(launch_rotary(M->dqkv, D.qkv_ld, D.B, D.S, D.H, D.dh, D.rd, 1, s));
-      GemmArgs wq = gargs(M->dqkv, D.qkv_ld, A.a, d, D.qkv_ld, d, T, grad(M, pb + J_QKVW), d);
-      TRY(gemm(M, wq, LAY_MN, LAY_MN, EPI_F32));
+      TRY(wgrad(M, tr, false, M->dqkv, D.qkv_ld, D.qkv_ld, A.a, d, D.qkv_ld, d, T,
+                grad(M, pb + J_QKVW), d));
       SAT_HIP(launch_colsum_bf16(M->dqkv + 3 * d, D.qkv_ld, T, m, M->part, npT,
                                  grad(M, pb + J_FC1B), s));
       GemmArgs ga = gargs(M->dqkv, D.qkv_ld, shadow_t(M, pb + J_QKVW), D.qkv_ld, T, d, D.qkv_ld,
@@ -324,23 +339,21 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
       TRY(ln_bwd(M, M->dA, M->h_in[l], 1, pb + J_LN1G, A.mean1, A.rstd1, T));
     } else {
       SAT_HIP(launch_f32_to_bf16(M->dh, d, M->dh_bf, d, T, d, s));
-      GemmArgs w2 = gargs(M->dh_bf, d, A.g, m, d, m, T, grad(M, pb + B_FC2W), m);
-      TRY(gemm(M, w2, LAY_MN, LAY_MN, EPI_F32));
+      const bool tr = M->trans_blocks;
+      TRY(wgrad(M, tr, false, M->dh_bf, d, d, A.g, m, d, m, T, grad(M, pb + B_FC2W), m));
       SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + B_FC2B), s));
       GemmArgs du = gargs(M->dh_bf, d, shadow_t(M, pb + B_FC2W), d, T, m, d, M->du, m);
       du.aux = A.u;
       du.ldaux = m;
       du.gelu_erf = gelu_erf;
       TRY(gemm(M, du, LAY_K, LAY_K, EPI_DGELU_BF16));
-      GemmArgs w1 = gargs(M->du, m, A.c, d, m, d, T, grad(M, pb + B_FC1W), d);
-      TRY(gemm(M, w1, LAY_MN, LAY_MN, EPI_F32));
+      TRY(wgrad(M, tr, false, M->du, m, m, A.c, d, m, d, T, grad(M, pb + B_FC1W), d));
       SAT_HIP(launch_colsum_bf16(M->du, m, T, m, M->part, npT, grad(M, pb + B_FC1B), s));
       GemmArgs gc = gargs(M->du, m, shadow_t(M, pb + B_FC1W), m, T, d, m, M->dA, d);
       TRY(gemm(M, gc, LAY_K, LAY_K, EPI_F32));
       TRY(ln_bwd(M, M->dA, A.h_mid, 1, pb + B_LN2G, A.mean2, A.rstd2, T));
       SAT_HIP(launch_f32_to_bf16(M->dh, d, M->dh_bf, d, T, d, s));
-      GemmArgs wo = gargs(M->dh_bf, d, A.o, d, d, d, T, grad(M, pb + B_PROJW), d);
-      TRY(gemm(M, wo, LAY_MN, LAY_MN, EPI_F32));
+      TRY(wgrad(M, tr, false, M->dh_bf, d, d, A.o, d, d, d, T, grad(M, pb + B_PROJW), d));
       SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + B_PROJB), s));
       GemmArgs go = gargs(M->dh_bf, d, shadow_t(M, pb + B_PROJW), d, T, d, d, M->dout, d);
       TRY(gemm(M, go, LAY_K, LAY_K, EPI_BF16));
@@ -348,8 +361,7 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
         Timed tm(M, TK_ATTN_BWD, attn_bwd_flops);
         SAT_HIP(launch_attention_bwd(ab, s));
       }
-      GemmArgs wq = gargs(M->dqkv, 3 * d, A.a, d, 3 * d, d, T, grad(M, pb + B_QKVW), d);
-      TRY(gemm(M, wq, LAY_MN, LAY_MN, EPI_F32));
+      TRY(wgrad(M, tr, false, M->dqkv, 3 * d, 3 * d, A.a, d, 3 * d, d, T, grad(M, pb + B_QKVW), d));
       SAT_HIP(launch_colsum_bf16(M->dqkv, 3 * d, T, 3 * d, M->part, npT, grad(M, pb + B_QKVB), s));
       GemmArgs ga = gargs(M->dqkv, 3 * d, shadow_t(M, pb + B_QKVW), 3 * d, T, d, 3 * d, M->dA, d);
       TRY(gemm(M, ga, LAY_K, LAY_K, EPI_F32));
