@@ -566,6 +566,120 @@ hipError_t launch_adamw(float* p, const float* g, float* m, float* v, bf16* shad
   return hipGetLastError();
 }
 
+// AdamW over a table of segments, one launch per step.  A workgroup finds its
+// segment by binary search on first_block.  Flat segments: 8192 elements per
+// workgroup, float4 groups (offsets are multiples of 64 elements) and a scalar
+// tail.  Matrix segments: a 64 x 64 tile; thread (ty, tx) updates rows
+// 4 ty .. 4 ty + 3, columns 4 tx .. 4 tx + 3, stages the bf16 values
+// transposed in LDS, and the tile is written to shadow_t as 64 rows of 128
+// contiguous bytes.
+__global__ __launch_bounds__(256) void adamw_seg_kernel(float* __restrict__ p,
+                                                        const float* __restrict__ g,
+                                                        float* __restrict__ m,
+                                                        float* __restrict__ v,
+                                                        bf16* __restrict__ shadow,
+                                                        bf16* __restrict__ shadow_t,
+                                                        const AdamWSeg* __restrict__ segs, int nseg,
+                                                        AdamWConsts c) {
+  __shared__ __attribute__((aligned(16))) bf16 tt[64 * 72];  // [column][row], pitch 72
+  const int b = blockIdx.x;
+  int lo = 0, hi = nseg - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (segs[mid].first_block <= b) lo = mid;
+    else hi = mid - 1;
+  }
+  const AdamWSeg sg = segs[lo];
+  const int local = b - sg.first_block;
+  const int t = threadIdx.x;
+  if (sg.toff < 0) {
+    const long n = sg.rows;
+    const long base = sg.off + (long)local * kAdamWChunk;
+    const long cnt = min((long)kAdamWChunk, n - (long)local * kAdamWChunk);
+    const long c4 = cnt / 4;
+    for (long i = t; i < c4; i += 256) {
+      const long j = base + 4 * i;
+      floatx4 pp = __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(p + j));
+      const floatx4 gg = __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(g + j));
+      floatx4 mm = __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(m + j));
+      floatx4 vv = __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(v + j));
+      adamw_four(pp, gg, mm, vv, c);
+      __builtin_nontemporal_store(pp, reinterpret_cast<floatx4*>(p + j));
+      __builtin_nontemporal_store(mm, reinterpret_cast<floatx4*>(m + j));
+      __builtin_nontemporal_store(vv, reinterpret_cast<floatx4*>(v + j));
+      bf16x4 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = f2bf(pp[e]);
+      __builtin_nontemporal_store(o, reinterpret_cast<bf16x4*>(shadow + j));
+    }
+    for (long i = 4 * c4 + t; i < cnt; i += 256) {
+      const long j = base + i;
+      float pp = p[j], mm = m[j], vv = v[j];
+      adamw_one(pp, g[j], mm, vv, c);
+      p[j] = pp;
+      m[j] = mm;
+      v[j] = vv;
+      shadow[j] = f2bf(pp);
+    }
+    return;
+  }
+  const int tiles_n = (sg.cols + 63) / 64;
+  const int r0 = (local / tiles_n) * 64, c0 = (local % tiles_n) * 64;
+  const int ty = t >> 4, tx = t & 15;
+  const int col = c0 + 4 * tx;
+  bf16x4 o[4];  // o[i]: row 4 ty + i, columns 4 tx .. 4 tx + 3
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = r0 + 4 * ty + i;
+    o[i] = bf16x4{f2bf(0.f), f2bf(0.f), f2bf(0.f), f2bf(0.f)};
+    if (r < sg.rows && col < sg.cols) {
+      const long j = sg.off + (long)r * sg.cols + col;
+      floatx4 pp = __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(p + j));
+      const floatx4 gg = __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(g + j));
+      floatx4 mm = __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(m + j));
+      floatx4 vv = __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(v + j));
+      adamw_four(pp, gg, mm, vv, c);
+      __builtin_nontemporal_store(pp, reinterpret_cast<floatx4*>(p + j));
+      __builtin_nontemporal_store(mm, reinterpret_cast<floatx4*>(m + j));
+      __builtin_nontemporal_store(vv, reinterpret_cast<floatx4*>(v + j));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[i][e] = f2bf(pp[e]);
+      __builtin_nontemporal_store(o[i], reinterpret_cast<bf16x4*>(shadow + j));
+    }
+  }
+  // column 4 tx + e of the tile gets rows 4 ty .. 4 ty + 3
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const bf16x4 w = {o[0][e], o[1][e], o[2][e], o[3][e]};
+    *reinterpret_cast<bf16x4*>(tt + (4 * tx + e) * 72 + 4 * ty) = w;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int idx = t + 256 * k;
+    const int cc = idx >> 3, q = idx & 7;  // column of the tile, 8-row piece
+    if (c0 + cc < sg.cols && r0 + 8 * q < sg.trows) {
+      const bf16x8 w = *reinterpret_cast<const bf16x8*>(tt + cc * 72 + 8 * q);
+      __builtin_nontemporal_store(
+          w, reinterpret_cast<bf16x8*>(shadow_t + sg.toff + (long)(c0 + cc) * sg.trows + r0 + 8 * q));
+    }
+  }
+}
+
+int adamw_seg_blocks(const AdamWSeg& g) {
+  if (g.toff < 0) return (int)((g.rows + kAdamWChunk - 1) / kAdamWChunk);
+  return ((g.trows + 63) / 64) * ((g.cols + 63) / 64);
+}
+
+hipError_t launch_adamw_segments(float* p, const float* g, float* m, float* v, bf16* shadow,
+                                 bf16* shadow_t, const AdamWSeg* segs, int nseg,
+                                 int total_blocks, const AdamWConsts& c, hipStream_t s) {
+  if (nseg <= 0 || total_blocks <= 0) return hipSuccess;
+  hipLaunchKernelGGL(adamw_seg_kernel, dim3((unsigned)total_blocks), dim3(256), 0, s, p, g, m, v,
+                     shadow, shadow_t, segs, nseg, c);
+  return hipGetLastError();
+}
+
 hipError_t launch_init_normal(float* p, bf16* shadow, long n, uint64_t seed, uint32_t stream_id,
                               float std, hipStream_t s) {
   if (n <= 0) return hipSuccess;

@@ -148,6 +148,23 @@ struct AdamWConsts {
 AdamWConsts adamw_consts(double lr, double beta1, double beta2, double eps, double wd, long t);
 hipError_t launch_adamw(float* p, const float* g, float* m, float* v, bf16* shadow, long n,
                         const AdamWConsts& c, hipStream_t s);
+// One piece of the trainable parameters for the segmented AdamW below.
+// Flat segment (toff < 0): n = rows elements at off.  Matrix segment: the
+// [rows, cols] row-major matrix at off, updated in 64 x 64 tiles whose bf16
+// values are also written transposed, shadow_t[toff + c * trows + r]; rows
+// rows .. trows - 1 of the transposed copy are written as zeros.
+// first_block: index of the segment's first workgroup (64 x 64 tiles, or
+// chunks of 8192 elements); the table is sorted by it.
+struct AdamWSeg {
+  int64_t off, toff;
+  int32_t rows, trows, cols, first_block;
+};
+constexpr int kAdamWChunk = 8192;
+int adamw_seg_blocks(const AdamWSeg& g);
+// Runs over nseg segments (device table) with total_blocks workgroups.
+hipError_t launch_adamw_segments(float* p, const float* g, float* m, float* v, bf16* shadow,
+                                 bf16* shadow_t, const AdamWSeg* segs, int nseg,
+                                 int total_blocks, const AdamWConsts& c, hipStream_t s);
 // Counter-based N(0, std^2) init of n fp32 values (Philox-style hash of
 // (seed, tensor id, index) fed to Box-Muller); also writes the bf16 shadow.
 hipError_t launch_init_normal(float* p, bf16* shadow, long n, uint64_t seed, uint32_t stream_id,

@@ -203,6 +203,47 @@ struct Carver {
   }
 };
 
+// AdamW segments over the trainable suffix: one matrix segment per weight
+// with a transposed copy (the GPT-J q|k|v weight and the fc1 weight after it
+// form one), flat segments for everything between them (biases, LN
+// parameters, embeddings, alignment gaps and the arena's zero tail).
+void build_segments(sat_model* M) {
+  M->segs.clear();
+  int blocks = 0;
+  auto push = [&](AdamWSeg g) {
+    g.first_block = blocks;
+    blocks += adamw_seg_blocks(g);
+    M->segs.push_back(g);
+  };
+  auto flat = [&](size_t a, size_t b) {
+    while (a < b) {  // pieces below 2^31 elements
+      const size_t n = std::min<size_t>(b - a, (size_t)1 << 30);
+      push(AdamWSeg{(int64_t)a, -1, (int32_t)n, 0, 0, 0});
+      a += n;
+    }
+  };
+  const auto& P = M->params;
+  size_t cur = M->n_param_elems;  // first trainable element
+  for (const auto& p : P)
+    if (p.trainable) cur = std::min(cur, p.off);
+  for (size_t i = 0; i < P.size(); ++i) {
+    const ParamDesc& p = P[i];
+    if (!p.trainable || p.toff == SIZE_MAX || p.off < cur) continue;
+    long rows = p.rows;
+    // parameters stored right after it with the same width belong to the block
+    for (size_t j = i + 1; j < P.size() && rows < p.trows; ++j) {
+      if (P[j].cols != p.cols || P[j].off != p.off + (size_t)rows * p.cols) break;
+      rows += P[j].rows;
+    }
+    flat(cur, p.off);
+    push(AdamWSeg{(int64_t)p.off, (int64_t)p.toff, (int32_t)rows, (int32_t)p.trows,
+                  (int32_t)p.cols, 0});
+    cur = p.off + (size_t)rows * p.cols;
+  }
+  flat(cur, M->n_param_elems);
+  M->seg_blocks = blocks;
+}
+
 // Lays out every buffer; with base == nullptr it only measures.
 size_t carve(sat_model* M, char* base) {
   const Dims& D = M->D;
@@ -215,6 +256,8 @@ size_t carve(sat_model* M, char* base) {
   for (const auto& p : M->params)
     if (p.toff != SIZE_MAX) n_t = std::max(n_t, p.toff + (size_t)p.trows * p.cols);
   M->shadow_t = c.take<bf16>(n_t > 0 ? n_t : 8);
+  build_segments(M);
+  M->segs_dev = c.take<AdamWSeg>(M->segs.size() + 1);
   M->grad = c.take<float>(NP);
   M->mom = c.take<float>(NP);
   M->vel = c.take<float>(NP);

@@ -9,6 +9,7 @@
 #include <vector>
 
 #include "../../include/saturn.h"
+#include "kernels.h"
 
 typedef __bf16 bf16;
 
@@ -71,6 +72,11 @@ struct sat_model {
   float* master;
   bf16* shadow;
   bf16* shadow_t;  // transposed copies of the trainable weights of dX = dY W
+  // AdamW over the trainable parameters: segment table (host copy and device
+  // copy in the arena) and the workgroup count of one launch.
+  std::vector<AdamWSeg> segs;
+  AdamWSeg* segs_dev;
+  int seg_blocks;
   float* grad;
   float* mom;
   float* vel;

@@ -102,6 +102,9 @@ sat_status sat_run_init(sat_model* M) {
   SAT_HIP(launch_zero(M->grad, NP * 4, s));
   SAT_HIP(launch_zero(M->mom, NP * 4, s));
   SAT_HIP(launch_zero(M->vel, NP * 4, s));
+  if (!M->segs.empty())
+    SAT_HIP(hipMemcpyAsync(M->segs_dev, M->segs.data(), M->segs.size() * sizeof(AdamWSeg),
+                           hipMemcpyHostToDevice, s));
   for (size_t i = 0; i < M->params.size(); ++i) {
     const ParamDesc& p = M->params[i];
     long n = p.rows * p.cols;
@@ -412,11 +415,12 @@ sat_status sat_run_adamw(sat_model* M) {
   double nt = 0;
   for (const auto& p : M->params)
     if (p.toff != SIZE_MAX) nt += (double)p.trows * p.cols;
-  // bytes: AdamW 30 per element; each transposed weight element read and written as bf16
-  Timed tm(M, TK_ADAMW, 30.0 * n + 4.0 * nt);
-  SAT_HIP(launch_adamw(M->master + off, M->grad + off, M->mom + off, M->vel + off,
-                       M->shadow + off, n,
-                       adamw_consts(c.lr, c.beta1, c.beta2, c.eps, c.weight_decay, M->t),
-                       M->stream));
-  return sat_refresh_transposed(M);
+  // bytes: 30 per element (fp32 p, g, m, v read; p, m, v and the bf16 copy
+  // written) and 2 per element of the transposed copies
+  Timed tm(M, TK_ADAMW, 30.0 * n + 2.0 * nt);
+  SAT_HIP(launch_adamw_segments(M->master, M->grad, M->mom, M->vel, M->shadow, M->shadow_t,
+                                M->segs_dev, (int)M->segs.size(), M->seg_blocks,
+                                adamw_consts(c.lr, c.beta1, c.beta2, c.eps, c.weight_decay, M->t),
+                                M->stream));
+  return SAT_OK;
 }
