@@ -83,7 +83,8 @@ sat_status sat_op_attention_bwd(const void* q, const void* k, const void* v, int
 
 /* Rotary on interleaved pairs of the first rd dims of every q and k head, in
  * place; qk bf16 [B*S, ld] with q at column 0 and k at column H*dh.
- * inverse = 1 applies the transpose rotation (backward). */
+ * inverse = 1 applies the transpose rotation (backward).  ld and dh even, qk
+ * 4-byte aligned (SAT_EINVAL otherwise). */
 sat_status sat_op_rotary(void* qk, int64_t ld, int32_t B, int32_t S, int32_t H, int32_t dh,
                          int32_t rd, int32_t inverse, void* stream);
 

@@ -13,30 +13,32 @@
 namespace {
 
 // ---------------------------------------------------------------- rotary
-// One thread per (token, q|k, head, pair); angle = pos * 10000^(-2i/rd) in
-// double precision, then the 2x2 rotation (or its transpose for backward).
+// One thread per (token, pair i): angle = pos * 10000^(-2i/rd) in double
+// precision, rounded to float cos / sin once, then the 2x2 rotation (or its
+// transpose for backward) of pair i of every q and k head of the token.
+// Consecutive threads take consecutive pairs, so each head's rotated part is
+// read and written as one contiguous piece (a pair is one 4-byte word).
 __global__ void rotary_kernel(bf16* __restrict__ qk, long ld, int T, int S, int H, int dh, int rd,
                               int inverse) {
   const int half = rd / 2;
   long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  long total = (long)T * 2 * H * half;
-  if (idx >= total) return;
-  int i = idx % half;
-  long r = idx / half;
-  int h = r % H;
-  r /= H;
-  int which = r % 2;
-  int t = (int)(r / 2);
-  int pos = t % S;
+  if (idx >= (long)T * half) return;
+  const int i = idx % half;
+  const int t = (int)(idx / half);
+  const int pos = t % S;
   double ang = (double)pos * pow(10000.0, -2.0 * i / (double)rd);
   double sn, cs;
   sincos(ang, &sn, &cs);
-  float c = (float)cs, s = (float)sn;
-  if (inverse) s = -s;
-  bf16* p = qk + (long)t * ld + (long)which * H * dh + (long)h * dh + 2 * i;
-  float x0 = bf2f(p[0]), x1 = bf2f(p[1]);
-  p[0] = f2bf(x0 * c - x1 * s);
-  p[1] = f2bf(x0 * s + x1 * c);
+  const float c = (float)cs, s = inverse ? -(float)sn : (float)sn;
+  bf16* row = qk + (long)t * ld + 2 * i;
+  for (int hh = 0; hh < 2 * H; ++hh) {  // q heads, then k heads
+    uint32_t* p = reinterpret_cast<uint32_t*>(row + (long)hh * dh);
+    const uint32_t w = *p;
+    const float x0 = __uint_as_float(w << 16), x1 = __uint_as_float(w & 0xFFFF0000u);
+    const bf16 y0 = f2bf(x0 * c - x1 * s), y1 = f2bf(x0 * s + x1 * c);
+    *p = (uint32_t)__builtin_bit_cast(uint16_t, y0) |
+         ((uint32_t)__builtin_bit_cast(uint16_t, y1) << 16);
+  }
 }
 
 // ---------------------------------------------------------------- embedding
@@ -441,8 +443,9 @@ inline unsigned blocks_for(long n, int bs = 256) { return (unsigned)((n + bs - 1
 hipError_t launch_rotary(bf16* qk, long ld, int B, int S, int H, int dh, int rd, int inverse,
                          hipStream_t s) {
   if (rd <= 0) return hipSuccess;
-  if (rd % 2 || rd > dh) return hipErrorInvalidValue;
-  long total = (long)B * S * 2 * H * (rd / 2);
+  if (rd % 2 || rd > dh || ld % 2 || dh % 2 || (reinterpret_cast<uintptr_t>(qk) & 3))
+    return hipErrorInvalidValue;
+  long total = (long)B * S * (rd / 2);
   hipLaunchKernelGGL(rotary_kernel, dim3(blocks_for(total)), dim3(256), 0, s, qk, ld, B * S, S, H,
                      dh, rd, inverse);
   return hipGetLastError();

@@ -139,6 +139,8 @@ extern "C" sat_status sat_op_rotary(void* qk, int64_t ld, int32_t B, int32_t Sq,
   SAT_CHECK_ARG(qk != nullptr, "rotary: null pointer");
   SAT_CHECK_ARG(rd >= 0 && rd % 2 == 0 && rd <= dh, "rotary: rotary dim %d must be even and <= %d", rd, dh);
   SAT_CHECK_ARG(ld >= 2L * H * dh, "rotary: ld too small");
+  SAT_CHECK_ARG(ld % 2 == 0 && dh % 2 == 0 && ((uintptr_t)qk & 3) == 0,
+                "rotary: ld and head dim must be even and qk 4-byte aligned");
   SAT_HIP(launch_rotary((bf16*)qk, ld, B, Sq, H, dh, rd, inverse, S(stream)));
   return SAT_OK;
 }
