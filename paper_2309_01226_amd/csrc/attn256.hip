@@ -190,8 +190,12 @@ __global__ __launch_bounds__(NT, 1) void attn256_fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) bf16 smem[2 * 2 * TILE];  // 2 stages x (K, V)
   const int S = a.S;
   const int nqb = (S + QPB - 1) / QPB;
-  const int qb = a.causal ? (nqb - 1 - (int)blockIdx.x) : (int)blockIdx.x;  // heavy blocks first
-  const int bh = blockIdx.y, b = bh / a.H, h = bh % a.H;
+  // one-dimensional grid, query blocks outermost: with a causal mask every
+  // (batch, head)'s heaviest block is dispatched before any lighter one
+  const int BH = a.B * a.H;
+  const int xb = (int)blockIdx.x / BH, bh = (int)blockIdx.x % BH;
+  const int qb = a.causal ? (nqb - 1 - xb) : xb;
+  const int b = bh / a.H, h = bh % a.H;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 5;
@@ -316,12 +320,15 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dkdv_kernel(AttnBwdArgs a)
   __shared__ __attribute__((aligned(1024))) bf16 smem[2 * STG_B + 4 * 64 * 16 * 2];
   float* xbuf = reinterpret_cast<float*>(smem + 2 * STG_B);  // P exchange: [pair][16][64 lanes]
   const int S = a.f.S;
-  const int bh = blockIdx.y, b = bh / a.f.H, h = bh % a.f.H;
+  // one-dimensional grid, key blocks outermost: with a causal mask the
+  // first key blocks see the most queries and are dispatched first
+  const int BH = a.f.B * a.f.H;
+  const int bh = (int)blockIdx.x % BH, b = bh / a.f.H, h = bh % a.f.H;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 5;
   const int pair = wave & 3, role = wave >> 2;
-  const int k0 = blockIdx.x * KPW;
+  const int k0 = ((int)blockIdx.x / BH) * KPW;
   const int kmin = k0 + pair * 32;
   const int key = kmin + (lane & 31);
   const long hs = ((long)b * a.f.H + h) * S;
@@ -487,8 +494,11 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dq_kernel(AttnBwdArgs a) {
   float* xbuf = reinterpret_cast<float*>(smem + 2 * STG_Q);
   const int S = a.f.S;
   const int nqb = (S + QPW - 1) / QPW;
-  const int qb = a.f.causal ? (nqb - 1 - (int)blockIdx.x) : (int)blockIdx.x;  // heavy blocks first
-  const int bh = blockIdx.y, b = bh / a.f.H, h = bh % a.f.H;
+  // one-dimensional grid, query blocks outermost, heaviest first
+  const int BH = a.f.B * a.f.H;
+  const int xb = (int)blockIdx.x / BH, bh = (int)blockIdx.x % BH;
+  const int qb = a.f.causal ? (nqb - 1 - xb) : xb;
+  const int b = bh / a.f.H, h = bh % a.f.H;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 5;
@@ -624,19 +634,19 @@ bool attn256_bwd_eligible(const AttnBwdArgs& a) {
 }
 
 hipError_t launch_attn256_bwd_dkdv(const AttnBwdArgs& a, hipStream_t s) {
-  dim3 grid((a.f.S + KPW - 1) / KPW, a.f.B * a.f.H);
+  dim3 grid((unsigned)(((a.f.S + KPW - 1) / KPW) * a.f.B * a.f.H));
   hipLaunchKernelGGL(attn256_bwd_dkdv_kernel, grid, dim3(NT8), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_attn256_bwd_dq(const AttnBwdArgs& a, hipStream_t s) {
-  dim3 grid((a.f.S + QPW - 1) / QPW, a.f.B * a.f.H);
+  dim3 grid((unsigned)(((a.f.S + QPW - 1) / QPW) * a.f.B * a.f.H));
   hipLaunchKernelGGL(attn256_bwd_dq_kernel, grid, dim3(NT8), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_attn256_fwd(const AttnArgs& a, hipStream_t s) {
-  dim3 grid((a.S + QPB - 1) / QPB, a.B * a.H);
+  dim3 grid((unsigned)(((a.S + QPB - 1) / QPB) * a.B * a.H));
   hipLaunchKernelGGL(attn256_fwd_kernel, grid, dim3(NT), 0, s, a);
   return hipGetLastError();
 }
