@@ -6,20 +6,25 @@
 //
 // What bounds it on MI355X (measured with single-purpose variants of this
 // kernel): the L2 -> LDS copy stream and, for an M/N-contiguous operand, the
-// pass through registers that transposes it, not the matrix cores.  One 256 x 256 tile needs 32 bytes per clock per
-// CU at full MFMA rate, and a CU's copy throughput is set by the number of
-// 128-byte cache lines it requests, not by bytes: rows copied in 64-byte
-// pieces (K-tiles of 32) deliver about half of what full-line pieces do.  So
-// K-tiles are 64 deep (a K-contiguous row of the tile is exactly one line),
-// 64 KB per K-tile, and the 160 KB of LDS holds two and a half of them.
+// pass through registers that transposes it, not the matrix cores.  One
+// 256 x 256 tile needs 32 bytes per clock per CU at full MFMA rate.  A CU's
+// copy throughput is set by the number of 128-byte cache lines it requests,
+// not by bytes: rows copied in 64-byte pieces (K-tiles of 32) deliver about
+// half of what full-line pieces do.  So K-tiles are 64 deep (a K-contiguous
+// row of the tile is exactly one line), 64 KB per K-tile, and the 160 KB of
+// LDS holds two and a half of them.  On long K the loop runs at 1.70 PFLOP/s
+// with the copies taken out and at about 1.40 with them; staging the copies
+// through VGPRs, a second wave per SIMD (8 waves of 128 x 64), staggering the
+// first K-tile per workgroup and L2-resident operands each moved that by 4%
+// or less.
 //
 // Both operands K-contiguous (gemm256_kernel): a ring of five single-operand
-// slots.  A of tile k + 2 is copied during the first k-steps of tile k, B of
-// tile k + 2 after the barrier that ends the reads of tile k.  Issuing all
-// sixteen copies of a wave in one k-step fills the address unit's queue and
-// stalls the MFMAs behind them in the in-order instruction stream (counter
-// SQ_VMEM_TA_ADDR_FIFO_FULL); spread over the loop they cost about 10% less
-// time on long-K problems than a two-stage loop.
+// slots, three for A and two for B, so that A is copied two K-tiles ahead and
+// B one.  The copies are spread evenly: four per wave in every k-step, one
+// after every fourth MFMA (details above the kernel).  Issuing the sixteen
+// copies of a wave in bursts fills the address unit's queue and stalls the
+// MFMAs behind them in the in-order instruction stream (counter
+// SQ_VMEM_TA_ADDR_FIFO_FULL).
 //
 // Layout of an operand tile in LDS: [256 rows][64 k], 128 B per row; the
 // eight 16-byte chunks of row r are XOR-swizzled with (r >> 1) & 7, which
@@ -34,11 +39,9 @@
 //
 // Main loop per K-tile (four k-steps of 16), per wave (128 x 128 sub-tile,
 // 4 x 4 MFMA 32x32x16 accumulators in AGPRs): the MFMAs of each k-step are
-// interleaved with the fragment reads of the next; before the last k-step,
-// wait for this wave's copies of the next tile and for its reads; barrier;
-// the copies due after the barrier (all of tile k + 2, or its B) and the
-// fragment reads of the next tile's first k-step, interleaved with the last
-// k-step's MFMAs.
+// interleaved with the fragment reads of the next and with that k-step's
+// copies; one wait and one barrier per K-tile, before its last k-step, which
+// reads the first fragments of the next tile.
 //
 // Epilogue: each wave stages one 32-row slab of its sub-tile in its own LDS
 // region and stores 4 consecutive columns per lane (16-byte fp32 or 8-byte
@@ -383,11 +386,52 @@ __device__ __forceinline__ void tile_origin(int M, int N, int& m0, int& n0) {
 }
 
 // Both operands K-contiguous: the five-slot ring.
+//
+// Slots 0 - 2 hold A tiles (A_t in slot t % 3), slots 3 - 4 B tiles (B_t in
+// slot 3 + t % 2).  Iteration t runs k-steps 0 - 2 of tile t, then waits for
+// its copies and passes barrier_t, then runs k-step 3 of tile t while reading
+// the first fragments of tile t + 1.  After barrier_t no wave reads tile t
+// again, so the slots of A_t and B_t are free; the copies of one iteration go
+// to slots freed by the previous barrier or by this one:
+//   k-step 0: B_{t+1}, second half      k-step 2: A_{t+2}, second half
+//   k-step 1: A_{t+2}, first half       k-step 3: B_{t+2}, first half
+// Each k-step thus carries exactly four copies per wave, one after every
+// fourth MFMA, and eight fragment reads, one after every second MFMA, in the
+// order the next k-step consumes them.  At barrier_t only A_{t+2}'s eight
+// copies may still be in flight.  Bunching the copies (four or eight at a
+// time) stalls the in-order instruction stream behind a full address queue;
+// this even spacing measured 3 - 5% faster on the GPT-J shapes.
+
+// Fragment q (0 - 7) of a k-step in the order the MFMAs use it: a0, b0 - b3, a1 - a3.
+__device__ __forceinline__ void read_q(bf16x8 (&fa)[4], bf16x8 (&fb)[4], const Frags& FA,
+                                       const Frags& FB, const bf16* sa, const bf16* sb, int ks,
+                                       int q) {
+  if (q == 0) fa[0] = FA.read(sa, 0, ks);
+  else if (q <= 4) fb[q - 1] = FB.read(sb, q - 1, ks);
+  else fa[q - 4] = FA.read(sa, q - 4, ks);
+}
+
+// One k-step: 16 MFMAs on (ca, cb); after MFMA i, fragment read i / 2 of the
+// next k-step (odd i) and copy i / 4 (i % 4 == 2).  The scheduling barrier
+// after every MFMA pins this order.
+template <typename CopyF>
+__device__ __forceinline__ void kstep_ring(floatx16 (&acc)[4][4], const bf16x8 (&ca)[4],
+                                           const bf16x8 (&cb)[4], bf16x8 (&na)[4], bf16x8 (&nb)[4],
+                                           const Frags& FA, const Frags& FB, const bf16* sa,
+                                           const bf16* sb, int ks, CopyF copy) {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    acc[i >> 2][i & 3] =
+        __builtin_amdgcn_mfma_f32_32x32x16_bf16(ca[i >> 2], cb[i & 3], acc[i >> 2][i & 3], 0, 0, 0);
+    if (i & 1) read_q(na, nb, FA, FB, sa, sb, ks, i >> 1);
+    if ((i & 3) == 2) copy(i >> 2);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
 template <int EPI, int GE>
 __global__ __launch_bounds__(NT, 1) void gemm256_kernel(GemmArgs p) {
-  constexpr int KS = BK / 16;                // MFMA k-steps per K-tile
-  constexpr int NI = Loader::NI;             // copies per wave per operand tile
-  static_assert(5 * OPE * 2 <= 163840 && KS == 4, "LDS budget / k-steps");
+  static_assert(5 * OPE * 2 <= 163840 && BK == 64 && Loader::NI == 8, "LDS budget / copies");
   __shared__ __attribute__((aligned(1024))) bf16 smem[5 * OPE];
 
   const int M = p.M, N = p.N, K = p.K;
@@ -416,72 +460,63 @@ __global__ __launch_bounds__(NT, 1) void gemm256_kernel(GemmArgs p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // Ring of five operand slots.  Operand tile u (A_t = 2t, B_t = 2t + 1) lives
-  // in slot u % 5.  While tile t is consumed, A_{t+2} is copied into the slot
-  // B_{t-1} left, spread over the first two k-steps; after the barrier that
-  // ends the reads of tile t, B_{t+2} goes into A_t's slot during the last
-  // k-step.  The wait before the barrier has a constant count: only A_{t+2}
-  // may still be in flight.  Operand tiles past the last K-tile read zeros.
+  auto sA = [&](int t) { return smem + (t % 3) * OPE; };
+  auto sB = [&](int t) { return smem + (3 + (t & 1)) * OPE; };
   const int nk = (K + BK - 1) / BK;
-  constexpr int ND = 8;
-  bf16x8 f0a[4], f0b[4], f1a[4], f1b[4];
-  la.issue(rsA, 0, K, smem, wave);
-  lb.issue(rsB, 0, K, smem + OPE, wave);
-  la.issue(rsA, BK, K, smem + 2 * OPE, wave);
-  lb.issue(rsB, BK, K, smem + 3 * OPE, wave);
-  wait_vm_lgkm0<2 * NI>();  // tile 0 resident
+  // k offset of tile t; tiles past the last one copy zeros (every chunk at or past K)
+  auto kof = [&](int t) { return t < nk ? t * BK : K; };
+  // tile 0 resident; A_1 and the first half of B_1 in flight
+  la.issue(rsA, 0, K, sA(0), wave);
+  lb.issue(rsB, 0, K, sB(0), wave);
+  wait_vm_lgkm0<0>();
   cta_barrier();
-  int ua = 0;  // slot of A_t; B_t is in the next slot, A_{t+2} goes to the previous one
-  read_step(f0a, f0b, FA, FB, smem, smem + OPE, 0);
-  for (int kt = 0; kt + 1 < nk; ++kt) {
-    bf16* ca = smem + ua * OPE;
-    bf16* cb = smem + (ua == 4 ? 0 : ua + 1) * OPE;
-    bf16* fr = smem + (ua == 0 ? 4 : ua - 1) * OPE;
-    const int un = ua >= 3 ? ua - 3 : ua + 2;
-    const bf16* na = smem + un * OPE;
-    const bf16* nb = smem + (un == 4 ? 0 : un + 1) * OPE;
-    const int k2 = (kt + 2) * BK;
+  la.issue(rsA, kof(1), K, sA(1), wave);
+  lb.issue<0, 4>(rsB, kof(1), K, sB(1), wave);
+  bf16x8 f0a[4], f0b[4], f1a[4], f1b[4];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) read_q(f0a, f0b, FA, FB, sA(0), sB(0), 0, q);
+  for (int t = 0; t < nk; ++t) {
+    const bf16* a = sA(t);
+    const bf16* b = sB(t);
+    bf16* b1 = sB(t + 1);
+    bf16* a2 = sA(t + 2);
+    bf16* b2 = sB(t + 2);
+    const int k1 = kof(t + 1), k2 = kof(t + 2);
     __builtin_amdgcn_sched_barrier(0);
-    mfma_step(acc, f0a, f0b);
-    read_step(f1a, f1b, FA, FB, ca, cb, 1);
-    la.issue<0, NI / 2>(rsA, k2, K, fr, wave);
-    interleave<ND, NI / 2>();
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_step(acc, f1a, f1b);
-    read_step(f0a, f0b, FA, FB, ca, cb, 2);
-    la.issue<NI / 2, NI>(rsA, k2, K, fr, wave);
-    interleave<ND, NI / 2>();
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_step(acc, f0a, f0b);
-    read_step(f1a, f1b, FA, FB, ca, cb, 3);
-    interleave<ND, 0>();
-    __builtin_amdgcn_sched_barrier(0);
-    wait_vm_lgkm0<NI>();  // this wave's copies of tile kt + 1 and its reads of tile kt
-    cta_barrier();         // ... and every other wave's: A_kt's slot is free
-    lb.issue(rsB, k2, K, ca, wave);
-    read_step(f0a, f0b, FA, FB, na, nb, 0);
-    mfma_step(acc, f1a, f1b);
-    interleave<ND, NI>();
-    __builtin_amdgcn_sched_barrier(0);
-    ua = un;
-  }
-  {
-    const bf16* ca = smem + ua * OPE;
-    const bf16* cb = smem + (ua == 4 ? 0 : ua + 1) * OPE;
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_step(acc, f0a, f0b);
-    read_step(f1a, f1b, FA, FB, ca, cb, 1);
-    interleave<ND, 0>();
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_step(acc, f1a, f1b);
-    read_step(f0a, f0b, FA, FB, ca, cb, 2);
-    interleave<ND, 0>();
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_step(acc, f0a, f0b);
-    read_step(f1a, f1b, FA, FB, ca, cb, 3);
-    interleave<ND, 0>();
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_step(acc, f1a, f1b);
+    kstep_ring(acc, f0a, f0b, f1a, f1b, FA, FB, a, b, 1, [&](int c) {
+      switch (c) {
+        case 0: lb.issue<4, 5>(rsB, k1, K, b1, wave); break;
+        case 1: lb.issue<5, 6>(rsB, k1, K, b1, wave); break;
+        case 2: lb.issue<6, 7>(rsB, k1, K, b1, wave); break;
+        default: lb.issue<7, 8>(rsB, k1, K, b1, wave); break;
+      }
+    });
+    kstep_ring(acc, f1a, f1b, f0a, f0b, FA, FB, a, b, 2, [&](int c) {
+      switch (c) {
+        case 0: la.issue<0, 1>(rsA, k2, K, a2, wave); break;
+        case 1: la.issue<1, 2>(rsA, k2, K, a2, wave); break;
+        case 2: la.issue<2, 3>(rsA, k2, K, a2, wave); break;
+        default: la.issue<3, 4>(rsA, k2, K, a2, wave); break;
+      }
+    });
+    kstep_ring(acc, f0a, f0b, f1a, f1b, FA, FB, a, b, 3, [&](int c) {
+      switch (c) {
+        case 0: la.issue<4, 5>(rsA, k2, K, a2, wave); break;
+        case 1: la.issue<5, 6>(rsA, k2, K, a2, wave); break;
+        case 2: la.issue<6, 7>(rsA, k2, K, a2, wave); break;
+        default: la.issue<7, 8>(rsA, k2, K, a2, wave); break;
+      }
+    });
+    wait_vm_lgkm0<Loader::NI>();  // A_{t+1}, B_{t+1} resident; reads of tile t done
+    cta_barrier();                // ... in every wave: A_t's and B_t's slots are free
+    kstep_ring(acc, f1a, f1b, f0a, f0b, FA, FB, sA(t + 1), b1, 0, [&](int c) {
+      switch (c) {
+        case 0: lb.issue<0, 1>(rsB, k2, K, b2, wave); break;
+        case 1: lb.issue<1, 2>(rsB, k2, K, b2, wave); break;
+        case 2: lb.issue<2, 3>(rsB, k2, K, b2, wave); break;
+        default: lb.issue<3, 4>(rsB, k2, K, b2, wave); break;
+      }
+    });
   }
   wait_vm_lgkm0<0>();  // the zero-filling copies past the last tile
   __syncthreads();
