@@ -328,7 +328,7 @@ def main():
     if q_n:
         achieved = q_fl / q_n / (q_ms / q_n * 1e-3) / 1e12
         out["roofline"] = {
-            "kernel": "gemm_kernel<A K-major, B K-major, bf16 epilogue>: fused QKV + fc1 forward "
+            "kernel": "gemm256_kernel<2, 0> (bf16 epilogue, GELU on the fc1 columns): fused QKV + fc1 forward "
                       f"({m.rows()} x {3 * kw['d_model'] + kw['d_mlp'] if kw['arch'] == 'gptj' else 3 * kw['d_model']}"
                       f" x {kw['d_model']})",
             "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
