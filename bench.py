@@ -189,6 +189,9 @@ def bench_grid(args):
     kws = grid_members()
     streams = [torch.cuda.Stream() for _ in kws]
     models = [Model(kw, stream=st) for kw, st in zip(kws, streams)]
+    if args.separate_adamw:
+        for m in models:
+            m.set_option("fused_adamw", 0)
     rows = max(kw["batch"] for kw in kws)
     K, W = args.steps, args.warmup
     batches = []
@@ -242,6 +245,9 @@ def main():
     ap.add_argument("--config", default="gptj", choices=sorted(WORKLOADS))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--separate-adamw", action="store_true",
+                    help="update every tensor in the separate AdamW pass (SAT_OPT_FUSED_ADAMW 0) "
+                         "instead of fusing eligible weights' steps into their weight-gradient products")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration) and exit")
     args = ap.parse_args()
@@ -265,6 +271,8 @@ def main():
     kw = preset(args.config)
     torch.cuda.set_device(0)
     m = Model(kw)
+    if args.separate_adamw:
+        m.set_option("fused_adamw", 0)
     n_all, n_train, flops = m.stats()
     assert abs(flops - step_flops(kw)) <= 1e-9 * flops, (flops, step_flops(kw))
     K, W = args.steps, args.warmup

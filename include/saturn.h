@@ -121,7 +121,10 @@ sat_status sat_param_info(const sat_model* m, int32_t i, const char** name, int6
 sat_status sat_param_read(sat_model* m, int32_t i, float* host);
 /* Writes the fp32 master and refreshes the bf16 shadow. */
 sat_status sat_param_write(sat_model* m, int32_t i, const float* host);
-/* Gradient of the last sat_train_step; zeros for frozen tensors. */
+/* Gradient of the last sat_train_step; zeros for frozen tensors.
+ * SAT_ENOTSUP when that step applied tensor i's AdamW step inside its
+ * weight-gradient product with SAT_OPT_KEEP_GRADS off: that gradient was
+ * never stored. */
 sat_status sat_grad_read(sat_model* m, int32_t i, float* host);
 /* Residual stream entering block `layer` (fp32 [batch * seq, d_model]) after
  * the last forward; layer = n_layers gives the stream entering the final LN. */
@@ -133,6 +136,20 @@ sat_status sat_state_write(sat_model* m, int32_t i, const float* mom, const floa
 /* Number of trainable parameters (elements) and algorithmic FLOPs of one step. */
 sat_status sat_model_stats(const sat_model* m, int64_t* n_params, int64_t* n_trainable,
                            double* step_flops);
+
+/* ---- options ---------------------------------------------------------------
+ * SAT_OPT_FUSED_ADAMW (default 1): the AdamW step of every weight matrix
+ *   whose weight-gradient product runs in the 256 x 256 GEMM kernel is applied
+ *   in that product's epilogue (the same fp32 arithmetic on the same fp32
+ *   gradient as the separate pass), so the gradient makes no round trip
+ *   through the gradient arena.  0: every tensor is updated by the separate
+ *   AdamW pass after the backward.
+ * SAT_OPT_KEEP_GRADS (default 0): 1 also writes the gradients of those
+ *   weights to the gradient arena, so that sat_grad_read returns them.
+ * value is 0 or 1; the setting applies from the next train step.
+ * Errors: SAT_EINVAL (null model, unknown option or value), SAT_ESTATE. */
+typedef enum { SAT_OPT_FUSED_ADAMW = 1, SAT_OPT_KEEP_GRADS = 2 } sat_option;
+sat_status sat_model_set_option(sat_model* m, int32_t option, int32_t value);
 
 /* ---- measurement ---------------------------------------------------------
  * Per-launch timing of one kernel class with HIP events recorded on the

@@ -16,6 +16,7 @@ SAT_OK, SAT_EINVAL, SAT_ENOMEM, SAT_EHIP, SAT_ESTATE, SAT_ENONFINITE, SAT_ENOTSU
 STATUS_NAMES = {0: "SAT_OK", -1: "SAT_EINVAL", -2: "SAT_ENOMEM", -3: "SAT_EHIP", -4: "SAT_ESTATE",
                 -5: "SAT_ENONFINITE", -6: "SAT_ENOTSUP"}
 ARCH = {"gpt2": 0, "gptj": 1, "vit": 2}
+OPTIONS = {"fused_adamw": 1, "keep_grads": 2}
 
 
 class SatError(RuntimeError):
@@ -73,6 +74,7 @@ SIGNATURES = {
     "sat_state_write": (C.c_int, [_VP, _I32, _VP, _VP, C.c_int64]),
     "sat_model_stats": (C.c_int, [_VP, C.POINTER(C.c_int64), C.POINTER(C.c_int64), C.POINTER(C.c_double)]),
     "sat_model_set_timing": (C.c_int, [_VP, _I32, _I32]),
+    "sat_model_set_option": (C.c_int, [_VP, _I32, _I32]),
     "sat_model_timing_read": (C.c_int, [_VP, C.POINTER(C.c_double), C.POINTER(C.c_int64), C.POINTER(C.c_double)]),
     "sat_op_gemm": (C.c_int, [C.POINTER(sat_gemm_desc), _VP]),
     "sat_op_layernorm_fwd": (C.c_int, [_VP, _I64, _I64, _VP, _VP, _VP, _I64, _VP, _VP, _I32, _I32, _F32, _VP]),

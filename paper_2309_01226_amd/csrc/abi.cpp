@@ -84,6 +84,10 @@ extern "C" sat_status sat_model_create(const sat_config* cfg, void* arena, size_
   m->failed = false;
   m->timing_kind = 0;
   m->timing_used = 0;
+  m->opt_fused = true;
+  m->opt_keep_grads = false;
+  m->last_step_fused = false;
+  m->last_step_kept = false;
   hipGetDevice(&m->device);
   size_t need = sat_model_layout(m, nullptr);
   if (arena == nullptr) {
@@ -154,6 +158,7 @@ extern "C" sat_status sat_train_step(sat_model* m, const void* inputs, const int
   if (st != SAT_OK) return st;
   SAT_CHECK_ARG(inputs != nullptr && labels != nullptr, "null inputs or labels");
   st = mark(m, sat_run_forward(m, inputs, labels));
+  if (st == SAT_OK) st = mark(m, sat_adamw_begin(m));
   if (st == SAT_OK) st = mark(m, sat_run_backward(m, inputs));
   if (st == SAT_OK) st = mark(m, sat_run_adamw(m));
   if (st != SAT_OK) return st;
@@ -221,7 +226,31 @@ extern "C" sat_status sat_grad_read(sat_model* m, int32_t i, float* host) {
   if (st != SAT_OK) return st;
   SAT_CHECK_ARG(host != nullptr, "null host buffer");
   const ParamDesc& p = m->params[i];
+  // a weight stored after a fused one in the same matrix (GPT-J fc1 after q|k|v)
+  bool fused = p.fused_opt;
+  for (int32_t j = i - 1; j >= 0 && !fused; --j) {
+    const ParamDesc& q = m->params[j];
+    if (q.toff == SIZE_MAX || q.cols != p.cols || q.off + (size_t)q.trows * q.cols <= p.off) break;
+    fused = q.fused_opt;
+  }
+  if (fused && p.trainable && m->last_step_fused && !m->last_step_kept) {
+    sat_set_error("the gradient of %s was not stored: its AdamW step ran in its weight-gradient "
+                  "product (set SAT_OPT_KEEP_GRADS to keep it)", p.name.c_str());
+    return SAT_ENOTSUP;
+  }
   return copy_d2h(m, host, m->grad + p.off, (size_t)p.rows * p.cols * 4);
+}
+
+extern "C" sat_status sat_model_set_option(sat_model* m, int32_t option, int32_t value) {
+  sat_status st = check_model(m);
+  if (st != SAT_OK) return st;
+  SAT_CHECK_ARG(value == 0 || value == 1, "option value %d is not 0 or 1", value);
+  switch (option) {
+    case SAT_OPT_FUSED_ADAMW: m->opt_fused = value != 0; return SAT_OK;
+    case SAT_OPT_KEEP_GRADS: m->opt_keep_grads = value != 0; return SAT_OK;
+  }
+  sat_set_error("unknown option %d", option);
+  return SAT_EINVAL;
 }
 
 extern "C" sat_status sat_activation_read(sat_model* m, int32_t layer, float* host) {

@@ -9,6 +9,7 @@
 
 #include "common.h"
 #include "kernels.h"
+#include "adamw_math.h"
 
 namespace {
 
@@ -298,26 +299,6 @@ __global__ __launch_bounds__(256) void count_valid_kernel(const int32_t* __restr
 }
 
 // ---------------------------------------------------------------- AdamW
-__device__ __forceinline__ void adamw_one(float& p, float g, float& m, float& v,
-                                          const AdamWConsts& c) {
-  p = p - c.lr_wd * p;
-  m = c.b1 * m + c.omb1 * g;
-  v = c.b2 * v + c.omb2 * g * g;
-  p = p - c.step * m / (sqrtf(v) / c.bc2s + c.eps);
-}
-
-__device__ __forceinline__ void adamw_four(floatx4& p, floatx4 g, floatx4& m, floatx4& v,
-                                           const AdamWConsts& c) {
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    float pe = p[e], me = m[e], ve = v[e];
-    adamw_one(pe, g[e], me, ve, c);
-    p[e] = pe;
-    m[e] = me;
-    v[e] = ve;
-  }
-}
-
 // Grid-stride over float4 groups, two groups per iteration with all eight
 // loads issued first.  Every byte is touched once per step, so loads and
 // stores are non-temporal (they stream past the caches).

@@ -46,6 +46,7 @@
 // Epilogue: each wave stages one 32-row slab of its sub-tile in its own LDS
 // region and stores 4 consecutive columns per lane (16-byte fp32 or 8-byte
 // bf16 vectors), so no workgroup barrier is needed between slabs.
+#include "adamw_math.h"
 #include "common.h"
 #include "kernels.h"
 
@@ -374,6 +375,115 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, floatx16 (&acc)[4][4
   }
 }
 
+// EPI_ADAMW: the tile is the gradient of a weight W [M, N]; apply one AdamW
+// step to the matching elements of W instead of storing the gradient.  Each
+// wave stages a 32-row slab of its fp32 sub-tile in its own LDS region (as the
+// other epilogues do), updates it four rows at a time with the master /
+// moment loads of the next four rows in flight, and stages the updated bf16
+// values transposed ([128 columns][32 rows], pitch TP) in a second region, from
+// which the transposed copy is written as 16-byte pieces of 8 rows.  Element
+// loads and stores stream past the caches: every byte is touched once.
+constexpr int TP = 40;  // bf16 pitch of one column of the transposed staging
+
+__device__ __forceinline__ void epilogue_adamw(const GemmArgs& p, floatx16 (&acc)[4][4],
+                                               float* stage, int m0, int n0, int wave, int lane) {
+  const int wm = wave >> 1, wn = wave & 1;
+  float* st = stage + wave * 32 * EP;
+  bf16* tt = reinterpret_cast<bf16*>(stage + 4 * 32 * EP) + wave * 128 * TP;
+  const int cl = 4 * (lane & 31);
+  const int col = n0 + wn * 128 + cl;
+  const long N = p.N;
+  const bool colok = col < p.N;  // N % 8 == 0: a 4-column vector is wholly inside or outside
+  const AdamWConsts c = p.opt_c;
+  // Buffer resources from the tile's first row: element offsets stay below
+  // 2^31 bytes, and an offset past the range (rows at or past M) reads zeros
+  // and drops stores, so the loop has no branches (which would turn every
+  // wait for loads into a wait for everything).
+  constexpr int NT_AUX = 2;  // nontemporal
+  const long tile0 = (long)m0 * N;
+  auto rsrc = [](const void* q) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(q), (short)0, 0x7FFFFFFF, 0x00020000);
+  };
+  const __amdgpu_buffer_rsrc_t rP = rsrc(p.opt_p + tile0), rM = rsrc(p.opt_m + tile0),
+                               rV = rsrc(p.opt_v + tile0), rS = rsrc(p.opt_sh + tile0);
+  // the wave's first column of the transposed copy
+  const __amdgpu_buffer_rsrc_t rT = rsrc(p.opt_sht + (long)(n0 + wn * 128) * p.opt_trows);
+  const bool keep = p.out != nullptr;
+  const __amdgpu_buffer_rsrc_t rG =
+      rsrc(keep ? reinterpret_cast<float*>(p.out) + (long)m0 * p.ldo : p.opt_p);
+  // fully unrolled: a slab index that is not a compile-time constant would put
+  // the accumulators in scratch memory
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r0 = wm * 128 + 32 * i;  // slab's first row within the tile
+    const long rowbase = m0 + r0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        st[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * EP + 32 * j + (lane & 31)] = acc[i][j][r];
+    // Four groups of four rows per lane, software-pipelined: the loads of
+    // group g + 1 are issued before the stores of group g, because a wave's
+    // one vmcnt counts loads and stores in issue order.
+    auto offs = [&](int g, int u, uint32_t& oe, uint32_t& og) {
+      const int rl = 2 * (4 * g + u) + (lane >> 5);
+      const bool ok = colok && rowbase + rl < p.M;
+      oe = ok ? (uint32_t)(((long)(r0 + rl) * N + col) * 4) : OOB;
+      og = ok ? (uint32_t)(((long)(r0 + rl) * p.ldo + col) * 4) : OOB;
+    };
+    floatx4 pv[2][4], mv[2][4], vv[2][4];
+    auto load = [&](int g, int buf) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        uint32_t oe, og;
+        offs(g, u, oe, og);
+        pv[buf][u] = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(rP, oe, 0, NT_AUX));
+        mv[buf][u] = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(rM, oe, 0, NT_AUX));
+        vv[buf][u] = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(rV, oe, 0, NT_AUX));
+      }
+    };
+    load(0, 0);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int buf = g & 1;
+      if (g + 1 < 4) load(g + 1, buf ^ 1);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int rl = 2 * (4 * g + u) + (lane >> 5);
+        uint32_t oe, og;
+        offs(g, u, oe, og);
+        const floatx4 gv = *reinterpret_cast<const floatx4*>(st + rl * EP + cl);
+        floatx4 pp = pv[buf][u], mm = mv[buf][u], vq = vv[buf][u];
+        adamw_four(pp, gv, mm, vq, c);
+        // rows past M: zeros in the transposed copy (nothing else is stored)
+        const bool ok = oe != OOB;
+        bf16x4 b;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) b[e] = f2bf(ok ? pp[e] : 0.f);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, pp), rP, oe, 0, NT_AUX);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, mm), rM, oe, 0, NT_AUX);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, vq), rV, oe, 0, NT_AUX);
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, b), rS, oe == OOB ? OOB : oe / 2, 0,
+                                              NT_AUX);
+        if (keep) __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, gv), rG, og, 0, NT_AUX);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) tt[(cl + e) * TP + rl] = b[e];
+      }
+    }
+    // column jj of the wave's 128, rows 8 q .. 8 q + 7 of the slab (zeros past M)
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int idx = lane + 64 * k;
+      const int jj = idx >> 2, q = idx & 3;
+      const long r8 = rowbase + 8 * q;
+      const bool ok = n0 + wn * 128 + jj < p.N && r8 < p.opt_trows;
+      const uint32_t o = ok ? (uint32_t)(((long)jj * p.opt_trows + r8) * 2) : OOB;
+      const bf16x8 w = *reinterpret_cast<const bf16x8*>(tt + jj * TP + 8 * q);
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, w), rT, o, 0, NT_AUX);
+    }
+  }
+}
+
 // Output tile of this workgroup.  Workgroups are dealt round-robin over the 8
 // XCDs; renumber so that each XCD walks a contiguous range of the tile order,
 // then order tiles in groups of 8 tile-rows so that the B tiles of a group
@@ -528,7 +638,10 @@ __global__ __launch_bounds__(NT, 1) void gemm256_kernel(GemmArgs p) {
   }
   wait_vm_lgkm0<0>();  // the zero-filling copies past the last tile
   __syncthreads();
-  epilogue<EPI, GE>(p, acc, reinterpret_cast<float*>(smem), m0, n0, wave, lane);
+  if constexpr (EPI == EPI_ADAMW)
+    epilogue_adamw(p, acc, reinterpret_cast<float*>(smem), m0, n0, wave, lane);
+  else
+    epilogue<EPI, GE>(p, acc, reinterpret_cast<float*>(smem), m0, n0, wave, lane);
 }
 
 // An M/N-contiguous operand tile (64 k-rows of 256 contiguous m or n) staged
@@ -738,7 +851,10 @@ template <int AL, int BL, int EPI>
 hipError_t launch_e(const GemmArgs& a, hipStream_t s) {
   dim3 grid((unsigned)(sat_cdiv(a.M, BT) * sat_cdiv(a.N, BT)));
   const bool ge = (EPI == EPI_BF16 || EPI == EPI_DGELU_BF16) && a.gelu_erf;
-  if constexpr (AL == LAY_K && BL == LAY_K) {
+  if constexpr (EPI == EPI_ADAMW) {
+    static_assert(AL == LAY_K && BL == LAY_K, "optimizer epilogue: K-contiguous operands");
+    hipLaunchKernelGGL((gemm256_kernel<EPI, 0>), grid, dim3(NT), 0, s, a);
+  } else if constexpr (AL == LAY_K && BL == LAY_K) {
     if (ge) hipLaunchKernelGGL((gemm256_kernel<EPI, 1>), grid, dim3(NT), 0, s, a);
     else hipLaunchKernelGGL((gemm256_kernel<EPI, 0>), grid, dim3(NT), 0, s, a);
   } else {
@@ -755,6 +871,9 @@ hipError_t launch_l(const GemmArgs& a, int epi, hipStream_t s) {
     case EPI_RESID_F32: return launch_e<AL, BL, EPI_RESID_F32>(a, s);
     case EPI_BF16: return launch_e<AL, BL, EPI_BF16>(a, s);
     case EPI_DGELU_BF16: return launch_e<AL, BL, EPI_DGELU_BF16>(a, s);
+    case EPI_ADAMW:
+      if constexpr (AL == LAY_K && BL == LAY_K) return launch_e<AL, BL, EPI_ADAMW>(a, s);
+      break;
   }
   return hipErrorInvalidValue;
 }
@@ -777,6 +896,14 @@ bool gemm256_eligible(const GemmArgs& a, int alay, int blay, int epi) {
   if (blay == LAY_K ? (a.K % 8 || (long)BT * a.ldb * 2 + 2L * a.K >= lim)
                     : (a.ldb < r8(a.N) || ((long)a.K + 256) * a.ldb * 2 >= lim))
     return false;
+  if (epi == EPI_ADAMW) {
+    // K-contiguous operands; 4-column vectors of W and 8-row pieces of its
+    // transposed copy; the gradient itself only if requested
+    auto a16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
+    return alay == LAY_K && blay == LAY_K && a.N % 8 == 0 && a16(a.opt_p) && a16(a.opt_m) &&
+           a16(a.opt_v) && al(a.opt_sh, 8) && a16(a.opt_sht) && a.opt_trows % 8 == 0 &&
+           a.opt_trows >= a.M && (a.out == nullptr || (a16(a.out) && a.ldo % 4 == 0));
+  }
   // epilogue: 4-column vectors
   if (a.ldo % 4) return false;
   if (epi == EPI_F32 || epi == EPI_RESID_F32) {

@@ -8,6 +8,16 @@
 
 typedef __bf16 bf16;
 
+// ---------------------------------------------------------------- AdamW constants
+// The scalar constants are formed on the host in double precision:
+//   p <- p - lr_wd * p;  m <- b1 m + omb1 g;  v <- b2 v + omb2 g^2;
+//   p <- p - step * m / (sqrt(v) / bc2s + eps)
+// with lr_wd = lr * wd, omb = 1 - beta, step = lr / (1 - beta1^t),
+// bc2s = sqrt(1 - beta2^t).
+struct AdamWConsts {
+  float lr_wd, b1, omb1, b2, omb2, step, bc2s, eps;
+};
+
 // ---------------------------------------------------------------- GEMM
 // C[m, n] = sum_k A(m, k) * B(n, k) on bf16 operands, fp32 accumulation.
 //   A layout 0: A(m, k) = A[m * lda + k]      layout 1: A(m, k) = A[k * lda + m]
@@ -18,6 +28,7 @@ enum GemmEpilogue {
   EPI_RESID_F32 = 1,  // out_f32[m, n] = resid[m, n] + C + bias   (resid may alias out)
   EPI_BF16 = 2,       // out_bf16[m, n] = C + bias; and out2[m, n - gelu_col0] = GELU(C + bias)
   EPI_DGELU_BF16 = 3, // out_bf16[m, n] = C * GELU'(aux[m, n])
+  EPI_ADAMW = 4,      // C is the gradient of a weight: one AdamW step on it (opt_* below)
 };
 
 struct GemmArgs {
@@ -37,6 +48,19 @@ struct GemmArgs {
   const bf16* aux;    // EPI_DGELU_BF16: GELU pre-activation
   long ldaux;
   int gelu_erf;       // 0 = tanh form, 1 = erf form
+  // EPI_ADAMW: C[m, n] is the gradient of the weight W [M, N] (row pitch N)
+  // whose fp32 master values, moments and bf16 copy start at opt_p, opt_m,
+  // opt_v, opt_sh.  The epilogue applies one AdamW step (opt_c) to W, writes
+  // the updated bf16 values there and, transposed, at opt_sht[n * opt_trows +
+  // m] (rows M .. opt_trows - 1 of that copy as zeros), and writes C itself
+  // as fp32 to out (pitch ldo) only when out is not null.
+  float* opt_p;
+  float* opt_m;
+  float* opt_v;
+  bf16* opt_sh;
+  bf16* opt_sht;
+  long opt_trows;
+  AdamWConsts opt_c;
 };
 
 hipError_t launch_gemm(const GemmArgs& a, int alay, int blay, int epi, hipStream_t s);
@@ -137,14 +161,6 @@ hipError_t launch_loss_finalize(const float* row_loss, int n, const float* inv_n
 // inv_n[0] = 1 / max(1, number of labels >= 0)
 hipError_t launch_count_valid(const int32_t* labels, int n, float* inv_n, hipStream_t s);
 // Fused AdamW over n contiguous fp32 parameters with bf16 shadow refresh.
-// The scalar constants are formed on the host in double precision:
-//   p <- p - lr_wd * p;  m <- b1 m + omb1 g;  v <- b2 v + omb2 g^2;
-//   p <- p - step * m / (sqrt(v) / bc2s + eps)
-// with lr_wd = lr * wd, omb = 1 - beta, step = lr / (1 - beta1^t),
-// bc2s = sqrt(1 - beta2^t).
-struct AdamWConsts {
-  float lr_wd, b1, omb1, b2, omb2, step, bc2s, eps;
-};
 AdamWConsts adamw_consts(double lr, double beta1, double beta2, double eps, double wd, long t);
 hipError_t launch_adamw(float* p, const float* g, float* m, float* v, bf16* shadow, long n,
                         const AdamWConsts& c, hipStream_t s);

@@ -115,6 +115,7 @@ static void add_param(std::vector<ParamDesc>& P, size_t& off, const std::string&
   p.trainable = false;
   p.toff = SIZE_MAX;
   p.trows = 0;
+  p.fused_opt = false;
   P.push_back(p);
   off = align_up(off + (size_t)rows * cols, kAlignElems);
 }
@@ -203,45 +204,70 @@ struct Carver {
   }
 };
 
+// Whether the weight-gradient product of a [rows, cols] weight (K = k
+// token-contiguous rows) runs in the 256 x 256 kernel, so that its AdamW step
+// can be fused into the product's epilogue: enough tiles for every CU, whole
+// 8-column vectors, and the transposed copy in pieces of 8 rows.  The operand
+// and parameter sections are 256-byte aligned by construction.
+bool fused_opt_ok(long rows, long cols, long trows, long k) {
+  return k % 8 == 0 && cols % 8 == 0 && trows % 8 == 0 && trows >= rows &&
+         ((rows + 255) / 256) * ((cols + 255) / 256) >= 256;
+}
+
 // AdamW segments over the trainable suffix: one matrix segment per weight
 // with a transposed copy (the GPT-J q|k|v weight and the fc1 weight after it
 // form one), flat segments for everything between them (biases, LN
-// parameters, embeddings, alignment gaps and the arena's zero tail).
+// parameters, embeddings, alignment gaps and the arena's zero tail).  The
+// full table serves the unfused optimizer; the rest table leaves out the
+// matrices whose update is fused into their weight-gradient products.
 void build_segments(sat_model* M) {
-  M->segs.clear();
-  int blocks = 0;
-  auto push = [&](AdamWSeg g) {
-    g.first_block = blocks;
-    blocks += adamw_seg_blocks(g);
-    M->segs.push_back(g);
-  };
-  auto flat = [&](size_t a, size_t b) {
-    while (a < b) {  // pieces below 2^31 elements
-      const size_t n = std::min<size_t>(b - a, (size_t)1 << 30);
-      push(AdamWSeg{(int64_t)a, -1, (int32_t)n, 0, 0, 0});
-      a += n;
+  const Dims& D = M->D;
+  auto& P = M->params;
+  for (auto& p : P) p.fused_opt = false;
+  auto build = [&](bool skip_fused, std::vector<AdamWSeg>& segs, int& blocks, double& bytes) {
+    segs.clear();
+    blocks = 0;
+    bytes = 0.0;
+    auto push = [&](AdamWSeg g) {
+      g.first_block = blocks;
+      blocks += adamw_seg_blocks(g);
+      segs.push_back(g);
+      // 30 bytes per element (fp32 p, g, m, v read; p, m, v, bf16 copy
+      // written), 2 per element of a transposed copy
+      bytes += 30.0 * (double)g.rows * (g.toff < 0 ? 1 : g.cols) +
+               (g.toff < 0 ? 0.0 : 2.0 * (double)g.trows * g.cols);
+    };
+    auto flat = [&](size_t a, size_t b) {
+      while (a < b) {  // pieces below 2^31 elements
+        const size_t n = std::min<size_t>(b - a, (size_t)1 << 30);
+        push(AdamWSeg{(int64_t)a, -1, (int32_t)n, 0, 0, 0});
+        a += n;
+      }
+    };
+    size_t cur = M->n_param_elems;  // first trainable element
+    for (const auto& p : P)
+      if (p.trainable) cur = std::min(cur, p.off);
+    for (size_t i = 0; i < P.size(); ++i) {
+      ParamDesc& p = P[i];
+      if (!p.trainable || p.toff == SIZE_MAX || p.off < cur) continue;
+      long rows = p.rows;
+      // parameters stored right after it with the same width belong to the block
+      for (size_t j = i + 1; j < P.size() && rows < p.trows; ++j) {
+        if (P[j].cols != p.cols || P[j].off != p.off + (size_t)rows * p.cols) break;
+        rows += P[j].rows;
+      }
+      flat(cur, p.off);
+      const long k = p.group == D.L ? D.rows_head : D.T;
+      p.fused_opt = fused_opt_ok(rows, p.cols, p.trows, k);
+      if (!(skip_fused && p.fused_opt))
+        push(AdamWSeg{(int64_t)p.off, (int64_t)p.toff, (int32_t)rows, (int32_t)p.trows,
+                      (int32_t)p.cols, 0});
+      cur = p.off + (size_t)rows * p.cols;
     }
+    flat(cur, M->n_param_elems);
   };
-  const auto& P = M->params;
-  size_t cur = M->n_param_elems;  // first trainable element
-  for (const auto& p : P)
-    if (p.trainable) cur = std::min(cur, p.off);
-  for (size_t i = 0; i < P.size(); ++i) {
-    const ParamDesc& p = P[i];
-    if (!p.trainable || p.toff == SIZE_MAX || p.off < cur) continue;
-    long rows = p.rows;
-    // parameters stored right after it with the same width belong to the block
-    for (size_t j = i + 1; j < P.size() && rows < p.trows; ++j) {
-      if (P[j].cols != p.cols || P[j].off != p.off + (size_t)rows * p.cols) break;
-      rows += P[j].rows;
-    }
-    flat(cur, p.off);
-    push(AdamWSeg{(int64_t)p.off, (int64_t)p.toff, (int32_t)rows, (int32_t)p.trows,
-                  (int32_t)p.cols, 0});
-    cur = p.off + (size_t)rows * p.cols;
-  }
-  flat(cur, M->n_param_elems);
-  M->seg_blocks = blocks;
+  build(false, M->segs, M->seg_blocks, M->seg_bytes);
+  build(true, M->segs_rest, M->seg_rest_blocks, M->seg_rest_bytes);
 }
 
 // Lays out every buffer; with base == nullptr it only measures.
@@ -258,6 +284,7 @@ size_t carve(sat_model* M, char* base) {
   M->shadow_t = c.take<bf16>(n_t > 0 ? n_t : 8);
   build_segments(M);
   M->segs_dev = c.take<AdamWSeg>(M->segs.size() + 1);
+  M->segs_rest_dev = c.take<AdamWSeg>(M->segs_rest.size() + 1);
   M->grad = c.take<float>(NP);
   M->mom = c.take<float>(NP);
   M->vel = c.take<float>(NP);

@@ -33,6 +33,10 @@ struct ParamDesc {
   // [3d + m, d] matrix, the head's covers the padded vocabulary.
   size_t toff;
   long trows;
+  // The AdamW step of this weight (with the parameters stored after it in
+  // the same matrix segment) runs in the epilogue of its weight-gradient
+  // product whenever the optimizer is fused (see sat_model::opt_fused).
+  bool fused_opt;
 };
 
 struct LayerActs {
@@ -77,6 +81,21 @@ struct sat_model {
   std::vector<AdamWSeg> segs;
   AdamWSeg* segs_dev;
   int seg_blocks;
+  double seg_bytes;  // algorithmic bytes of one launch over the table
+  // The same without the matrices whose update is fused into their
+  // weight-gradient products (the table launched when the optimizer is fused).
+  std::vector<AdamWSeg> segs_rest;
+  AdamWSeg* segs_rest_dev;
+  int seg_rest_blocks;
+  double seg_rest_bytes;
+  // Options (sat_model_set_option): fuse the AdamW step of eligible weights
+  // into their weight-gradient products (default on); also write those
+  // weights' gradients to the gradient arena (default off).
+  bool opt_fused;
+  bool opt_keep_grads;
+  bool last_step_fused;   // the last train step updated fused weights in their products
+  bool last_step_kept;    // ... and kept their gradients
+  AdamWConsts adamw_c;    // constants of the step in progress
   float* grad;
   float* mom;
   float* vel;
@@ -127,6 +146,10 @@ double sat_step_flops(const Dims& D);
 // step.cpp
 sat_status sat_run_forward(sat_model* M, const void* inputs, const int32_t* labels);
 sat_status sat_run_backward(sat_model* M, const void* inputs);
+// AdamW: begin (t += 1 and the step's constants, before the backward, whose
+// fused weight-gradient products apply them), end (one launch over the
+// segment table of everything not updated by those products).
+sat_status sat_adamw_begin(sat_model* M);
 sat_status sat_run_adamw(sat_model* M);
 sat_status sat_run_init(sat_model* M);
 // Rewrites shadow_t from shadow (all transposed weights, or parameter i only).

@@ -105,6 +105,9 @@ sat_status sat_run_init(sat_model* M) {
   if (!M->segs.empty())
     SAT_HIP(hipMemcpyAsync(M->segs_dev, M->segs.data(), M->segs.size() * sizeof(AdamWSeg),
                            hipMemcpyHostToDevice, s));
+  if (!M->segs_rest.empty())
+    SAT_HIP(hipMemcpyAsync(M->segs_rest_dev, M->segs_rest.data(),
+                           M->segs_rest.size() * sizeof(AdamWSeg), hipMemcpyHostToDevice, s));
   for (size_t i = 0; i < M->params.size(); ++i) {
     const ParamDesc& p = M->params[i];
     long n = p.rows * p.cols;
@@ -228,13 +231,34 @@ sat_status sat_run_forward(sat_model* M, const void* inputs, const int32_t* labe
 // With token-contiguous scratch (trans), both operands are first transposed
 // into it (ycols >= Mr: the transposed width of Y, a multiple of 8), so the
 // product reads K-contiguous operands; y_ready: tA already holds Y^T.
+// pidx: the weight's parameter index.  When its AdamW step is fused, the
+// product's epilogue applies the step to the weight (and writes the gradient
+// only if the model keeps gradients).
 static sat_status wgrad(sat_model* M, bool trans, bool y_ready, const bf16* Y, long ldy,
-                        int ycols, const bf16* X, long ldx, int Mr, int N, int T, float* out,
-                        long ldo) {
+                        int ycols, const bf16* X, long ldx, int Mr, int N, int T, int pidx) {
+  const ParamDesc& P = M->params[pidx];
+  float* out = grad(M, pidx);
+  const long ldo = P.cols;
   if (trans) {
     if (!y_ready) SAT_HIP(launch_transpose_bf16(Y, ldy, M->tA, T, T, ycols, M->stream));
     SAT_HIP(launch_transpose_bf16(X, ldx, M->tB, T, T, N, M->stream));
     GemmArgs w = gargs(M->tA, T, M->tB, T, Mr, N, T, out, ldo);
+    if (M->opt_fused && P.fused_opt) {
+      if (!M->opt_keep_grads) w.out = nullptr;
+      w.opt_p = M->master + P.off;
+      w.opt_m = M->mom + P.off;
+      w.opt_v = M->vel + P.off;
+      w.opt_sh = M->shadow + P.off;
+      w.opt_sht = M->shadow_t + P.toff;
+      w.opt_trows = P.trows;
+      w.opt_c = M->adamw_c;
+      if (!gemm256_eligible(w, LAY_K, LAY_K, EPI_ADAMW)) {
+        sat_set_error("internal: fused optimizer step of %s not eligible for the 256 x 256 kernel",
+                      P.name.c_str());
+        return SAT_EINVAL;
+      }
+      return gemm(M, w, LAY_K, LAY_K, EPI_ADAMW);
+    }
     return gemm(M, w, LAY_K, LAY_K, EPI_F32);
   }
   GemmArgs w = gargs(Y, ldy, X, ldx, Mr, N, T, out, ldo);
@@ -266,14 +290,16 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
 
   // ---- head
   {
-    TRY(wgrad(M, M->trans_head, false, M->dz, D.Vp, D.Vp, M->f, d, D.V, d, R, grad(M, hb + 2), d));
-    if (D.arch != SAT_GPT2)
-      SAT_HIP(launch_colsum_bf16(M->dz, D.Vp, R, D.V, M->part, R < 256 ? R : 256,
-                                 grad(M, hb + 3), s));
+    // Every input-gradient product of a weight runs before its weight-gradient
+    // product, which may apply the weight's AdamW step in its epilogue.
     // K = Vp: the padding columns of dz are zero and the parameter arena has a
     // zero tail, so the extra products vanish and the 16-byte path applies.
     GemmArgs g = gargs(M->dz, D.Vp, shadow_t(M, hb + 2), D.Vp, R, d, D.Vp, M->dA, d);
     TRY(gemm(M, g, LAY_K, LAY_K, EPI_F32));
+    TRY(wgrad(M, M->trans_head, false, M->dz, D.Vp, D.Vp, M->f, d, D.V, d, R, hb + 2));
+    if (D.arch != SAT_GPT2)
+      SAT_HIP(launch_colsum_bf16(M->dz, D.Vp, R, D.V, M->part, R < 256 ? R : 256,
+                                 grad(M, hb + 3), s));
     SAT_HIP(launch_zero(M->dh, (long)T * d * 4, s));
     const long rstride = (D.arch == SAT_VIT) ? D.S : 1;
     // LN_f backward writes rows r * rstride of dh (CLS rows for ViT)
@@ -317,57 +343,56 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
     if (gptj) {
       SAT_HIP(launch_f32_to_bf16(M->dh, d, M->dh_bf, d, T, d, s));
       const bool tr = M->trans_blocks;
-      TRY(wgrad(M, tr, false, M->dh_bf, d, d, A.g, m, d, m, T, grad(M, pb + J_FC2W), m));
       SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + J_FC2B), s));
       GemmArgs du = gargs(M->dh_bf, d, shadow_t(M, pb + J_FC2W), d, T, m, d, M->dqkv + 3 * d, D.qkv_ld);
       du.aux = A.qkv + 3 * d;
       du.ldaux = D.qkv_ld;
       du.gelu_erf = 0;
       TRY(gemm(M, du, LAY_K, LAY_K, EPI_DGELU_BF16));
-      TRY(wgrad(M, tr, true, M->dh_bf, d, d, A.o, d, d, d, T, grad(M, pb + J_PROJW), d));
       GemmArgs go = gargs(M->dh_bf, d, shadow_t(M, pb + J_PROJW), d, T, d, d, M->dout, d);
       TRY(gemm(M, go, LAY_K, LAY_K, EPI_BF16));
+      TRY(wgrad(M, tr, false, M->dh_bf, d, d, A.g, m, d, m, T, pb + J_FC2W));
+      TRY(wgrad(M, tr, true, M->dh_bf, d, d, A.o, d, d, d, T, pb + J_PROJW));
       {
         Timed tm(M, TK_ATTN_BWD, attn_bwd_flops);
         SAT_HIP(launch_attention_bwd(ab, s));
       }
       SAT_HIP(launch_rotary(M->dqkv, D.qkv_ld, D.B, D.S, D.H, D.dh, D.rd, 1, s));
-      TRY(wgrad(M, tr, false, M->dqkv, D.qkv_ld, D.qkv_ld, A.a, d, D.qkv_ld, d, T,
-                grad(M, pb + J_QKVW), d));
-      SAT_HIP(launch_colsum_bf16(M->dqkv + 3 * d, D.qkv_ld, T, m, M->part, npT,
-                                 grad(M, pb + J_FC1B), s));
       GemmArgs ga = gargs(M->dqkv, D.qkv_ld, shadow_t(M, pb + J_QKVW), D.qkv_ld, T, d, D.qkv_ld,
                           M->dA, d);
       TRY(gemm(M, ga, LAY_K, LAY_K, EPI_F32));
+      TRY(wgrad(M, tr, false, M->dqkv, D.qkv_ld, D.qkv_ld, A.a, d, D.qkv_ld, d, T, pb + J_QKVW));
+      SAT_HIP(launch_colsum_bf16(M->dqkv + 3 * d, D.qkv_ld, T, m, M->part, npT,
+                                 grad(M, pb + J_FC1B), s));
       TRY(ln_bwd(M, M->dA, M->h_in[l], 1, pb + J_LN1G, A.mean1, A.rstd1, T));
     } else {
       SAT_HIP(launch_f32_to_bf16(M->dh, d, M->dh_bf, d, T, d, s));
       const bool tr = M->trans_blocks;
-      TRY(wgrad(M, tr, false, M->dh_bf, d, d, A.g, m, d, m, T, grad(M, pb + B_FC2W), m));
       SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + B_FC2B), s));
       GemmArgs du = gargs(M->dh_bf, d, shadow_t(M, pb + B_FC2W), d, T, m, d, M->du, m);
       du.aux = A.u;
       du.ldaux = m;
       du.gelu_erf = gelu_erf;
       TRY(gemm(M, du, LAY_K, LAY_K, EPI_DGELU_BF16));
-      TRY(wgrad(M, tr, false, M->du, m, m, A.c, d, m, d, T, grad(M, pb + B_FC1W), d));
-      SAT_HIP(launch_colsum_bf16(M->du, m, T, m, M->part, npT, grad(M, pb + B_FC1B), s));
       GemmArgs gc = gargs(M->du, m, shadow_t(M, pb + B_FC1W), m, T, d, m, M->dA, d);
       TRY(gemm(M, gc, LAY_K, LAY_K, EPI_F32));
+      TRY(wgrad(M, tr, false, M->dh_bf, d, d, A.g, m, d, m, T, pb + B_FC2W));
+      TRY(wgrad(M, tr, false, M->du, m, m, A.c, d, m, d, T, pb + B_FC1W));
+      SAT_HIP(launch_colsum_bf16(M->du, m, T, m, M->part, npT, grad(M, pb + B_FC1B), s));
       TRY(ln_bwd(M, M->dA, A.h_mid, 1, pb + B_LN2G, A.mean2, A.rstd2, T));
       SAT_HIP(launch_f32_to_bf16(M->dh, d, M->dh_bf, d, T, d, s));
-      TRY(wgrad(M, tr, false, M->dh_bf, d, d, A.o, d, d, d, T, grad(M, pb + B_PROJW), d));
       SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + B_PROJB), s));
       GemmArgs go = gargs(M->dh_bf, d, shadow_t(M, pb + B_PROJW), d, T, d, d, M->dout, d);
       TRY(gemm(M, go, LAY_K, LAY_K, EPI_BF16));
+      TRY(wgrad(M, tr, false, M->dh_bf, d, d, A.o, d, d, d, T, pb + B_PROJW));
       {
         Timed tm(M, TK_ATTN_BWD, attn_bwd_flops);
         SAT_HIP(launch_attention_bwd(ab, s));
       }
-      TRY(wgrad(M, tr, false, M->dqkv, 3 * d, 3 * d, A.a, d, 3 * d, d, T, grad(M, pb + B_QKVW), d));
-      SAT_HIP(launch_colsum_bf16(M->dqkv, 3 * d, T, 3 * d, M->part, npT, grad(M, pb + B_QKVB), s));
       GemmArgs ga = gargs(M->dqkv, 3 * d, shadow_t(M, pb + B_QKVW), 3 * d, T, d, 3 * d, M->dA, d);
       TRY(gemm(M, ga, LAY_K, LAY_K, EPI_F32));
+      TRY(wgrad(M, tr, false, M->dqkv, 3 * d, 3 * d, A.a, d, 3 * d, d, T, pb + B_QKVW));
+      SAT_HIP(launch_colsum_bf16(M->dqkv, 3 * d, T, 3 * d, M->part, npT, grad(M, pb + B_QKVB), s));
       TRY(ln_bwd(M, M->dA, M->h_in[l], 1, pb + B_LN1G, A.mean1, A.rstd1, T));
     }
   }
@@ -407,20 +432,22 @@ sat_status sat_refresh_transposed(sat_model* M, int only) {
   return SAT_OK;
 }
 
-sat_status sat_run_adamw(sat_model* M) {
+sat_status sat_adamw_begin(sat_model* M) {
   M->t += 1;
   const sat_config& c = M->cfg;
-  size_t off = M->train_off;
-  long n = (long)(M->n_param_elems - off);
-  double nt = 0;
-  for (const auto& p : M->params)
-    if (p.toff != SIZE_MAX) nt += (double)p.trows * p.cols;
-  // bytes: 30 per element (fp32 p, g, m, v read; p, m, v and the bf16 copy
-  // written) and 2 per element of the transposed copies
-  Timed tm(M, TK_ADAMW, 30.0 * n + 2.0 * nt);
+  M->adamw_c = adamw_consts(c.lr, c.beta1, c.beta2, c.eps, c.weight_decay, M->t);
+  M->last_step_fused = M->opt_fused;
+  M->last_step_kept = M->opt_keep_grads;
+  return SAT_OK;
+}
+
+sat_status sat_run_adamw(sat_model* M) {
+  const bool fused = M->opt_fused;
+  const std::vector<AdamWSeg>& segs = fused ? M->segs_rest : M->segs;
+  Timed tm(M, TK_ADAMW, fused ? M->seg_rest_bytes : M->seg_bytes);
   SAT_HIP(launch_adamw_segments(M->master, M->grad, M->mom, M->vel, M->shadow, M->shadow_t,
-                                M->segs_dev, (int)M->segs.size(), M->seg_blocks,
-                                adamw_consts(c.lr, c.beta1, c.beta2, c.eps, c.weight_decay, M->t),
+                                fused ? M->segs_rest_dev : M->segs_dev, (int)segs.size(),
+                                fused ? M->seg_rest_blocks : M->seg_blocks, M->adamw_c,
                                 M->stream));
   return SAT_OK;
 }

@@ -172,6 +172,10 @@ class Model:
         return n.value, nt.value, fl.value
 
     # ---------------------------------------------------------------- timing
+    def set_option(self, name, value):
+        """sat_model_set_option: "fused_adamw" or "keep_grads", value 0 / 1."""
+        _lib.call("sat_model_set_option", self.h, _lib.OPTIONS[name], int(value))
+
     def set_timing(self, kind, max_launches=4096):
         _lib.call("sat_model_set_timing", self.h, kind, max_launches)
 
