@@ -162,6 +162,34 @@ sat_status sat_model_set_timing(sat_model* m, int32_t kind, int32_t max_launches
  * algorithmic work (FLOPs; bytes for AdamW), then resets the counters. */
 sat_status sat_model_timing_read(sat_model* m, double* total_ms, int64_t* launches, double* work);
 
+/* ---- profiling (the Trial Runner's runtime estimate, Sec. 3.2) ------------
+ * Creates a model of cfg on the calling thread's current device (arena and a
+ * synthetic batch of the task's shape allocated and freed by the call), runs
+ * `warmup` untimed and `steps` timed train steps on hip_stream (borrowed; NULL
+ * = the null stream), then destroys it.  The batch comes from a hash of
+ * cfg->seed: decoder tokens uniform in [0, vocab) with next-token labels, ViT
+ * images uniform in [-1, 1) with uniform class labels.  Step times come from
+ * HIP events recorded between consecutive steps on the stream.  Because every
+ * step of a task does the same work, the epoch time is extrapolated as the
+ * mean step time times ceil(samples_per_epoch / batch) (0 samples: no epoch
+ * estimate).  The call waits for the stream.
+ * Errors: SAT_EINVAL (configuration, counts, struct_size), SAT_ENOMEM,
+ * SAT_EHIP.  Out-params are written only on SAT_OK. */
+typedef struct {
+  uint32_t struct_size;  /* set by the caller: sizeof(sat_profile_result) */
+  int32_t steps;         /* timed steps */
+  double step_ms_mean, step_ms_min, step_ms_max;
+  double tokens_per_s;   /* rows entering the loss per second (ViT: batch * (patches + 1)) */
+  double step_tflop;     /* algorithmic FLOPs of one step, 1e12 */
+  double achieved_tflops;
+  int64_t steps_per_epoch;
+  double epoch_ms;       /* extrapolated epoch time */
+  uint64_t arena_bytes;  /* device memory of the model */
+  float final_loss;      /* eval loss on the profiling batch after the last step */
+} sat_profile_result;
+sat_status sat_profile(const sat_config* cfg, void* hip_stream, int32_t warmup, int32_t steps,
+                       int64_t samples_per_epoch, sat_profile_result* out);
+
 const char* sat_last_error(void);
 
 #ifdef __cplusplus

@@ -53,6 +53,16 @@ class sat_gemm_desc(C.Structure):
     ]
 
 
+class sat_profile_result(C.Structure):
+    _fields_ = [
+        ("struct_size", C.c_uint32), ("steps", C.c_int32),
+        ("step_ms_mean", C.c_double), ("step_ms_min", C.c_double), ("step_ms_max", C.c_double),
+        ("tokens_per_s", C.c_double), ("step_tflop", C.c_double), ("achieved_tflops", C.c_double),
+        ("steps_per_epoch", C.c_int64), ("epoch_ms", C.c_double), ("arena_bytes", C.c_uint64),
+        ("final_loss", C.c_float),
+    ]
+
+
 _VP, _I32, _I64, _F32 = C.c_void_p, C.c_int32, C.c_int64, C.c_float
 
 # name -> (restype, argtypes); restype int means a sat_status to check
@@ -75,6 +85,7 @@ SIGNATURES = {
     "sat_model_stats": (C.c_int, [_VP, C.POINTER(C.c_int64), C.POINTER(C.c_int64), C.POINTER(C.c_double)]),
     "sat_model_set_timing": (C.c_int, [_VP, _I32, _I32]),
     "sat_model_set_option": (C.c_int, [_VP, _I32, _I32]),
+    "sat_profile": (C.c_int, [C.POINTER(sat_config), _VP, _I32, _I32, _I64, C.POINTER(sat_profile_result)]),
     "sat_model_timing_read": (C.c_int, [_VP, C.POINTER(C.c_double), C.POINTER(C.c_int64), C.POINTER(C.c_double)]),
     "sat_op_gemm": (C.c_int, [C.POINTER(sat_gemm_desc), _VP]),
     "sat_op_layernorm_fwd": (C.c_int, [_VP, _I64, _I64, _VP, _VP, _VP, _I64, _VP, _VP, _I32, _I32, _F32, _VP]),

@@ -519,6 +519,56 @@ hipError_t launch_loss_finalize(const float* row_loss, int n, const float* inv_n
   return hipGetLastError();
 }
 
+// Synthetic batches for profiling runs: a 32-bit integer hash (the finaliser
+// of MurmurHash3) of (seed, index) gives uniform tokens, labels and image
+// values; token stream b is hashed at positions 0 .. S, inputs take 0 .. S-1
+// and labels 1 .. S (the next token).
+__device__ __forceinline__ uint32_t mix32(uint32_t h) {
+  h ^= h >> 16;
+  h *= 0x85EBCA6Bu;
+  h ^= h >> 13;
+  h *= 0xC2B2AE35u;
+  h ^= h >> 16;
+  return h;
+}
+__device__ __forceinline__ uint32_t hash2(uint32_t seed, uint32_t i) {
+  return mix32(mix32(seed ^ 0x9E3779B9u) + i);
+}
+
+__global__ void synth_tokens_kernel(int32_t* __restrict__ x, int32_t* __restrict__ y, int B, int S,
+                                    int V, uint32_t seed) {
+  const long n = (long)B * S;
+  for (long t = (long)blockIdx.x * blockDim.x + threadIdx.x; t < n; t += (long)gridDim.x * blockDim.x) {
+    const long b = t / S, s = t % S;
+    const uint32_t base = (uint32_t)(b * (S + 1) + s);
+    x[t] = (int32_t)(hash2(seed, base) % (uint32_t)V);
+    y[t] = (int32_t)(hash2(seed, base + 1) % (uint32_t)V);
+  }
+}
+
+__global__ void synth_images_kernel(float* __restrict__ img, long n, int32_t* __restrict__ y, int B,
+                                    int classes, uint32_t seed) {
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x)
+    img[i] = (float)(hash2(seed, (uint32_t)i) >> 8) * (2.f / 16777216.f) - 1.f;  // uniform [-1, 1)
+  const long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < B) y[t] = (int32_t)(hash2(seed ^ 0x5bd1e995u, (uint32_t)t) % (uint32_t)classes);
+}
+
+hipError_t launch_synth_tokens(int32_t* x, int32_t* y, int B, int S, int V, uint32_t seed,
+                               hipStream_t s) {
+  if ((long)B * S <= 0) return hipSuccess;
+  hipLaunchKernelGGL(synth_tokens_kernel, dim3(blocks_for((long)B * S)), dim3(256), 0, s, x, y, B, S,
+                     V, seed);
+  return hipGetLastError();
+}
+
+hipError_t launch_synth_images(float* img, long n, int32_t* y, int B, int classes, uint32_t seed,
+                               hipStream_t s) {
+  hipLaunchKernelGGL(synth_images_kernel, dim3(blocks_for(n > B ? n : B)), dim3(256), 0, s, img, n, y,
+                     B, classes, seed);
+  return hipGetLastError();
+}
+
 hipError_t launch_count_valid(const int32_t* labels, int n, float* inv_n, hipStream_t s) {
   hipLaunchKernelGGL(count_valid_kernel, dim3(1), dim3(256), 0, s, labels, n, inv_n);
   return hipGetLastError();

@@ -160,6 +160,13 @@ hipError_t launch_loss_finalize(const float* row_loss, int n, const float* inv_n
                                 hipStream_t s);
 // inv_n[0] = 1 / max(1, number of labels >= 0)
 hipError_t launch_count_valid(const int32_t* labels, int n, float* inv_n, hipStream_t s);
+// Synthetic profiling batches from a hash of (seed, index): tokens x [B, S]
+// uniform in [0, V) with y the next token of the same stream; images of n
+// values uniform in [-1, 1) with labels y [B] uniform in [0, classes).
+hipError_t launch_synth_tokens(int32_t* x, int32_t* y, int B, int S, int V, uint32_t seed,
+                               hipStream_t s);
+hipError_t launch_synth_images(float* img, long n, int32_t* y, int B, int classes, uint32_t seed,
+                               hipStream_t s);
 // Fused AdamW over n contiguous fp32 parameters with bf16 shadow refresh.
 AdamWConsts adamw_consts(double lr, double beta1, double beta2, double eps, double wd, long t);
 hipError_t launch_adamw(float* p, const float* g, float* m, float* v, bf16* shadow, long n,
