@@ -294,6 +294,8 @@ def main():
                     help="with --config grid: profile, plan and run the grid (stream packing)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--checkpoint", action="store_true",
+                    help="activation checkpointing: recompute each block's activations in the backward")
     ap.add_argument("--separate-adamw", action="store_true",
                     help="update every tensor in the separate AdamW pass (SAT_OPT_FUSED_ADAMW 0) "
                          "instead of fusing eligible weights' steps into their weight-gradient products")
@@ -318,6 +320,8 @@ def main():
     from paper_2309_01226_amd.model import TIMING, Model, device_batch
 
     kw = preset(args.config)
+    if args.checkpoint:
+        kw["checkpoint"] = 1
     torch.cuda.set_device(0)
     m = Model(kw)
     if args.separate_adamw:
@@ -383,7 +387,8 @@ def main():
         "config": {"workload": WORKLOADS[args.config], "name": args.config,
                    "global_batch": kw["batch"], "seq_len": m.rows() // kw["batch"],
                    "tokens_per_step": tokens, "params": n_all, "trainable_params": n_train,
-                   "frozen_layers": kw.get("frozen_layers", 0)},
+                   "frozen_layers": kw.get("frozen_layers", 0), "checkpoint": kw.get("checkpoint", 0),
+                   "arena_gb": m.nbytes / 1e9},
         "step_tflop": flops / 1e12,
         "achieved_tflops": step_tflops,
         "mfu_step": step_tflops / PEAK_BF16_TFLOPS,

@@ -61,6 +61,13 @@ typedef struct {
   int32_t rotary_dim;   /* GPTJ: even, <= head dim; others 0 */
   int32_t batch;        /* rows per step, fixed per model */
   int32_t frozen_layers;/* k in [0, n_layers]: k > 0 freezes the embeddings and blocks [0, k) */
+  int32_t checkpoint;   /* activation checkpointing, 0 or 1: 1 keeps only each block's input
+                          (the residual stream) and recomputes the block's forward activations
+                          just before its backward, with the same kernels on the same input,
+                          so results are bitwise those of 0; saves all but one block's saved
+                          activations, and costs each block's forward except its last
+                          products (GPT-J: out-projection and fc2; GPT2 / VIT: fc2) once more
+                          per step, which the step's algorithmic FLOPs do not count. */
   double lr, beta1, beta2, eps, weight_decay; /* AdamW, decoupled decay on every trainable
                           tensor; double so that 1 - beta is exact to float precision */
   float init_std;       /* std of the N(0, std^2) initialisation of matrices and tables */

@@ -32,6 +32,7 @@ class sat_config(C.Structure):
         ("vocab", C.c_int32), ("seq_len", C.c_int32),
         ("img_size", C.c_int32), ("patch", C.c_int32), ("channels", C.c_int32),
         ("rotary_dim", C.c_int32), ("batch", C.c_int32), ("frozen_layers", C.c_int32),
+        ("checkpoint", C.c_int32),
         ("lr", C.c_double), ("beta1", C.c_double), ("beta2", C.c_double), ("eps", C.c_double),
         ("weight_decay", C.c_double), ("init_std", C.c_float), ("ln_eps", C.c_float),
         ("seed", C.c_uint64),

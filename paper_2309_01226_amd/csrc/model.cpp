@@ -51,6 +51,7 @@ sat_status sat_validate_config(const sat_config* c) {
   SAT_CHECK_ARG(c->batch >= 1, "batch must be >= 1");
   SAT_CHECK_ARG(c->frozen_layers >= 0 && c->frozen_layers <= c->n_layers,
                 "frozen_layers %d not in [0, n_layers]", c->frozen_layers);
+  SAT_CHECK_ARG(c->checkpoint == 0 || c->checkpoint == 1, "checkpoint must be 0 or 1");
   SAT_CHECK_ARG(c->lr >= 0.f && c->beta1 >= 0.f && c->beta1 < 1.f && c->beta2 >= 0.f &&
                     c->beta2 < 1.f && c->eps > 0.f && c->weight_decay >= 0.f,
                 "invalid AdamW hyper-parameters");
@@ -101,6 +102,7 @@ void sat_model_dims(const sat_config& c, Dims* d) {
   d->T = d->B * d->S;
   d->rows_head = (c.arch == SAT_VIT) ? d->B : d->T;
   d->qkv_ld = (c.arch == SAT_GPTJ) ? 3 * d->d + d->m : 3 * d->d;
+  d->ckpt = c.checkpoint != 0;
 }
 
 static void add_param(std::vector<ParamDesc>& P, size_t& off, const std::string& name, long rows,
@@ -293,8 +295,9 @@ size_t carve(sat_model* M, char* base) {
   // residual stream entering every block and the final LN
   M->h_in.assign(D.L + 1, nullptr);
   for (int l = 0; l <= D.L; ++l) M->h_in[l] = c.take<float>(T * d);
-  // per-layer saved activations: blocks >= k get their own, frozen blocks share one set
-  const int nsets = (D.k > 0) ? D.L - D.k + 1 : D.L;
+  // per-layer saved activations: blocks >= k get their own, frozen blocks share
+  // one set; with activation checkpointing every block uses the same set
+  const int nsets = D.ckpt ? 1 : (D.k > 0) ? D.L - D.k + 1 : D.L;
   M->acts.assign(nsets, LayerActs());
   for (int s = 0; s < nsets; ++s) {
     LayerActs& A = M->acts[s];

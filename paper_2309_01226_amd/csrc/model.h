@@ -19,6 +19,7 @@ struct Dims {
   int np, pd;      // ViT: patches per image, values per patch
   int rows_head;   // rows entering the head (T, or B for ViT)
   int qkv_ld;      // row pitch of the q|k|v (|u for GPT-J) buffer
+  bool ckpt;       // activation checkpointing: one saved-activation set, recomputed per block
 };
 
 struct ParamDesc {

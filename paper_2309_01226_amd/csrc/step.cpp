@@ -91,6 +91,7 @@ enum { J_LN1G = 0, J_LN1B, J_QKVW, J_FC1W, J_FC1B, J_PROJW, J_FC2W, J_FC2B };
 
 const LayerActs& sat_layer_acts(const sat_model* M, int l) {
   const int k = M->D.k;
+  if (M->D.ckpt) return M->acts[0];  // one set, rebuilt before each block's backward
   return (l < k) ? M->acts[0] : M->acts[l - k + (k > 0 ? 1 : 0)];
 }
 
@@ -121,13 +122,99 @@ sat_status sat_run_init(sat_model* M) {
   return sat_refresh_transposed(M);
 }
 
-sat_status sat_run_forward(sat_model* M, const void* inputs, const int32_t* labels) {
+// Forward of block l from its input h_in[l] into its saved-activation set.
+// recompute: the activations the backward of block l reads, rebuilt just
+// before it (activation checkpointing) with the same kernels on the same
+// input, so they are bitwise the values of the forward pass; the products
+// whose results only feed the block's output (kept in h_in[l + 1]) are
+// skipped, and nothing is counted in the per-kernel timing.
+static sat_status block_forward(sat_model* M, int l, bool recompute) {
   const Dims& D = M->D;
   hipStream_t s = M->stream;
   const int T = D.T, d = D.d, m = D.m;
   const float eps = M->cfg.ln_eps;
   const int gelu_erf = D.arch == SAT_VIT ? 1 : 0;
   const bool gptj = D.arch == SAT_GPTJ;
+  const int tk_qkv = recompute ? TK_ALL_GEMM : TK_QKV_FWD;
+  const LayerActs& A = sat_layer_acts(M, l);
+  const int pb = block_base(M, l);
+  SAT_HIP(launch_layernorm_fwd(M->h_in[l], d, 1, master(M, pb + 0), master(M, pb + 1), A.a, d,
+                               A.mean1, A.rstd1, T, d, eps, s));
+  if (gptj) {
+    // fused q | k | v | u = a [W_qkv; W_fc1]^T (+ fc1 bias on u), g = GELU(u)
+    GemmArgs a = gargs(A.a, d, shadow(M, pb + J_QKVW), d, T, D.qkv_ld, d, A.qkv, D.qkv_ld);
+    a.bias = master(M, pb + J_FC1B);
+    a.bias_col0 = 3 * d;
+    a.out2 = A.g;
+    a.ldo2 = m;
+    a.gelu_col0 = 3 * d;
+    a.gelu_erf = 0;
+    TRY(gemm(M, a, LAY_K, LAY_K, EPI_BF16, tk_qkv));
+    SAT_HIP(launch_rotary(A.qkv, D.qkv_ld, D.B, D.S, D.H, D.dh, D.rd, 0, s));
+  } else {
+    GemmArgs a = gargs(A.a, d, shadow(M, pb + B_QKVW), d, T, 3 * d, d, A.qkv, 3 * d);
+    a.bias = master(M, pb + B_QKVB);
+    TRY(gemm(M, a, LAY_K, LAY_K, EPI_BF16, tk_qkv));
+  }
+  {
+    AttnArgs at;
+    at.q = A.qkv;
+    at.k = A.qkv + d;
+    at.v = A.qkv + 2 * d;
+    at.ldq = at.ldk = at.ldv = D.qkv_ld;
+    at.o = A.o;
+    at.ldo = d;
+    at.lse = A.lse;
+    at.B = D.B;
+    at.H = D.H;
+    at.S = D.S;
+    at.dh = D.dh;
+    at.causal = D.arch != SAT_VIT;
+    at.scale = 1.f / sqrtf((float)D.dh);
+    if (recompute) {
+      SAT_HIP(launch_attention_fwd(at, s));
+    } else {
+      Timed tm(M, TK_ATTN_FWD, 4.0 * D.B * D.H * (double)D.S * D.S * D.dh * (at.causal ? 0.5 : 1.0));
+      SAT_HIP(launch_attention_fwd(at, s));
+    }
+  }
+  if (gptj) {
+    if (recompute) return SAT_OK;
+    GemmArgs a = gargs(A.o, d, shadow(M, pb + J_PROJW), d, T, d, d, M->h_in[l + 1], d);
+    a.resid = M->h_in[l];
+    TRY(gemm(M, a, LAY_K, LAY_K, EPI_RESID_F32));
+    GemmArgs b = gargs(A.g, m, shadow(M, pb + J_FC2W), m, T, d, m, M->h_in[l + 1], d);
+    b.resid = M->h_in[l + 1];
+    b.bias = master(M, pb + J_FC2B);
+    TRY(gemm(M, b, LAY_K, LAY_K, EPI_RESID_F32));
+  } else {
+    GemmArgs a = gargs(A.o, d, shadow(M, pb + B_PROJW), d, T, d, d, A.h_mid, d);
+    a.resid = M->h_in[l];
+    a.bias = master(M, pb + B_PROJB);
+    TRY(gemm(M, a, LAY_K, LAY_K, EPI_RESID_F32));
+    SAT_HIP(launch_layernorm_fwd(A.h_mid, d, 1, master(M, pb + B_LN2G), master(M, pb + B_LN2B),
+                                 A.c, d, A.mean2, A.rstd2, T, d, eps, s));
+    GemmArgs b = gargs(A.c, d, shadow(M, pb + B_FC1W), d, T, m, d, A.u, m);
+    b.bias = master(M, pb + B_FC1B);
+    b.out2 = A.g;
+    b.ldo2 = m;
+    b.gelu_col0 = 0;
+    b.gelu_erf = gelu_erf;
+    TRY(gemm(M, b, LAY_K, LAY_K, EPI_BF16));
+    if (recompute) return SAT_OK;
+    GemmArgs c = gargs(A.g, m, shadow(M, pb + B_FC2W), m, T, d, m, M->h_in[l + 1], d);
+    c.resid = A.h_mid;
+    c.bias = master(M, pb + B_FC2B);
+    TRY(gemm(M, c, LAY_K, LAY_K, EPI_RESID_F32));
+  }
+  return SAT_OK;
+}
+
+sat_status sat_run_forward(sat_model* M, const void* inputs, const int32_t* labels) {
+  const Dims& D = M->D;
+  hipStream_t s = M->stream;
+  const int T = D.T, d = D.d;
+  const float eps = M->cfg.ln_eps;
 
   // ---- embeddings
   if (D.arch == SAT_VIT) {
@@ -144,73 +231,7 @@ sat_status sat_run_forward(sat_model* M, const void* inputs, const int32_t* labe
   }
 
   // ---- blocks
-  for (int l = 0; l < D.L; ++l) {
-    const LayerActs& A = sat_layer_acts(M, l);
-    const int pb = block_base(M, l);
-    SAT_HIP(launch_layernorm_fwd(M->h_in[l], d, 1, master(M, pb + 0), master(M, pb + 1), A.a, d,
-                                 A.mean1, A.rstd1, T, d, eps, s));
-    if (gptj) {
-      // fused q | k | v | u = a [W_qkv; W_fc1]^T (+ fc1 bias on u), g = GELU(u)
-      GemmArgs a = gargs(A.a, d, shadow(M, pb + J_QKVW), d, T, D.qkv_ld, d, A.qkv, D.qkv_ld);
-      a.bias = master(M, pb + J_FC1B);
-      a.bias_col0 = 3 * d;
-      a.out2 = A.g;
-      a.ldo2 = m;
-      a.gelu_col0 = 3 * d;
-      a.gelu_erf = 0;
-      TRY(gemm(M, a, LAY_K, LAY_K, EPI_BF16, TK_QKV_FWD));
-      SAT_HIP(launch_rotary(A.qkv, D.qkv_ld, D.B, D.S, D.H, D.dh, D.rd, 0, s));
-    } else {
-      GemmArgs a = gargs(A.a, d, shadow(M, pb + B_QKVW), d, T, 3 * d, d, A.qkv, 3 * d);
-      a.bias = master(M, pb + B_QKVB);
-      TRY(gemm(M, a, LAY_K, LAY_K, EPI_BF16, TK_QKV_FWD));
-    }
-    {
-      AttnArgs at;
-      at.q = A.qkv;
-      at.k = A.qkv + d;
-      at.v = A.qkv + 2 * d;
-      at.ldq = at.ldk = at.ldv = D.qkv_ld;
-      at.o = A.o;
-      at.ldo = d;
-      at.lse = A.lse;
-      at.B = D.B;
-      at.H = D.H;
-      at.S = D.S;
-      at.dh = D.dh;
-      at.causal = D.arch != SAT_VIT;
-      at.scale = 1.f / sqrtf((float)D.dh);
-      Timed tm(M, TK_ATTN_FWD, 4.0 * D.B * D.H * (double)D.S * D.S * D.dh * (at.causal ? 0.5 : 1.0));
-      SAT_HIP(launch_attention_fwd(at, s));
-    }
-    if (gptj) {
-      GemmArgs a = gargs(A.o, d, shadow(M, pb + J_PROJW), d, T, d, d, M->h_in[l + 1], d);
-      a.resid = M->h_in[l];
-      TRY(gemm(M, a, LAY_K, LAY_K, EPI_RESID_F32));
-      GemmArgs b = gargs(A.g, m, shadow(M, pb + J_FC2W), m, T, d, m, M->h_in[l + 1], d);
-      b.resid = M->h_in[l + 1];
-      b.bias = master(M, pb + J_FC2B);
-      TRY(gemm(M, b, LAY_K, LAY_K, EPI_RESID_F32));
-    } else {
-      GemmArgs a = gargs(A.o, d, shadow(M, pb + B_PROJW), d, T, d, d, A.h_mid, d);
-      a.resid = M->h_in[l];
-      a.bias = master(M, pb + B_PROJB);
-      TRY(gemm(M, a, LAY_K, LAY_K, EPI_RESID_F32));
-      SAT_HIP(launch_layernorm_fwd(A.h_mid, d, 1, master(M, pb + B_LN2G), master(M, pb + B_LN2B),
-                                   A.c, d, A.mean2, A.rstd2, T, d, eps, s));
-      GemmArgs b = gargs(A.c, d, shadow(M, pb + B_FC1W), d, T, m, d, A.u, m);
-      b.bias = master(M, pb + B_FC1B);
-      b.out2 = A.g;
-      b.ldo2 = m;
-      b.gelu_col0 = 0;
-      b.gelu_erf = gelu_erf;
-      TRY(gemm(M, b, LAY_K, LAY_K, EPI_BF16));
-      GemmArgs c = gargs(A.g, m, shadow(M, pb + B_FC2W), m, T, d, m, M->h_in[l + 1], d);
-      c.resid = A.h_mid;
-      c.bias = master(M, pb + B_FC2B);
-      TRY(gemm(M, c, LAY_K, LAY_K, EPI_RESID_F32));
-    }
-  }
+  for (int l = 0; l < D.L; ++l) TRY(block_forward(M, l, false));
 
   // ---- final LN, head, cross-entropy
   const int hb = head_base(M);
@@ -314,6 +335,7 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
 
   // ---- blocks L-1 .. k
   for (int l = D.L - 1; l >= D.k; --l) {
+    if (D.ckpt) TRY(block_forward(M, l, true));
     const LayerActs& A = sat_layer_acts(M, l);
     const int pb = block_base(M, l);
     AttnBwdArgs ab;

@@ -15,7 +15,7 @@ from . import _lib
 def make_config(arch, n_layers, d_model, n_heads, d_mlp, vocab, seq_len=0, batch=1,
                 frozen_layers=0, rotary_dim=0, img_size=0, patch=0, channels=3, lr=1e-3,
                 beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01, init_std=0.02, ln_eps=1e-5,
-                seed=0):
+                seed=0, checkpoint=0):
     c = _lib.sat_config()
     c.struct_size = C.sizeof(_lib.sat_config)
     c.arch = _lib.ARCH[arch]
@@ -23,6 +23,7 @@ def make_config(arch, n_layers, d_model, n_heads, d_mlp, vocab, seq_len=0, batch
     c.vocab, c.seq_len = vocab, seq_len
     c.img_size, c.patch, c.channels = img_size, patch, channels
     c.rotary_dim, c.batch, c.frozen_layers = rotary_dim, batch, frozen_layers
+    c.checkpoint = int(checkpoint)
     c.lr, c.beta1, c.beta2, c.eps, c.weight_decay = lr, beta1, beta2, eps, weight_decay
     c.init_std, c.ln_eps, c.seed = init_std, ln_eps, seed
     return c
