@@ -29,7 +29,14 @@ extern "C" {
  * equal out).  2: bf16 out = C + bias, and, when out2 != NULL, bf16
  * out2[m, n - gelu_col0] = GELU(C + bias) for n >= gelu_col0.  3: bf16 out =
  * C * GELU'(aux[m, n]).  bias (fp32, may be NULL) applies to columns
- * n >= bias_col0 as bias[n - bias_col0].  gelu_erf: 0 tanh form, 1 erf form. */
+ * n >= bias_col0 as bias[n - bias_col0].  gelu_erf: 0 tanh form, 1 erf form.
+ * splitk_ws (fp32 device scratch of splitk_ws_elems elements, may be NULL):
+ * with it, an epilogue-0/1 product on layout-0 operands that has fewer than
+ * 256 output tiles of 256 x 256 and K >= 1024 runs split-K: K slices of at
+ * least 512 write fp32 partials there, then one reduction adds them in slice
+ * order with bias and residual.  Results then differ from the unsplit
+ * product by summation order only.  The scratch is used only when it holds
+ * slices * M * N elements; the call makes no allocation. */
 typedef struct {
   const void* A;
   const void* B;
@@ -48,6 +55,8 @@ typedef struct {
   const void* aux;
   int64_t ldaux;
   int32_t gelu_erf;
+  float* splitk_ws;
+  int64_t splitk_ws_elems;
 } sat_gemm_desc;
 sat_status sat_op_gemm(const sat_gemm_desc* d, void* stream);
 

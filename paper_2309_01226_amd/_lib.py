@@ -51,6 +51,7 @@ class sat_gemm_desc(C.Structure):
         ("out2", C.c_void_p), ("ldo2", C.c_int64), ("gelu_col0", C.c_int32),
         ("aux", C.c_void_p), ("ldaux", C.c_int64),
         ("gelu_erf", C.c_int32),
+        ("splitk_ws", C.c_void_p), ("splitk_ws_elems", C.c_int64),
     ]
 
 

@@ -639,6 +639,30 @@ inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 
 hipError_t launch_gemm(const GemmArgs& a, int alay, int blay, int epi, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   if (a.K <= 0) return hipErrorInvalidValue;
+  // fp32 outputs with too few tiles to fill the chip: split-K into the
+  // caller's workspace, then one reduction that applies bias and residual
+  if ((epi == EPI_F32 || epi == EPI_RESID_F32) && alay == LAY_K && blay == LAY_K &&
+      a.splitk <= 1 && a.splitk_ws != nullptr) {
+    int kc = 0;
+    const int S = gemm_splitk(a.M, a.N, a.K, &kc);
+    if (S > 1 && (long)S * a.M * a.N <= a.splitk_ws_elems) {
+      GemmArgs b = a;
+      b.out = a.splitk_ws;
+      b.ldo = a.N;
+      b.bias = nullptr;
+      b.resid = nullptr;
+      b.splitk = S;
+      b.splitk_kc = kc;
+      b.split_stride = (long)a.M * a.N;
+      if (gemm256_eligible(b, LAY_K, LAY_K, EPI_F32)) {
+        hipError_t e = launch_gemm256(b, LAY_K, LAY_K, EPI_F32, s);
+        if (e != hipSuccess) return e;
+        return launch_splitk_reduce(a.splitk_ws, S, b.split_stride, a.M, a.N,
+                                    reinterpret_cast<float*>(a.out), a.ldo, a.bias, a.bias_col0,
+                                    epi == EPI_RESID_F32 ? a.resid : nullptr, a.ldr, s);
+      }
+    }
+  }
   if (gemm256_eligible(a, alay, blay, epi)) return launch_gemm256(a, alay, blay, epi, s);
   // the optimizer epilogue exists in the 256 x 256 kernel only
   if (epi == EPI_ADAMW) return hipErrorInvalidValue;

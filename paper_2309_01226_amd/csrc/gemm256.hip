@@ -46,6 +46,8 @@
 // Epilogue: each wave stages one 32-row slab of its sub-tile in its own LDS
 // region and stores 4 consecutive columns per lane (16-byte fp32 or 8-byte
 // bf16 vectors), so no workgroup barrier is needed between slabs.
+#include <algorithm>
+
 #include "adamw_math.h"
 #include "common.h"
 #include "kernels.h"
@@ -488,11 +490,18 @@ __device__ __forceinline__ void epilogue_adamw(const GemmArgs& p, floatx16 (&acc
 // XCDs; renumber so that each XCD walks a contiguous range of the tile order,
 // then order tiles in groups of 8 tile-rows so that the B tiles of a group
 // stay in L2.
-__device__ __forceinline__ void tile_origin(int M, int N, int& m0, int& n0) {
-  const int tiles_m = (M + BT - 1) / BT, tiles_n = (N + BT - 1) / BT;
-  const int nwg = tiles_m * tiles_n;
+// With split-K the grid is (slice, tile) pairs: the renumbered id gives the
+// slice (id / tiles) and the tile (id % tiles), so each XCD walks tiles of one
+// slice.
+__device__ __forceinline__ int xcd_order_id() {
+  const int nwg = gridDim.x;
   int bid = blockIdx.x;
   if ((nwg & 7) == 0) bid = (bid & 7) * (nwg >> 3) + (bid >> 3);
+  return bid;
+}
+
+__device__ __forceinline__ void tile_origin(int M, int N, int bid, int& m0, int& n0) {
+  const int tiles_m = (M + BT - 1) / BT, tiles_n = (N + BT - 1) / BT;
   constexpr int G = 8;
   const int per_group = G * tiles_n;
   const int group = bid / per_group;
@@ -552,17 +561,28 @@ __global__ __launch_bounds__(NT, 1) void gemm256_kernel(GemmArgs p) {
   static_assert(5 * OPE * 2 <= 163840 && BK == 64 && Loader::NI == 8, "LDS budget / copies");
   __shared__ __attribute__((aligned(1024))) bf16 smem[5 * OPE];
 
-  const int M = p.M, N = p.N, K = p.K;
-  int m0, n0;
-  tile_origin(M, N, m0, n0);
+  const int M = p.M, N = p.N;
+  int m0, n0, bid = xcd_order_id();
+  // split-K: slice `split` covers k in [kb, kb + K) and writes its partial
+  // product to the slice's own output block
+  const bool sk = EPI == EPI_F32 && p.splitk > 1;
+  int split = 0;
+  if (sk) {
+    const int tiles = ((M + BT - 1) / BT) * ((N + BT - 1) / BT);
+    split = bid / tiles;
+    bid -= split * tiles;
+  }
+  tile_origin(M, N, bid, m0, n0);
+  const int kb = split * p.splitk_kc;
+  const int K = sk ? min(p.splitk_kc, p.K - kb) : p.K;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave >> 1, wn = wave & 1;
 
   __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(p.A + (long)m0 * p.lda), (short)0, 0x7FFFFFFF, 0x00020000);
+      (void*)(p.A + (long)m0 * p.lda + kb), (short)0, 0x7FFFFFFF, 0x00020000);
   __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(p.B + (long)n0 * p.ldb), (short)0, 0x7FFFFFFF, 0x00020000);
+      (void*)(p.B + (long)n0 * p.ldb + kb), (short)0, 0x7FFFFFFF, 0x00020000);
   Loader la, lb;
   la.init(p.lda, M - m0, wave);
   lb.init(p.ldb, N - n0, wave);
@@ -638,10 +658,19 @@ __global__ __launch_bounds__(NT, 1) void gemm256_kernel(GemmArgs p) {
   }
   wait_vm_lgkm0<0>();  // the zero-filling copies past the last tile
   __syncthreads();
-  if constexpr (EPI == EPI_ADAMW)
+  if constexpr (EPI == EPI_ADAMW) {
     epilogue_adamw(p, acc, reinterpret_cast<float*>(smem), m0, n0, wave, lane);
-  else
+  } else if constexpr (EPI == EPI_F32) {
+    if (split > 0) {
+      GemmArgs q = p;
+      q.out = reinterpret_cast<float*>(p.out) + split * p.split_stride;
+      epilogue<EPI, GE>(q, acc, reinterpret_cast<float*>(smem), m0, n0, wave, lane);
+    } else {
+      epilogue<EPI, GE>(p, acc, reinterpret_cast<float*>(smem), m0, n0, wave, lane);
+    }
+  } else {
     epilogue<EPI, GE>(p, acc, reinterpret_cast<float*>(smem), m0, n0, wave, lane);
+  }
 }
 
 // An M/N-contiguous operand tile (64 k-rows of 256 contiguous m or n) staged
@@ -732,7 +761,7 @@ __global__ __launch_bounds__(NT, 1) void gemm256_rs_kernel(GemmArgs p) {
 
   const int M = p.M, N = p.N, K = p.K;
   int m0, n0;
-  tile_origin(M, N, m0, n0);
+  tile_origin(M, N, xcd_order_id(), m0, n0);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave >> 1, wn = wave & 1;
@@ -849,7 +878,8 @@ __global__ __launch_bounds__(NT, 1) void gemm256_rs_kernel(GemmArgs p) {
 
 template <int AL, int BL, int EPI>
 hipError_t launch_e(const GemmArgs& a, hipStream_t s) {
-  dim3 grid((unsigned)(sat_cdiv(a.M, BT) * sat_cdiv(a.N, BT)));
+  const int slices = (EPI == EPI_F32 && a.splitk > 1) ? a.splitk : 1;
+  dim3 grid((unsigned)(sat_cdiv(a.M, BT) * sat_cdiv(a.N, BT) * slices));
   const bool ge = (EPI == EPI_BF16 || EPI == EPI_DGELU_BF16) && a.gelu_erf;
   if constexpr (EPI == EPI_ADAMW) {
     static_assert(AL == LAY_K && BL == LAY_K, "optimizer epilogue: K-contiguous operands");
@@ -884,8 +914,16 @@ inline bool al(const void* p, int bytes) { return (reinterpret_cast<uintptr_t>(p
 
 bool gemm256_eligible(const GemmArgs& a, int alay, int blay, int epi) {
   if (a.M <= 0 || a.N <= 0 || a.K <= 0) return false;
-  // enough 256 x 256 tiles to give every CU one
-  if ((long)sat_cdiv(a.M, BT) * sat_cdiv(a.N, BT) < 256) return false;
+  if (a.splitk > 1) {
+    // split-K: fp32 partials without bias, K-contiguous operands, whole 64-deep slices
+    if (epi != EPI_F32 || alay != LAY_K || blay != LAY_K || a.bias != nullptr ||
+        a.splitk_kc <= 0 || a.splitk_kc % BK || (long)(a.splitk - 1) * a.splitk_kc >= a.K ||
+        a.split_stride < (long)(a.M - 1) * a.ldo + a.N)
+      return false;
+  }
+  // enough 256 x 256 tiles to give every CU one; split-K products are small
+  // by construction and run whatever their tile count
+  if (a.splitk <= 1 && (long)sat_cdiv(a.M, BT) * sat_cdiv(a.N, BT) < 256) return false;
   auto r8 = [](long x) { return (x + 7) / 8 * 8; };
   const long lim = 1L << 31;
   // operands: 16-byte copies, 32-bit buffer offsets
@@ -923,4 +961,77 @@ hipError_t launch_gemm256(const GemmArgs& a, int alay, int blay, int epi, hipStr
   if (alay == LAY_K && blay == LAY_MN) return launch_l<LAY_K, LAY_MN>(a, epi, s);
   if (alay == LAY_MN && blay == LAY_K) return launch_l<LAY_MN, LAY_K>(a, epi, s);
   return launch_l<LAY_MN, LAY_MN>(a, epi, s);
+}
+
+int gemm_splitk(int M, int N, int K, int* kc) {
+  const long tiles = (long)sat_cdiv(M, BT) * sat_cdiv(N, BT);
+  if (M <= 0 || N <= 0 || tiles >= 256 || K < 1024) return 1;
+  int S = (int)std::min<long>((256 + tiles - 1) / tiles, K / 512);
+  S = std::min(S, 16);
+  if (S < 2) return 1;
+  const int c = (sat_cdiv(K, S) + BK - 1) / BK * BK;
+  if (kc) *kc = c;
+  return sat_cdiv(K, c);
+}
+
+long gemm_splitk_ws_elems(int M, int N, int K) {
+  int kc = 0;
+  const int S = gemm_splitk(M, N, K, &kc);
+  return S > 1 ? (long)S * M * N : 0;
+}
+
+namespace {
+
+// One thread per 4 consecutive outputs of a row; slices summed in order.
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ ws, int S,
+                                                            long stride, int M, int N,
+                                                            float* __restrict__ out, long ldo,
+                                                            const float* __restrict__ bias,
+                                                            int bias_col0,
+                                                            const float* __restrict__ resid,
+                                                            long ldr, bool vec) {
+  const int n4 = (N + 3) / 4;
+  const long total = (long)M * n4;
+  for (long t = (long)blockIdx.x * blockDim.x + threadIdx.x; t < total;
+       t += (long)gridDim.x * blockDim.x) {
+    const long m = t / n4;
+    const int n = (int)(t - m * n4) * 4;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    if (vec) {
+      for (int s = 0; s < S; ++s) {
+        const floatx4 x = __builtin_nontemporal_load(
+            reinterpret_cast<const floatx4*>(ws + s * stride + m * N + n));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[e] += x[e];
+      }
+    } else {
+      for (int s = 0; s < S; ++s)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (n + e < N) acc[e] += ws[s * stride + m * N + n + e];
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int c = n + e;
+      if (c >= N) break;
+      float v = acc[e];
+      if (bias != nullptr && c >= bias_col0) v += bias[c - bias_col0];
+      if (resid != nullptr) v = resid[m * ldr + c] + v;
+      out[m * ldo + c] = v;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_splitk_reduce(const float* ws, int S, long stride, int M, int N, float* out,
+                                long ldo, const float* bias, int bias_col0, const float* resid,
+                                long ldr, hipStream_t s) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  const long total = (long)M * ((N + 3) / 4);
+  const bool vec = N % 4 == 0 && stride % 4 == 0 && (reinterpret_cast<uintptr_t>(ws) & 15) == 0;
+  const unsigned blocks = (unsigned)std::min<long>((total + 255) / 256, 8192);
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, ws, S, stride, M, N, out,
+                     ldo, bias, bias_col0, resid, ldr, vec);
+  return hipGetLastError();
 }

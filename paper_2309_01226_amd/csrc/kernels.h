@@ -61,6 +61,17 @@ struct GemmArgs {
   bf16* opt_sht;
   long opt_trows;
   AdamWConsts opt_c;
+  // Split-K (256 x 256 kernel, EPI_F32, both operands K-contiguous, no bias):
+  // splitk > 1 cuts K into slices of splitk_kc (a multiple of 64); slice s
+  // writes its fp32 partial product to out + s * split_stride.
+  int splitk;
+  int splitk_kc;
+  long split_stride;
+  // Optional caller-owned fp32 workspace of splitk_ws_elems elements; with it,
+  // launch_gemm runs fp32-output products that have too few 256 x 256 tiles
+  // to fill the chip as split-K plus a reduction (gemm_splitk below).
+  float* splitk_ws;
+  long splitk_ws_elems;
 };
 
 hipError_t launch_gemm(const GemmArgs& a, int alay, int blay, int epi, hipStream_t s);
@@ -68,6 +79,18 @@ hipError_t launch_gemm(const GemmArgs& a, int alay, int blay, int epi, hipStream
 // launch_gemm dispatches to it when gemm256_eligible holds.
 bool gemm256_eligible(const GemmArgs& a, int alay, int blay, int epi);
 hipError_t launch_gemm256(const GemmArgs& a, int alay, int blay, int epi, hipStream_t s);
+// K slices launch_gemm uses for an fp32-output [M, N] product of depth K when
+// a workspace is given (1: none; *kc: slice depth), and the workspace that
+// then takes (fp32 elements; 0 when not split).  A product is split when it
+// has fewer than 256 tiles of 256 x 256 and K >= 1024: into enough slices to
+// give every CU a tile where K allows, each at least 512 deep, at most 16.
+int gemm_splitk(int M, int N, int K, int* kc);
+long gemm_splitk_ws_elems(int M, int N, int K);
+// out[m, n] = sum over s of ws[s * stride + m * N + n] (s in order) + bias[n -
+// bias_col0] (n >= bias_col0; null: none) + resid[m * ldr + n] (null: none).
+hipError_t launch_splitk_reduce(const float* ws, int S, long stride, int M, int N, float* out,
+                                long ldo, const float* bias, int bias_col0, const float* resid,
+                                long ldr, hipStream_t s);
 
 // ---------------------------------------------------------------- LayerNorm
 // y = (x - mean) * rstd * g + b over rows of length d; x fp32, y bf16.

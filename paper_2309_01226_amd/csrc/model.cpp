@@ -321,6 +321,26 @@ size_t carve(sat_model* M, char* base) {
       A.u = nullptr;  // u lives in qkv[:, 3d:]
     }
   }
+  // split-K workspace: the largest need of the step's fp32-output products
+  // (weight gradients with K = tokens, input gradients into the residual
+  // width, the forward residual products, the head's products)
+  {
+    const int Ti = (int)T, di = (int)d, mi = (int)m, R = D.rows_head;
+    long ws = 0;
+    auto need = [&](int Mg, int Ng, int Kg) { ws = std::max(ws, gemm_splitk_ws_elems(Mg, Ng, Kg)); };
+    need(D.qkv_ld, di, Ti);
+    need(di, di, Ti);
+    need(mi, di, Ti);
+    need(di, mi, Ti);
+    need(Ti, di, D.qkv_ld);
+    need(Ti, di, mi);
+    need(Ti, di, di);
+    need(D.V, di, R);
+    need(R, di, D.Vp);
+    need(R, D.V, di);
+    M->splitk_ws_elems = ws;
+    M->splitk_ws = ws > 0 ? c.take<float>((size_t)ws) : nullptr;
+  }
   // head
   const long R = D.rows_head;
   M->f = c.take<bf16>(R * d);

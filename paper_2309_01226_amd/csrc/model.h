@@ -127,6 +127,9 @@ struct sat_model {
   bf16* tB;
   bool trans_blocks;  // tA / tB serve the blocks (T % 8 == 0)
   bool trans_head;    // ... and the head (rows_head % 8 == 0)
+  // split-K workspace of the fp32-output products with too few tiles
+  float* splitk_ws;
+  long splitk_ws_elems;
   float* delta;
   float* part;
   int n_part;

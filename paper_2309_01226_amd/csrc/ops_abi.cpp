@@ -51,6 +51,9 @@ extern "C" sat_status sat_op_gemm(const sat_gemm_desc* d, void* stream) {
   a.out2 = (bf16*)d->out2; a.ldo2 = d->ldo2; a.gelu_col0 = d->gelu_col0;
   a.aux = (const bf16*)d->aux; a.ldaux = d->ldaux;
   a.gelu_erf = d->gelu_erf;
+  SAT_CHECK_ARG(d->splitk_ws_elems >= 0, "sat_op_gemm: negative splitk_ws_elems");
+  a.splitk_ws = d->splitk_ws;
+  a.splitk_ws_elems = d->splitk_ws ? d->splitk_ws_elems : 0;
   SAT_HIP(launch_gemm(a, d->a_layout, d->b_layout, d->epilogue, S(stream)));
   return SAT_OK;
 }

@@ -51,7 +51,11 @@ GemmArgs gargs(const bf16* A, long lda, const bf16* B, long ldb, int Mr, int N, 
 sat_status gemm(sat_model* M, const GemmArgs& a, int alay, int blay, int epi,
                 int tk = TK_ALL_GEMM) {
   Timed t(M, tk, 2.0 * a.M * a.N * (double)a.K);
-  SAT_HIP(launch_gemm(a, alay, blay, epi, M->stream));
+  // fp32-output products with too few tiles run split-K in this workspace
+  GemmArgs b = a;
+  b.splitk_ws = M->splitk_ws;
+  b.splitk_ws_elems = M->splitk_ws_elems;
+  SAT_HIP(launch_gemm(b, alay, blay, epi, M->stream));
   return SAT_OK;
 }
 

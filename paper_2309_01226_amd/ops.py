@@ -32,13 +32,15 @@ def _need(t, dtype, name):
 
 def gemm(A, B, M, N, K, out, *, lda, ldb, a_layout=LAY_K, b_layout=LAY_K, epilogue=EPI_F32,
          ldo=None, bias=None, bias_col0=0, resid=None, ldr=None, out2=None, ldo2=0, gelu_col0=0,
-         aux=None, ldaux=0, gelu_erf=0):
-    """C[m, n] = sum_k A(m, k) B(n, k) with the chosen epilogue (see saturn_ops.h)."""
+         aux=None, ldaux=0, gelu_erf=0, splitk_ws=None):
+    """C[m, n] = sum_k A(m, k) B(n, k) with the chosen epilogue (see saturn_ops.h);
+    splitk_ws: optional fp32 scratch that lets a small fp32-output product run split-K."""
     _need(A, torch.bfloat16, "A")
     _need(B, torch.bfloat16, "B")
     _need(bias, torch.float32, "bias")
     _need(resid, torch.float32, "resid")
     _need(aux, torch.bfloat16, "aux")
+    _need(splitk_ws, torch.float32, "splitk_ws")
     need_a = (M - 1) * lda + K if a_layout == LAY_K else (K - 1) * lda + M
     need_b = (N - 1) * ldb + K if b_layout == LAY_K else (K - 1) * ldb + N
     if A.numel() < need_a or B.numel() < need_b:
@@ -53,7 +55,9 @@ def gemm(A, B, M, N, K, out, *, lda, ldb, a_layout=LAY_K, b_layout=LAY_K, epilog
         bias=None if bias is None else bias.data_ptr(), bias_col0=bias_col0,
         resid=None if resid is None else resid.data_ptr(), ldr=ldo if ldr is None else ldr,
         out2=None if out2 is None else out2.data_ptr(), ldo2=ldo2, gelu_col0=gelu_col0,
-        aux=None if aux is None else aux.data_ptr(), ldaux=ldaux, gelu_erf=gelu_erf)
+        aux=None if aux is None else aux.data_ptr(), ldaux=ldaux, gelu_erf=gelu_erf,
+        splitk_ws=None if splitk_ws is None else splitk_ws.data_ptr(),
+        splitk_ws_elems=0 if splitk_ws is None else splitk_ws.numel())
     _lib.call("sat_op_gemm", C.byref(d), _stream())
     return out
 

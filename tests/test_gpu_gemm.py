@@ -133,3 +133,41 @@ def test_gemm_large_tiles_sampled(a_layout, b_layout, epi):
         ops.gemm(Ad, Bd, M, N, K, o3, aux=to_dev_bf16(U), ldaux=N, gelu_erf=1, **kw)
         torch.cuda.synchronize()
         assert rel(host(o3)[rows], C * O.gelu_grad(U[rows], 1)) < 4e-3
+
+
+# Split-K: fp32-output products with fewer than 256 tiles of 256 x 256 and
+# K >= 1024, given a workspace.  Shapes: one tile, ragged M / N, a K that is
+# not a multiple of the slice depth (last slice shorter) and not a multiple of
+# 64, and a residual + bias epilogue with the residual aliasing the output.
+SPLITK = [(256, 256, 2048, 0), (300, 520, 4160, 0), (768, 768, 8192, 0), (520, 264, 3008, 1),
+          (1000, 40, 1032, 1)]
+
+
+@pytest.mark.parametrize("M,N,K,resid", SPLITK)
+def test_gemm_splitk(M, N, K, resid):
+    from paper_2309_01226_amd import ops
+    flush(f"gemm split-K M={M} N={N} K={K} resid={resid}")
+    rng = np.random.default_rng(M + N + K)
+    A, B, Ad, Bd, lda, ldb = _operands(rng, M, N, K, 0, 0)
+    bias = rng.normal(size=N)
+    R = rng.normal(size=(M, N))
+    ws = torch.full((16 * M * N,), float("nan"), device="cuda", dtype=torch.float32)
+    out = to_dev_f32(R) if resid else torch.empty(M, N, device="cuda", dtype=torch.float32)
+    kw = dict(bias=to_dev_f32(bias), epilogue=ops.EPI_RESID_F32 if resid else ops.EPI_F32)
+    if resid:
+        kw.update(resid=out, ldr=N)
+    ops.gemm(Ad, Bd, M, N, K, out, lda=lda, ldb=ldb, splitk_ws=ws, **kw)
+    # the same product without a workspace (no split)
+    out1 = to_dev_f32(R) if resid else torch.empty(M, N, device="cuda", dtype=torch.float32)
+    if resid:
+        kw.update(resid=out1)
+    ops.gemm(Ad, Bd, M, N, K, out1, lda=lda, ldb=ldb, **kw)
+    torch.cuda.synchronize()
+    ref = O.gemm(A, B) + bias + (R if resid else 0.0)
+    got = host(out)
+    assert np.isfinite(got).all()
+    assert rel(got, ref) < 2e-6
+    assert rel(got, host(out1)) < 2e-6
+    # the split path ran: at least two slices of partial products were written
+    n_used = int(torch.isfinite(ws).sum().item())
+    assert n_used >= 2 * M * N, n_used

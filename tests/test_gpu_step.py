@@ -46,6 +46,10 @@ CASES = {
                          seq_len=32, batch=2, lr=1e-3, frozen_layers=1),
     "small_gptj_k1": dict(arch="gptj", n_layers=2, d_model=128, n_heads=2, d_mlp=256, vocab=97,
                           seq_len=40, batch=2, rotary_dim=16, lr=1e-3, frozen_layers=1),
+    # 2048 tokens: the weight-gradient products (1 - 4 output tiles, K = 2048), the
+    # fc1 input gradient and the fc2 forward (K = 1024) run split-K
+    "gpt2_splitk": dict(arch="gpt2", n_layers=2, d_model=256, n_heads=4, d_mlp=1024, vocab=512,
+                        seq_len=1024, batch=2, lr=1e-3),
 }
 
 
