@@ -67,7 +67,7 @@ sat_status sat_op_layernorm_fwd(const float* x, int64_t ldx, int64_t row_stride,
                                 int32_t rows, int32_t d, float eps, void* stream);
 /* LayerNorm backward: dres[r] += dx[r] (fp32, same row addressing as x);
  * dg, db fp32 [d] (overwritten).  work: fp32 scratch of 2*n_part*d floats,
- * n_part = min(rows, 256). */
+ * n_part = min(rows, 1024). */
 sat_status sat_op_layernorm_bwd(const float* dy, int64_t lddy, const float* x, int64_t ldx,
                                 int64_t row_stride, const float* g, const float* mean,
                                 const float* rstd, float* dres, int64_t ldres, float* dg,

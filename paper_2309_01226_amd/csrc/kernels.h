@@ -107,6 +107,9 @@ hipError_t launch_layernorm_bwd(const float* dy, long lddy, const float* x, long
                                 long row_stride, const float* g, const float* mean,
                                 const float* rstd, float* dres, long ldres, float* part_g,
                                 float* part_b, int rows, int d, int n_part, hipStream_t s);
+// Partial-sum rows (workgroups) the LayerNorm backward uses for `rows` rows:
+// the dg / db partials take 2 * ln_bwd_parts(rows) * d floats.
+int ln_bwd_parts(int rows);
 hipError_t launch_colsum_partials(const float* part, int n_part, int d, float* out,
                                   hipStream_t s);
 // out[c] = sum_r X[r, c] for a bf16 or fp32 matrix, deterministic two-pass.

@@ -382,7 +382,10 @@ size_t carve(sat_model* M, char* base) {
   M->n_part = (int)(T < 256 ? T : 256);
   long wide = D.qkv_ld > D.Vp ? D.qkv_ld : D.Vp;
   if (D.arch == SAT_VIT && D.pd > wide) wide = D.pd;
-  M->part = c.take<float>((size_t)2 * M->n_part * (wide > d ? wide : d));
+  // column-sum partials: n_part rows of the widest bias; LayerNorm partials:
+  // ln_bwd_parts(rows) rows of d, for dg and db
+  const size_t lnp = (size_t)2 * ln_bwd_parts((int)std::max<long>(T, D.rows_head)) * d;
+  M->part = c.take<float>(std::max((size_t)2 * M->n_part * (wide > d ? wide : d), lnp));
   M->sortbuf = c.take<int32_t>(T > 0 ? T : 1);
   return align_up(c.off, kAlignBytes);
 }

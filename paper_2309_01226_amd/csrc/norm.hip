@@ -93,7 +93,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(
   int it = 0;
   for (int row = r0; row < r1; row += 2, ++it) {
     const bool two = row + 1 < r1;
-    float4 dv[2][NC4], xh[2][NC4];
+    float4 dv[2][NC4], xh[2][NC4], rv[2][NC4];
     float mu[2], rs[2], s[2][2];
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
@@ -102,15 +102,19 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(
       rs[q] = rstd[rr];
       const float* dyr = dy + (long)rr * lddy;
       const float* xr = x + (long)rr * row_stride * ldx;
+      const float* drr = dres + (long)rr * row_stride * ldres;
       s[q][0] = s[q][1] = 0.f;
 #pragma unroll
       for (int j = 0; j < NC4; ++j) {
         const int col = (j * 256 + tid) * 4;
         float4 xv = make_float4(0.f, 0.f, 0.f, 0.f);
         dv[q][j] = xv;
+        rv[q][j] = xv;
         if (col < d) {
+          // the residual gradient is loaded with dy and x, not after the row sums
           dv[q][j] = *reinterpret_cast<const float4*>(dyr + col);
           xv = *reinterpret_cast<const float4*>(xr + col);
+          rv[q][j] = *reinterpret_cast<const float4*>(drr + col);
         }
         float4 h = make_float4((xv.x - mu[q]) * rs[q], (xv.y - mu[q]) * rs[q], (xv.z - mu[q]) * rs[q],
                                (xv.w - mu[q]) * rs[q]);
@@ -148,7 +152,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(
         const int col = (j * 256 + tid) * 4;
         if (col < d) {
           const float4 v = dv[q][j], h = xh[q][j];
-          float4 o = *reinterpret_cast<float4*>(dr + col);
+          float4 o = rv[q][j];
           o.x += rs[q] * (v.x * gg[j].x - m1 - h.x * m2);
           o.y += rs[q] * (v.y * gg[j].y - m1 - h.y * m2);
           o.z += rs[q] * (v.z * gg[j].z - m1 - h.z * m2);
@@ -172,21 +176,53 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(
 
 // out[c] = sum_p part[p, c] in a fixed order: wave w sums p = w, w + 8, ...,
 // then the eight wave sums are added in order.  64 columns per workgroup.
-__global__ __launch_bounds__(512) void colsum_partials_kernel(const float* __restrict__ part, int n_part,
-                                                              int d, float* __restrict__ out) {
-  __shared__ float red[8][64];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int c = blockIdx.x * 64 + lane;
-  float s = 0.f;
-  if (c < d)
-    for (int p = w; p < n_part; p += 8) s += part[(long)p * d + c];
-  red[w][lane] = s;
+// out[c] = sum over p of part[p * d + c].  A workgroup owns 16 columns: 64
+// row lanes of 4 threads (4 columns each, one 16-byte load per row), then a
+// fixed-order tree over the row lanes, so the sum does not depend on timing.
+template <bool VEC>
+__global__ __launch_bounds__(256) void colsum_partials_kernel(const float* __restrict__ part,
+                                                              int n_part, int d,
+                                                              float* __restrict__ out) {
+  __shared__ float4 red[64][4];
+  const int c4 = threadIdx.x & 3, rl = threadIdx.x >> 2;
+  const int c = blockIdx.x * 16 + 4 * c4;
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (VEC) {
+    if (c < d)
+      for (int p = rl; p < n_part; p += 64) {
+        const float4 v = *reinterpret_cast<const float4*>(part + (long)p * d + c);
+        s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+      }
+  } else {
+    for (int p = rl; p < n_part; p += 64) {
+      const float* r = part + (long)p * d;
+      if (c < d) s.x += r[c];
+      if (c + 1 < d) s.y += r[c + 1];
+      if (c + 2 < d) s.z += r[c + 2];
+      if (c + 3 < d) s.w += r[c + 3];
+    }
+  }
+  red[rl][c4] = s;
   __syncthreads();
-  if (w == 0 && c < d) {
-    float t = red[0][lane];
 #pragma unroll
-    for (int k = 1; k < 8; ++k) t += red[k][lane];
-    out[c] = t;
+  for (int w = 32; w >= 1; w >>= 1) {
+    if (rl < w) {
+      const float4 o = red[rl + w][c4];
+      float4& t = red[rl][c4];
+      t.x += o.x; t.y += o.y; t.z += o.z; t.w += o.w;
+    }
+    __syncthreads();
+  }
+  if (rl == 0) {
+    const float4 t = red[0][c4];
+    if (VEC) {
+      if (c < d) *reinterpret_cast<float4*>(out + c) = t;
+    } else {
+      if (c < d) out[c] = t.x;
+      if (c + 1 < d) out[c + 1] = t.y;
+      if (c + 2 < d) out[c + 2] = t.z;
+      if (c + 3 < d) out[c + 3] = t.w;
+    }
   }
 }
 
@@ -273,11 +309,19 @@ hipError_t launch_layernorm_bwd(const float* dy, long lddy, const float* x, long
 #undef LNB
 }
 
+int ln_bwd_parts(int rows) { return rows < 1024 ? rows : 1024; }
+
 hipError_t launch_colsum_partials(const float* part, int n_part, int d, float* out,
                                   hipStream_t s) {
   if (d <= 0) return hipSuccess;
-  hipLaunchKernelGGL(colsum_partials_kernel, dim3(sat_cdiv(d, 64)), dim3(512), 0, s, part, n_part, d,
-                     out);
+  const bool vec = d % 4 == 0 && (reinterpret_cast<uintptr_t>(part) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(out) & 15) == 0;
+  if (vec)
+    hipLaunchKernelGGL(colsum_partials_kernel<true>, dim3(sat_cdiv(d, 16)), dim3(256), 0, s, part,
+                       n_part, d, out);
+  else
+    hipLaunchKernelGGL(colsum_partials_kernel<false>, dim3(sat_cdiv(d, 16)), dim3(256), 0, s, part,
+                       n_part, d, out);
   return hipGetLastError();
 }
 

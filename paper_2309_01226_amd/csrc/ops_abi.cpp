@@ -84,7 +84,7 @@ extern "C" sat_status sat_op_layernorm_bwd(const float* dy, int64_t lddy, const 
   SAT_CHECK_ARG(lddy >= d && lddy % 4 == 0 && ldx >= d && ldx % 4 == 0 && ldres >= d &&
                     ldres % 4 == 0 && row_stride >= 1,
                 "layernorm_bwd: bad leading dimensions");
-  int n_part = rows < 256 ? rows : 256;
+  const int n_part = ln_bwd_parts(rows);
   SAT_HIP(launch_layernorm_bwd(dy, lddy, x, ldx, row_stride, g, mean, rstd, dres, ldres, work,
                                work + (long)n_part * d, rows, d, n_part, S(stream)));
   SAT_HIP(launch_colsum_partials(work, n_part, d, dg, S(stream)));

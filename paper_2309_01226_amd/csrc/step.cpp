@@ -293,7 +293,7 @@ static sat_status wgrad(sat_model* M, bool trans, bool y_ready, const bf16* Y, l
 static sat_status ln_bwd(sat_model* M, const float* dy, const float* x, long row_stride,
                          int gidx, const float* mean, const float* rstd, int rows) {
   const int d = M->D.d;
-  const int np_ = rows < 256 ? rows : 256;
+  const int np_ = ln_bwd_parts(rows);
   float* pg = M->part;
   float* pbb = M->part + (size_t)np_ * d;
   SAT_HIP(launch_layernorm_bwd(dy, d, x, d, row_stride, master(M, gidx), mean, rstd, M->dh, d, pg,
@@ -328,7 +328,7 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
     SAT_HIP(launch_zero(M->dh, (long)T * d * 4, s));
     const long rstride = (D.arch == SAT_VIT) ? D.S : 1;
     // LN_f backward writes rows r * rstride of dh (CLS rows for ViT)
-    const int np_ = R < 256 ? R : 256;
+    const int np_ = ln_bwd_parts(R);
     float* pg = M->part;
     float* pbb = M->part + (size_t)np_ * d;
     SAT_HIP(launch_layernorm_bwd(M->dA, d, M->h_in[D.L], d, rstride, master(M, hb + 0), M->meanf,

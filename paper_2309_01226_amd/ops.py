@@ -75,7 +75,7 @@ def layernorm_fwd(x, g, b, y, mean, rstd, rows, d, eps, *, ldx=None, row_stride=
 
 def layernorm_bwd(dy, x, g, mean, rstd, dres, dg, db, rows, d, *, lddy=None, ldx=None, row_stride=1,
                   ldres=None):
-    n_part = min(rows, 256)
+    n_part = min(rows, 1024)
     work = torch.empty(2 * n_part * d, device=dy.device, dtype=torch.float32)
     _lib.call("sat_op_layernorm_bwd", _p(dy), lddy or d, _p(x), ldx or d, row_stride, _p(g),
               _p(mean), _p(rstd), _p(dres), ldres or d, _p(dg), _p(db), _p(work), rows, d, _stream())
