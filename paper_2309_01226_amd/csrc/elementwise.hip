@@ -278,6 +278,85 @@ __global__ __launch_bounds__(256) void xent_kernel(const float* __restrict__ z, 
   if (threadIdx.x == 0) row_loss[row] = lse - zr[y];
 }
 
+// Rows of at most 13 * 4096 logits: one 1024-thread workgroup per row keeps
+// the row in registers (thread t holds columns 4 t + 4096 g .. + 3, g < NV4),
+// so the logits are read once and exp is taken once per element:
+// p = exp(z - max), lse = max + log(sum p), dz = (p / sum p - onehot) * inv_n.
+// Block max and sum go through LDS in a fixed order.
+template <int NV4>
+__global__ __launch_bounds__(1024) void xent_reg_kernel(const float* __restrict__ z, long ldz,
+                                                        const int32_t* __restrict__ labels, int V,
+                                                        float* __restrict__ row_loss,
+                                                        bf16* __restrict__ dz, long lddz,
+                                                        const float* __restrict__ inv_n_p) {
+  __shared__ float red[16];
+  const int row = blockIdx.x;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const float* zr = z + (long)row * ldz;
+  const int y = labels[row];
+  floatx4 v[NV4];
+  float m = -INFINITY;
+#pragma unroll
+  for (int g = 0; g < NV4; ++g) {
+    const int c = 4 * t + 4096 * g;
+    v[g] = floatx4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    if (c + 3 < V) {
+      v[g] = __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(zr + c));
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (c + e < V) v[g][e] = zr[c + e];
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) m = fmaxf(m, v[g][e]);
+  }
+  m = wave_max(m);
+  if (lane == 0) red[wave] = m;
+  __syncthreads();
+  float M = red[0];
+#pragma unroll
+  for (int w = 1; w < 16; ++w) M = fmaxf(M, red[w]);
+  __syncthreads();
+  float s = 0.f;
+#pragma unroll
+  for (int g = 0; g < NV4; ++g)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[g][e] = __expf(v[g][e] - M);  // exp(-inf) = 0 past V
+      s += v[g][e];
+    }
+  s = wave_sum(s);
+  if (lane == 0) red[wave] = s;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < 16; ++w) tot += red[w];
+  const float lse = M + __logf(tot);
+  bf16* dr = dz + (long)row * lddz;
+  const int cpad = (int)min((long)((V + 7) & ~7), lddz);  // zero the row padding too
+  const float inv_n = y < 0 ? 0.f : *inv_n_p;
+  const float rt = 1.f / tot;
+#pragma unroll
+  for (int g = 0; g < NV4; ++g) {
+    const int c = 4 * t + 4096 * g;
+    if (c >= cpad) continue;
+    bf16x4 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float pr = c + e < V ? v[g][e] * rt : 0.f;
+      o[e] = f2bf((pr - (c + e == y ? 1.f : 0.f)) * inv_n);
+    }
+    if (c + 3 < cpad) {
+      __builtin_nontemporal_store(o, reinterpret_cast<bf16x4*>(dr + c));
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (c + e < cpad) dr[c + e] = o[e];
+    }
+  }
+  if (t == 0) row_loss[row] = y < 0 ? 0.f : lse - zr[y];
+}
+
 // Single block: out[0] = (sum of row_loss in a fixed tree order) * inv_n.
 __global__ __launch_bounds__(256) void loss_finalize_kernel(const float* __restrict__ row_loss,
                                                             int n, const float* __restrict__ inv_n,
@@ -508,8 +587,20 @@ hipError_t launch_sum_rows_batched(const float* dh, float* out, int B, int S, in
 hipError_t launch_xent(const float* z, long ldz, const int32_t* labels, int N, int V,
                        float* row_loss, bf16* dz, long lddz, const float* inv_n, hipStream_t s) {
   if (N <= 0) return hipSuccess;
-  hipLaunchKernelGGL(xent_kernel, dim3(N), dim3(256), 0, s, z, ldz, labels, V, row_loss, dz, lddz,
-                     inv_n);
+  const int nv4 = (V + 4095) / 4096;
+  // 1024 threads leave 128 VGPRs per thread: up to 13 groups of 4 logits stay in registers
+  const bool reg = nv4 <= 13 && ldz % 4 == 0 && lddz % 4 == 0 &&
+                   (reinterpret_cast<uintptr_t>(z) & 15) == 0 && (reinterpret_cast<uintptr_t>(dz) & 7) == 0;
+#define XREG(NV) hipLaunchKernelGGL(xent_reg_kernel<NV>, dim3(N), dim3(1024), 0, s, z, ldz, labels, V, \
+                                    row_loss, dz, lddz, inv_n)
+  if (reg && nv4 <= 1) XREG(1);
+  else if (reg && nv4 <= 4) XREG(4);
+  else if (reg && nv4 <= 8) XREG(8);
+  else if (reg) XREG(13);
+  else
+    hipLaunchKernelGGL(xent_kernel, dim3(N), dim3(256), 0, s, z, ldz, labels, V, row_loss, dz, lddz,
+                       inv_n);
+#undef XREG
   return hipGetLastError();
 }
 
