@@ -106,7 +106,10 @@ hipError_t launch_layernorm_fwd(const float* x, long ldx, long row_stride, const
 hipError_t launch_layernorm_bwd(const float* dy, long lddy, const float* x, long ldx,
                                 long row_stride, const float* g, const float* mean,
                                 const float* rstd, float* dres, long ldres, float* part_g,
-                                float* part_b, int rows, int d, int n_part, hipStream_t s);
+                                float* part_b, int rows, int d, int n_part, hipStream_t s,
+                                bf16* dres_bf = nullptr, long ldbf = 0);
+// dres_bf (row_stride 1 only; null: none): also writes the updated dres rows
+// rounded to bf16 at dres_bf + r * ldbf.
 // Partial-sum rows (workgroups) the LayerNorm backward uses for `rows` rows:
 // the dg / db partials take 2 * ln_bwd_parts(rows) * d floats.
 int ln_bwd_parts(int rows);

@@ -77,7 +77,8 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(
     const float* __restrict__ dy, long lddy, const float* __restrict__ x, long ldx,
     long row_stride, const float* __restrict__ g, const float* __restrict__ mean,
     const float* __restrict__ rstd, float* __restrict__ dres, long ldres,
-    float* __restrict__ part_g, float* __restrict__ part_b, int rows, int d, int rpb) {
+    float* __restrict__ part_g, float* __restrict__ part_b, int rows, int d, int rpb,
+    bf16* __restrict__ dres_bf, long ldbf) {
   __shared__ float red[2][4][4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r0 = blockIdx.x * rpb, r1 = min(rows, r0 + rpb);
@@ -158,6 +159,10 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(
           o.z += rs[q] * (v.z * gg[j].z - m1 - h.z * m2);
           o.w += rs[q] * (v.w * gg[j].w - m1 - h.w * m2);
           *reinterpret_cast<float4*>(dr + col) = o;
+          if (dres_bf != nullptr) {
+            const bf16x4 ob = {f2bf(o.x), f2bf(o.y), f2bf(o.z), f2bf(o.w)};
+            *reinterpret_cast<bf16x4*>(dres_bf + (long)rr * ldbf + col) = ob;
+          }
           pg[j].x += v.x * h.x; pg[j].y += v.y * h.y; pg[j].z += v.z * h.z; pg[j].w += v.w * h.w;
           pb[j].x += v.x; pb[j].y += v.y; pb[j].z += v.z; pb[j].w += v.w;
         }
@@ -268,11 +273,11 @@ template <int NC4>
 hipError_t ln_bwd_launch(const float* dy, long lddy, const float* x, long ldx, long rs,
                          const float* g, const float* mean, const float* rstd, float* dres,
                          long ldres, float* pg, float* pb, int rows, int d, int n_part,
-                         hipStream_t s) {
+                         hipStream_t s, bf16* dres_bf, long ldbf) {
   // exactly n_part workgroups, so every partial row is written (zeros past the last row)
   const int rpb = sat_cdiv(rows, n_part);
   hipLaunchKernelGGL(ln_bwd_kernel<NC4>, dim3(n_part), dim3(256), 0, s, dy, lddy, x,
-                     ldx, rs, g, mean, rstd, dres, ldres, pg, pb, rows, d, rpb);
+                     ldx, rs, g, mean, rstd, dres, ldres, pg, pb, rows, d, rpb, dres_bf, ldbf);
   return hipGetLastError();
 }
 
@@ -296,13 +301,17 @@ hipError_t launch_layernorm_fwd(const float* x, long ldx, long row_stride, const
 hipError_t launch_layernorm_bwd(const float* dy, long lddy, const float* x, long ldx,
                                 long row_stride, const float* g, const float* mean,
                                 const float* rstd, float* dres, long ldres, float* part_g,
-                                float* part_b, int rows, int d, int n_part, hipStream_t s) {
+                                float* part_b, int rows, int d, int n_part, hipStream_t s,
+                                bf16* dres_bf, long ldbf) {
   if (rows <= 0) return hipSuccess;
+  if (dres_bf != nullptr && (row_stride != 1 || ldbf % 4 != 0 ||
+                             (reinterpret_cast<uintptr_t>(dres_bf) & 7) != 0))
+    return hipErrorInvalidValue;
   if (d % 4 != 0 || d > 64 * 4 * 16 || lddy % 4 != 0 || ldx % 4 != 0 || ldres % 4 != 0 ||
       n_part <= 0)
     return hipErrorInvalidValue;
   const int nc = sat_cdiv(d, 1024);
-#define LNB(NC) ln_bwd_launch<NC>(dy, lddy, x, ldx, row_stride, g, mean, rstd, dres, ldres, part_g, part_b, rows, d, n_part, s)
+#define LNB(NC) ln_bwd_launch<NC>(dy, lddy, x, ldx, row_stride, g, mean, rstd, dres, ldres, part_g, part_b, rows, d, n_part, s, dres_bf, ldbf)
   if (nc <= 1) return LNB(1);
   if (nc <= 2) return LNB(2);
   return LNB(4);

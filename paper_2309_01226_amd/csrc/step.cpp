@@ -290,6 +290,8 @@ static sat_status wgrad(sat_model* M, bool trans, bool y_ready, const bf16* Y, l
   return gemm(M, w, LAY_MN, LAY_MN, EPI_F32);
 }
 
+// LayerNorm backward into the residual gradient dh, which it also rounds into
+// dh_bf, the bf16 copy the next products read.
 static sat_status ln_bwd(sat_model* M, const float* dy, const float* x, long row_stride,
                          int gidx, const float* mean, const float* rstd, int rows) {
   const int d = M->D.d;
@@ -297,7 +299,7 @@ static sat_status ln_bwd(sat_model* M, const float* dy, const float* x, long row
   float* pg = M->part;
   float* pbb = M->part + (size_t)np_ * d;
   SAT_HIP(launch_layernorm_bwd(dy, d, x, d, row_stride, master(M, gidx), mean, rstd, M->dh, d, pg,
-                               pbb, rows, d, np_, M->stream));
+                               pbb, rows, d, np_, M->stream, M->dh_bf, d));
   SAT_HIP(launch_colsum_partials(pg, np_, d, grad(M, gidx), M->stream));
   SAT_HIP(launch_colsum_partials(pbb, np_, d, grad(M, gidx + 1), M->stream));
   return SAT_OK;
@@ -332,7 +334,10 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
     float* pg = M->part;
     float* pbb = M->part + (size_t)np_ * d;
     SAT_HIP(launch_layernorm_bwd(M->dA, d, M->h_in[D.L], d, rstride, master(M, hb + 0), M->meanf,
-                                 M->rstdf, M->dh, d, pg, pbb, R, d, np_, s));
+                                 M->rstdf, M->dh, d, pg, pbb, R, d, np_, s,
+                                 rstride == 1 ? M->dh_bf : nullptr, d));
+    if (rstride != 1)  // ViT: only the CLS rows of dh were written
+      SAT_HIP(launch_f32_to_bf16(M->dh, d, M->dh_bf, d, T, d, s));
     SAT_HIP(launch_colsum_partials(pg, np_, d, grad(M, hb + 0), s));
     SAT_HIP(launch_colsum_partials(pbb, np_, d, grad(M, hb + 1), s));
   }
@@ -366,8 +371,9 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
     const double attn_bwd_flops =
         8.0 * D.B * D.H * (double)D.S * D.S * D.dh * (ab.f.causal ? 0.5 : 1.0);
 
+    // dh_bf: the bf16 copy of dh, written by the LayerNorm backward that last
+    // updated dh (the head's, or the block above's)
     if (gptj) {
-      SAT_HIP(launch_f32_to_bf16(M->dh, d, M->dh_bf, d, T, d, s));
       const bool tr = M->trans_blocks;
       SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + J_FC2B), s));
       GemmArgs du = gargs(M->dh_bf, d, shadow_t(M, pb + J_FC2W), d, T, m, d, M->dqkv + 3 * d, D.qkv_ld);
@@ -392,7 +398,6 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
                                  grad(M, pb + J_FC1B), s));
       TRY(ln_bwd(M, M->dA, M->h_in[l], 1, pb + J_LN1G, A.mean1, A.rstd1, T));
     } else {
-      SAT_HIP(launch_f32_to_bf16(M->dh, d, M->dh_bf, d, T, d, s));
       const bool tr = M->trans_blocks;
       SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + B_FC2B), s));
       GemmArgs du = gargs(M->dh_bf, d, shadow_t(M, pb + B_FC2W), d, T, m, d, M->du, m);
@@ -406,7 +411,6 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
       TRY(wgrad(M, tr, false, M->du, m, m, A.c, d, m, d, T, pb + B_FC1W));
       SAT_HIP(launch_colsum_bf16(M->du, m, T, m, M->part, npT, grad(M, pb + B_FC1B), s));
       TRY(ln_bwd(M, M->dA, A.h_mid, 1, pb + B_LN2G, A.mean2, A.rstd2, T));
-      SAT_HIP(launch_f32_to_bf16(M->dh, d, M->dh_bf, d, T, d, s));
       SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + B_PROJB), s));
       GemmArgs go = gargs(M->dh_bf, d, shadow_t(M, pb + B_PROJW), d, T, d, d, M->dout, d);
       TRY(gemm(M, go, LAY_K, LAY_K, EPI_BF16));
