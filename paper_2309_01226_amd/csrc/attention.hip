@@ -1216,6 +1216,7 @@ hipError_t fwd_launch(const AttnArgs& a, hipStream_t s) {
 template <int DH>
 hipError_t bwd_launch(const AttnBwdArgs& a, hipStream_t s) {
   using C = AttnCfg<DH>;
+  if ((DH == 64 || DH == 80) && attn_small_bwd_eligible(a)) return launch_attn_small_bwd(a, s);
   long rows = (long)a.f.B * a.f.S * a.f.H;
   hipLaunchKernelGGL(attn_delta_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
@@ -1255,6 +1256,7 @@ hipError_t launch_attention_fwd(const AttnArgs& a, hipStream_t s) {
   if (a.B * a.H * a.S == 0) return hipSuccess;
   if (!ok16(a.q, a.ldq) || !ok16(a.k, a.ldk) || !ok16(a.v, a.ldv)) return hipErrorInvalidValue;
   if (attn256_fwd_eligible(a)) return launch_attn256_fwd(a, s);
+  if (attn_small_fwd_eligible(a)) return launch_attn_small_fwd(a, s);
   switch (a.dh) {
     case 16: return fwd_launch<16>(a, s);
     case 32: return fwd_launch<32>(a, s);

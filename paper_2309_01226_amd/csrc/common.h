@@ -37,7 +37,7 @@ __device__ __forceinline__ double wave_sum_d(double v) {
   return v;
 }
 
-// GELU, tanh approximation and exact erf form, and their derivatives.
+// GELU, tanh approximation and erf form, and their derivatives.
 // tanh(y) is evaluated as 1 - 2 / (exp(2y) + 1) with the hardware base-2
 // exponential and reciprocal (about 1 ulp each), which saturates correctly at
 // both ends (exp overflow gives 1, underflow gives -1).
@@ -54,13 +54,29 @@ __device__ __forceinline__ float gelu_tanh_grad_f(float x) {
   float t = tanh_fast(c * (x + a * x * x * x));
   return 0.5f * (1.f + t) + 0.5f * x * (1.f - t * t) * c * (1.f + 3.f * a * x * x);
 }
+// 1 + erf(z) for the erf-form GELU, from Abramowitz & Stegun 7.1.26
+// (Hastings' rational approximation): erfc(|z|) ~= q = t P(t) exp(-z^2),
+// t = 1 / (1 + p |z|), absolute error at most 1.5e-7.  For z < 0 the result
+// is q itself, so the negative tail keeps its relative accuracy (no
+// cancellation in 1 + erf).  exp(-z^2) is returned as well: at
+// z = x / sqrt(2) it is the Gaussian density factor of GELU'.
+__device__ __forceinline__ float one_plus_erf(float z, float& ez2) {
+  const float az = fabsf(z);
+  const float t = __builtin_amdgcn_rcpf(__builtin_fmaf(0.3275911f, az, 1.f));
+  const float poly =
+      t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
+  ez2 = __builtin_amdgcn_exp2f(-1.4426950408889634f * az * az);
+  const float q = poly * ez2;
+  return z >= 0.f ? 2.f - q : q;
+}
 __device__ __forceinline__ float gelu_erf_f(float x) {
-  return 0.5f * x * (1.f + erff(x * 0.7071067811865476f));
+  float e;
+  return 0.5f * x * one_plus_erf(x * 0.7071067811865476f, e);
 }
 __device__ __forceinline__ float gelu_erf_grad_f(float x) {
-  float cdf = 0.5f * (1.f + erff(x * 0.7071067811865476f));
-  float pdf = 0.3989422804014327f * __expf(-0.5f * x * x);
-  return cdf + x * pdf;
+  float e;
+  const float cdf = 0.5f * one_plus_erf(x * 0.7071067811865476f, e);
+  return cdf + x * (0.3989422804014327f * e);
 }
 __device__ __forceinline__ float gelu_f(float x, int erf_form) {
   return erf_form ? gelu_erf_f(x) : gelu_tanh_f(x);

@@ -151,6 +151,12 @@ hipError_t launch_attention_bwd(const AttnBwdArgs& a, hipStream_t s);
 bool attn256_bwd_eligible(const AttnBwdArgs& a);
 hipError_t launch_attn256_bwd_dkdv(const AttnBwdArgs& a, hipStream_t s);
 hipError_t launch_attn256_bwd_dq(const AttnBwdArgs& a, hipStream_t s);
+// 64- and 80-wide heads (attn_small.hip): forward, and dK / dV then dQ after
+// launch_attention_bwd has computed delta.
+bool attn_small_fwd_eligible(const AttnArgs& a);
+bool attn_small_bwd_eligible(const AttnBwdArgs& a);
+hipError_t launch_attn_small_fwd(const AttnArgs& a, hipStream_t s);
+hipError_t launch_attn_small_bwd(const AttnBwdArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- elementwise
 // GPT-J rotary on interleaved pairs of the first rd dims of every q and k head,

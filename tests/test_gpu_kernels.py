@@ -83,7 +83,11 @@ ATTN = [(2, 3, 100, 16, True), (1, 2, 257, 80, False), (2, 2, 300, 64, True), (1
         (1, 1, 1, 64, True), (1, 2, 129, 128, False), (2, 1, 70, 32, False),
         # pipelined kernels: several 32-row blocks, ragged tails, both masks
         (2, 1, 520, 256, True), (1, 2, 97, 256, False), (1, 1, 5, 256, True), (2, 2, 333, 128, True),
-        (1, 3, 200, 64, False), (1, 1, 31, 128, True)]
+        (1, 3, 200, 64, False), (1, 1, 31, 128, True),
+        # 64- and 80-wide heads: several 128-row workgroups, diagonal and tail
+        # blocks, single-key tails (257 = 4 x 64 + 1), empty waves
+        (2, 3, 640, 64, True), (1, 1, 33, 64, False), (1, 2, 257, 64, True), (3, 2, 513, 80, True),
+        (2, 2, 190, 80, True), (2, 2, 1, 80, False), (1, 2, 385, 80, False)]
 
 
 @pytest.mark.parametrize("B,H,S,dh,causal", ATTN)
