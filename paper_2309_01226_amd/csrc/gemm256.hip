@@ -966,10 +966,27 @@ hipError_t launch_gemm256(const GemmArgs& a, int alay, int blay, int epi, hipStr
 int gemm_splitk(int M, int N, int K, int* kc) {
   const long tiles = (long)sat_cdiv(M, BT) * sat_cdiv(N, BT);
   if (M <= 0 || N <= 0 || tiles >= 256 || K < 1024) return 1;
-  int S = (int)std::min<long>((256 + tiles - 1) / tiles, K / 512);
-  S = std::min(S, 16);
-  if (S < 2) return 1;
-  const int c = (sat_cdiv(K, S) + BK - 1) / BK * BK;
+  // Estimated time of S slices, in K-tile steps of one tile: the slices run
+  // in rounds of 256 workgroups (one per CU), each round as long as one
+  // slice; the reduction streams S partial products plus the output (about
+  // 9 MB per K-tile step at the measured GEMM and copy rates).  A slice
+  // count that spills a few workgroups into a second round loses to a
+  // smaller one that fits in the first.
+  const int Smax = std::min(16, K / 512);
+  int best = 1;
+  double best_cost = (double)sat_cdiv(K, BK);
+  for (int S = 2; S <= Smax; ++S) {
+    const int c = (sat_cdiv(K, S) + BK - 1) / BK * BK;
+    const int Se = sat_cdiv(K, c);
+    const double rounds = (double)((tiles * Se + 255) / 256);
+    const double cost = rounds * (c / BK) + (double)(Se + 1) * M * N * 4.0 / 9e6;
+    if (cost < best_cost) {
+      best_cost = cost;
+      best = S;
+    }
+  }
+  if (best < 2) return 1;
+  const int c = (sat_cdiv(K, best) + BK - 1) / BK * BK;
   if (kc) *kc = c;
   return sat_cdiv(K, c);
 }
