@@ -125,6 +125,48 @@ def test_attention_fwd_bwd(B, H, S, dh, causal):
         assert err <= 2e-2 * max(np.linalg.norm(ref), floor), (part, err, np.linalg.norm(ref))
 
 
+# Attention at the full per-layer shapes the step launches (GPT-J, GPT-2-small,
+# ViT-H/14, a grid member at batch 16), checked on sampled heads (the first
+# and the last (batch, head) plus one in between) against the oracle.
+FULL_ATTN = [(2, 16, 2048, 256, True), (8, 12, 1024, 64, True), (64, 16, 257, 80, False),
+             (16, 16, 512, 64, True)]
+
+
+@pytest.mark.parametrize("B,H,S,dh,causal", FULL_ATTN)
+def test_attention_full_size_sampled(B, H, S, dh, causal):
+    flush(f"attention full size B={B} H={H} S={S} dh={dh} causal={causal}")
+    rng = np.random.default_rng(B * H + S)
+    d = H * dh
+    buf = rng.standard_normal(size=(B * S, 3 * d), dtype=np.float32)
+    buf = bf16_round(buf)
+    qkv = to_dev_bf16(buf)
+    o = torch.empty(B * S, d, device="cuda", dtype=torch.bfloat16)
+    lse = torch.empty(B * H * S, device="cuda")
+    scale = 1.0 / math.sqrt(dh)
+    K = ops()
+    K.attention_fwd(qkv, qkv[:, d:], qkv[:, 2 * d:], o, lse, B, H, S, dh, causal, scale,
+                    ldq=3 * d, ldk=3 * d, ldv=3 * d, ldo=d)
+    do = bf16_round(rng.standard_normal(size=(B * S, d), dtype=np.float32))
+    dq = torch.empty(B * S, 3 * d, device="cuda", dtype=torch.bfloat16)
+    K.attention_bwd(qkv, qkv[:, d:], qkv[:, 2 * d:], o, lse, to_dev_bf16(do), dq, dq[:, d:],
+                    dq[:, 2 * d:], B, H, S, dh, causal, scale, ldq=3 * d, ldk=3 * d, ldv=3 * d,
+                    ldo=d, lddo=d, lddq=3 * d, lddk=3 * d, lddv=3 * d)
+    torch.cuda.synchronize()
+    go, glse, gd = host(o), host(lse).reshape(B, H, S), host(dq)
+    for b, h in ((0, 0), (B // 2, H // 3), (B - 1, H - 1)):
+        rows = slice(b * S, (b + 1) * S)
+        part = lambda x, j: x[rows, j * d + h * dh: j * d + (h + 1) * dh].astype(np.float64)[None, None]
+        q, k, v = part(buf, 0), part(buf, 1), part(buf, 2)
+        ro, rlse, probs = O.attention(q, k, v, causal)
+        assert rel(go[rows, h * dh:(h + 1) * dh], ro[0, 0]) < 1e-2, (b, h)
+        assert np.max(np.abs(glse[b, h] - rlse[0, 0])) < 1e-4 * max(1.0, np.abs(rlse).max()), (b, h)
+        dos = do[rows, h * dh:(h + 1) * dh].astype(np.float64)[None, None]
+        rdq, rdk, rdv = O.attention_bwd(dos, q, k, v, probs)
+        for j, ref in ((0, rdq), (1, rdk), (2, rdv)):
+            err = np.linalg.norm(gd[rows, j * d + h * dh: j * d + (h + 1) * dh] - ref[0, 0])
+            assert err <= 2e-2 * np.linalg.norm(ref), (b, h, j, err, np.linalg.norm(ref))
+
+
 # ------------------------------------------------------------------ rotary
 
 @pytest.mark.parametrize("inverse", [False, True])
