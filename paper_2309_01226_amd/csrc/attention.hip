@@ -1217,6 +1217,10 @@ template <int DH>
 hipError_t bwd_launch(const AttnBwdArgs& a, hipStream_t s) {
   using C = AttnCfg<DH>;
   if ((DH == 64 || DH == 80) && attn_small_bwd_eligible(a)) return launch_attn_small_bwd(a, s);
+  if (DH == 256 && attn256_bwd_eligible(a)) {  // dQ (which also writes delta), then dK / dV
+    hipError_t e = launch_attn256_bwd_dq(a, s);
+    return e != hipSuccess ? e : launch_attn256_bwd_dkdv(a, s);
+  }
   long rows = (long)a.f.B * a.f.S * a.f.H;
   hipLaunchKernelGGL(attn_delta_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
@@ -1225,15 +1229,10 @@ hipError_t bwd_launch(const AttnBwdArgs& a, hipStream_t s) {
     constexpr int D = (DH == 64 || DH == 128 || DH == 256) ? DH : 64;
     constexpr bool PAIR = D == 256;
     constexpr int KPW = PAIR ? WG_ROWS / 2 : WG_ROWS;
-    if (D == 256 && attn256_bwd_eligible(a)) {
-      e = launch_attn256_bwd_dkdv(a, s);
-    } else {
-      dim3 gkv((a.f.S + KPW - 1) / KPW, a.f.B * a.f.H);
-      hipLaunchKernelGGL((attn_bwd_dkdv_fast<D, PAIR>), gkv, dim3(NT), 0, s, a);
-      e = hipGetLastError();
-    }
+    dim3 gkv((a.f.S + KPW - 1) / KPW, a.f.B * a.f.H);
+    hipLaunchKernelGGL((attn_bwd_dkdv_fast<D, PAIR>), gkv, dim3(NT), 0, s, a);
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (D == 256 && attn256_bwd_eligible(a)) return launch_attn256_bwd_dq(a, s);
     dim3 gq((a.f.S + WG_ROWS - 1) / WG_ROWS, a.f.B * a.f.H);
     hipLaunchKernelGGL((attn_bwd_dq_fast<D>), gq, dim3(NT), 0, s, a);
     return hipGetLastError();

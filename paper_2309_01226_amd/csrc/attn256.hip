@@ -485,7 +485,8 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dkdv_kernel(AttnBwdArgs a)
 // dO, forms dP^T = V dO^T, takes P^T from its partner through LDS and
 // accumulates dQ^T += K^T dS^T, dS^T = P^T (dP^T - delta).  Lanes own queries,
 // so lse and delta are per-lane scalars.  K rows are read as row fragments and
-// transposed (K^T) from the same dual-swizzled tile.
+// transposed (K^T) from the same dual-swizzled tile.  This kernel runs before
+// the dK / dV kernel and also computes delta = rowsum(dO * O) for it.
 constexpr int QPW = 128;   // queries per workgroup
 constexpr int STG_Q = 2 * QT;  // K rows, V rows of a 32-key block
 
@@ -523,7 +524,25 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dq_kernel(AttnBwdArgs a) {
     for (int c = 0; c < DH / 16; ++c)
       rf[c] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rq, qo, 32 * c, 0));
   }
-  const float lsd = q < S ? (role ? a.delta[hs + q] : a.f.lse[hs + q] * LOG2E) : 0.f;
+  // role A: lse2 of this lane's query; role B: delta = rowsum(dO * O), from
+  // the two halves of the row (lanes l and l + 32), also stored for the dK / dV
+  // kernel, which runs after this one
+  float lsd;
+  if (role == 0) {
+    lsd = q < S ? a.f.lse[hs + q] * LOG2E : 0.f;
+  } else {
+    const __amdgpu_buffer_rsrc_t ro = rows_rsrc(a.f.o + (long)b * S * a.f.ldo + (long)h * DH, pq0, a.f.ldo);
+    const uint32_t oo = q < S ? (uint32_t)(((long)(lane & 31) * a.f.ldo + 8 * g) * 2) : OOB;
+    float acc = 0.f;
+#pragma unroll
+    for (int c = 0; c < DH / 16; ++c) {
+      const bf16x8 ov = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(ro, oo, 32 * c, 0));
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc = __builtin_fmaf(bf2f(rf[c][e]), bf2f(ov[e]), acc);
+    }
+    lsd = halves_sum(acc);
+    if (g == 0 && q < S) a.delta[hs + q] = lsd;
+  }
   floatx16 acc[DH / 32];  // dQ^T (role B): dims 32 ot + acc_row(r, g), query = lane
 #pragma unroll
   for (int t = 0; t < DH / 32; ++t) acc[t] = zero16();
@@ -628,6 +647,7 @@ bool attn256_bwd_eligible(const AttnBwdArgs& a) {
   auto ok = [](const void* p, long ld) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0 && ld % 8 == 0; };
   auto ok8 = [](const void* p, long ld) { return (reinterpret_cast<uintptr_t>(p) & 7) == 0 && ld % 4 == 0; };
   return attn256_fwd_eligible(a.f) && ok(a.dout, a.lddo) && ok8(a.dk, a.lddk) && ok8(a.dv, a.lddv) &&
+         ok(a.f.o, a.f.ldo) && (long)QPW * a.f.ldo * 2 < (1L << 30) && a.delta != nullptr &&
          (long)KPW * a.f.ldk * 2 < (1L << 30) && (long)KPW * a.f.ldv * 2 < (1L << 30) &&
          (long)QPW * a.f.ldq * 2 < (1L << 30) && (long)QPW * a.lddo * 2 < (1L << 30) &&
          (reinterpret_cast<uintptr_t>(a.dq) & 7) == 0 && a.lddq % 4 == 0;

@@ -14,23 +14,47 @@
 namespace {
 
 // ---------------------------------------------------------------- rotary
-// One thread per (token, pair i): angle = pos * 10000^(-2i/rd) in double
-// precision, rounded to float cos / sin once, then the 2x2 rotation (or its
-// transpose for backward) of pair i of every q and k head of the token.
+// Angle of pair i at position pos: pos * 10000^(-2i/rd), in double precision,
+// rounded to float cos / sin once.
+__device__ __forceinline__ void rope_cs(int pos, int i, int rd, float& c, float& sn) {
+  const double ang = (double)pos * pow(10000.0, -2.0 * i / (double)rd);
+  double sd, cd;
+  sincos(ang, &sd, &cd);
+  c = (float)cd;
+  sn = (float)sd;
+}
+
+__global__ void rope_table_kernel(float2* __restrict__ cs, int S, int rd) {
+  const int half = rd / 2;
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long)S * half) return;
+  float c, sn;
+  rope_cs((int)(idx / half), (int)(idx % half), rd, c, sn);
+  cs[idx] = make_float2(c, sn);
+}
+
+// One thread per (token, pair i): the 2x2 rotation (or its transpose for
+// backward) of pair i of every q and k head of the token, with cos / sin from
+// the table cs[pos][i] when given (the same values computed inline otherwise).
 // Consecutive threads take consecutive pairs, so each head's rotated part is
 // read and written as one contiguous piece (a pair is one 4-byte word).
 __global__ void rotary_kernel(bf16* __restrict__ qk, long ld, int T, int S, int H, int dh, int rd,
-                              int inverse) {
+                              int inverse, const float2* __restrict__ cs) {
   const int half = rd / 2;
   long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (long)T * half) return;
   const int i = idx % half;
   const int t = (int)(idx / half);
   const int pos = t % S;
-  double ang = (double)pos * pow(10000.0, -2.0 * i / (double)rd);
-  double sn, cs;
-  sincos(ang, &sn, &cs);
-  const float c = (float)cs, s = inverse ? -(float)sn : (float)sn;
+  float c, sn;
+  if (cs != nullptr) {
+    const float2 v = cs[(long)pos * half + i];
+    c = v.x;
+    sn = v.y;
+  } else {
+    rope_cs(pos, i, rd, c, sn);
+  }
+  const float s = inverse ? -sn : sn;
   bf16* row = qk + (long)t * ld + 2 * i;
   for (int hh = 0; hh < 2 * H; ++hh) {  // q heads, then k heads
     uint32_t* p = reinterpret_cast<uint32_t*>(row + (long)hh * dh);
@@ -500,14 +524,21 @@ inline unsigned blocks_for(long n, int bs = 256) { return (unsigned)((n + bs - 1
 
 }  // namespace
 
+hipError_t launch_rope_table(float2* cs, int S, int rd, hipStream_t s) {
+  if (rd <= 0 || S <= 0) return hipSuccess;
+  if (rd % 2) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(rope_table_kernel, dim3(blocks_for((long)S * (rd / 2))), dim3(256), 0, s, cs, S, rd);
+  return hipGetLastError();
+}
+
 hipError_t launch_rotary(bf16* qk, long ld, int B, int S, int H, int dh, int rd, int inverse,
-                         hipStream_t s) {
+                         hipStream_t s, const float2* cs) {
   if (rd <= 0) return hipSuccess;
   if (rd % 2 || rd > dh || ld % 2 || dh % 2 || (reinterpret_cast<uintptr_t>(qk) & 3))
     return hipErrorInvalidValue;
   long total = (long)B * S * (rd / 2);
   hipLaunchKernelGGL(rotary_kernel, dim3(blocks_for(total)), dim3(256), 0, s, qk, ld, B * S, S, H,
-                     dh, rd, inverse);
+                     dh, rd, inverse, cs);
   return hipGetLastError();
 }
 

@@ -160,9 +160,13 @@ hipError_t launch_attn_small_bwd(const AttnBwdArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- elementwise
 // GPT-J rotary on interleaved pairs of the first rd dims of every q and k head,
-// in place on the bf16 [T, ld] buffer (q at column 0, k at column d).
+// in place on the bf16 [T, ld] buffer (q at column 0, k at column d).  cs: the
+// table of launch_rope_table for this S and rd, or null to compute the angles
+// inline (same values).
 hipError_t launch_rotary(bf16* qk, long ld, int B, int S, int H, int dh, int rd, int inverse,
-                         hipStream_t s);
+                         hipStream_t s, const float2* cs = nullptr);
+// cs[pos * (rd / 2) + i] = (cos, sin) of pos * 10000^(-2i/rd), pos < S.
+hipError_t launch_rope_table(float2* cs, int S, int rd, hipStream_t s);
 // h0[t, :] = wte[tok[t], :] (+ wpe[t % S, :])
 hipError_t launch_embed_fwd(const int32_t* tok, const float* wte, const float* wpe, float* h,
                             int T, int S, int d, int V, hipStream_t s);

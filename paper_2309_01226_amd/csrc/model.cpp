@@ -379,6 +379,7 @@ size_t carve(sat_model* M, char* base) {
     M->tB = nb > 0 ? c.take<bf16>(nb) : nullptr;
   }
   M->delta = c.take<float>((size_t)D.B * D.H * D.S);
+  M->rope_cs = D.rd > 0 ? c.take<float2>((size_t)D.S * (D.rd / 2)) : nullptr;
   M->n_part = (int)(T < 256 ? T : 256);
   long wide = D.qkv_ld > D.Vp ? D.qkv_ld : D.Vp;
   if (D.arch == SAT_VIT && D.pd > wide) wide = D.pd;

@@ -131,6 +131,7 @@ struct sat_model {
   float* splitk_ws;
   long splitk_ws_elems;
   float* delta;
+  float2* rope_cs;  // rotary (cos, sin) per (position, pair); null without rotary
   float* part;
   int n_part;
   int32_t* sortbuf;

@@ -123,6 +123,7 @@ sat_status sat_run_init(sat_model* M) {
     else
       SAT_HIP(launch_fill(dst, sh, n, p.kind == 2 ? 1.f : 0.f, s));
   }
+  if (M->rope_cs) SAT_HIP(launch_rope_table(M->rope_cs, M->D.S, M->D.rd, s));
   return sat_refresh_transposed(M);
 }
 
@@ -154,7 +155,7 @@ static sat_status block_forward(sat_model* M, int l, bool recompute) {
     a.gelu_col0 = 3 * d;
     a.gelu_erf = 0;
     TRY(gemm(M, a, LAY_K, LAY_K, EPI_BF16, tk_qkv));
-    SAT_HIP(launch_rotary(A.qkv, D.qkv_ld, D.B, D.S, D.H, D.dh, D.rd, 0, s));
+    SAT_HIP(launch_rotary(A.qkv, D.qkv_ld, D.B, D.S, D.H, D.dh, D.rd, 0, s, M->rope_cs));
   } else {
     GemmArgs a = gargs(A.a, d, shadow(M, pb + B_QKVW), d, T, 3 * d, d, A.qkv, 3 * d);
     a.bias = master(M, pb + B_QKVB);
@@ -389,7 +390,7 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
         Timed tm(M, TK_ATTN_BWD, attn_bwd_flops);
         SAT_HIP(launch_attention_bwd(ab, s));
       }
-      SAT_HIP(launch_rotary(M->dqkv, D.qkv_ld, D.B, D.S, D.H, D.dh, D.rd, 1, s));
+      SAT_HIP(launch_rotary(M->dqkv, D.qkv_ld, D.B, D.S, D.H, D.dh, D.rd, 1, s, M->rope_cs));
       GemmArgs ga = gargs(M->dqkv, D.qkv_ld, shadow_t(M, pb + J_QKVW), D.qkv_ld, T, d, D.qkv_ld,
                           M->dA, d);
       TRY(gemm(M, ga, LAY_K, LAY_K, EPI_F32));
