@@ -33,11 +33,46 @@ __global__ void rope_table_kernel(float2* __restrict__ cs, int S, int rd) {
   cs[idx] = make_float2(c, sn);
 }
 
-// One thread per (token, pair i): the 2x2 rotation (or its transpose for
-// backward) of pair i of every q and k head of the token, with cos / sin from
-// the table cs[pos][i] when given (the same values computed inline otherwise).
-// Consecutive threads take consecutive pairs, so each head's rotated part is
-// read and written as one contiguous piece (a pair is one 4-byte word).
+// One thread per (token, q or k head, 8 dims = 4 pairs) of the rotated part:
+// one 16-byte load and store, the 2x2 rotation (or its transpose for
+// backward) of each pair with cos / sin from the table cs[pos][i] when given
+// (the same values computed inline otherwise).  Needs rd % 8 == 0, dh and ld
+// multiples of 8 and a 16-byte aligned buffer (launch_rotary checks).
+__global__ void rotary8_kernel(bf16* __restrict__ qk, long ld, int T, int S, int H, int dh, int rd,
+                               int inverse, const float2* __restrict__ cs) {
+  const int c8 = rd / 8;
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long)T * 2 * H * c8) return;
+  const int c = idx % c8;
+  const long th = idx / c8;
+  const int hh = th % (2 * H);  // q heads, then k heads
+  const int t = (int)(th / (2 * H));
+  const int pos = t % S;
+  u32x4* p = reinterpret_cast<u32x4*>(qk + (long)t * ld + (long)hh * dh + 8 * c);
+  u32x4 w = *p;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int i = 4 * c + j;
+    float cc, sn;
+    if (cs != nullptr) {
+      const float2 v = cs[(long)pos * (rd / 2) + i];
+      cc = v.x;
+      sn = v.y;
+    } else {
+      rope_cs(pos, i, rd, cc, sn);
+    }
+    const float s = inverse ? -sn : sn;
+    const float x0 = __uint_as_float(w[j] << 16), x1 = __uint_as_float(w[j] & 0xFFFF0000u);
+    const bf16 y0 = f2bf(x0 * cc - x1 * s), y1 = f2bf(x0 * s + x1 * cc);
+    w[j] = (uint32_t)__builtin_bit_cast(uint16_t, y0) | ((uint32_t)__builtin_bit_cast(uint16_t, y1) << 16);
+  }
+  *p = w;
+}
+
+// General form (any even rd): one thread per (token, pair i), all heads,
+// with the same arithmetic.  Consecutive threads take consecutive pairs, so
+// each head's rotated part is read and written as one contiguous piece (a
+// pair is one 4-byte word).
 __global__ void rotary_kernel(bf16* __restrict__ qk, long ld, int T, int S, int H, int dh, int rd,
                               int inverse, const float2* __restrict__ cs) {
   const int half = rd / 2;
@@ -536,6 +571,12 @@ hipError_t launch_rotary(bf16* qk, long ld, int B, int S, int H, int dh, int rd,
   if (rd <= 0) return hipSuccess;
   if (rd % 2 || rd > dh || ld % 2 || dh % 2 || (reinterpret_cast<uintptr_t>(qk) & 3))
     return hipErrorInvalidValue;
+  if (rd % 8 == 0 && dh % 8 == 0 && ld % 8 == 0 && (reinterpret_cast<uintptr_t>(qk) & 15) == 0) {
+    const long total = (long)B * S * 2 * H * (rd / 8);
+    hipLaunchKernelGGL(rotary8_kernel, dim3(blocks_for(total)), dim3(256), 0, s, qk, ld, B * S, S, H,
+                       dh, rd, inverse, cs);
+    return hipGetLastError();
+  }
   long total = (long)B * S * (rd / 2);
   hipLaunchKernelGGL(rotary_kernel, dim3(blocks_for(total)), dim3(256), 0, s, qk, ld, B * S, S, H,
                      dh, rd, inverse, cs);

@@ -169,10 +169,12 @@ def test_attention_full_size_sampled(B, H, S, dh, causal):
 
 # ------------------------------------------------------------------ rotary
 
+# rd % 8 == 0 takes the 16-byte kernel, other even rd the per-pair one
 @pytest.mark.parametrize("inverse", [False, True])
-def test_rotary(inverse):
+@pytest.mark.parametrize("dh,rd", [(32, 8), (32, 6), (256, 64)])
+def test_rotary(inverse, dh, rd):
     rng = np.random.default_rng(21)
-    B, S, H, dh, rd = 2, 300, 3, 32, 8
+    B, S, H = 2, 300, 3
     d = H * dh
     buf = bf16_round(rng.normal(size=(B * S, 3 * d)))
     dev = to_dev_bf16(buf)
