@@ -11,7 +11,11 @@ tile-row holding 8 of its 256 rows) take the fused path; the out-projection
   * fused and separate updates (SAT_OPT_FUSED_ADAMW 1 / 0) give bitwise equal
     losses, parameters and moments over three steps: the same fp32 AdamW
     arithmetic on the same fp32 gradient, and the transposed bf16 copies the
-    next step's input-gradient products read;
+    next step's input-gradient products read.  Without kept gradients the
+    products apply each tile's update during the workgroup's next tile
+    (persistent grid of 256 workgroups, the last tile's update drained at
+    the end); 448 tiles give some workgroups a deferred tile and others
+    only a drained one;
   * with SAT_OPT_KEEP_GRADS the fused path stores gradients bitwise equal to
     the separate path's; without it, reading a fused weight's gradient fails
     with SAT_ENOTSUP while every other tensor's gradient is readable;
@@ -35,25 +39,30 @@ KW_ORACLE = dict(KW, d_mlp=2048, vocab=512, seq_len=128)
 FUSED = ("h0.attn.qkv.w", "h0.mlp.fc1.w", "h0.mlp.fc2.w", "head.w")
 
 
-def _models(*opts):
+def _models(*opts, kw=KW):
     from paper_2309_01226_amd.model import Model
     out = []
     for o in opts:
-        m = Model(KW)
+        m = Model(kw)
         for k, v in o.items():
             m.set_option(k, v)
         out.append(m)
     return out
 
 
-def test_fused_equals_separate():
+# The weight-gradient products run with K = batch x seq_len tokens: 512 leaves
+# most row groups of a deferred update to the drain after the main loop, 4096
+# fills exactly the main loop's 64 K-tiles, 8192 finishes them half-way.
+@pytest.mark.parametrize("seq_len", [256, 2048, 4096])
+def test_fused_equals_separate(seq_len):
     from paper_2309_01226_amd.model import device_batch
-    a, b = _models({}, {"fused_adamw": 0})
+    kw = dict(KW, seq_len=seq_len)
+    a, b = _models({}, {"fused_adamw": 0}, kw=kw)
     Pa0, Pb0 = a.params(), b.params()
     for n in Pa0:
         assert np.array_equal(Pa0[n], Pb0[n]), n
     for step in range(3):
-        x, y = device_batch(KW, seed=0, step=step)
+        x, y = device_batch(kw, seed=0, step=step)
         la, lb = a.train_step(x, y), b.train_step(x, y)
         flush(f"step {step}: fused {la!r} separate {lb!r}")
         assert la == lb, (step, la, lb)
@@ -66,7 +75,7 @@ def test_fused_equals_separate():
         assert np.array_equal(Sa[n][0], Sb[n][0]) and np.array_equal(Sa[n][1], Sb[n][1]), ("state", n)
     for n in FUSED:  # the fused weights did move
         assert not np.array_equal(Pa[n], Pa0[n]), n
-    x, y = device_batch(KW, seed=0, step=3)
+    x, y = device_batch(kw, seed=0, step=3)
     assert a.eval_loss(x, y) == b.eval_loss(x, y)
     a.close()
     b.close()
