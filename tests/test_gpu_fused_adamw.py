@@ -11,11 +11,7 @@ tile-row holding 8 of its 256 rows) take the fused path; the out-projection
   * fused and separate updates (SAT_OPT_FUSED_ADAMW 1 / 0) give bitwise equal
     losses, parameters and moments over three steps: the same fp32 AdamW
     arithmetic on the same fp32 gradient, and the transposed bf16 copies the
-    next step's input-gradient products read.  Without kept gradients the
-    products apply each tile's update during the workgroup's next tile
-    (persistent grid of 256 workgroups, the last tile's update drained at
-    the end); 448 tiles give some workgroups a deferred tile and others
-    only a drained one;
+    next step's input-gradient products read;
   * with SAT_OPT_KEEP_GRADS the fused path stores gradients bitwise equal to
     the separate path's; without it, reading a fused weight's gradient fails
     with SAT_ENOTSUP while every other tensor's gradient is readable;
@@ -50,9 +46,8 @@ def _models(*opts, kw=KW):
     return out
 
 
-# The weight-gradient products run with K = batch x seq_len tokens: 512 leaves
-# most row groups of a deferred update to the drain after the main loop, 4096
-# fills exactly the main loop's 64 K-tiles, 8192 finishes them half-way.
+# The weight-gradient products run with K = batch x seq_len tokens: 512, 4096
+# (the GPT-J step's K) and 8192.
 @pytest.mark.parametrize("seq_len", [256, 2048, 4096])
 def test_fused_equals_separate(seq_len):
     from paper_2309_01226_amd.model import device_batch
