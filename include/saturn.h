@@ -163,10 +163,13 @@ sat_status sat_model_set_option(sat_model* m, int32_t option, int32_t value);
  * model's stream around each matching launch (at most max_launches between
  * two reads; later launches are not timed).  kind: 0 off, 1 the forward QKV
  * product (GPT-J: the fused QKV + fc1 product), 2 every GEMM, 3 the AdamW
- * update, 4 attention forward, 5 attention backward.  Waits for the stream. */
+ * update, 4 attention forward, 5 attention backward, 6 LayerNorm forward,
+ * 7 LayerNorm backward (the row kernel, not the gain / shift column sums),
+ * 8 softmax cross-entropy.  Waits for the stream. */
 sat_status sat_model_set_timing(sat_model* m, int32_t kind, int32_t max_launches);
 /* Sum of the timed launches' durations (ms), their count and their
- * algorithmic work (FLOPs; bytes for AdamW), then resets the counters. */
+ * algorithmic work (FLOPs; bytes for AdamW, LayerNorm and cross-entropy),
+ * then resets the counters. */
 sat_status sat_model_timing_read(sat_model* m, double* total_ms, int64_t* launches, double* work);
 
 /* ---- profiling (the Trial Runner's runtime estimate, Sec. 3.2) ------------

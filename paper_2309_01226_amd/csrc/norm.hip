@@ -66,6 +66,72 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x
   }
 }
 
+// Wide rows (d >= 1024): one workgroup per row, each thread holding NCH float4
+// chunks (columns (c * 256 + tid) * 4 .. +3), the two row sums combined
+// across the four waves through LDS in a fixed order.  With one wave per row
+// every wave of the grid fits on the chip at once, so all rows load together
+// and then all store together; with a workgroup per row the grid runs in
+// more than one round and one round's stores overlap the next one's loads.
+template <int NCH>
+__global__ __launch_bounds__(256) void ln_fwd_wg_kernel(const float* __restrict__ x, long ldx,
+                                                        long row_stride,
+                                                        const float* __restrict__ g,
+                                                        const float* __restrict__ b,
+                                                        bf16* __restrict__ y, long ldy,
+                                                        float* __restrict__ mean,
+                                                        float* __restrict__ rstd, int d,
+                                                        float eps) {
+  __shared__ float red[2][4];
+  const int row = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const float* xr = x + (long)row * row_stride * ldx;
+  float4 v[NCH];
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int col = (c * 256 + tid) * 4;
+    if (col < d) v[c] = *reinterpret_cast<const float4*>(xr + col);
+    else v[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+    s += v[c].x + v[c].y + v[c].z + v[c].w;
+  }
+  s = wave_sum(s);
+  if (lane == 0) red[0][wave] = s;
+  __syncthreads();
+  const float mu = (red[0][0] + red[0][1] + red[0][2] + red[0][3]) / d;
+  float q = 0.f;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int col = (c * 256 + tid) * 4;
+    if (col < d) {
+      const float a0 = v[c].x - mu, a1 = v[c].y - mu, a2 = v[c].z - mu, a3 = v[c].w - mu;
+      q += a0 * a0 + a1 * a1 + a2 * a2 + a3 * a3;
+    }
+  }
+  q = wave_sum(q);
+  if (lane == 0) red[1][wave] = q;
+  __syncthreads();
+  const float rs = rsqrtf((red[1][0] + red[1][1] + red[1][2] + red[1][3]) / d + eps);
+  bf16* yr = y + (long)row * ldy;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int col = (c * 256 + tid) * 4;
+    if (col < d) {
+      const float4 gg = *reinterpret_cast<const float4*>(g + col);
+      const float4 bb = *reinterpret_cast<const float4*>(b + col);
+      bf16x4 o;
+      o[0] = f2bf((v[c].x - mu) * rs * gg.x + bb.x);
+      o[1] = f2bf((v[c].y - mu) * rs * gg.y + bb.y);
+      o[2] = f2bf((v[c].z - mu) * rs * gg.z + bb.z);
+      o[3] = f2bf((v[c].w - mu) * rs * gg.w + bb.w);
+      *reinterpret_cast<bf16x4*>(yr + col) = o;
+    }
+  }
+  if (tid == 0) {
+    mean[row] = mu;
+    rstd[row] = rs;
+  }
+}
+
 // Backward: workgroup p owns rows [p * rpb, (p + 1) * rpb); each thread owns
 // the columns (j * 256 + tid) * 4 .. +3 and keeps their dg / db partial sums
 // in registers, so the workgroup writes one partial row per tensor and needs
@@ -269,6 +335,15 @@ hipError_t ln_fwd_launch(const float* x, long ldx, long rs, const float* g, cons
   return hipGetLastError();
 }
 
+template <int NCH>
+hipError_t ln_fwd_wg_launch(const float* x, long ldx, long rs, const float* g, const float* b,
+                            bf16* y, long ldy, float* mean, float* rstd, int rows, int d, float eps,
+                            hipStream_t s) {
+  hipLaunchKernelGGL(ln_fwd_wg_kernel<NCH>, dim3(rows), dim3(256), 0, s, x, ldx, rs, g, b, y, ldy,
+                     mean, rstd, d, eps);
+  return hipGetLastError();
+}
+
 template <int NC4>
 hipError_t ln_bwd_launch(const float* dy, long lddy, const float* x, long ldx, long rs,
                          const float* g, const float* mean, const float* rstd, float* dres,
@@ -289,6 +364,13 @@ hipError_t launch_layernorm_fwd(const float* x, long ldx, long row_stride, const
   if (rows <= 0) return hipSuccess;
   if (d % 4 != 0 || d > 64 * 4 * LN_MAXC || ldx % 4 != 0 || ldy % 4 != 0)
     return hipErrorInvalidValue;
+  if (d >= 1024) {
+    const int nch = sat_cdiv(d, 1024);
+    if (nch <= 1) return ln_fwd_wg_launch<1>(x, ldx, row_stride, g, b, y, ldy, mean, rstd, rows, d, eps, s);
+    if (nch <= 2) return ln_fwd_wg_launch<2>(x, ldx, row_stride, g, b, y, ldy, mean, rstd, rows, d, eps, s);
+    if (nch <= 4) return ln_fwd_wg_launch<4>(x, ldx, row_stride, g, b, y, ldy, mean, rstd, rows, d, eps, s);
+    return ln_fwd_wg_launch<8>(x, ldx, row_stride, g, b, y, ldy, mean, rstd, rows, d, eps, s);
+  }
   int nc = sat_cdiv(d, 256);
   if (nc <= 1) return ln_fwd_launch<1>(x, ldx, row_stride, g, b, y, ldy, mean, rstd, rows, d, eps, s);
   if (nc <= 2) return ln_fwd_launch<2>(x, ldx, row_stride, g, b, y, ldy, mean, rstd, rows, d, eps, s);

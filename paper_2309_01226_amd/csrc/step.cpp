@@ -12,7 +12,22 @@
 
 namespace {
 
-enum { TK_OFF = 0, TK_QKV_FWD = 1, TK_ALL_GEMM = 2, TK_ADAMW = 3, TK_ATTN_FWD = 4, TK_ATTN_BWD = 5 };
+enum {
+  TK_OFF = 0, TK_QKV_FWD = 1, TK_ALL_GEMM = 2, TK_ADAMW = 3, TK_ATTN_FWD = 4, TK_ATTN_BWD = 5,
+  TK_LN_FWD = 6, TK_LN_BWD = 7, TK_XENT = 8
+};
+
+// Algorithmic bytes of the bandwidth kernels (each operand read once, each
+// result written once): LayerNorm forward reads fp32 x and writes bf16 y plus
+// the two per-row statistics; the backward reads dy, x and the residual
+// gradient it accumulates into, writes that gradient back (and its bf16 copy),
+// and reads the statistics; cross-entropy reads fp32 logits and the label and
+// writes the bf16 logit gradient and the row loss.
+double ln_fwd_bytes(long rows, int d) { return rows * (double)d * (4 + 2) + rows * 8.0 + d * 8.0; }
+double ln_bwd_bytes(long rows, int d, bool bf) {
+  return rows * (double)d * (4 + 4 + 4 + 4 + (bf ? 2 : 0)) + rows * 8.0 + d * 4.0;
+}
+double xent_bytes(long rows, long V) { return rows * (double)V * (4 + 2) + rows * 8.0; }
 
 struct Timed {
   sat_model* M;
@@ -143,8 +158,11 @@ static sat_status block_forward(sat_model* M, int l, bool recompute) {
   const int tk_qkv = recompute ? TK_ALL_GEMM : TK_QKV_FWD;
   const LayerActs& A = sat_layer_acts(M, l);
   const int pb = block_base(M, l);
-  SAT_HIP(launch_layernorm_fwd(M->h_in[l], d, 1, master(M, pb + 0), master(M, pb + 1), A.a, d,
-                               A.mean1, A.rstd1, T, d, eps, s));
+  {
+    Timed tm(M, TK_LN_FWD, ln_fwd_bytes(T, d));
+    SAT_HIP(launch_layernorm_fwd(M->h_in[l], d, 1, master(M, pb + 0), master(M, pb + 1), A.a, d,
+                                 A.mean1, A.rstd1, T, d, eps, s));
+  }
   if (gptj) {
     // fused q | k | v | u = a [W_qkv; W_fc1]^T (+ fc1 bias on u), g = GELU(u)
     GemmArgs a = gargs(A.a, d, shadow(M, pb + J_QKVW), d, T, D.qkv_ld, d, A.qkv, D.qkv_ld);
@@ -197,8 +215,11 @@ static sat_status block_forward(sat_model* M, int l, bool recompute) {
     a.resid = M->h_in[l];
     a.bias = master(M, pb + B_PROJB);
     TRY(gemm(M, a, LAY_K, LAY_K, EPI_RESID_F32));
-    SAT_HIP(launch_layernorm_fwd(A.h_mid, d, 1, master(M, pb + B_LN2G), master(M, pb + B_LN2B),
-                                 A.c, d, A.mean2, A.rstd2, T, d, eps, s));
+    {
+      Timed tm(M, TK_LN_FWD, ln_fwd_bytes(T, d));
+      SAT_HIP(launch_layernorm_fwd(A.h_mid, d, 1, master(M, pb + B_LN2G), master(M, pb + B_LN2B),
+                                   A.c, d, A.mean2, A.rstd2, T, d, eps, s));
+    }
     GemmArgs b = gargs(A.c, d, shadow(M, pb + B_FC1W), d, T, m, d, A.u, m);
     b.bias = master(M, pb + B_FC1B);
     b.out2 = A.g;
@@ -242,13 +263,19 @@ sat_status sat_run_forward(sat_model* M, const void* inputs, const int32_t* labe
   const int hb = head_base(M);
   const int R = D.rows_head;
   const long rstride = (D.arch == SAT_VIT) ? D.S : 1;
-  SAT_HIP(launch_layernorm_fwd(M->h_in[D.L], d, rstride, master(M, hb + 0), master(M, hb + 1),
-                               M->f, d, M->meanf, M->rstdf, R, d, eps, s));
+  {
+    Timed tm(M, TK_LN_FWD, ln_fwd_bytes(R, d));
+    SAT_HIP(launch_layernorm_fwd(M->h_in[D.L], d, rstride, master(M, hb + 0), master(M, hb + 1),
+                                 M->f, d, M->meanf, M->rstdf, R, d, eps, s));
+  }
   GemmArgs a = gargs(M->f, d, shadow(M, hb + 2), d, R, D.V, d, M->logits, D.Vp);
   if (D.arch != SAT_GPT2) a.bias = master(M, hb + 3);
   TRY(gemm(M, a, LAY_K, LAY_K, EPI_F32));
   SAT_HIP(launch_count_valid(labels, R, M->scal + 1, s));
-  SAT_HIP(launch_xent(M->logits, D.Vp, labels, R, D.V, M->row_loss, M->dz, D.Vp, M->scal + 1, s));
+  {
+    Timed tm(M, TK_XENT, xent_bytes(R, D.V));
+    SAT_HIP(launch_xent(M->logits, D.Vp, labels, R, D.V, M->row_loss, M->dz, D.Vp, M->scal + 1, s));
+  }
   SAT_HIP(launch_loss_finalize(M->row_loss, R, M->scal + 1, M->scal, s));
   return SAT_OK;
 }
@@ -299,8 +326,11 @@ static sat_status ln_bwd(sat_model* M, const float* dy, const float* x, long row
   const int np_ = ln_bwd_parts(rows);
   float* pg = M->part;
   float* pbb = M->part + (size_t)np_ * d;
-  SAT_HIP(launch_layernorm_bwd(dy, d, x, d, row_stride, master(M, gidx), mean, rstd, M->dh, d, pg,
-                               pbb, rows, d, np_, M->stream, M->dh_bf, d));
+  {
+    Timed tm(M, TK_LN_BWD, ln_bwd_bytes(rows, d, true));
+    SAT_HIP(launch_layernorm_bwd(dy, d, x, d, row_stride, master(M, gidx), mean, rstd, M->dh, d, pg,
+                                 pbb, rows, d, np_, M->stream, M->dh_bf, d));
+  }
   SAT_HIP(launch_colsum_partials(pg, np_, d, grad(M, gidx), M->stream));
   SAT_HIP(launch_colsum_partials(pbb, np_, d, grad(M, gidx + 1), M->stream));
   return SAT_OK;
@@ -334,9 +364,12 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
     const int np_ = ln_bwd_parts(R);
     float* pg = M->part;
     float* pbb = M->part + (size_t)np_ * d;
-    SAT_HIP(launch_layernorm_bwd(M->dA, d, M->h_in[D.L], d, rstride, master(M, hb + 0), M->meanf,
-                                 M->rstdf, M->dh, d, pg, pbb, R, d, np_, s,
-                                 rstride == 1 ? M->dh_bf : nullptr, d));
+    {
+      Timed tm(M, TK_LN_BWD, ln_bwd_bytes(R, d, rstride == 1));
+      SAT_HIP(launch_layernorm_bwd(M->dA, d, M->h_in[D.L], d, rstride, master(M, hb + 0),
+                                   M->meanf, M->rstdf, M->dh, d, pg, pbb, R, d, np_, s,
+                                   rstride == 1 ? M->dh_bf : nullptr, d));
+    }
     if (rstride != 1)  // ViT: only the CLS rows of dh were written
       SAT_HIP(launch_f32_to_bf16(M->dh, d, M->dh_bf, d, T, d, s));
     SAT_HIP(launch_colsum_partials(pg, np_, d, grad(M, hb + 0), s));

@@ -20,7 +20,8 @@ def ops():
 
 # ------------------------------------------------------------------ LayerNorm
 
-@pytest.mark.parametrize("rows,d", [(1, 64), (37, 768), (300, 1280), (64, 4096), (5, 16)])
+@pytest.mark.parametrize("rows,d", [(1, 64), (37, 768), (300, 1280), (64, 4096), (5, 16),
+                                    (9, 1028)])
 def test_layernorm_fwd_bwd(rows, d):
     flush(f"layernorm rows={rows} d={d}")
     rng = np.random.default_rng(rows + d)
@@ -47,10 +48,29 @@ def test_layernorm_fwd_bwd(rows, d):
     assert rel(host(dg), rdg) < 1e-5 and rel(host(db), rdb) < 1e-5
 
 
-def test_layernorm_strided_rows():
-    """Rows picked with a stride (the ViT head normalises only the CLS rows)."""
+def test_layernorm_fwd_widest():
+    """The widest row the forward accepts (8192; the backward stops at 4096)."""
+    rng = np.random.default_rng(11)
+    rows, d = 3, 8192
+    x = rng.normal(-0.2, 1.5, size=(rows, d)).astype(np.float32)
+    g = (1 + 0.3 * rng.normal(size=d)).astype(np.float32)
+    b = (0.3 * rng.normal(size=d)).astype(np.float32)
+    y = torch.empty(rows, d, device="cuda", dtype=torch.bfloat16)
+    mean = torch.empty(rows, device="cuda")
+    rstd = torch.empty(rows, device="cuda")
+    ops().layernorm_fwd(to_dev_f32(x), to_dev_f32(g), to_dev_f32(b), y, mean, rstd, rows, d, 1e-5)
+    torch.cuda.synchronize()
+    ry, rmean, rrstd = O.layernorm_fwd(x, g, b, 1e-5)
+    assert rel(host(y), ry) < 4e-3
+    assert rel(host(mean), rmean) < 1e-5 and rel(host(rstd), rrstd) < 1e-5
+
+
+@pytest.mark.parametrize("d", [128, 1280])
+def test_layernorm_strided_rows(d):
+    """Rows picked with a stride (the ViT head normalises only the CLS rows);
+    widths below and above 1024 take the one-wave and one-workgroup row kernels."""
     rng = np.random.default_rng(3)
-    B, S, d = 7, 5, 128
+    B, S = 7, 5
     x = rng.normal(size=(B * S, d)).astype(np.float32)
     g = np.ones(d, np.float32)
     b = np.zeros(d, np.float32)
