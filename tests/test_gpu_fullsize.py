@@ -1,0 +1,125 @@
+"""Whole-step checks at the full sizes of the workloads, in the launch
+configuration the benchmark times.
+
+  * One full-width GPT-J block (d 4096, 16 heads of 256 with rotary on 64,
+    parallel attention + MLP, MLP 16384, vocabulary 50400) trained one step on
+    2 x 2048 tokens: every GEMM, attention and bandwidth kernel runs with the
+    grids and tile counts of the 28-layer step, and the AdamW update of the
+    large matrices runs in the weight-gradient epilogue.  The two sequences of
+    the batch are identical, so the mean loss and every gradient equal those
+    of the one sequence, which the float64 oracle computes at half the cost.
+    Tolerances are the end-to-end ones: loss, activations and logits 2e-2,
+    gradients 3e-2 (relative Frobenius), parameters after the step 1e-2.
+  * Every full-depth workload (GPT-2-small, GPT-J, ViT-H/14, a GPT-2-medium
+    grid member with and without its frozen prefix): the loss at
+    initialisation matches the closed form ln V + 2e-4 d for 0.02-std weights
+    within 3 %, the training step's forward agrees with the evaluation
+    forward, and one step lowers the loss on the same batch.
+"""
+
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests.gpu_util import flush, rel
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "loss_at_init.txt")
+
+
+def _golden_l0():
+    out = {}
+    with open(GOLDEN) as fh:
+        for line in fh:
+            if line.startswith("#") or not line.strip():
+                continue
+            name, _, _, _, l0 = line.split()
+            out[name] = float(l0)
+    return out
+
+
+def _release():
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def test_gptj_full_width_block_step():
+    from paper_2309_01226_amd.configs import preset
+    from paper_2309_01226_amd.inputs import batch_for
+    from paper_2309_01226_amd.model import Model
+
+    kw = preset("gptj", n_layers=1)
+    B, S, d, V = kw["batch"], kw["seq_len"], kw["d_model"], kw["vocab"]
+    xh, yh = batch_for(kw, seed=0, step=0)
+    xh, yh = np.array(xh), np.array(yh)
+    xh[1:] = xh[0]
+    yh[1:] = yh[0]
+    flush(f"full-width GPT-J block: B {B} S {S} d {d} V {V}, fused AdamW with kept gradients")
+    m = Model(kw)
+    m.set_option("keep_grads", 1)
+    P0 = m.params()
+    gl = m.train_step(torch.as_tensor(xh).cuda(), torch.as_tensor(yh).cuda())
+    acts = [m.activation(l) for l in range(kw["n_layers"] + 1)]
+    logits = m.logits()
+    G = m.grads()
+    P1 = m.params()
+    m.close()
+    del m
+    _release()
+
+    ocfg = oracle.Config(**{k: v for k, v in dict(kw, batch=1).items()
+                            if k in oracle.Config.__dataclass_fields__})
+    flush("oracle: one step on the single sequence (float64)")
+    P = {n: v.astype(np.float64) for n, v in P0.items()}
+    loss, og, Po, _, cache = oracle.train_step(ocfg, P, {}, xh[:1], yh[:1])
+    flush(f"gpu loss {gl:.6f} oracle {loss:.6f}")
+    assert abs(gl - loss) / abs(loss) < 2e-2
+
+    for l, a in enumerate(acts):
+        a = a.reshape(B, S, d)
+        assert rel(a[0], cache["acts"][l].reshape(S, d)) < 2e-2, ("act", l)
+        assert rel(a[1], a[0]) < 1e-6, ("identical sequences differ", l)
+    z = logits.reshape(B, S, V)
+    assert rel(z[0], cache["logits"].reshape(S, V)) < 2e-2
+    del logits, z
+
+    lr = kw["lr"]
+    for n, g in G.items():
+        e = rel(g, og[n])
+        assert e < 3e-2, ("grad", n, e)
+        p = P1[n]
+        if n.endswith(".b"):  # zero-started: within two step sizes of the oracle
+            assert np.max(np.abs(p - Po[n])) <= 2 * lr * 1.001, ("bias", n)
+        else:
+            assert rel(p, Po[n]) < 1e-2, ("param", n)
+
+
+FULL = [("gpt2s", {}), ("gptj", {}), ("vith", {}), ("gpt2m", {}), ("gpt2m", {"frozen_layers": 12})]
+
+
+@pytest.mark.parametrize("name,over", FULL, ids=[f"{n}{'_k12' if o else ''}" for n, o in FULL])
+def test_full_depth_loss_at_init_and_one_step(name, over):
+    from paper_2309_01226_amd.configs import preset
+    from paper_2309_01226_amd.model import Model, device_batch
+
+    kw = preset(name, **over)
+    l0 = _golden_l0()[name]
+    flush(f"full-depth {name} {over}: expected loss at init {l0:.4f}")
+    _release()
+    m = Model(kw)
+    x, y = device_batch(kw, seed=0, step=0)
+    e0 = m.eval_loss(x, y)
+    t0 = m.train_step(x, y)
+    e1 = m.eval_loss(x, y)
+    flush(f"eval {e0:.6f} train {t0:.6f} after one step {e1:.6f}")
+    m.close()
+    del m, x, y
+    _release()
+    assert np.isfinite([e0, t0, e1]).all()
+    assert abs(e0 - l0) / l0 < 3e-2
+    assert abs(t0 - e0) / e0 < 1e-5
+    assert e1 < e0
