@@ -66,12 +66,14 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x
   }
 }
 
-// Wide rows (d >= 1024): one workgroup per row, each thread holding NCH float4
-// chunks (columns (c * 256 + tid) * 4 .. +3), the two row sums combined
-// across the four waves through LDS in a fixed order.  With one wave per row
-// every wave of the grid fits on the chip at once, so all rows load together
-// and then all store together; with a workgroup per row the grid runs in
-// more than one round and one round's stores overlap the next one's loads.
+// Wide rows (d >= 1024): each workgroup walks the rows blockIdx.x,
+// blockIdx.x + gridDim.x, ..., each thread holding NCH float4 chunks of a row
+// (columns (c * 256 + tid) * 4 .. +3); the two row sums are combined across
+// the four waves through LDS in a fixed order.  The next row's loads are
+// issued before the current row is reduced and stored, so every workgroup
+// keeps reads in flight while it writes (a grid of one workgroup per row
+// gets the same overlap only between dispatch rounds).  The gain and shift
+// chunks are loaded once per workgroup.
 template <int NCH>
 __global__ __launch_bounds__(256) void ln_fwd_wg_kernel(const float* __restrict__ x, long ldx,
                                                         long row_stride,
@@ -79,56 +81,73 @@ __global__ __launch_bounds__(256) void ln_fwd_wg_kernel(const float* __restrict_
                                                         const float* __restrict__ b,
                                                         bf16* __restrict__ y, long ldy,
                                                         float* __restrict__ mean,
-                                                        float* __restrict__ rstd, int d,
+                                                        float* __restrict__ rstd, int rows, int d,
                                                         float eps) {
   __shared__ float red[2][4];
-  const int row = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const float* xr = x + (long)row * row_stride * ldx;
-  float4 v[NCH];
-  float s = 0.f;
+  float4 v[NCH], vn[NCH], gg[NCH], bb[NCH];
+  int row = blockIdx.x;
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
     const int col = (c * 256 + tid) * 4;
-    if (col < d) v[c] = *reinterpret_cast<const float4*>(xr + col);
-    else v[c] = make_float4(0.f, 0.f, 0.f, 0.f);
-    s += v[c].x + v[c].y + v[c].z + v[c].w;
+    const float* xr = x + (long)row * row_stride * ldx;
+    v[c] = col < d ? *reinterpret_cast<const float4*>(xr + col) : make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  s = wave_sum(s);
-  if (lane == 0) red[0][wave] = s;
-  __syncthreads();
-  const float mu = (red[0][0] + red[0][1] + red[0][2] + red[0][3]) / d;
-  float q = 0.f;
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
     const int col = (c * 256 + tid) * 4;
-    if (col < d) {
-      const float a0 = v[c].x - mu, a1 = v[c].y - mu, a2 = v[c].z - mu, a3 = v[c].w - mu;
-      q += a0 * a0 + a1 * a1 + a2 * a2 + a3 * a3;
+    gg[c] = col < d ? *reinterpret_cast<const float4*>(g + col) : make_float4(0.f, 0.f, 0.f, 0.f);
+    bb[c] = col < d ? *reinterpret_cast<const float4*>(b + col) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  for (; row < rows; row += gridDim.x) {
+    const int nrow = row + (int)gridDim.x;
+    if (nrow < rows) {
+      const float* xn = x + (long)nrow * row_stride * ldx;
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        const int col = (c * 256 + tid) * 4;
+        vn[c] = col < d ? *reinterpret_cast<const float4*>(xn + col) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
     }
-  }
-  q = wave_sum(q);
-  if (lane == 0) red[1][wave] = q;
-  __syncthreads();
-  const float rs = rsqrtf((red[1][0] + red[1][1] + red[1][2] + red[1][3]) / d + eps);
-  bf16* yr = y + (long)row * ldy;
+    float s = 0.f;
 #pragma unroll
-  for (int c = 0; c < NCH; ++c) {
-    const int col = (c * 256 + tid) * 4;
-    if (col < d) {
-      const float4 gg = *reinterpret_cast<const float4*>(g + col);
-      const float4 bb = *reinterpret_cast<const float4*>(b + col);
-      bf16x4 o;
-      o[0] = f2bf((v[c].x - mu) * rs * gg.x + bb.x);
-      o[1] = f2bf((v[c].y - mu) * rs * gg.y + bb.y);
-      o[2] = f2bf((v[c].z - mu) * rs * gg.z + bb.z);
-      o[3] = f2bf((v[c].w - mu) * rs * gg.w + bb.w);
-      *reinterpret_cast<bf16x4*>(yr + col) = o;
+    for (int c = 0; c < NCH; ++c) s += v[c].x + v[c].y + v[c].z + v[c].w;
+    s = wave_sum(s);
+    if (lane == 0) red[0][wave] = s;
+    __syncthreads();
+    const float mu = (red[0][0] + red[0][1] + red[0][2] + red[0][3]) / d;
+    float q = 0.f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int col = (c * 256 + tid) * 4;
+      if (col < d) {
+        const float a0 = v[c].x - mu, a1 = v[c].y - mu, a2 = v[c].z - mu, a3 = v[c].w - mu;
+        q += a0 * a0 + a1 * a1 + a2 * a2 + a3 * a3;
+      }
     }
-  }
-  if (tid == 0) {
-    mean[row] = mu;
-    rstd[row] = rs;
+    q = wave_sum(q);
+    if (lane == 0) red[1][wave] = q;
+    __syncthreads();
+    const float rs = rsqrtf((red[1][0] + red[1][1] + red[1][2] + red[1][3]) / d + eps);
+    bf16* yr = y + (long)row * ldy;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int col = (c * 256 + tid) * 4;
+      if (col < d) {
+        bf16x4 o;
+        o[0] = f2bf((v[c].x - mu) * rs * gg[c].x + bb[c].x);
+        o[1] = f2bf((v[c].y - mu) * rs * gg[c].y + bb[c].y);
+        o[2] = f2bf((v[c].z - mu) * rs * gg[c].z + bb[c].z);
+        o[3] = f2bf((v[c].w - mu) * rs * gg[c].w + bb[c].w);
+        *reinterpret_cast<bf16x4*>(yr + col) = o;
+      }
+    }
+    if (tid == 0) {
+      mean[row] = mu;
+      rstd[row] = rs;
+    }
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) v[c] = vn[c];
   }
 }
 
@@ -339,8 +358,10 @@ template <int NCH>
 hipError_t ln_fwd_wg_launch(const float* x, long ldx, long rs, const float* g, const float* b,
                             bf16* y, long ldy, float* mean, float* rstd, int rows, int d, float eps,
                             hipStream_t s) {
-  hipLaunchKernelGGL(ln_fwd_wg_kernel<NCH>, dim3(rows), dim3(256), 0, s, x, ldx, rs, g, b, y, ldy,
-                     mean, rstd, d, eps);
+  // enough workgroups for 8 per CU on 256 CUs; each walks rows / grid rows
+  const int grid = rows < 2048 ? rows : 2048;
+  hipLaunchKernelGGL(ln_fwd_wg_kernel<NCH>, dim3(grid), dim3(256), 0, s, x, ldx, rs, g, b, y, ldy,
+                     mean, rstd, rows, d, eps);
   return hipGetLastError();
 }
 
