@@ -123,3 +123,14 @@ def test_op_argument_checks_make_no_launch():
     assert L.sat_op_attention_fwd(C.c_void_p(16), C.c_void_p(16), C.c_void_p(16), 8, 8, 8,
                                   C.c_void_p(16), 8, C.c_void_p(16), 1, 1, 4, 48, 1,
                                   C.c_float(1.0), None) == -1  # head dim 48 unsupported
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    """Without the built library every entry point raises: no CPU fallback."""
+    from paper_2309_01226_amd import _lib as L
+    monkeypatch.setattr(L, "LIB_PATH", str(tmp_path / "libsaturn.so"))
+    monkeypatch.setattr(L, "_lib", None)
+    with pytest.raises(ImportError):
+        L.lib()
+    with pytest.raises(ImportError):
+        L.call("sat_model_destroy", None)
