@@ -1,13 +1,17 @@
 """Whole-step checks at the full sizes of the workloads, in the launch
 configuration the benchmark times.
 
-  * One full-width GPT-J block (d 4096, 16 heads of 256 with rotary on 64,
-    parallel attention + MLP, MLP 16384, vocabulary 50400) trained one step on
-    2 x 2048 tokens: every GEMM, attention and bandwidth kernel runs with the
-    grids and tile counts of the 28-layer step, and the AdamW update of the
-    large matrices runs in the weight-gradient epilogue.  The two sequences of
-    the batch are identical, so the mean loss and every gradient equal those
-    of the one sequence, which the float64 oracle computes at half the cost.
+  * One or two full-width blocks of each workload at its full batch and
+    sequence length, trained one step: GPT-J (d 4096, 16 heads of 256 with
+    rotary on 64, parallel attention + MLP, MLP 16384, vocabulary 50400,
+    2 x 2048 tokens), GPT-2-small (8 x 1024 tokens), ViT-H/14 (64 images of
+    257 tokens, 80-wide heads) and a GPT-2-medium grid member (8 x 512 tokens)
+    with its bottom block frozen.  Every GEMM, attention and bandwidth kernel
+    runs with the grids, tile counts and split-K choices of the full-depth
+    step, and the AdamW update of the large matrices runs in the
+    weight-gradient epilogue.  All samples of the batch are one repeated
+    sample, so the mean loss and every gradient equal that sample's, which
+    the float64 oracle computes at a fraction of the cost.
     Tolerances are the end-to-end ones: loss, activations and logits 2e-2,
     gradients 3e-2 (relative Frobenius), parameters after the step 1e-2.
   * Every full-depth workload (GPT-2-small, GPT-J, ViT-H/14, a GPT-2-medium
@@ -47,18 +51,23 @@ def _release():
     torch.cuda.empty_cache()
 
 
-def test_gptj_full_width_block_step():
+WIDTH = [("gptj", dict(n_layers=1)), ("gpt2s", dict(n_layers=1)), ("vith", dict(n_layers=1)),
+         ("gpt2m", dict(n_layers=2, frozen_layers=1))]
+
+
+@pytest.mark.parametrize("name,over", WIDTH, ids=[n for n, _ in WIDTH])
+def test_full_width_block_step(name, over):
     from paper_2309_01226_amd.configs import preset
     from paper_2309_01226_amd.inputs import batch_for
     from paper_2309_01226_amd.model import Model
 
-    kw = preset("gptj", n_layers=1)
-    B, S, d, V = kw["batch"], kw["seq_len"], kw["d_model"], kw["vocab"]
+    kw = preset(name, **over)
+    B, d = kw["batch"], kw["d_model"]
     xh, yh = batch_for(kw, seed=0, step=0)
     xh, yh = np.array(xh), np.array(yh)
     xh[1:] = xh[0]
     yh[1:] = yh[0]
-    flush(f"full-width GPT-J block: B {B} S {S} d {d} V {V}, fused AdamW with kept gradients")
+    flush(f"full-width {name} {over}: batch {B} of one repeated sample, fused AdamW, kept gradients")
     m = Model(kw)
     m.set_option("keep_grads", 1)
     P0 = m.params()
@@ -73,22 +82,27 @@ def test_gptj_full_width_block_step():
 
     ocfg = oracle.Config(**{k: v for k, v in dict(kw, batch=1).items()
                             if k in oracle.Config.__dataclass_fields__})
-    flush("oracle: one step on the single sequence (float64)")
+    train = oracle.trainable_mask(ocfg)
+    flush("oracle: one step on the single sample (float64)")
     P = {n: v.astype(np.float64) for n, v in P0.items()}
     loss, og, Po, _, cache = oracle.train_step(ocfg, P, {}, xh[:1], yh[:1])
     flush(f"gpu loss {gl:.6f} oracle {loss:.6f}")
     assert abs(gl - loss) / abs(loss) < 2e-2
 
     for l, a in enumerate(acts):
-        a = a.reshape(B, S, d)
-        assert rel(a[0], cache["acts"][l].reshape(S, d)) < 2e-2, ("act", l)
-        assert rel(a[1], a[0]) < 1e-6, ("identical sequences differ", l)
-    z = logits.reshape(B, S, V)
-    assert rel(z[0], cache["logits"].reshape(S, V)) < 2e-2
+        a = a.reshape(B, -1)
+        assert rel(a[0], cache["acts"][l].reshape(-1)) < 2e-2, ("act", l)
+        assert rel(a[1], a[0]) < 1e-6, ("identical samples differ", l)
+    z = logits.reshape(B, -1)
+    assert rel(z[0], cache["logits"].reshape(-1)) < 2e-2
     del logits, z
 
     lr = kw["lr"]
     for n, g in G.items():
+        if not train[n]:
+            assert not g.any(), ("frozen grad written", n)
+            assert np.array_equal(P1[n], P0[n]), ("frozen param changed", n)
+            continue
         e = rel(g, og[n])
         assert e < 3e-2, ("grad", n, e)
         p = P1[n]
