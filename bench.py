@@ -13,20 +13,29 @@ pass); the diagnostics report the optimizer's share of the step and the
 bandwidth of the separate pass over all parameters.
 
 Reported beside the throughput:
-  roofline      the dominant kernel (the fused QKV + fc1 forward GEMM,
-                4096 x 28672 x 4096) timed with HIP events on the model's
-                stream around each of its launches inside the timed region;
-                achieved = algorithmic FLOPs per launch / mean launch time.
+  roofline      the dominant kernel by time: the weight-gradient product of
+                the fused QKV + fc1 weight (28672 x 4096 x 4096 tokens), whose
+                epilogue also applies that weight's AdamW step (28 B per
+                weight element: read p, m, v; write p, m, v, the bf16 copy and
+                its transpose).  Timed with HIP events on the model's stream
+                around each of its launches inside the timed region; achieved
+                = algorithmic FLOPs per launch / mean launch time, against the
+                dense bf16 MFMA peak, and beside it the fraction of the serial
+                bound (FLOPs at MFMA peak plus the update's bytes at HBM peak).
                 traffic = HBM bytes per launch from rocprofv3 FETCH_SIZE /
                 WRITE_SIZE counters scaled by the same counters of a 1 GiB
                 device copy (bench.py --copy-calibration), read from
                 profiles/ when they were taken on the current GEMM source
-                (else null).
+                (else null).  roofline_qkv_fwd: the same for the fused QKV +
+                fc1 forward product (timed in a diagnostic step).
+  step_ms       median, p10 and p90 of the timed steps (HIP events between
+                consecutive steps on the model's stream).
   cpu_baseline  the float64 oracle timed on this host on a bounded sample
-                (one GPT-J-shaped block plus embedding and head, one sequence
-                of 2048 tokens; AdamW over that block's tensors), scaled to the
+                (two GPT-J-shaped blocks plus embedding and head, one sequence
+                of 2048 tokens; AdamW over one block's tensors), scaled to the
                 full step by algorithmic FLOPs (forward + backward) and by
-                parameter count (AdamW).
+                parameter count (AdamW), with the CPU model, the BLAS library
+                and its thread count.
 """
 
 import argparse
@@ -91,18 +100,41 @@ def n_params(kw):
     return sum(int(__import__("numpy").prod(s)) for _, s, _ in oracle.param_spec(cfg))
 
 
+def _cpu_info():
+    """CPU model name (from /proc/cpuinfo) and the BLAS library numpy uses."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    blas, threads = "unknown", os.cpu_count()
+    try:
+        from threadpoolctl import threadpool_info
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if info:
+            blas = ", ".join(f"{i.get('internal_api')} {i.get('version')} ({os.path.basename(i.get('filepath', ''))})"
+                             for i in info)
+            threads = max(i.get("num_threads", 1) for i in info)
+    except Exception:
+        pass
+    return model, blas, threads
+
+
 def cpu_baseline(kw, seed):
-    """Oracle fwd+bwd and AdamW on a bounded sample of the same workload."""
+    """Oracle fwd+bwd and AdamW on a bounded sample of the same workload: two
+    blocks of the real per-layer shapes, one row of the batch (ViT: four
+    images), the full embedding and head; the full step's time is
+    extrapolated by FLOPs and parameter count."""
     import numpy as np
 
     import oracle
     from paper_2309_01226_amd.inputs import batch_for
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = os.cpu_count()
-    sample = dict(kw, n_layers=1, frozen_layers=0)
+    cpu_model, blas, threads = _cpu_info()
+    L_s = min(2, kw["n_layers"])
+    sample = dict(kw, n_layers=L_s, frozen_layers=0)
     if kw["arch"] == "vit":
         sample["batch"] = 4
     else:
@@ -117,7 +149,7 @@ def cpu_baseline(kw, seed):
     G = oracle.backward(cfg, P, cache)
     t_fb = time.perf_counter() - t0
     del cache
-    # AdamW timed on the block's tensors only (bounded work), scaled by count
+    # AdamW timed on the first block's tensors only (bounded work), scaled by count
     t0 = time.perf_counter()
     p_s = 0
     for n in G:
@@ -140,12 +172,18 @@ def cpu_baseline(kw, seed):
         "unit": "tokens/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": (f"float64 numpy oracle, one block of the same shapes with batch {sample['batch']} x "
+        "sample": (f"float64 numpy oracle, {L_s} blocks of the same shapes with batch {sample['batch']} x "
                    f"{srows // sample['batch']} tokens ({srows} tokens) plus the full embedding/head: "
-                   f"fwd+bwd {t_fb:.2f} s scaled by FLOPs x{f_full / f_s:.1f}; AdamW over the block's "
+                   f"fwd+bwd {t_fb:.2f} s scaled by FLOPs x{f_full / f_s:.1f} (extrapolated to "
+                   f"{kw['n_layers']} blocks and the full batch); AdamW over one block's "
                    f"{p_s / 1e6:.0f} M params {t_opt:.2f} s scaled by params x{p_full / p_s:.1f}; "
                    f"estimated full step {est:.1f} s"),
         "sample_seconds": round(t_fb + t_opt, 2),
+        "extrapolated": True,
+        "cpu_model": cpu_model,
+        "blas": blas,
+        "blas_threads": threads,
+        "host_cpus": os.cpu_count(),
     }
 
 
@@ -162,11 +200,11 @@ PAPER_CONTEXT = {
 }
 
 
-def bandwidth_summary(diag, sep_ms, sep_bytes):
+def bandwidth_summary(diag, sep_ms, sep_bytes, n_trainable):
     """Achieved HBM GB/s of the bandwidth-bound kernels inside one step
     (algorithmic bytes over the HIP-event durations of their launches), with
     the fraction of the 8 TB/s peak.  The separate AdamW pass is the one over
-    all parameters (fusion off).  LayerNorm tensors of one call (25-300 MB)
+    all parameters (fusion off), at 30 B per parameter.  LayerNorm tensors of one call (25-300 MB)
     may partly hit the 256 MB Infinity Cache, as they do in the step."""
     out = {}
     for name in ("ln_fwd", "ln_bwd", "xent"):
@@ -176,15 +214,21 @@ def bandwidth_summary(diag, sep_ms, sep_bytes):
             out[name] = {"launches": n, "us_per_launch": ms / n * 1e3, "bytes_per_launch": nbytes / n,
                          "gbs": gbs, "frac_hbm": gbs / PEAK_HBM_GBS}
     if sep_ms:
-        gbs = sep_bytes / (sep_ms * 1e-3) / 1e9
-        out["adamw_all_params"] = {"ms": sep_ms, "bytes": sep_bytes, "gbs": gbs, "frac_hbm": gbs / PEAK_HBM_GBS}
+        # 30 B per trainable parameter: read p, g, m, v (16 B); write p, m, v
+        # and the bf16 shadow (14 B).  The pass also writes the transposed bf16
+        # copy of each weight matrix (2 B per element), counted in bytes_moved.
+        b30 = 30.0 * n_trainable
+        gbs = b30 / (sep_ms * 1e-3) / 1e9
+        out["adamw_all_params"] = {"ms": sep_ms, "bytes_30_per_param": b30, "gbs": gbs,
+                                   "frac_hbm": gbs / PEAK_HBM_GBS, "bytes_moved": sep_bytes,
+                                   "gbs_moved": sep_bytes / (sep_ms * 1e-3) / 1e9}
     return out
 
 
-def traffic_from_profiles():
-    """HBM bytes per launch of the dominant GEMM from the committed counter
-    summary, if it was taken on the current GEMM source (else None)."""
-    path = os.path.join(ROOT, "profiles", "gemm_qkv_fc1_fwd_gptj_traffic.txt")
+def traffic_from_profiles(name):
+    """HBM bytes per launch of a GEMM from the committed counter summary
+    profiles/<name>, if it was taken on the current GEMM source (else None)."""
+    path = os.path.join(ROOT, "profiles", name)
     src = os.path.join(ROOT, "paper_2309_01226_amd", "csrc", "gemm256.hip")
     try:
         rec = {}
@@ -366,15 +410,19 @@ def main():
     for t in range(W):
         m.train_step(*batches[t], sync=False)
     torch.cuda.synchronize()
-    per_step = kw["n_layers"]
-    m.set_timing(TIMING["qkv_fwd_gemm"], per_step * K + 8)
+    per_step = kw["n_layers"] - kw.get("frozen_layers", 0)
+    m.set_timing(TIMING["qkv_wgrad_gemm"], per_step * K + 8)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    ev[0].record(m.stream)
     for t in range(K):
         m.train_step(*batches[W + t], sync=False)
+        ev[t + 1].record(m.stream)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
-    q_ms, q_n, q_fl = m.timing_read()
+    w_ms, w_n, w_fl = m.timing_read()
+    step_ms = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(K))
 
     # diagnostics outside the timed region: one step per kernel class, as
     # timed (AdamW of the eligible weights fused into their weight-gradient
@@ -382,7 +430,7 @@ def main():
     # over all parameters is the optimizer's bandwidth kernel, and the GEMM
     # time without the fused epilogues gives the optimizer's share of the step
     diag = {}
-    for name in ("adamw", "all_gemm", "attn_fwd", "attn_bwd", "ln_fwd", "ln_bwd", "xent"):
+    for name in ("qkv_fwd_gemm", "adamw", "all_gemm", "attn_fwd", "attn_bwd", "ln_fwd", "ln_bwd", "xent"):
         m.set_timing(TIMING[name], 4096)
         m.train_step(*batches[0], sync=False)
         diag[name] = m.timing_read()
@@ -411,6 +459,10 @@ def main():
         "steps": K,
         "warmup": W,
         "ms_per_step": ms_step,
+        "step_ms": {"median": step_ms[len(step_ms) // 2] if K % 2 else
+                    0.5 * (step_ms[K // 2 - 1] + step_ms[K // 2]),
+                    "p10": step_ms[int(0.1 * (K - 1))], "p90": step_ms[int(round(0.9 * (K - 1)))],
+                    "min": step_ms[0], "max": step_ms[-1]},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -441,18 +493,42 @@ def main():
         "attention": {"fwd_ms": diag["attn_fwd"][0], "bwd_ms": diag["attn_bwd"][0],
                       "fwd_tflops": diag["attn_fwd"][2] / max(diag["attn_fwd"][0], 1e-9) / 1e9,
                       "bwd_tflops": diag["attn_bwd"][2] / max(diag["attn_bwd"][0], 1e-9) / 1e9},
-        "bandwidth_kernels": bandwidth_summary(diag, sep_ms, sep_bytes),
+        "bandwidth_kernels": bandwidth_summary(diag, sep_ms, sep_bytes, n_train),
         "loss_after": loss,
         "paper_context": PAPER_CONTEXT,
     }
+    ncols = 3 * kw["d_model"] + kw["d_mlp"] if kw["arch"] == "gptj" else 3 * kw["d_model"]
+    if w_n:
+        fused = not args.separate_adamw
+        achieved = w_fl / w_n / (w_ms / w_n * 1e-3) / 1e12
+        opt_bytes = 28.0 * ncols * kw["d_model"] if fused else 0.0
+        serial_us = (w_fl / w_n / (PEAK_BF16_TFLOPS * 1e12) + opt_bytes / (PEAK_HBM_GBS * 1e9)) * 1e6
+        out["roofline"] = {
+            "kernel": (f"gemm256_kernel<4, 0> (AdamW epilogue): weight gradient of the fused QKV + fc1 weight "
+                       f"({ncols} x {kw['d_model']} x {m.rows()} tokens) with that weight's AdamW step"
+                       if fused else
+                       f"gemm256_kernel<0, 0>: weight gradient of the fused QKV + fc1 weight "
+                       f"({ncols} x {kw['d_model']} x {m.rows()} tokens)"),
+            "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS,
+            "traffic": traffic_from_profiles("gemm_qkv_wgrad_adamw_gptj_traffic.txt") if fused else None,
+            "launches": w_n, "avg_ms": w_ms / w_n, "flop_per_launch": w_fl / w_n,
+            "optimizer_bytes_per_launch": opt_bytes,
+            "optimizer_bytes_per_element": 28 if fused else 0,
+            "serial_bound_us": serial_us,
+            "frac_of_serial_bound": serial_us / (w_ms / w_n * 1e3),
+            "note": "dominant kernel by time per step; serial bound = FLOPs at the MFMA peak plus the "
+                    "fused AdamW bytes at the 8 TB/s HBM peak",
+        }
+    q_ms, q_n, q_fl = diag["qkv_fwd_gemm"]
     if q_n:
         achieved = q_fl / q_n / (q_ms / q_n * 1e-3) / 1e12
-        out["roofline"] = {
+        out["roofline_qkv_fwd"] = {
             "kernel": "gemm256_kernel<2, 0> (bf16 epilogue, GELU on the fc1 columns): fused QKV + fc1 forward "
-                      f"({m.rows()} x {3 * kw['d_model'] + kw['d_mlp'] if kw['arch'] == 'gptj' else 3 * kw['d_model']}"
-                      f" x {kw['d_model']})",
+                      f"({m.rows()} x {ncols} x {kw['d_model']})",
             "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic_from_profiles(),
+            "frac": achieved / PEAK_BF16_TFLOPS,
+            "traffic": traffic_from_profiles("gemm_qkv_fc1_fwd_gptj_traffic.txt"),
             "launches": q_n, "avg_ms": q_ms / q_n, "flop_per_launch": q_fl / q_n,
         }
     if not args.no_cpu_baseline:

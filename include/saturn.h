@@ -33,7 +33,9 @@ typedef struct sat_model sat_model; /* opaque, owned by the library */
 typedef enum {
   SAT_OK = 0,
   SAT_EINVAL = -1,      /* invalid configuration or argument */
-  SAT_ENOMEM = -2,      /* the arena is too small (or device allocation failed) */
+  SAT_ENOMEM = -2,      /* the arena is too small (or device allocation failed); the analogue of
+                           a parallelism's search reporting an out-of-memory plan as a null
+                           result (Sec. 3.1, Parallelism Library, the search function) */
   SAT_EHIP = -3,        /* a HIP runtime call failed */
   SAT_ESTATE = -4,      /* the model is in a failed state */
   SAT_ENONFINITE = -5,  /* the loss read back is NaN or infinite */
@@ -76,11 +78,17 @@ typedef struct {
 } sat_config;
 
 /* Bytes of device memory a model of this configuration needs (parameters,
- * bf16 shadow, gradients, AdamW moments, activations, workspace).
+ * bf16 shadow, gradients, AdamW moments, activations, workspace).  This is the
+ * memory side of a parallelism's search for one task on one GPU (Sec. 3.1,
+ * Parallelism Library): a caller learns before creation whether the task fits.
  * Errors: SAT_EINVAL for an invalid configuration. */
 sat_status sat_model_arena_bytes(const sat_config* cfg, size_t* bytes);
 
-/* Create a model on the current HIP device.
+/* Create a model on the current HIP device: the model-initialisation half of a
+ * Task, with its hyper-parameters taken from cfg (Sec. 3.1, Trainer API: a
+ * task is a model-initialisation function, a data-loading function and its
+ * hyper-parameters).  Data loading stays with the caller, who passes device
+ * batches to sat_train_step.
  *   arena: device pointer of at least arena_bytes bytes, borrowed until
  *          sat_model_destroy; NULL makes the library allocate (and own) it.
  *   hip_stream: hipStream_t every kernel of this model is enqueued on (NULL =
@@ -93,7 +101,11 @@ sat_status sat_model_create(const sat_config* cfg, void* arena, size_t arena_byt
                             void* hip_stream, sat_model** out);
 
 /* One fine-tuning step: forward, backward down to block k, AdamW on the
- * trainable tensors (t += 1), all enqueued on the model's stream.
+ * trainable tensors (t += 1), all enqueued on the model's stream.  One SGD
+ * iteration of a task, the unit a parallelism's execute function repeats to
+ * train the task (Sec. 3.1, Parallelism Library) and the unit the Trial
+ * Runner times (Sec. 3.2, Profiler); which layers train is the layer-wise
+ * fine-tuning choice of model selection (Abstract; Sec. 2, Model selection).
  *   inputs: device pointer; decoders int32 tokens [batch, seq_len] in
  *           [0, vocab); VIT fp32 images [batch, channels, img, img].
  *   labels: device pointer, int32; decoders [batch, seq_len], VIT [batch];
@@ -108,12 +120,18 @@ sat_status sat_train_step(sat_model* m, const void* inputs, const int32_t* label
                           float* loss_out);
 
 /* Forward only; writes the mean loss to the host pointer loss_out (waits for
- * the stream).  Changes no parameter or optimizer state. */
+ * the stream).  Changes no parameter or optimizer state.  The loss by which
+ * model selection compares the trained configurations (Sec. 2, Model
+ * selection: training and comparing model configurations).
+ * Arguments as for sat_train_step; loss_out must not be NULL.
+ * Errors: SAT_EINVAL (null model or pointers), SAT_ESTATE, SAT_EHIP,
+ * SAT_ENONFINITE. */
 sat_status sat_eval_loss(sat_model* m, const void* inputs, const int32_t* labels,
                          float* loss_out);
 
 /* Release the model (and the arena when the library allocated it).  Waits for
- * the model's stream.  NULL is accepted. */
+ * the model's stream.  NULL is accepted.  Ends a task's use of its GPU memory,
+ * which the schedule then gives to the next task (Sec. 3.3, Joint Optimizer and Executor). */
 sat_status sat_model_destroy(sat_model* m);
 
 /* ---- parameter table and test / resume accessors --------------------------
@@ -165,14 +183,19 @@ sat_status sat_model_set_option(sat_model* m, int32_t option, int32_t value);
  * product (GPT-J: the fused QKV + fc1 product), 2 every GEMM, 3 the AdamW
  * update, 4 attention forward, 5 attention backward, 6 LayerNorm forward,
  * 7 LayerNorm backward (the row kernel, not the gain / shift column sums),
- * 8 softmax cross-entropy.  Waits for the stream. */
+ * 8 softmax cross-entropy, 9 the weight-gradient product of the QKV weight
+ * (GPT-J: of the fused QKV + fc1 weight; with SAT_OPT_FUSED_ADAMW, the product
+ * whose epilogue applies that weight's AdamW step; its work is counted as the
+ * product's FLOPs).  Waits for the stream. */
 sat_status sat_model_set_timing(sat_model* m, int32_t kind, int32_t max_launches);
 /* Sum of the timed launches' durations (ms), their count and their
  * algorithmic work (FLOPs; bytes for AdamW, LayerNorm and cross-entropy),
  * then resets the counters. */
 sat_status sat_model_timing_read(sat_model* m, double* total_ms, int64_t* launches, double* work);
 
-/* ---- profiling (the Trial Runner's runtime estimate, Sec. 3.2) ------------
+/* ---- profiling (the Trial Runner's runtime estimate, Sec. 3.2, Profiler:
+ * epoch times extrapolated from the mean of a few minibatches, which holds
+ * because every SGD step of a task does the same work) --------------------
  * Creates a model of cfg on the calling thread's current device (arena and a
  * synthetic batch of the task's shape allocated and freed by the call), runs
  * `warmup` untimed and `steps` timed train steps on hip_stream (borrowed; NULL
@@ -199,6 +222,16 @@ typedef struct {
 } sat_profile_result;
 sat_status sat_profile(const sat_config* cfg, void* hip_stream, int32_t warmup, int32_t steps,
                        int64_t samples_per_epoch, sat_profile_result* out);
+/* The synthetic batch sat_profile trains on, written into caller device
+ * buffers on hip_stream (no wait): decoders int32 tokens [batch, seq_len] and
+ * labels [batch, seq_len], where row b is a stream of seq_len + 1 hashed
+ * tokens in [0, vocab), inputs its first seq_len and labels its last seq_len
+ * (labels[b, s] = inputs[b, s + 1] for s < seq_len - 1); VIT fp32 images
+ * [batch, channels, img, img] uniform in [-1, 1) and int32 labels [batch] in
+ * [0, vocab).  The Trial Runner's minibatches are the task's own data
+ * (Sec. 3.2, Profiler); here they stand in for it with the task's shape.
+ * Errors: SAT_EINVAL (configuration, null pointers), SAT_EHIP. */
+sat_status sat_profile_batch(const sat_config* cfg, void* inputs, int32_t* labels, void* hip_stream);
 
 const char* sat_last_error(void);
 

@@ -88,6 +88,7 @@ SIGNATURES = {
     "sat_model_set_timing": (C.c_int, [_VP, _I32, _I32]),
     "sat_model_set_option": (C.c_int, [_VP, _I32, _I32]),
     "sat_profile": (C.c_int, [C.POINTER(sat_config), _VP, _I32, _I32, _I64, C.POINTER(sat_profile_result)]),
+    "sat_profile_batch": (C.c_int, [C.POINTER(sat_config), _VP, _VP, _VP]),
     "sat_model_timing_read": (C.c_int, [_VP, C.POINTER(C.c_double), C.POINTER(C.c_int64), C.POINTER(C.c_double)]),
     "sat_op_gemm": (C.c_int, [C.POINTER(sat_gemm_desc), _VP]),
     "sat_op_layernorm_fwd": (C.c_int, [_VP, _I64, _I64, _VP, _VP, _VP, _I64, _VP, _VP, _I32, _I32, _F32, _VP]),

@@ -315,7 +315,7 @@ extern "C" sat_status sat_model_stats(const sat_model* m, int64_t* n_params, int
 extern "C" sat_status sat_model_set_timing(sat_model* m, int32_t kind, int32_t max_launches) {
   sat_status st = check_model(m);
   if (st != SAT_OK) return st;
-  SAT_CHECK_ARG(kind >= 0 && kind <= 8, "unknown timing kind %d", kind);
+  SAT_CHECK_ARG(kind >= 0 && kind <= 9, "unknown timing kind %d", kind);
   SAT_CHECK_ARG(max_launches >= 0 && max_launches <= (1 << 20), "bad max_launches");
   st = sync(m);
   if (st != SAT_OK) return st;

@@ -32,6 +32,28 @@ struct Events {
 
 }  // namespace
 
+extern "C" sat_status sat_profile_batch(const sat_config* cfg, void* inputs, int32_t* labels,
+                                        void* hip_stream) {
+  SAT_CHECK_ARG(cfg != nullptr && inputs != nullptr && labels != nullptr,
+                "null configuration or buffer");
+  sat_status st = sat_validate_config(cfg);
+  if (st != SAT_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+  const uint32_t seed = (uint32_t)(cfg->seed ^ (cfg->seed >> 32)) ^ 0x51ED270Bu;
+  hipError_t e;
+  if (cfg->arch == SAT_VIT) {
+    const long n_in = (long)cfg->batch * cfg->channels * cfg->img_size * cfg->img_size;
+    e = launch_synth_images((float*)inputs, n_in, labels, cfg->batch, cfg->vocab, seed, s);
+  } else {
+    e = launch_synth_tokens((int32_t*)inputs, labels, cfg->batch, cfg->seq_len, cfg->vocab, seed, s);
+  }
+  if (e != hipSuccess) {
+    sat_set_error("synthetic batch: %s", hipGetErrorString(e));
+    return SAT_EHIP;
+  }
+  return SAT_OK;
+}
+
 extern "C" sat_status sat_profile(const sat_config* cfg, void* hip_stream, int32_t warmup,
                                   int32_t steps, int64_t samples_per_epoch,
                                   sat_profile_result* out) {
@@ -72,14 +94,8 @@ extern "C" sat_status sat_profile(const sat_config* cfg, void* hip_stream, int32
     sat_set_error("hipMalloc of the profiling batch failed: %s", hipGetErrorString(e));
     return fail(SAT_ENOMEM);
   }
-  const uint32_t seed = (uint32_t)(cfg->seed ^ (cfg->seed >> 32)) ^ 0x51ED270Bu;
-  e = vit ? launch_synth_images((float*)in.p, n_in, (int32_t*)lab.p, cfg->batch, cfg->vocab, seed, s)
-          : launch_synth_tokens((int32_t*)in.p, (int32_t*)lab.p, cfg->batch, cfg->seq_len, cfg->vocab,
-                                seed, s);
-  if (e != hipSuccess) {
-    sat_set_error("synthetic batch: %s", hipGetErrorString(e));
-    return fail(SAT_EHIP);
-  }
+  st = sat_profile_batch(cfg, in.p, (int32_t*)lab.p, hip_stream);
+  if (st != SAT_OK) return fail(st);
   for (int i = 0; i < warmup; ++i) {
     st = sat_train_step(m, in.p, (const int32_t*)lab.p, nullptr);
     if (st != SAT_OK) return fail(st);

@@ -14,7 +14,7 @@ namespace {
 
 enum {
   TK_OFF = 0, TK_QKV_FWD = 1, TK_ALL_GEMM = 2, TK_ADAMW = 3, TK_ATTN_FWD = 4, TK_ATTN_BWD = 5,
-  TK_LN_FWD = 6, TK_LN_BWD = 7, TK_XENT = 8
+  TK_LN_FWD = 6, TK_LN_BWD = 7, TK_XENT = 8, TK_QKV_WGRAD = 9
 };
 
 // Algorithmic bytes of the bandwidth kernels (each operand read once, each
@@ -35,7 +35,8 @@ struct Timed {
   Timed(sat_model* m, int kind, double work) : M(m) {
     if (m->timing_kind == TK_OFF) return;
     bool match = (m->timing_kind == kind) ||
-                 (m->timing_kind == TK_ALL_GEMM && (kind == TK_QKV_FWD || kind == TK_ALL_GEMM));
+                 (m->timing_kind == TK_ALL_GEMM &&
+                  (kind == TK_QKV_FWD || kind == TK_ALL_GEMM || kind == TK_QKV_WGRAD));
     if (!match || m->timing_used >= m->timing.size()) return;
     rec = &m->timing[m->timing_used++];
     rec->flops = work;
@@ -288,7 +289,8 @@ sat_status sat_run_forward(sat_model* M, const void* inputs, const int32_t* labe
 // product's epilogue applies the step to the weight (and writes the gradient
 // only if the model keeps gradients).
 static sat_status wgrad(sat_model* M, bool trans, bool y_ready, const bf16* Y, long ldy,
-                        int ycols, const bf16* X, long ldx, int Mr, int N, int T, int pidx) {
+                        int ycols, const bf16* X, long ldx, int Mr, int N, int T, int pidx,
+                        int tk = TK_ALL_GEMM) {
   const ParamDesc& P = M->params[pidx];
   float* out = grad(M, pidx);
   const long ldo = P.cols;
@@ -310,12 +312,12 @@ static sat_status wgrad(sat_model* M, bool trans, bool y_ready, const bf16* Y, l
                       P.name.c_str());
         return SAT_EINVAL;
       }
-      return gemm(M, w, LAY_K, LAY_K, EPI_ADAMW);
+      return gemm(M, w, LAY_K, LAY_K, EPI_ADAMW, tk);
     }
-    return gemm(M, w, LAY_K, LAY_K, EPI_F32);
+    return gemm(M, w, LAY_K, LAY_K, EPI_F32, tk);
   }
   GemmArgs w = gargs(Y, ldy, X, ldx, Mr, N, T, out, ldo);
-  return gemm(M, w, LAY_MN, LAY_MN, EPI_F32);
+  return gemm(M, w, LAY_MN, LAY_MN, EPI_F32, tk);
 }
 
 // LayerNorm backward into the residual gradient dh, which it also rounds into
@@ -427,7 +429,8 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
       GemmArgs ga = gargs(M->dqkv, D.qkv_ld, shadow_t(M, pb + J_QKVW), D.qkv_ld, T, d, D.qkv_ld,
                           M->dA, d);
       TRY(gemm(M, ga, LAY_K, LAY_K, EPI_F32));
-      TRY(wgrad(M, tr, false, M->dqkv, D.qkv_ld, D.qkv_ld, A.a, d, D.qkv_ld, d, T, pb + J_QKVW));
+      TRY(wgrad(M, tr, false, M->dqkv, D.qkv_ld, D.qkv_ld, A.a, d, D.qkv_ld, d, T, pb + J_QKVW,
+                TK_QKV_WGRAD));
       SAT_HIP(launch_colsum_bf16(M->dqkv + 3 * d, D.qkv_ld, T, m, M->part, npT,
                                  grad(M, pb + J_FC1B), s));
       TRY(ln_bwd(M, M->dA, M->h_in[l], 1, pb + J_LN1G, A.mean1, A.rstd1, T));
@@ -455,7 +458,8 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
       }
       GemmArgs ga = gargs(M->dqkv, 3 * d, shadow_t(M, pb + B_QKVW), 3 * d, T, d, 3 * d, M->dA, d);
       TRY(gemm(M, ga, LAY_K, LAY_K, EPI_F32));
-      TRY(wgrad(M, tr, false, M->dqkv, 3 * d, 3 * d, A.a, d, 3 * d, d, T, pb + B_QKVW));
+      TRY(wgrad(M, tr, false, M->dqkv, 3 * d, 3 * d, A.a, d, 3 * d, d, T, pb + B_QKVW,
+                TK_QKV_WGRAD));
       SAT_HIP(launch_colsum_bf16(M->dqkv, 3 * d, T, 3 * d, M->part, npT, grad(M, pb + B_QKVB), s));
       TRY(ln_bwd(M, M->dA, M->h_in[l], 1, pb + B_LN1G, A.mean1, A.rstd1, T));
     }

@@ -187,7 +187,7 @@ class Model:
 
 
 TIMING = {"off": 0, "qkv_fwd_gemm": 1, "all_gemm": 2, "adamw": 3, "attn_fwd": 4, "attn_bwd": 5,
-          "ln_fwd": 6, "ln_bwd": 7, "xent": 8}
+          "ln_fwd": 6, "ln_bwd": 7, "xent": 8, "qkv_wgrad_gemm": 9}
 
 
 def device_batch(cfg_kwargs, seed=0, step=0, rows=None, device="cuda"):

@@ -9,6 +9,7 @@ logic:
 
   profile(kw)              sat_profile: mean step time of a task (and its epoch
                            time extrapolated from it), measured by the library
+  profile_batch(kw)        the synthetic batch sat_profile trains on
   measure_slowdown(kw, L)  step time of one task when L copies of it run at
                            once on L streams, relative to running alone
   lpt_lanes(costs, L)      longest-processing-time-first list scheduling of
@@ -40,6 +41,26 @@ def profile(cfg_kwargs, warmup=2, steps=5, samples_per_epoch=0, stream=None):
     _lib.call("sat_profile", C.byref(cfg), C.c_void_p(st.cuda_stream), int(warmup), int(steps),
               int(samples_per_epoch), C.byref(r))
     return {k: getattr(r, k) for k, _ in r._fields_ if k != "struct_size"}
+
+
+def profile_batch(cfg_kwargs, stream=None):
+    """The synthetic batch sat_profile trains on (sat_profile_batch), as
+    device tensors (inputs, labels)."""
+    import torch
+    cfg = make_config(**cfg_kwargs)
+    B = cfg_kwargs["batch"]
+    if cfg_kwargs["arch"] == "vit":
+        c, i = cfg_kwargs.get("channels", 3), cfg_kwargs["img_size"]
+        x = torch.empty(B, c, i, i, device="cuda", dtype=torch.float32)
+        y = torch.empty(B, device="cuda", dtype=torch.int32)
+    else:
+        x = torch.empty(B, cfg_kwargs["seq_len"], device="cuda", dtype=torch.int32)
+        y = torch.empty_like(x)
+    st = stream if stream is not None else torch.cuda.current_stream()
+    _lib.call("sat_profile_batch", C.byref(cfg), C.c_void_p(x.data_ptr()), C.c_void_p(y.data_ptr()),
+              C.c_void_p(st.cuda_stream))
+    st.synchronize()
+    return x, y
 
 
 def measure_slowdown(cfg_kwargs, n_lanes, steps=5, warmup=2, seed=0):

@@ -4,6 +4,8 @@ on the same values, so a checkpointed model must train bitwise like one that
 kept every block's activations: equal losses, gradients, parameters and
 optimizer state after every step, for each architecture and with frozen
 layers; and its arena must be smaller by all but one block's activation set.
+The checkpointed step is also held against the float64 oracle directly, with
+the same three-step parity run as the step tests.
 """
 
 import numpy as np
@@ -52,3 +54,16 @@ def test_checkpoint_bitwise(name):
     assert ck < full or sets == 1
     a.close()
     b.close()
+
+
+ORACLE_CASES = ["tiny_gpt2", "small_gptj", "small_vit", "small_gptj_k1"]
+
+
+@pytest.mark.parametrize("name", ORACLE_CASES)
+def test_checkpoint_oracle_parity(name):
+    """With checkpointing on, the three-step parity run against the float64
+    oracle (loss, activations, logits, gradients, exact AdamW, parameters,
+    frozen tensors) holds as it does without it."""
+    from tests.test_gpu_step import CASES as STEP_CASES, run_parity
+    flush(f"checkpointed step parity case {name}")
+    run_parity(dict(STEP_CASES[name], checkpoint=1))

@@ -13,7 +13,9 @@ configuration the benchmark times.
     sample, so the mean loss and every gradient equal that sample's, which
     the float64 oracle computes at a fraction of the cost.
     Tolerances are the end-to-end ones: loss, activations and logits 2e-2,
-    gradients 3e-2 (relative Frobenius), parameters after the step 1e-2.
+    gradients 3e-2 (relative Frobenius), parameters after the step 1e-2;
+    zero-started tensors (biases, LN shifts) by the sign of their update
+    wherever the oracle's first moment is above 5 % of its RMS.
   * Every full-depth workload (GPT-2-small, GPT-J, ViT-H/14, a GPT-2-medium
     grid member with and without its frozen prefix): the loss at
     initialisation matches the closed form ln V + 2e-4 d for 0.02-std weights
@@ -85,7 +87,7 @@ def test_full_width_block_step(name, over):
     train = oracle.trainable_mask(ocfg)
     flush("oracle: one step on the single sample (float64)")
     P = {n: v.astype(np.float64) for n, v in P0.items()}
-    loss, og, Po, _, cache = oracle.train_step(ocfg, P, {}, xh[:1], yh[:1])
+    loss, og, Po, ostate, cache = oracle.train_step(ocfg, P, {}, xh[:1], yh[:1])
     flush(f"gpu loss {gl:.6f} oracle {loss:.6f}")
     assert abs(gl - loss) / abs(loss) < 2e-2
 
@@ -106,7 +108,21 @@ def test_full_width_block_step(name, over):
         e = rel(g, og[n])
         assert e < 3e-2, ("grad", n, e)
         p = P1[n]
-        if n.endswith(".b"):  # zero-started: within two step sizes of the oracle
+        if n.endswith(".b"):
+            # zero-started: one AdamW step moves every entry by about lr * sign(g),
+            # so check the update's sign wherever the oracle's first moment is not
+            # small (bf16 noise may flip entries whose gradient is near zero), and
+            # the size everywhere
+            keep = np.ones(p.shape, bool)
+            if n.endswith("attn.qkv.b"):   # the key part's true gradient is exactly zero
+                keep[d:2 * d] = False
+            om = ostate["m"][n]
+            big = keep & (np.abs(om) > 0.05 * np.sqrt(np.mean(om[keep] ** 2)))
+            assert big.any(), n
+            du_g = (p - P0[n])[big]
+            du_o = (Po[n] - P[n])[big]
+            flips = int(np.sum(np.sign(du_g) != np.sign(du_o)))
+            assert flips == 0, ("update sign", n, flips, int(big.sum()))
             assert np.max(np.abs(p - Po[n])) <= 2 * lr * 1.001, ("bias", n)
         else:
             assert rel(p, Po[n]) < 1e-2, ("param", n)

@@ -127,3 +127,119 @@ def test_grid_streams_bitwise_equal_serial_runs():
         for n in alone[1]:
             assert np.array_equal(alone[1][n], conc[i][1][n]), ("grad", i, n)
             assert np.array_equal(alone[2][n], conc[i][2][n]), ("param", i, n)
+
+
+# ---------------------------------------------------------------- member width
+
+def _release():
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def test_grid_member_width_concurrent_match_oracle():
+    """The eight grid members at their real width (GPT-2-medium shape: d 1024,
+    16 heads, MLP 4096, vocabulary 50257, 512 tokens per row; two blocks each),
+    with the grid's learning rates and batch sizes and the bottom block frozen
+    where (lr index + batch index) is odd, all enqueued together on eight
+    streams for one step.  Every row of every batch is one repeated sample, so
+    each member's loss and gradients equal that sample's, which the float64
+    oracle computes once; each member's update is the oracle's AdamW at its own
+    learning rate (and frozen prefix).  Two members are also run alone on the
+    default stream and must match their concurrent run bitwise."""
+    from paper_2309_01226_amd.configs import GRID_BATCHES, GRID_LRS, preset
+    from paper_2309_01226_amd.inputs import decoder_batch
+    from paper_2309_01226_amd.model import Model
+
+    kws = []
+    for i, lr in enumerate(GRID_LRS):
+        for j, b in enumerate(GRID_BATCHES):
+            kws.append(preset("gpt2m", n_layers=2, lr=lr, batch=b, frozen_layers=1 if (i + j) % 2 else 0))
+    flush("grid member width: 8 members on 8 streams",
+          [(k["lr"], k["batch"], k["frozen_layers"]) for k in kws])
+    x, y = decoder_batch(max(GRID_BATCHES), 512, 50257, seed=11, step=0)
+    x, y = np.array(x), np.array(y)
+    x[1:] = x[0]
+    y[1:] = y[0]
+
+    def run(members, streams):
+        models = [Model(kw, stream=s) for kw, s in zip(members, streams)]
+        for m in models:
+            m.set_option("keep_grads", 1)
+        P0 = models[0].params()
+        data = []
+        for kw, s in zip(members, streams):
+            with torch.cuda.stream(s):
+                data.append((torch.as_tensor(x[:kw["batch"]]).cuda(), torch.as_tensor(y[:kw["batch"]]).cuda()))
+        torch.cuda.synchronize()
+        for m, (xd, yd) in zip(models, data):
+            m.train_step(xd, yd, sync=False)
+        torch.cuda.synchronize()
+        out = []
+        for m, (xd, yd) in zip(models, data):
+            out.append(dict(loss=m.eval_loss(xd, yd), acts=[m.activation(l) for l in range(3)],
+                            grads=m.grads(), params=m.params()))
+            m.close()
+        del models, data
+        _release()
+        return P0, out
+
+    P0, res = run(kws, [torch.cuda.Stream() for _ in kws])
+
+    base = kws[0]
+    ocfg = oracle.Config(**{k: v for k, v in dict(base, batch=1, frozen_layers=0).items()
+                            if k in oracle.Config.__dataclass_fields__})
+    P = {n: v.astype(np.float64) for n, v in P0.items()}
+    flush("oracle: forward and backward of the single sample (float64)")
+    loss0, cache = oracle.forward(ocfg, P, x[:1], y[:1])
+    og = oracle.backward(ocfg, P, cache)
+    for kw, r in zip(kws, res):
+        k = kw["frozen_layers"]
+        mcfg = oracle.Config(**{kk: v for kk, v in dict(kw, batch=1).items()
+                                if kk in oracle.Config.__dataclass_fields__})
+        train = oracle.trainable_mask(mcfg)
+        # the oracle's step at this member's learning rate, from the shared start
+        Po = {}
+        mo = {}
+        for n in P:
+            if train[n]:
+                Po[n], mo[n], _ = oracle.adamw_update(mcfg, P[n], og[n], np.zeros_like(P[n]),
+                                                      np.zeros_like(P[n]), 1)
+        ol, _ = oracle.forward(mcfg, {n: Po.get(n, P[n]) for n in P}, x[:1], y[:1])
+        flush(f"member lr={kw['lr']} b={kw['batch']} k={k}: loss after step gpu {r['loss']:.6f} "
+              f"oracle {ol:.6f}")
+        assert abs(r["loss"] - ol) / ol < 2e-2
+        for l, a in enumerate(r["acts"]):
+            a = a.reshape(kw["batch"], -1)
+            assert rel(a[-1], a[0]) < 1e-6, ("identical samples differ", l)
+        num = den = 0.0
+        for n, g in r["grads"].items():
+            p = r["params"][n]
+            if not train[n]:
+                assert not g.any(), ("frozen grad written", n)
+                assert np.array_equal(p, P0[n]), ("frozen param changed", n)
+                continue
+            assert rel(g, og[n]) < 3e-2, ("grad", n, rel(g, og[n]))
+            num += float(np.sum((p - Po[n]) ** 2))
+            den += float(np.sum(Po[n] ** 2))
+            if n.endswith(".b"):
+                keep = np.ones(p.shape, bool)
+                if n.endswith("attn.qkv.b"):
+                    keep[1024:2048] = False
+                om = mo[n]
+                big = keep & (np.abs(om) > 0.05 * np.sqrt(np.mean(om[keep] ** 2)))
+                du_g = (p - P0[n])[big]
+                du_o = (Po[n] - P[n])[big]
+                assert np.array_equal(np.sign(du_g), np.sign(du_o)), ("update sign", n)
+                assert np.max(np.abs(p - Po[n])) <= 2 * kw["lr"] * 1.001, ("bias", n)
+            else:
+                assert rel(p, Po[n]) < 1e-2, ("param", n, rel(p, Po[n]))
+        assert np.sqrt(num / den) < 1e-2
+    # the same step for two members alone on the default stream: bitwise equal
+    for i in (0, 1):
+        flush(f"member {i} alone on the default stream")
+        _, alone = run([kws[i]], [torch.cuda.current_stream()])
+        a, c = alone[0], res[i]
+        assert a["loss"] == c["loss"], i
+        for n in a["grads"]:
+            assert np.array_equal(a["grads"][n], c["grads"][n]), ("grad", i, n)
+            assert np.array_equal(a["params"][n], c["params"][n]), ("param", i, n)

@@ -20,8 +20,13 @@ def ops():
 
 # ------------------------------------------------------------------ LayerNorm
 
+# The wide-row forward runs at most 2048 workgroups that walk rows with a
+# stride of the grid and load the next row before storing the current one:
+# 4096 and 16448 rows (GPT-J, ViT-H/14 per step), 5000 and 2049 rows (not a
+# multiple of 2048: the last rows of the walk belong to some workgroups only).
 @pytest.mark.parametrize("rows,d", [(1, 64), (37, 768), (300, 1280), (64, 4096), (5, 16),
-                                    (9, 1028)])
+                                    (9, 1028), (4096, 4096), (16448, 1280), (5000, 1280),
+                                    (2049, 4096)])
 def test_layernorm_fwd_bwd(rows, d):
     flush(f"layernorm rows={rows} d={d}")
     rng = np.random.default_rng(rows + d)
@@ -65,12 +70,13 @@ def test_layernorm_fwd_widest():
     assert rel(host(mean), rmean) < 1e-5 and rel(host(rstd), rrstd) < 1e-5
 
 
-@pytest.mark.parametrize("d", [128, 1280])
-def test_layernorm_strided_rows(d):
+@pytest.mark.parametrize("d,B,S", [(128, 7, 5), (1280, 7, 5), (1280, 64, 257), (4096, 3000, 2)])
+def test_layernorm_strided_rows(d, B, S):
     """Rows picked with a stride (the ViT head normalises only the CLS rows);
-    widths below and above 1024 take the one-wave and one-workgroup row kernels."""
-    rng = np.random.default_rng(3)
-    B, S = 7, 5
+    widths below and above 1024 take the one-wave and one-workgroup row
+    kernels; 3000 strided rows of 4096 run the multi-row walk of the latter."""
+    flush(f"layernorm strided rows d={d} rows={B} stride={S}")
+    rng = np.random.default_rng(3 + B)
     x = rng.normal(size=(B * S, d)).astype(np.float32)
     g = np.ones(d, np.float32)
     b = np.zeros(d, np.float32)
