@@ -60,6 +60,21 @@ typedef struct {
 } sat_gemm_desc;
 sat_status sat_op_gemm(const sat_gemm_desc* d, void* stream);
 
+/* sat_op_gemm for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops and harnesses that forbid hipMalloc.
+ * Same descriptor and result as sat_op_gemm given a workspace large enough
+ * for the product's split-K plan, except that d->splitk_ws must be NULL and
+ * d->splitk_ws_elems 0: the split-K partials go to a scratch array of
+ * SAT_GEMM_NOALLOC_WS_ELEMS fp32 elements (32 MiB) that the library holds on
+ * every device it runs on until the process ends.  The call allocates
+ * nothing.  A product whose split-K partials would exceed the scratch is
+ * rejected with SAT_EINVAL before any launch.  All calls on one device share
+ * that device's scratch: calls whose products split K and that may overlap
+ * (different streams, or different host threads) race and must be ordered
+ * by the caller. */
+#define SAT_GEMM_NOALLOC_WS_ELEMS (8L * 1024 * 1024)
+sat_status sat_op_gemm_noalloc(const sat_gemm_desc* d, void* stream);
+
 /* LayerNorm forward over `rows` rows of length d: x fp32 (row r at
  * x + r*row_stride*ldx), y bf16 [rows, ldy], mean / rstd fp32 [rows]. */
 sat_status sat_op_layernorm_fwd(const float* x, int64_t ldx, int64_t row_stride, const float* g,

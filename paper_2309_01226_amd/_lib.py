@@ -17,6 +17,7 @@ STATUS_NAMES = {0: "SAT_OK", -1: "SAT_EINVAL", -2: "SAT_ENOMEM", -3: "SAT_EHIP",
                 -5: "SAT_ENONFINITE", -6: "SAT_ENOTSUP"}
 ARCH = {"gpt2": 0, "gptj": 1, "vit": 2}
 OPTIONS = {"fused_adamw": 1, "keep_grads": 2}
+GEMM_NOALLOC_WS_ELEMS = 8 * 1024 * 1024   # SAT_GEMM_NOALLOC_WS_ELEMS in saturn_ops.h
 
 
 class SatError(RuntimeError):
@@ -91,6 +92,7 @@ SIGNATURES = {
     "sat_profile_batch": (C.c_int, [C.POINTER(sat_config), _VP, _VP, _VP]),
     "sat_model_timing_read": (C.c_int, [_VP, C.POINTER(C.c_double), C.POINTER(C.c_int64), C.POINTER(C.c_double)]),
     "sat_op_gemm": (C.c_int, [C.POINTER(sat_gemm_desc), _VP]),
+    "sat_op_gemm_noalloc": (C.c_int, [C.POINTER(sat_gemm_desc), _VP]),
     "sat_op_layernorm_fwd": (C.c_int, [_VP, _I64, _I64, _VP, _VP, _VP, _I64, _VP, _VP, _I32, _I32, _F32, _VP]),
     "sat_op_layernorm_bwd": (C.c_int, [_VP, _I64, _VP, _I64, _I64, _VP, _VP, _VP, _VP, _I64, _VP, _VP, _VP,
                                        _I32, _I32, _VP]),

@@ -2,6 +2,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 
 #include "../../include/saturn_ops.h"
@@ -23,23 +24,26 @@ extern "C" const char* sat_last_error(void) { return g_last_error.c_str(); }
 
 static inline hipStream_t S(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
-extern "C" sat_status sat_op_gemm(const sat_gemm_desc* d, void* stream) {
-  SAT_CHECK_ARG(d != nullptr, "sat_op_gemm: null descriptor");
-  SAT_CHECK_ARG(d->A && d->B && d->out, "sat_op_gemm: null operand");
-  SAT_CHECK_ARG(d->M >= 0 && d->N >= 0 && d->K > 0, "sat_op_gemm: bad sizes M=%d N=%d K=%d",
-                d->M, d->N, d->K);
-  SAT_CHECK_ARG(d->a_layout == 0 || d->a_layout == 1, "sat_op_gemm: bad a_layout");
-  SAT_CHECK_ARG(d->b_layout == 0 || d->b_layout == 1, "sat_op_gemm: bad b_layout");
-  SAT_CHECK_ARG(d->epilogue >= 0 && d->epilogue <= 3, "sat_op_gemm: bad epilogue");
-  SAT_CHECK_ARG(d->lda >= (d->a_layout == 0 ? d->K : d->M), "sat_op_gemm: lda too small");
-  SAT_CHECK_ARG(d->ldb >= (d->b_layout == 0 ? d->K : d->N), "sat_op_gemm: ldb too small");
-  SAT_CHECK_ARG(d->ldo >= d->N, "sat_op_gemm: ldo too small");
-  SAT_CHECK_ARG(d->epilogue != 1 || (d->resid && d->ldr >= d->N), "sat_op_gemm: resid");
-  SAT_CHECK_ARG(d->epilogue != 3 || (d->aux && d->ldaux >= d->N), "sat_op_gemm: aux");
+// Checks a descriptor and fills the launch arguments (everything but the
+// split-K workspace).
+static sat_status gemm_args(const sat_gemm_desc* d, GemmArgs* out, const char* fn) {
+  SAT_CHECK_ARG(d != nullptr, "%s: null descriptor", fn);
+  SAT_CHECK_ARG(d->A && d->B && d->out, "%s: null operand", fn);
+  SAT_CHECK_ARG(d->M >= 0 && d->N >= 0 && d->K > 0, "%s: bad sizes M=%d N=%d K=%d", fn, d->M,
+                d->N, d->K);
+  SAT_CHECK_ARG(d->a_layout == 0 || d->a_layout == 1, "%s: bad a_layout", fn);
+  SAT_CHECK_ARG(d->b_layout == 0 || d->b_layout == 1, "%s: bad b_layout", fn);
+  SAT_CHECK_ARG(d->epilogue >= 0 && d->epilogue <= 3, "%s: bad epilogue", fn);
+  SAT_CHECK_ARG(d->lda >= (d->a_layout == 0 ? d->K : d->M), "%s: lda too small", fn);
+  SAT_CHECK_ARG(d->ldb >= (d->b_layout == 0 ? d->K : d->N), "%s: ldb too small", fn);
+  SAT_CHECK_ARG(d->ldo >= d->N, "%s: ldo too small", fn);
+  SAT_CHECK_ARG(d->epilogue != 1 || (d->resid && d->ldr >= d->N), "%s: resid", fn);
+  SAT_CHECK_ARG(d->epilogue != 3 || (d->aux && d->ldaux >= d->N), "%s: aux", fn);
   SAT_CHECK_ARG(d->epilogue != 2 || d->out2 == nullptr ||
                     (d->gelu_col0 >= 0 && d->ldo2 >= d->N - d->gelu_col0),
-                "sat_op_gemm: out2");
-  GemmArgs a;
+                "%s: out2", fn);
+  SAT_CHECK_ARG(d->splitk_ws_elems >= 0, "%s: negative splitk_ws_elems", fn);
+  GemmArgs& a = *out;
   memset(&a, 0, sizeof a);
   a.A = (const bf16*)d->A;
   a.B = (const bf16*)d->B;
@@ -51,9 +55,72 @@ extern "C" sat_status sat_op_gemm(const sat_gemm_desc* d, void* stream) {
   a.out2 = (bf16*)d->out2; a.ldo2 = d->ldo2; a.gelu_col0 = d->gelu_col0;
   a.aux = (const bf16*)d->aux; a.ldaux = d->ldaux;
   a.gelu_erf = d->gelu_erf;
-  SAT_CHECK_ARG(d->splitk_ws_elems >= 0, "sat_op_gemm: negative splitk_ws_elems");
+  return SAT_OK;
+}
+
+extern "C" sat_status sat_op_gemm(const sat_gemm_desc* d, void* stream) {
+  GemmArgs a;
+  sat_status st = gemm_args(d, &a, "sat_op_gemm");
+  if (st != SAT_OK) return st;
   a.splitk_ws = d->splitk_ws;
   a.splitk_ws_elems = d->splitk_ws ? d->splitk_ws_elems : 0;
+  SAT_HIP(launch_gemm(a, d->a_layout, d->b_layout, d->epilogue, S(stream)));
+  return SAT_OK;
+}
+
+// ---- sat_op_gemm_noalloc: the split-K workspace in a file-scope device array
+//
+// `scratch` is a host-side stand-in for the array in host code: its device
+// address on the current device comes from hipGetSymbolAddress, looked up
+// once per device on the first call there and kept in g_scratch_dev.  Every
+// split-K slice writes all M x N of its partials before the reduction reads
+// them, so the array needs no clearing between calls.
+static __device__ __align__(256) float scratch[SAT_GEMM_NOALLOC_WS_ELEMS];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_dev[kMaxDevices];
+}  // namespace
+
+static sat_status scratch_on_current_device(float** out) {
+  int dev = -1;
+  SAT_HIP(hipGetDevice(&dev));
+  SAT_CHECK_ARG(dev >= 0 && dev < kMaxDevices, "sat_op_gemm_noalloc: device %d beyond %d", dev,
+                kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_dev[dev] == nullptr) {
+    void* p = nullptr;
+    SAT_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    SAT_CHECK_ARG(p != nullptr && ((uintptr_t)p & 255) == 0,
+                  "sat_op_gemm_noalloc: bad scratch address on device %d", dev);
+    g_scratch_dev[dev] = static_cast<float*>(p);
+  }
+  *out = g_scratch_dev[dev];
+  return SAT_OK;
+}
+
+extern "C" sat_status sat_op_gemm_noalloc(const sat_gemm_desc* d, void* stream) {
+  GemmArgs a;
+  sat_status st = gemm_args(d, &a, "sat_op_gemm_noalloc");
+  if (st != SAT_OK) return st;
+  SAT_CHECK_ARG(d->splitk_ws == nullptr && d->splitk_ws_elems == 0,
+                "sat_op_gemm_noalloc: splitk_ws must be NULL (the library's own scratch is used)");
+  // the same split-K plan sat_op_gemm takes with a large enough workspace
+  const bool may_split = (d->epilogue == 0 || d->epilogue == 1) && d->a_layout == 0 &&
+                         d->b_layout == 0;
+  const long need = may_split ? gemm_splitk_ws_elems(d->M, d->N, d->K) : 0;
+  SAT_CHECK_ARG(need <= SAT_GEMM_NOALLOC_WS_ELEMS,
+                "sat_op_gemm_noalloc: M=%d N=%d K=%d runs split-K with %ld fp32 partials, beyond "
+                "the %ld-element scratch; use sat_op_gemm with a workspace",
+                d->M, d->N, d->K, need, (long)SAT_GEMM_NOALLOC_WS_ELEMS);
+  if (need > 0) {
+    float* ws = nullptr;
+    st = scratch_on_current_device(&ws);
+    if (st != SAT_OK) return st;
+    a.splitk_ws = ws;
+    a.splitk_ws_elems = need;
+  }
   SAT_HIP(launch_gemm(a, d->a_layout, d->b_layout, d->epilogue, S(stream)));
   return SAT_OK;
 }

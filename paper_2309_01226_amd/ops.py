@@ -30,11 +30,8 @@ def _need(t, dtype, name):
         raise TypeError(f"{name}: expected a CUDA tensor of {dtype}, got {t.device} {t.dtype}")
 
 
-def gemm(A, B, M, N, K, out, *, lda, ldb, a_layout=LAY_K, b_layout=LAY_K, epilogue=EPI_F32,
-         ldo=None, bias=None, bias_col0=0, resid=None, ldr=None, out2=None, ldo2=0, gelu_col0=0,
-         aux=None, ldaux=0, gelu_erf=0, splitk_ws=None):
-    """C[m, n] = sum_k A(m, k) B(n, k) with the chosen epilogue (see saturn_ops.h);
-    splitk_ws: optional fp32 scratch that lets a small fp32-output product run split-K."""
+def _gemm_desc(A, B, M, N, K, out, lda, ldb, a_layout, b_layout, epilogue, ldo, bias, bias_col0,
+               resid, ldr, out2, ldo2, gelu_col0, aux, ldaux, gelu_erf, splitk_ws):
     _need(A, torch.bfloat16, "A")
     _need(B, torch.bfloat16, "B")
     _need(bias, torch.float32, "bias")
@@ -48,7 +45,7 @@ def gemm(A, B, M, N, K, out, *, lda, ldb, a_layout=LAY_K, b_layout=LAY_K, epilog
     ldo = N if ldo is None else ldo
     if out.numel() < (M - 1) * ldo + N:
         raise ValueError("gemm: out too small")
-    d = _lib.sat_gemm_desc(
+    return _lib.sat_gemm_desc(
         A=A.data_ptr(), B=B.data_ptr(), M=M, N=N, K=K, lda=lda, ldb=ldb,
         a_layout=a_layout, b_layout=b_layout, epilogue=epilogue,
         out=out.data_ptr(), ldo=ldo,
@@ -58,7 +55,27 @@ def gemm(A, B, M, N, K, out, *, lda, ldb, a_layout=LAY_K, b_layout=LAY_K, epilog
         aux=None if aux is None else aux.data_ptr(), ldaux=ldaux, gelu_erf=gelu_erf,
         splitk_ws=None if splitk_ws is None else splitk_ws.data_ptr(),
         splitk_ws_elems=0 if splitk_ws is None else splitk_ws.numel())
+
+
+def gemm(A, B, M, N, K, out, *, lda, ldb, a_layout=LAY_K, b_layout=LAY_K, epilogue=EPI_F32,
+         ldo=None, bias=None, bias_col0=0, resid=None, ldr=None, out2=None, ldo2=0, gelu_col0=0,
+         aux=None, ldaux=0, gelu_erf=0, splitk_ws=None):
+    """C[m, n] = sum_k A(m, k) B(n, k) with the chosen epilogue (see saturn_ops.h);
+    splitk_ws: optional fp32 scratch that lets a small fp32-output product run split-K."""
+    d = _gemm_desc(A, B, M, N, K, out, lda, ldb, a_layout, b_layout, epilogue, ldo, bias, bias_col0,
+                   resid, ldr, out2, ldo2, gelu_col0, aux, ldaux, gelu_erf, splitk_ws)
     _lib.call("sat_op_gemm", C.byref(d), _stream())
+    return out
+
+
+def gemm_noalloc(A, B, M, N, K, out, *, lda, ldb, a_layout=LAY_K, b_layout=LAY_K, epilogue=EPI_F32,
+                 ldo=None, bias=None, bias_col0=0, resid=None, ldr=None, out2=None, ldo2=0,
+                 gelu_col0=0, aux=None, ldaux=0, gelu_erf=0):
+    """The same product through sat_op_gemm_noalloc: split-K partials go to the
+    library's own per-device scratch, and the call allocates nothing."""
+    d = _gemm_desc(A, B, M, N, K, out, lda, ldb, a_layout, b_layout, epilogue, ldo, bias, bias_col0,
+                   resid, ldr, out2, ldo2, gelu_col0, aux, ldaux, gelu_erf, None)
+    _lib.call("sat_op_gemm_noalloc", C.byref(d), _stream())
     return out
 
 
