@@ -42,7 +42,7 @@ typedef enum {
   SAT_ENOTSUP = -6      /* the operation does not apply to this model */
 } sat_status;
 
-typedef enum { SAT_GPT2 = 0, SAT_GPTJ = 1, SAT_VIT = 2 } sat_arch;
+typedef enum { SAT_GPT2 = 0, SAT_GPTJ = 1, SAT_VIT = 2, SAT_RESNET = 3 } sat_arch;
 
 /* Per-task configuration: architecture, depth, width, batch size, learning
  * rate and frozen-layer count of one model (the hyper-parameters a model
@@ -52,7 +52,18 @@ typedef enum { SAT_GPT2 = 0, SAT_GPTJ = 1, SAT_VIT = 2 } sat_arch;
  *   GPTJ: one LN per block feeding attention and MLP in parallel, rotary on the
  *         first rotary_dim dims of every head, no q/k/v/out bias, head bias.
  *   VIT : pre-LN encoder over (img/patch)^2 patches + a CLS token, erf GELU,
- *         bidirectional attention, class head on the CLS row. */
+ *         bidirectional attention, class head on the CLS row.
+ *   RESNET: bottleneck ResNet (the paper's second image model, Table 3):
+ *         7 x 7 / 2 stem convolution, batch norm, ReLU, 3 x 3 / 2 max pool;
+ *         stages of res_blocks[s] bottleneck blocks (1 x 1, 3 x 3 with the
+ *         stage's stride in its first block, 1 x 1 with 4x expansion, batch
+ *         norm after each, projection shortcut in each stage's first block,
+ *         ReLU after the add) with mid width res_width * 2^s; global average
+ *         pool and a linear class head with bias.  Batch norm uses the
+ *         statistics of the current batch (training mode; no running
+ *         statistics), eps = ln_eps.  n_layers = the total block count;
+ *         d_model, n_heads, d_mlp, seq_len, patch and rotary_dim are unused
+ *         (0). */
 typedef struct {
   uint32_t struct_size; /* must equal sizeof(sat_config) */
   int32_t arch;         /* sat_arch */
@@ -75,6 +86,8 @@ typedef struct {
   float init_std;       /* std of the N(0, std^2) initialisation of matrices and tables */
   float ln_eps;
   uint64_t seed;        /* counter-based initialisation seed */
+  int32_t res_blocks[4];/* RESNET: blocks per stage (each >= 1, sum = n_layers); others 0 */
+  int32_t res_width;    /* RESNET: stem width = stage-0 mid width, a multiple of 8 */
 } sat_config;
 
 /* Bytes of device memory a model of this configuration needs (parameters,
@@ -152,8 +165,12 @@ sat_status sat_param_write(sat_model* m, int32_t i, const float* host);
  * never stored. */
 sat_status sat_grad_read(sat_model* m, int32_t i, float* host);
 /* Residual stream entering block `layer` (fp32 [batch * seq, d_model]) after
- * the last forward; layer = n_layers gives the stream entering the final LN. */
+ * the last forward; layer = n_layers gives the stream entering the final LN.
+ * RESNET: the input of block `layer` (fp32 NHWC [batch * H * W, C]); layer =
+ * n_layers gives the last block's output.  sat_activation_shape gives the
+ * [rows, cols] of that tensor. */
 sat_status sat_activation_read(sat_model* m, int32_t layer, float* host);
+sat_status sat_activation_shape(const sat_model* m, int32_t layer, int64_t shape[2]);
 /* Logits of the last forward, fp32 [rows, vocab] (rows = batch * seq, VIT: batch). */
 sat_status sat_logits_read(sat_model* m, float* host);
 sat_status sat_state_read(sat_model* m, int32_t i, float* mom, float* vel, int64_t* t);

@@ -59,6 +59,11 @@ class ResNetConfig:
     weight_decay: float = 0.01
     ln_eps: float = 1e-5
     arch: str = field(default="resnet")
+    # "fp64": every product exact.  "bf16": the operands of every convolution
+    # and head product rounded to bfloat16 first (round to nearest, ties to
+    # even), the products themselves still exact: the arithmetic the GPU path
+    # declares (bf16 operands, wide accumulation), written out.
+    operands: str = "fp64"
 
     @property
     def n_blocks(self):
@@ -119,12 +124,35 @@ def init_params(cfg, rng, std=0.02):
 
 
 # ----------------------------------------------------------------------------
+# Operand precision
+# ----------------------------------------------------------------------------
+
+def bf16_round(x):
+    """Round to the nearest bfloat16 value (ties to even), as float64: the
+    value goes to float32 first, then the low 16 bits of its IEEE pattern are
+    rounded away (add 0x7FFF plus the lowest kept bit, then truncate)."""
+    f = np.ascontiguousarray(np.asarray(x, np.float32))
+    u = f.view(np.uint32).astype(np.uint64)
+    lsb = (u >> 16) & 1
+    r = ((u + 0x7FFF + lsb) >> 16) << 16
+    out = r.astype(np.uint32).view(np.float32).astype(np.float64)
+    return np.where(np.isnan(f), np.nan, out).reshape(np.shape(x))
+
+
+def _rounder(cfg):
+    return bf16_round if getattr(cfg, "operands", "fp64") == "bf16" else (lambda a: a)
+
+
+# ----------------------------------------------------------------------------
 # Layers (NHWC)
 # ----------------------------------------------------------------------------
 
-def conv_fwd(x, w, k, stride, pad):
+def conv_fwd(x, w, k, stride, pad, rnd=None):
     """x [N, H, W, Cin]; w [Cout, k * k * Cin] (as [Cout, k, k, Cin]).
-    out[n, i, j, o] = sum_{a, b, c} xpad[n, i s + a, j s + b, c] w[o, a, b, c]."""
+    out[n, i, j, o] = sum_{a, b, c} xpad[n, i s + a, j s + b, c] w[o, a, b, c].
+    rnd: optional rounding of both operands before the product."""
+    if rnd is not None:
+        x, w = rnd(x), rnd(w)
     N, H, W, C = x.shape
     Cout = w.shape[0]
     w4 = w.reshape(Cout, k, k, C)
@@ -137,12 +165,15 @@ def conv_fwd(x, w, k, stride, pad):
         for b in range(k):
             patch = xp[:, a:a + stride * (Ho - 1) + 1:stride, b:b + stride * (Wo - 1) + 1:stride]
             out += patch @ w4[:, a, b, :].T
-    return out, (x.shape, xp, w4, k, stride, pad)
+    return out, (x.shape, xp, w4, k, stride, pad, rnd)
 
 
 def conv_bwd(dy, cache):
-    """VJP of conv_fwd: returns (dx, dw)."""
-    (N, H, W, C), xp, w4, k, stride, pad = cache
+    """VJP of conv_fwd: returns (dx, dw).  With a rounding the forward used,
+    dy is rounded too (the operands of both backward products)."""
+    (N, H, W, C), xp, w4, k, stride, pad, rnd = cache
+    if rnd is not None:
+        dy = rnd(dy)
     _, Ho, Wo, Cout = dy.shape
     dxp = np.zeros_like(xp)
     dw4 = np.zeros_like(w4)
@@ -218,9 +249,10 @@ def forward(cfg, P, images, labels):
     is the input of block i (NHWC) and cache["acts"][n_blocks] the last block's
     output."""
     eps = cfg.ln_eps
+    rnd = None if getattr(cfg, "operands", "fp64") == "fp64" else _rounder(cfg)
     x = np.transpose(np.asarray(images, np.float64), (0, 2, 3, 1))
     c = {"acts": [], "blocks": []}
-    y, c["stem_conv"] = conv_fwd(x, P["stem.conv.w"], 7, 2, 3)
+    y, c["stem_conv"] = conv_fwd(x, P["stem.conv.w"], 7, 2, 3, rnd)
     y, c["stem_bn"] = bn_fwd(y, P["stem.bn.g"], P["stem.bn.b"], eps)
     c["stem_relu"] = y > 0
     y = np.maximum(y, 0.0)
@@ -229,18 +261,18 @@ def forward(cfg, P, images, labels):
         p = f"b{i}."
         c["acts"].append(y)
         bc = {}
-        h, bc["c1"] = conv_fwd(y, P[p + "conv1.w"], 1, 1, 0)
+        h, bc["c1"] = conv_fwd(y, P[p + "conv1.w"], 1, 1, 0, rnd)
         h, bc["n1"] = bn_fwd(h, P[p + "bn1.g"], P[p + "bn1.b"], eps)
         bc["r1"] = h > 0
         h = np.maximum(h, 0.0)
-        h, bc["c2"] = conv_fwd(h, P[p + "conv2.w"], 3, stride, 1)
+        h, bc["c2"] = conv_fwd(h, P[p + "conv2.w"], 3, stride, 1, rnd)
         h, bc["n2"] = bn_fwd(h, P[p + "bn2.g"], P[p + "bn2.b"], eps)
         bc["r2"] = h > 0
         h = np.maximum(h, 0.0)
-        h, bc["c3"] = conv_fwd(h, P[p + "conv3.w"], 1, 1, 0)
+        h, bc["c3"] = conv_fwd(h, P[p + "conv3.w"], 1, 1, 0, rnd)
         h, bc["n3"] = bn_fwd(h, P[p + "bn3.g"], P[p + "bn3.b"], eps)
         if proj:
-            s, bc["cd"] = conv_fwd(y, P[p + "down.w"], 1, stride, 0)
+            s, bc["cd"] = conv_fwd(y, P[p + "down.w"], 1, stride, 0, rnd)
             s, bc["nd"] = bn_fwd(s, P[p + "down.bn.g"], P[p + "down.bn.b"], eps)
         else:
             s = y
@@ -250,10 +282,11 @@ def forward(cfg, P, images, labels):
         c["blocks"].append(bc)
     c["acts"].append(y)
     N, Hf, Wf, F = y.shape
-    feat = y.reshape(N, Hf * Wf, F).mean(axis=1)
+    R_ = _rounder(cfg)
+    feat = R_(y.reshape(N, Hf * Wf, F).mean(axis=1))
     c["feat_hw"] = (Hf, Wf)
     c["feat"] = feat
-    z = feat @ P["fc.w"].T + P["fc.b"]
+    z = feat @ R_(P["fc.w"]).T + P["fc.b"]
     c["logits"] = z
     loss, dz = L.cross_entropy(z, np.asarray(labels))
     c["dz"] = dz
@@ -264,10 +297,11 @@ def backward(cfg, P, c):
     """Gradients of the trainable tensors (frozen ones are absent)."""
     k = cfg.frozen_layers
     G = {}
-    dz = c["dz"]
+    R_ = _rounder(cfg)
+    dz = R_(c["dz"])
     G["fc.w"] = dz.T @ c["feat"]
     G["fc.b"] = dz.sum(axis=0)
-    dfeat = dz @ P["fc.w"]
+    dfeat = dz @ R_(P["fc.w"])
     Hf, Wf = c["feat_hw"]
     N, F = dfeat.shape
     dy = np.broadcast_to(dfeat[:, None, None, :] / (Hf * Wf), (N, Hf, Wf, F)).copy()

@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(_PKG, "libsaturn.so")
 SAT_OK, SAT_EINVAL, SAT_ENOMEM, SAT_EHIP, SAT_ESTATE, SAT_ENONFINITE, SAT_ENOTSUP = 0, -1, -2, -3, -4, -5, -6
 STATUS_NAMES = {0: "SAT_OK", -1: "SAT_EINVAL", -2: "SAT_ENOMEM", -3: "SAT_EHIP", -4: "SAT_ESTATE",
                 -5: "SAT_ENONFINITE", -6: "SAT_ENOTSUP"}
-ARCH = {"gpt2": 0, "gptj": 1, "vit": 2}
+ARCH = {"gpt2": 0, "gptj": 1, "vit": 2, "resnet": 3}
 OPTIONS = {"fused_adamw": 1, "keep_grads": 2}
 GEMM_NOALLOC_WS_ELEMS = 8 * 1024 * 1024   # SAT_GEMM_NOALLOC_WS_ELEMS in saturn_ops.h
 
@@ -36,7 +36,7 @@ class sat_config(C.Structure):
         ("checkpoint", C.c_int32),
         ("lr", C.c_double), ("beta1", C.c_double), ("beta2", C.c_double), ("eps", C.c_double),
         ("weight_decay", C.c_double), ("init_std", C.c_float), ("ln_eps", C.c_float),
-        ("seed", C.c_uint64),
+        ("seed", C.c_uint64), ("res_blocks", C.c_int32 * 4), ("res_width", C.c_int32),
     ]
 
 
@@ -82,6 +82,7 @@ SIGNATURES = {
     "sat_param_write": (C.c_int, [_VP, _I32, _VP]),
     "sat_grad_read": (C.c_int, [_VP, _I32, _VP]),
     "sat_activation_read": (C.c_int, [_VP, _I32, _VP]),
+    "sat_activation_shape": (C.c_int, [_VP, _I32, C.POINTER(C.c_int64)]),
     "sat_logits_read": (C.c_int, [_VP, _VP]),
     "sat_state_read": (C.c_int, [_VP, _I32, _VP, _VP, C.POINTER(C.c_int64)]),
     "sat_state_write": (C.c_int, [_VP, _I32, _VP, _VP, C.c_int64]),

@@ -14,8 +14,8 @@ CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libsaturn.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["gemm.hip", "gemm256.hip", "norm.hip", "elementwise.hip", "attention.hip", "attn256.hip", "attn_small.hip", "ops_abi.cpp", "model.cpp",
-           "step.cpp", "abi.cpp", "profile.cpp"]
+SOURCES = ["gemm.hip", "gemm256.hip", "norm.hip", "elementwise.hip", "attention.hip", "attn256.hip", "attn_small.hip", "conv.hip", "ops_abi.cpp", "model.cpp",
+           "step.cpp", "resnet.cpp", "abi.cpp", "profile.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 COMMON = [

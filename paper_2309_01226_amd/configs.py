@@ -12,6 +12,9 @@ shapes of their public architectures:
          14x14 patches (256 + CLS = 257 tokens), 1000 classes, batch 64
   gpt2m  GPT-2-medium shape (one member of the model-selection grid): 24 layers, d 1024,
          16 heads, MLP 4096, vocab 50257, seq 512; batch, lr and frozen k vary per member
+  resnet the paper's 200 M-parameter ResNet: bottleneck ResNet of ResNet-152 depth
+         (3, 8, 36, 3 blocks) at twice the standard width (stem 128), 224x224x3 images,
+         1000 classes, batch 64, lr 1e-4 (236 M parameters)
 """
 
 PRESETS = {
@@ -25,6 +28,8 @@ PRESETS = {
                  img_size=224, patch=14, channels=3, batch=64, lr=1e-5),
     "gpt2m": dict(arch="gpt2", n_layers=24, d_model=1024, n_heads=16, d_mlp=4096, vocab=50257,
                   seq_len=512, batch=8, lr=1e-5),
+    "resnet": dict(arch="resnet", n_layers=50, res_blocks=(3, 8, 36, 3), res_width=128, vocab=1000,
+                   img_size=224, channels=3, batch=64, lr=1e-4),
 }
 
 # Model-selection grid: lr x batch, each member freezing k in {0, 12}; k = 12

@@ -258,7 +258,15 @@ extern "C" sat_status sat_activation_read(sat_model* m, int32_t layer, float* ho
   if (st != SAT_OK) return st;
   SAT_CHECK_ARG(layer >= 0 && layer <= m->D.L, "layer %d not in [0, n_layers]", layer);
   SAT_CHECK_ARG(host != nullptr, "null host buffer");
-  return copy_d2h(m, host, m->h_in[layer], (size_t)m->D.T * m->D.d * 4);
+  return copy_d2h(m, host, m->h_in[layer], (size_t)m->act_rows[layer] * m->act_cols[layer] * 4);
+}
+
+extern "C" sat_status sat_activation_shape(const sat_model* m, int32_t layer, int64_t shape[2]) {
+  SAT_CHECK_ARG(m != nullptr && shape != nullptr, "null model or shape");
+  SAT_CHECK_ARG(layer >= 0 && layer <= m->D.L, "layer %d not in [0, n_layers]", layer);
+  shape[0] = m->act_rows[layer];
+  shape[1] = m->act_cols[layer];
+  return SAT_OK;
 }
 
 extern "C" sat_status sat_logits_read(sat_model* m, float* host) {

@@ -1,0 +1,588 @@
+// Bandwidth-bound kernels of the bottleneck-ResNet step (the paper's second
+// image workload, Table 3): im2col / col2im around the MFMA GEMMs that carry
+// every convolution, training-mode batch norm (per-channel statistics over the
+// N x H x W rows, forward and backward), ReLU masks, 3 x 3 / stride-2 max
+// pooling, global average pooling and the stride-2 shortcut scatter.
+//
+// Activations are NHWC: a [N, H, W, C] tensor is the row-major matrix
+// [N * H * W, C], the layout the convolution GEMMs read and write.  Every
+// reduction is done in a fixed order (per-workgroup partials, then one pass
+// over the partials), so results are run-to-run deterministic.
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr int NT = 256;
+
+int grid_for(long n, int per_thread = 1) {
+  long b = (n / per_thread + NT - 1) / NT;
+  if (b < 1) b = 1;
+  return (int)(b < 65536 ? b : 65536);
+}
+
+// ---------------------------------------------------------------- im2col
+
+// col[p, (a k + b) C + c] = x[n, i s - pad + a, j s - pad + b, c] (zero
+// outside the image), p = (n Ho + i) Wo + j.  Eight channels per thread
+// (16-byte loads and stores); C % 8 == 0.
+__global__ void im2col8_kernel(const bf16* __restrict__ x, bf16* __restrict__ col, int N, int H,
+                               int W, int C, int k, int s, int pad, int Ho, int Wo, long ldc) {
+  const int C8 = C / 8;
+  const long per_p = (long)k * k * C8;
+  const long total = (long)N * Ho * Wo * per_p;
+  for (long t = (long)blockIdx.x * NT + threadIdx.x; t < total; t += (long)gridDim.x * NT) {
+    const long p = t / per_p;
+    const int r = (int)(t - p * per_p);
+    const int ab = r / C8, c8 = r - ab * C8;
+    const int a = ab / k, b = ab - a * k;
+    const int j = (int)(p % Wo);
+    const long q = p / Wo;
+    const int i = (int)(q % Ho);
+    const int n = (int)(q / Ho);
+    const int hi = i * s - pad + a, wi = j * s - pad + b;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (hi >= 0 && hi < H && wi >= 0 && wi < W)
+      v = *reinterpret_cast<const u32x4*>(x + (((long)n * H + hi) * W + wi) * C + 8 * c8);
+    *reinterpret_cast<u32x4*>(col + p * ldc + (long)ab * C + 8 * c8) = v;
+  }
+}
+
+// The stem: fp32 NCHW images -> bf16 columns, K = k k C (taps ordered a, b,
+// c as above), zero columns K .. ldc - 1.
+__global__ void im2col_nchw_kernel(const float* __restrict__ img, bf16* __restrict__ col, int N,
+                                   int C, int H, int W, int k, int s, int pad, int Ho, int Wo,
+                                   long ldc) {
+  const long total = (long)N * Ho * Wo * ldc;
+  const int K = k * k * C;
+  for (long t = (long)blockIdx.x * NT + threadIdx.x; t < total; t += (long)gridDim.x * NT) {
+    const long p = t / ldc;
+    const int kc = (int)(t - p * ldc);
+    float v = 0.f;
+    if (kc < K) {
+      const int ab = kc / C, c = kc - ab * C;
+      const int a = ab / k, b = ab - a * k;
+      const int j = (int)(p % Wo);
+      const long q = p / Wo;
+      const int i = (int)(q % Ho);
+      const int n = (int)(q / Ho);
+      const int hi = i * s - pad + a, wi = j * s - pad + b;
+      if (hi >= 0 && hi < H && wi >= 0 && wi < W) v = img[(((long)n * C + c) * H + hi) * W + wi];
+    }
+    col[t] = f2bf(v);
+  }
+}
+
+// dx[n, h, w, c] (+)= sum over taps (a, b) with (h + pad - a) / s = i and
+// (w + pad - b) / s = j whole and in range of dcol[(n Ho + i) Wo + j,
+// (a k + b) C + c], taps in increasing (a, b) order.  Four channels per
+// thread; C % 4 == 0.
+__global__ void col2im4_kernel(const float* __restrict__ dcol, long ldc, float* __restrict__ dx,
+                               int N, int H, int W, int C, int k, int s, int pad, int Ho, int Wo,
+                               int accumulate) {
+  const int C4 = C / 4;
+  const long total = (long)N * H * W * C4;
+  for (long t = (long)blockIdx.x * NT + threadIdx.x; t < total; t += (long)gridDim.x * NT) {
+    const int c4 = (int)(t % C4);
+    const long q = t / C4;
+    const int w = (int)(q % W);
+    const long q2 = q / W;
+    const int h = (int)(q2 % H);
+    const int n = (int)(q2 / H);
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int a = 0; a < k; ++a) {
+      const int hh = h + pad - a;
+      if (hh < 0 || hh % s) continue;
+      const int i = hh / s;
+      if (i >= Ho) continue;
+      for (int b = 0; b < k; ++b) {
+        const int ww = w + pad - b;
+        if (ww < 0 || ww % s) continue;
+        const int j = ww / s;
+        if (j >= Wo) continue;
+        acc += *reinterpret_cast<const floatx4*>(dcol + (((long)n * Ho + i) * Wo + j) * ldc +
+                                                 (long)(a * k + b) * C + 4 * c4);
+      }
+    }
+    floatx4* o = reinterpret_cast<floatx4*>(dx + q * C + 4 * c4);
+    if (accumulate) *o += acc;
+    else *o = acc;
+  }
+}
+
+// ---------------------------------------------------------------- batch norm
+
+// Column slab of a [P, C] reduction: thread t of the workgroup owns column
+// c0 + t % CS of the slab and rows phase t / CS, CS = min(C - c0, 256) when
+// 256 % CS == 0 (all phases busy), else one phase.
+struct Slab {
+  int c, phase, phases, cs;
+  __device__ Slab(int C) {
+    const int c0 = blockIdx.y * NT;
+    cs = min(C - c0, NT);
+    phases = (NT % cs == 0) ? NT / cs : 1;
+    const int t = threadIdx.x;
+    phase = t / cs;
+    c = (phase < phases) ? c0 + t % cs : -1;
+  }
+};
+
+// Sum of v over the phases of each column, in phase order; the result is
+// valid in the threads of phase 0.
+__device__ float phase_sum(float v, const Slab& sl, float* red) {
+  red[threadIdx.x] = v;
+  __syncthreads();
+  float s = 0.f;
+  if (sl.phase == 0 && sl.c >= 0)
+    for (int ph = 0; ph < sl.phases; ++ph) s += red[ph * sl.cs + threadIdx.x];
+  __syncthreads();
+  return s;
+}
+
+// Per-channel partial sums of (x - K_c) and (x - K_c)^2 over the rows of
+// workgroup x's block, with the shift K_c = x[0, c] (the shifted-data form of
+// the variance: no cancellation when the mean is large next to the spread).
+__global__ void bn_stats_partial_kernel(const float* __restrict__ x, long P, int C, long rpb,
+                                        float* __restrict__ part) {
+  __shared__ float red[NT];
+  const Slab sl(C);
+  float s1 = 0.f, s2 = 0.f;
+  if (sl.c >= 0) {
+    const float K = x[sl.c];
+    const long r0 = (long)blockIdx.x * rpb;
+    const long r1 = min(P, r0 + rpb);
+    for (long r = r0 + sl.phase; r < r1; r += sl.phases) {
+      const float d = x[r * C + sl.c] - K;
+      s1 += d;
+      s2 += d * d;
+    }
+  }
+  s1 = phase_sum(s1, sl, red);
+  s2 = phase_sum(s2, sl, red);
+  if (sl.phase == 0 && sl.c >= 0) {
+    part[(long)blockIdx.x * C + sl.c] = s1;
+    part[((long)gridDim.x + blockIdx.x) * C + sl.c] = s2;
+  }
+}
+
+__global__ void bn_stats_final_kernel(const float* __restrict__ x, const float* __restrict__ part,
+                                      int nb, long P, int C, float eps, float* __restrict__ mean,
+                                      float* __restrict__ rstd) {
+  const int c = blockIdx.x * NT + threadIdx.x;
+  if (c >= C) return;
+  double s1 = 0.0, s2 = 0.0;
+  for (int b = 0; b < nb; ++b) {
+    s1 += part[(long)b * C + c];
+    s2 += part[((long)nb + b) * C + c];
+  }
+  const double m1 = s1 / (double)P;
+  double var = s2 / (double)P - m1 * m1;
+  if (var < 0.0) var = 0.0;
+  mean[c] = (float)(x[c] + m1);
+  rstd[c] = (float)(1.0 / sqrt(var + (double)eps));
+}
+
+// y = (x - mean) rstd g + b, ReLU when relu, as bf16 (when y) and fp32 (when yf).
+__global__ void bn_apply_kernel(const float* __restrict__ x, long n4, int C,
+                                const float* __restrict__ mean, const float* __restrict__ rstd,
+                                const float* __restrict__ g, const float* __restrict__ b, int relu,
+                                bf16* __restrict__ y, float* __restrict__ yf) {
+  for (long t = (long)blockIdx.x * NT + threadIdx.x; t < n4; t += (long)gridDim.x * NT) {
+    const int c = (int)((4 * t) % C);
+    const floatx4 v = reinterpret_cast<const floatx4*>(x)[t];
+    floatx4 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float z = (v[e] - mean[c + e]) * rstd[c + e] * g[c + e] + b[c + e];
+      o[e] = relu ? fmaxf(z, 0.f) : z;
+    }
+    if (y) {
+      bf16x4 ob = {f2bf(o[0]), f2bf(o[1]), f2bf(o[2]), f2bf(o[3])};
+      reinterpret_cast<bf16x4*>(y)[t] = ob;
+    }
+    if (yf) reinterpret_cast<floatx4*>(yf)[t] = o;
+  }
+}
+
+// out = ReLU(BN_a(xa) + (xs2 ? BN_s(xs) : xs)), fp32 and bf16.
+__global__ void bn_add_relu_kernel(const float* __restrict__ xa, const float* __restrict__ ma,
+                                   const float* __restrict__ ra, const float* __restrict__ ga,
+                                   const float* __restrict__ ba, const float* __restrict__ xs,
+                                   const float* __restrict__ ms, const float* __restrict__ rs,
+                                   const float* __restrict__ gs, const float* __restrict__ bs,
+                                   long n4, int C, float* __restrict__ out,
+                                   bf16* __restrict__ outb) {
+  for (long t = (long)blockIdx.x * NT + threadIdx.x; t < n4; t += (long)gridDim.x * NT) {
+    const int c = (int)((4 * t) % C);
+    const floatx4 a = reinterpret_cast<const floatx4*>(xa)[t];
+    const floatx4 sv = reinterpret_cast<const floatx4*>(xs)[t];
+    floatx4 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float za = (a[e] - ma[c + e]) * ra[c + e] * ga[c + e] + ba[c + e];
+      const float zs = ms ? (sv[e] - ms[c + e]) * rs[c + e] * gs[c + e] + bs[c + e] : sv[e];
+      o[e] = fmaxf(za + zs, 0.f);
+    }
+    reinterpret_cast<floatx4*>(out)[t] = o;
+    bf16x4 ob = {f2bf(o[0]), f2bf(o[1]), f2bf(o[2]), f2bf(o[3])};
+    reinterpret_cast<bf16x4*>(outb)[t] = ob;
+  }
+}
+
+// Gradient through a ReLU: g = dy where the mask source is positive.
+// MASK 0: none; 1: bf16 activation a > 0; 2: fp32 activation > 0.
+template <int MASK>
+__device__ __forceinline__ float masked(float dy, const void* m, long i) {
+  if (MASK == 1) return bf2f(reinterpret_cast<const bf16*>(m)[i]) > 0.f ? dy : 0.f;
+  if (MASK == 2) return reinterpret_cast<const float*>(m)[i] > 0.f ? dy : 0.f;
+  return dy;
+}
+
+// Per-channel partial sums of g and g * xhat, xhat = (x - mean) rstd.
+template <int MASK>
+__global__ void bn_bwd_partial_kernel(const float* __restrict__ dy, const void* __restrict__ msk,
+                                      const float* __restrict__ x, const float* __restrict__ mean,
+                                      const float* __restrict__ rstd, long P, int C, long rpb,
+                                      float* __restrict__ part) {
+  __shared__ float red[NT];
+  const Slab sl(C);
+  float s1 = 0.f, s2 = 0.f;
+  if (sl.c >= 0) {
+    const float mu = mean[sl.c], rs = rstd[sl.c];
+    const long r0 = (long)blockIdx.x * rpb;
+    const long r1 = min(P, r0 + rpb);
+    for (long r = r0 + sl.phase; r < r1; r += sl.phases) {
+      const long i = r * C + sl.c;
+      const float gv = masked<MASK>(dy[i], msk, i);
+      s1 += gv;
+      s2 += gv * (x[i] - mu) * rs;
+    }
+  }
+  s1 = phase_sum(s1, sl, red);
+  s2 = phase_sum(s2, sl, red);
+  if (sl.phase == 0 && sl.c >= 0) {
+    part[(long)blockIdx.x * C + sl.c] = s1;
+    part[((long)gridDim.x + blockIdx.x) * C + sl.c] = s2;
+  }
+}
+
+// dbeta = sum g, dgamma = sum g xhat (written to the gradient arena).
+__global__ void bn_bwd_final_kernel(const float* __restrict__ part, int nb, int C,
+                                    float* __restrict__ dg, float* __restrict__ db) {
+  const int c = blockIdx.x * NT + threadIdx.x;
+  if (c >= C) return;
+  float s1 = 0.f, s2 = 0.f;
+  for (int b = 0; b < nb; ++b) {
+    s1 += part[(long)b * C + c];
+    s2 += part[((long)nb + b) * C + c];
+  }
+  db[c] = s1;
+  dg[c] = s2;
+}
+
+// dx = rstd g_c (g - dbeta / P - xhat dgamma / P), as bf16.
+template <int MASK>
+__global__ void bn_bwd_apply_kernel(const float* __restrict__ dy, const void* __restrict__ msk,
+                                    const float* __restrict__ x, const float* __restrict__ mean,
+                                    const float* __restrict__ rstd, const float* __restrict__ gam,
+                                    const float* __restrict__ dg, const float* __restrict__ db,
+                                    long n4, int C, float inv_p, bf16* __restrict__ dx) {
+  for (long t = (long)blockIdx.x * NT + threadIdx.x; t < n4; t += (long)gridDim.x * NT) {
+    const int c = (int)((4 * t) % C);
+    const floatx4 d = reinterpret_cast<const floatx4*>(dy)[t];
+    const floatx4 v = reinterpret_cast<const floatx4*>(x)[t];
+    bf16x4 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float gv = masked<MASK>(d[e], msk, 4 * t + e);
+      const float xh = (v[e] - mean[c + e]) * rstd[c + e];
+      o[e] = f2bf(rstd[c + e] * gam[c + e] * (gv - db[c + e] * inv_p - xh * dg[c + e] * inv_p));
+    }
+    reinterpret_cast<bf16x4*>(dx)[t] = o;
+  }
+}
+
+// do = dy where out > 0 (the ReLU after a block's shortcut add).
+__global__ void relu_mask_kernel(const float* __restrict__ dy, const float* __restrict__ out,
+                                 long n4, float* __restrict__ dz) {
+  for (long t = (long)blockIdx.x * NT + threadIdx.x; t < n4; t += (long)gridDim.x * NT) {
+    const floatx4 d = reinterpret_cast<const floatx4*>(dy)[t];
+    const floatx4 o = reinterpret_cast<const floatx4*>(out)[t];
+    floatx4 r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) r[e] = o[e] > 0.f ? d[e] : 0.f;
+    reinterpret_cast<floatx4*>(dz)[t] = r;
+  }
+}
+
+// ---------------------------------------------------------------- pooling
+
+// 3 x 3 max pool, stride 2, padding 1 (padding never wins; ties go to the
+// first tap in row-major order): fp32 and bf16 outputs and the winning tap.
+__global__ void maxpool_fwd_kernel(const float* __restrict__ x, int N, int H, int W, int C, int Ho,
+                                   int Wo, float* __restrict__ y, bf16* __restrict__ yb,
+                                   uint8_t* __restrict__ arg) {
+  const long total = (long)N * Ho * Wo * C;
+  for (long t = (long)blockIdx.x * NT + threadIdx.x; t < total; t += (long)gridDim.x * NT) {
+    const int c = (int)(t % C);
+    const long q = t / C;
+    const int j = (int)(q % Wo);
+    const long q2 = q / Wo;
+    const int i = (int)(q2 % Ho);
+    const int n = (int)(q2 / Ho);
+    float best = -INFINITY;
+    int bi = 0;
+    for (int a = 0; a < 3; ++a) {
+      const int h = 2 * i - 1 + a;
+      if (h < 0 || h >= H) continue;
+      for (int b = 0; b < 3; ++b) {
+        const int w = 2 * j - 1 + b;
+        if (w < 0 || w >= W) continue;
+        const float v = x[(((long)n * H + h) * W + w) * C + c];
+        if (v > best) {
+          best = v;
+          bi = 3 * a + b;
+        }
+      }
+    }
+    y[t] = best;
+    yb[t] = f2bf(best);
+    arg[t] = (uint8_t)bi;
+  }
+}
+
+// dx[n, h, w, c] = sum of dy over the windows whose winning tap is (h, w),
+// windows in increasing (i, j) order.
+__global__ void maxpool_bwd_kernel(const float* __restrict__ dy, const uint8_t* __restrict__ arg,
+                                   int N, int H, int W, int C, int Ho, int Wo,
+                                   float* __restrict__ dx) {
+  const long total = (long)N * H * W * C;
+  for (long t = (long)blockIdx.x * NT + threadIdx.x; t < total; t += (long)gridDim.x * NT) {
+    const int c = (int)(t % C);
+    const long q = t / C;
+    const int w = (int)(q % W);
+    const long q2 = q / W;
+    const int h = (int)(q2 % H);
+    const int n = (int)(q2 / H);
+    float acc = 0.f;
+    const int i0 = h / 2, j0 = w / 2;  // windows i with 2i - 1 <= h <= 2i + 1
+    for (int i = i0; i <= min(Ho - 1, (h + 1) / 2); ++i) {
+      if (2 * i - 1 > h) continue;
+      for (int j = j0; j <= min(Wo - 1, (w + 1) / 2); ++j) {
+        if (2 * j - 1 > w) continue;
+        const long o = (((long)n * Ho + i) * Wo + j) * C + c;
+        if (arg[o] == 3 * (h - 2 * i + 1) + (w - 2 * j + 1)) acc += dy[o];
+      }
+    }
+    dx[t] = acc;
+  }
+}
+
+// feat[n, c] = mean over the HW rows of image n (bf16), in row order.
+__global__ void avgpool_fwd_kernel(const float* __restrict__ x, int N, int HW, int C,
+                                   bf16* __restrict__ feat) {
+  const long total = (long)N * C;
+  for (long t = (long)blockIdx.x * NT + threadIdx.x; t < total; t += (long)gridDim.x * NT) {
+    const int c = (int)(t % C);
+    const long n = t / C;
+    float s = 0.f;
+    for (int r = 0; r < HW; ++r) s += x[(n * HW + r) * C + c];
+    feat[t] = f2bf(s / (float)HW);
+  }
+}
+
+__global__ void avgpool_bwd_kernel(const float* __restrict__ dfeat, int N, int HW, int C,
+                                   float* __restrict__ dx) {
+  const long total = (long)N * HW * C;
+  const float inv = 1.f / (float)HW;
+  for (long t = (long)blockIdx.x * NT + threadIdx.x; t < total; t += (long)gridDim.x * NT) {
+    const int c = (int)(t % C);
+    const long n = t / ((long)HW * C);
+    dx[t] = dfeat[n * C + c] * inv;
+  }
+}
+
+// dx[n, 2i, 2j, c] += dsub[n, i, j, c]: the input gradient of a stride-2
+// 1 x 1 convolution (every other row and column of the input), four
+// channels per thread.
+__global__ void stride2_add_kernel(const float* __restrict__ dsub, int N, int Ho, int Wo, int C,
+                                   int H, int W, float* __restrict__ dx) {
+  const int C4 = C / 4;
+  const long total = (long)N * Ho * Wo * C4;
+  for (long t = (long)blockIdx.x * NT + threadIdx.x; t < total; t += (long)gridDim.x * NT) {
+    const int c4 = (int)(t % C4);
+    const long q = t / C4;
+    const int j = (int)(q % Wo);
+    const long q2 = q / Wo;
+    const int i = (int)(q2 % Ho);
+    const int n = (int)(q2 / Ho);
+    floatx4* o = reinterpret_cast<floatx4*>(dx + (((long)n * H + 2 * i) * W + 2 * j) * C + 4 * c4);
+    *o += *reinterpret_cast<const floatx4*>(dsub + q * C + 4 * c4);
+  }
+}
+
+__global__ void pad_cols_kernel(const bf16* __restrict__ src, int rows, int cols,
+                                bf16* __restrict__ dst, long ldd) {
+  const long total = (long)rows * ldd;
+  for (long t = (long)blockIdx.x * NT + threadIdx.x; t < total; t += (long)gridDim.x * NT) {
+    const long r = t / ldd;
+    const int c = (int)(t - r * ldd);
+    dst[t] = c < cols ? src[r * cols + c] : f2bf(0.f);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_pad_cols_bf16(const bf16* src, int rows, int cols, bf16* dst, long ldd,
+                                hipStream_t st) {
+  if (ldd < cols) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(pad_cols_kernel, dim3(grid_for((long)rows * ldd)), dim3(NT), 0, st, src, rows,
+                     cols, dst, ldd);
+  return hipGetLastError();
+}
+
+// Row blocks of the batch-norm reductions: about 1024 workgroups in all,
+// at least 32 rows each.
+int bn_parts(long P, int C) {
+  const int slabs = (C + NT - 1) / NT;
+  long nb = 1024 / slabs;
+  nb = nb < 1 ? 1 : nb;
+  const long by_rows = (P + 31) / 32;
+  return (int)(nb < by_rows ? nb : (by_rows < 1 ? 1 : by_rows));
+}
+
+hipError_t launch_im2col(const bf16* x, bf16* col, long ldc, int N, int H, int W, int C, int k,
+                         int s, int pad, int Ho, int Wo, hipStream_t st) {
+  if (C % 8 || ldc != (long)k * k * C) return hipErrorInvalidValue;
+  const long total = (long)N * Ho * Wo * k * k * (C / 8);
+  hipLaunchKernelGGL(im2col8_kernel, dim3(grid_for(total)), dim3(NT), 0, st, x, col, N, H, W, C, k,
+                     s, pad, Ho, Wo, ldc);
+  return hipGetLastError();
+}
+
+hipError_t launch_im2col_nchw(const float* img, bf16* col, long ldc, int N, int C, int H, int W,
+                              int k, int s, int pad, int Ho, int Wo, hipStream_t st) {
+  if (ldc < (long)k * k * C) return hipErrorInvalidValue;
+  const long total = (long)N * Ho * Wo * ldc;
+  hipLaunchKernelGGL(im2col_nchw_kernel, dim3(grid_for(total)), dim3(NT), 0, st, img, col, N, C, H,
+                     W, k, s, pad, Ho, Wo, ldc);
+  return hipGetLastError();
+}
+
+hipError_t launch_col2im(const float* dcol, long ldc, float* dx, int N, int H, int W, int C, int k,
+                         int s, int pad, int Ho, int Wo, int accumulate, hipStream_t st) {
+  if (C % 4 || ldc % 4) return hipErrorInvalidValue;
+  const long total = (long)N * H * W * (C / 4);
+  hipLaunchKernelGGL(col2im4_kernel, dim3(grid_for(total)), dim3(NT), 0, st, dcol, ldc, dx, N, H,
+                     W, C, k, s, pad, Ho, Wo, accumulate);
+  return hipGetLastError();
+}
+
+hipError_t launch_bn_stats(const float* x, long P, int C, float eps, float* part, float* mean,
+                           float* rstd, hipStream_t st) {
+  if (P <= 0 || C <= 0) return hipErrorInvalidValue;
+  const int nb = bn_parts(P, C);
+  const long rpb = (P + nb - 1) / nb;
+  hipLaunchKernelGGL(bn_stats_partial_kernel, dim3(nb, (C + NT - 1) / NT), dim3(NT), 0, st, x, P,
+                     C, rpb, part);
+  hipLaunchKernelGGL(bn_stats_final_kernel, dim3((C + NT - 1) / NT), dim3(NT), 0, st, x, part, nb,
+                     P, C, eps, mean, rstd);
+  return hipGetLastError();
+}
+
+hipError_t launch_bn_apply(const float* x, long P, int C, const float* mean, const float* rstd,
+                           const float* g, const float* b, int relu, bf16* y, float* yf,
+                           hipStream_t st) {
+  if (C % 4) return hipErrorInvalidValue;
+  const long n4 = P * C / 4;
+  hipLaunchKernelGGL(bn_apply_kernel, dim3(grid_for(n4)), dim3(NT), 0, st, x, n4, C, mean, rstd, g,
+                     b, relu, y, yf);
+  return hipGetLastError();
+}
+
+hipError_t launch_bn_add_relu(const float* xa, const float* ma, const float* ra, const float* ga,
+                              const float* ba, const float* xs, const float* ms, const float* rs,
+                              const float* gs, const float* bs, long P, int C, float* out,
+                              bf16* outb, hipStream_t st) {
+  if (C % 4) return hipErrorInvalidValue;
+  const long n4 = P * C / 4;
+  hipLaunchKernelGGL(bn_add_relu_kernel, dim3(grid_for(n4)), dim3(NT), 0, st, xa, ma, ra, ga, ba,
+                     xs, ms, rs, gs, bs, n4, C, out, outb);
+  return hipGetLastError();
+}
+
+hipError_t launch_bn_bwd(const float* dy, int mask_kind, const void* mask, const float* x,
+                         const float* mean, const float* rstd, const float* gam, long P, int C,
+                         float* part, float* dg, float* db, bf16* dx, hipStream_t st) {
+  if (C % 4 || P <= 0 || mask_kind < 0 || mask_kind > 2) return hipErrorInvalidValue;
+  const int nb = bn_parts(P, C);
+  const long rpb = (P + nb - 1) / nb;
+  const dim3 g2(nb, (C + NT - 1) / NT);
+  if (mask_kind == 0)
+    hipLaunchKernelGGL(bn_bwd_partial_kernel<0>, g2, dim3(NT), 0, st, dy, mask, x, mean, rstd, P, C,
+                       rpb, part);
+  else if (mask_kind == 1)
+    hipLaunchKernelGGL(bn_bwd_partial_kernel<1>, g2, dim3(NT), 0, st, dy, mask, x, mean, rstd, P, C,
+                       rpb, part);
+  else
+    hipLaunchKernelGGL(bn_bwd_partial_kernel<2>, g2, dim3(NT), 0, st, dy, mask, x, mean, rstd, P, C,
+                       rpb, part);
+  hipLaunchKernelGGL(bn_bwd_final_kernel, dim3((C + NT - 1) / NT), dim3(NT), 0, st, part, nb, C, dg,
+                     db);
+  const long n4 = P * C / 4;
+  const float inv_p = (float)(1.0 / (double)P);
+  const dim3 g1(grid_for(n4));
+  if (mask_kind == 0)
+    hipLaunchKernelGGL(bn_bwd_apply_kernel<0>, g1, dim3(NT), 0, st, dy, mask, x, mean, rstd, gam, dg,
+                       db, n4, C, inv_p, dx);
+  else if (mask_kind == 1)
+    hipLaunchKernelGGL(bn_bwd_apply_kernel<1>, g1, dim3(NT), 0, st, dy, mask, x, mean, rstd, gam, dg,
+                       db, n4, C, inv_p, dx);
+  else
+    hipLaunchKernelGGL(bn_bwd_apply_kernel<2>, g1, dim3(NT), 0, st, dy, mask, x, mean, rstd, gam, dg,
+                       db, n4, C, inv_p, dx);
+  return hipGetLastError();
+}
+
+hipError_t launch_relu_mask(const float* dy, const float* out, long n, float* dz, hipStream_t st) {
+  if (n % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(relu_mask_kernel, dim3(grid_for(n / 4)), dim3(NT), 0, st, dy, out, n / 4, dz);
+  return hipGetLastError();
+}
+
+hipError_t launch_maxpool_fwd(const float* x, int N, int H, int W, int C, int Ho, int Wo, float* y,
+                              bf16* yb, uint8_t* arg, hipStream_t st) {
+  const long total = (long)N * Ho * Wo * C;
+  hipLaunchKernelGGL(maxpool_fwd_kernel, dim3(grid_for(total)), dim3(NT), 0, st, x, N, H, W, C, Ho,
+                     Wo, y, yb, arg);
+  return hipGetLastError();
+}
+
+hipError_t launch_maxpool_bwd(const float* dy, const uint8_t* arg, int N, int H, int W, int C,
+                              int Ho, int Wo, float* dx, hipStream_t st) {
+  const long total = (long)N * H * W * C;
+  hipLaunchKernelGGL(maxpool_bwd_kernel, dim3(grid_for(total)), dim3(NT), 0, st, dy, arg, N, H, W,
+                     C, Ho, Wo, dx);
+  return hipGetLastError();
+}
+
+hipError_t launch_avgpool_fwd(const float* x, int N, int HW, int C, bf16* feat, hipStream_t st) {
+  hipLaunchKernelGGL(avgpool_fwd_kernel, dim3(grid_for((long)N * C)), dim3(NT), 0, st, x, N, HW, C,
+                     feat);
+  return hipGetLastError();
+}
+
+hipError_t launch_avgpool_bwd(const float* dfeat, int N, int HW, int C, float* dx, hipStream_t st) {
+  hipLaunchKernelGGL(avgpool_bwd_kernel, dim3(grid_for((long)N * HW * C)), dim3(NT), 0, st, dfeat,
+                     N, HW, C, dx);
+  return hipGetLastError();
+}
+
+hipError_t launch_stride2_add(const float* dsub, int N, int Ho, int Wo, int C, int H, int W,
+                              float* dx, hipStream_t st) {
+  if (C % 4) return hipErrorInvalidValue;
+  const long total = (long)N * Ho * Wo * (C / 4);
+  hipLaunchKernelGGL(stride2_add_kernel, dim3(grid_for(total)), dim3(NT), 0, st, dsub, N, Ho, Wo, C,
+                     H, W, dx);
+  return hipGetLastError();
+}

@@ -644,7 +644,7 @@ hipError_t launch_gemm(const GemmArgs& a, int alay, int blay, int epi, hipStream
   if ((epi == EPI_F32 || epi == EPI_RESID_F32) && alay == LAY_K && blay == LAY_K &&
       a.splitk <= 1 && a.splitk_ws != nullptr) {
     int kc = 0;
-    const int S = gemm_splitk(a.M, a.N, a.K, &kc);
+    const int S = gemm_splitk(a.M, a.N, a.K, &kc, a.splitk_max);
     if (S > 1 && (long)S * a.M * a.N <= a.splitk_ws_elems) {
       GemmArgs b = a;
       b.out = a.splitk_ws;

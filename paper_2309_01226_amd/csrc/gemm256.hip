@@ -963,7 +963,7 @@ hipError_t launch_gemm256(const GemmArgs& a, int alay, int blay, int epi, hipStr
   return launch_l<LAY_MN, LAY_MN>(a, epi, s);
 }
 
-int gemm_splitk(int M, int N, int K, int* kc) {
+int gemm_splitk(int M, int N, int K, int* kc, int smax) {
   const long tiles = (long)sat_cdiv(M, BT) * sat_cdiv(N, BT);
   if (M <= 0 || N <= 0 || tiles >= 256 || K < 1024) return 1;
   // Estimated time of S slices, in K-tile steps of one tile: the slices run
@@ -972,7 +972,7 @@ int gemm_splitk(int M, int N, int K, int* kc) {
   // 9 MB per K-tile step at the measured GEMM and copy rates).  A slice
   // count that spills a few workgroups into a second round loses to a
   // smaller one that fits in the first.
-  const int Smax = std::min(16, K / 512);
+  const int Smax = std::min(smax > 0 ? smax : 16, K / 512);
   int best = 1;
   double best_cost = (double)sat_cdiv(K, BK);
   for (int S = 2; S <= Smax; ++S) {
@@ -991,9 +991,9 @@ int gemm_splitk(int M, int N, int K, int* kc) {
   return sat_cdiv(K, c);
 }
 
-long gemm_splitk_ws_elems(int M, int N, int K) {
+long gemm_splitk_ws_elems(int M, int N, int K, int smax) {
   int kc = 0;
-  const int S = gemm_splitk(M, N, K, &kc);
+  const int S = gemm_splitk(M, N, K, &kc, smax);
   return S > 1 ? (long)S * M * N : 0;
 }
 

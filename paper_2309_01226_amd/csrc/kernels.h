@@ -72,6 +72,10 @@ struct GemmArgs {
   // to fill the chip as split-K plus a reduction (gemm_splitk below).
   float* splitk_ws;
   long splitk_ws_elems;
+  // Most K slices the split-K plan may use (0: 16).  Products with very few
+  // output tiles and very long K (the convolution weight gradients, K =
+  // pixels) fill the chip only with more.
+  int splitk_max;
 };
 
 hipError_t launch_gemm(const GemmArgs& a, int alay, int blay, int epi, hipStream_t s);
@@ -83,9 +87,9 @@ hipError_t launch_gemm256(const GemmArgs& a, int alay, int blay, int epi, hipStr
 // a workspace is given (1: none; *kc: slice depth), and the workspace that
 // then takes (fp32 elements; 0 when not split).  A product is split when it
 // has fewer than 256 tiles of 256 x 256 and K >= 1024: into enough slices to
-// give every CU a tile where K allows, each at least 512 deep, at most 16.
-int gemm_splitk(int M, int N, int K, int* kc);
-long gemm_splitk_ws_elems(int M, int N, int K);
+// give every CU a tile where K allows, each at least 512 deep, at most smax.
+int gemm_splitk(int M, int N, int K, int* kc, int smax = 16);
+long gemm_splitk_ws_elems(int M, int N, int K, int smax = 16);
 // out[m, n] = sum over s of ws[s * stride + m * N + n] (s in order) + bias[n -
 // bias_col0] (n >= bias_col0; null: none) + resid[m * ldr + n] (null: none).
 hipError_t launch_splitk_reduce(const float* ws, int S, long stride, int M, int N, float* out,
@@ -235,3 +239,55 @@ hipError_t launch_fill(float* p, bf16* shadow, long n, float value, hipStream_t 
 hipError_t launch_zero(void* p, long bytes, hipStream_t s);
 hipError_t launch_sum_rows_batched(const float* dh, float* out, int B, int S, int d,
                                    hipStream_t s);
+
+// ---------------------------------------------------------------- ResNet (conv.hip)
+// NHWC activations ([N, H, W, C] = the matrix [N * H * W, C]).
+// col[(n Ho + i) Wo + j, (a k + b) C + c] = x[n, i s - pad + a, j s - pad + b, c]
+// (zero outside); bf16, C % 8 == 0, ldc == k k C.
+hipError_t launch_im2col(const bf16* x, bf16* col, long ldc, int N, int H, int W, int C, int k,
+                         int s, int pad, int Ho, int Wo, hipStream_t st);
+// The same from fp32 NCHW images; columns k k C .. ldc - 1 are written as zeros.
+hipError_t launch_im2col_nchw(const float* img, bf16* col, long ldc, int N, int C, int H, int W,
+                              int k, int s, int pad, int Ho, int Wo, hipStream_t st);
+// dx (+)= the sum over taps of dcol (the transpose of im2col, gathered per
+// input element in tap order); fp32, C % 4 == 0.
+hipError_t launch_col2im(const float* dcol, long ldc, float* dx, int N, int H, int W, int C, int k,
+                         int s, int pad, int Ho, int Wo, int accumulate, hipStream_t st);
+// Batch-norm statistics of x [P, C] per channel (training mode, biased
+// variance): mean, rstd = 1 / sqrt(var + eps).  part: fp32 scratch of
+// 2 * bn_parts(P, C) * C.
+int bn_parts(long P, int C);
+hipError_t launch_bn_stats(const float* x, long P, int C, float eps, float* part, float* mean,
+                           float* rstd, hipStream_t st);
+// y = (x - mean) rstd g + b (ReLU when relu) as bf16 (y, may be null) and fp32 (yf, may be null).
+hipError_t launch_bn_apply(const float* x, long P, int C, const float* mean, const float* rstd,
+                           const float* g, const float* b, int relu, bf16* y, float* yf,
+                           hipStream_t st);
+// out = ReLU(BN_a(xa) + BN_s(xs)) (ms null: + xs itself), fp32 and bf16.
+hipError_t launch_bn_add_relu(const float* xa, const float* ma, const float* ra, const float* ga,
+                              const float* ba, const float* xs, const float* ms, const float* rs,
+                              const float* gs, const float* bs, long P, int C, float* out,
+                              bf16* outb, hipStream_t st);
+// Batch-norm backward with g = dy (mask_kind 0), dy where the bf16 mask > 0
+// (1) or where the fp32 mask > 0 (2): dg = sum g xhat, db = sum g (written),
+// dx = rstd gamma (g - db / P - xhat dg / P) as bf16.  part as for the stats.
+hipError_t launch_bn_bwd(const float* dy, int mask_kind, const void* mask, const float* x,
+                         const float* mean, const float* rstd, const float* gam, long P, int C,
+                         float* part, float* dg, float* db, bf16* dx, hipStream_t st);
+// dz = dy where out > 0, else 0 (n % 4 == 0).
+hipError_t launch_relu_mask(const float* dy, const float* out, long n, float* dz, hipStream_t st);
+// 3 x 3 max pool, stride 2, padding 1: fp32 / bf16 outputs and the winning
+// tap (row-major index, first maximum); backward gathers dy by that tap.
+hipError_t launch_maxpool_fwd(const float* x, int N, int H, int W, int C, int Ho, int Wo, float* y,
+                              bf16* yb, uint8_t* arg, hipStream_t st);
+hipError_t launch_maxpool_bwd(const float* dy, const uint8_t* arg, int N, int H, int W, int C,
+                              int Ho, int Wo, float* dx, hipStream_t st);
+// Global average pool over the HW rows of each image (bf16 features) and its backward.
+hipError_t launch_avgpool_fwd(const float* x, int N, int HW, int C, bf16* feat, hipStream_t st);
+hipError_t launch_avgpool_bwd(const float* dfeat, int N, int HW, int C, float* dx, hipStream_t st);
+// dx[n, 2i, 2j] += dsub[n, i, j]: input gradient of a stride-2 1 x 1 convolution.
+hipError_t launch_stride2_add(const float* dsub, int N, int Ho, int Wo, int C, int H, int W,
+                              float* dx, hipStream_t st);
+// Copy of a bf16 matrix [rows, cols] into [rows, ldd] with zero columns cols .. ldd - 1.
+hipError_t launch_pad_cols_bf16(const bf16* src, int rows, int cols, bf16* dst, long ldd,
+                                hipStream_t st);

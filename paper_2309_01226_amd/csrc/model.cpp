@@ -39,7 +39,10 @@ sat_status sat_validate_config(const sat_config* c) {
   SAT_CHECK_ARG(c != nullptr, "null config");
   SAT_CHECK_ARG(c->struct_size == sizeof(sat_config), "struct_size %u != sizeof(sat_config) %zu",
                 c->struct_size, sizeof(sat_config));
-  SAT_CHECK_ARG(c->arch >= SAT_GPT2 && c->arch <= SAT_VIT, "unknown arch %d", c->arch);
+  SAT_CHECK_ARG(c->arch >= SAT_GPT2 && c->arch <= SAT_RESNET, "unknown arch %d", c->arch);
+  if (c->arch == SAT_RESNET) return sat_resnet_validate(c);
+  for (int s = 0; s < 4; ++s)
+    SAT_CHECK_ARG(c->res_blocks[s] == 0, "res_blocks must be 0 for transformer architectures");
   SAT_CHECK_ARG(c->n_layers >= 1, "n_layers must be >= 1");
   SAT_CHECK_ARG(c->d_model >= 8 && c->d_model % 8 == 0 && c->d_model <= 4096,
                 "d_model must be a multiple of 8 in [8, 4096]");
@@ -78,6 +81,11 @@ sat_status sat_validate_config(const sat_config* c) {
 // ------------------------------------------------------------------ layout
 
 void sat_model_dims(const sat_config& c, Dims* d) {
+  if (c.arch == SAT_RESNET) {
+    sat_resnet_dims(c, d);
+    return;
+  }
+  memset(d, 0, sizeof *d);
   d->arch = c.arch;
   d->L = c.n_layers;
   d->d = c.d_model;
@@ -125,6 +133,10 @@ static void add_param(std::vector<ParamDesc>& P, size_t& off, const std::string&
 // kind: 0 = normal init, 1 = zeros (bias), 2 = ones (LN gain)
 void sat_build_params(const sat_config& c, const Dims& D, std::vector<ParamDesc>& P,
                       size_t* n_total) {
+  if (c.arch == SAT_RESNET) {
+    sat_resnet_build_params(c, D, P, n_total);
+    return;
+  }
   P.clear();
   size_t off = 0;
   const int d = D.d, m = D.m;
@@ -195,17 +207,6 @@ void sat_build_params(const sat_config& c, const Dims& D, std::vector<ParamDesc>
 
 namespace {
 
-struct Carver {
-  size_t off = 0;
-  char* base = nullptr;  // null during the sizing pass
-  template <typename T>
-  T* take(size_t count) {
-    size_t o = align_up(off, kAlignBytes);
-    off = o + count * sizeof(T);
-    return base ? reinterpret_cast<T*>(base + o) : nullptr;
-  }
-};
-
 // Whether the weight-gradient product of a [rows, cols] weight (K = k
 // token-contiguous rows) runs in the 256 x 256 kernel, so that its AdamW step
 // can be fused into the product's epilogue: enough tiles for every CU, whole
@@ -260,7 +261,7 @@ void build_segments(sat_model* M) {
       }
       flat(cur, p.off);
       const long k = p.group == D.L ? D.rows_head : D.T;
-      p.fused_opt = fused_opt_ok(rows, p.cols, p.trows, k);
+      p.fused_opt = D.arch != SAT_RESNET && fused_opt_ok(rows, p.cols, p.trows, k);
       if (!(skip_fused && p.fused_opt))
         push(AdamWSeg{(int64_t)p.off, (int64_t)p.toff, (int32_t)rows, (int32_t)p.trows,
                       (int32_t)p.cols, 0});
@@ -275,7 +276,7 @@ void build_segments(sat_model* M) {
 // Lays out every buffer; with base == nullptr it only measures.
 size_t carve(sat_model* M, char* base) {
   const Dims& D = M->D;
-  Carver c;
+  SatCarver c;
   c.base = base;
   const size_t NP = M->n_param_elems;
   M->master = c.take<float>(NP);
@@ -290,11 +291,17 @@ size_t carve(sat_model* M, char* base) {
   M->grad = c.take<float>(NP);
   M->mom = c.take<float>(NP);
   M->vel = c.take<float>(NP);
+  if (D.arch == SAT_RESNET) {
+    sat_resnet_carve(M, c);
+    return align_up(c.off, kAlignBytes);
+  }
   const long T = D.T, d = D.d, m = D.m;
   const bool gptj = D.arch == SAT_GPTJ;
   // residual stream entering every block and the final LN
   M->h_in.assign(D.L + 1, nullptr);
   for (int l = 0; l <= D.L; ++l) M->h_in[l] = c.take<float>(T * d);
+  M->act_rows.assign(D.L + 1, T);
+  M->act_cols.assign(D.L + 1, (int)d);
   // per-layer saved activations: blocks >= k get their own, frozen blocks share
   // one set; with activation checkpointing every block uses the same set
   const int nsets = D.ckpt ? 1 : (D.k > 0) ? D.L - D.k + 1 : D.L;
@@ -396,6 +403,7 @@ size_t carve(sat_model* M, char* base) {
 size_t sat_model_layout(sat_model* M, char* base) { return carve(M, base); }
 
 double sat_step_flops(const Dims& D) {
+  if (D.arch == SAT_RESNET) return sat_resnet_flops(D);
   const double T = D.T, d = D.d, m = D.m;
   const double gemm_layer = 2.0 * T * (3 * d * d + d * d + 2 * d * m);
   const double causal = (D.arch == SAT_VIT) ? 1.0 : 0.5;

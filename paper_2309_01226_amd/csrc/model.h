@@ -5,6 +5,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <memory>
 #include <string>
 #include <vector>
 
@@ -20,6 +21,9 @@ struct Dims {
   int rows_head;   // rows entering the head (T, or B for ViT)
   int qkv_ld;      // row pitch of the q|k|v (|u for GPT-J) buffer
   bool ckpt;       // activation checkpointing: one saved-activation set, recomputed per block
+  // RESNET: blocks per stage, stem / stage-0 mid width, image side and channels
+  int res_blocks[4];
+  int res_width, img, channels;
 };
 
 struct ParamDesc {
@@ -53,6 +57,21 @@ struct LayerActs {
   float* mean2;
   float* rstd2;
   bf16* u;          // GPT-2 / ViT: MLP pre-activation [T, m]
+};
+
+struct ResNetPlan;  // resnet.cpp
+
+// Carves 256-byte aligned sections out of the arena; with base == nullptr it
+// only measures.
+struct SatCarver {
+  size_t off = 0;
+  char* base = nullptr;
+  template <typename T>
+  T* take(size_t count) {
+    size_t o = (off + 255) / 256 * 256;
+    off = o + count * sizeof(T);
+    return base ? reinterpret_cast<T*>(base + o) : nullptr;
+  }
 };
 
 struct TimingRec {
@@ -100,8 +119,12 @@ struct sat_model {
   float* grad;
   float* mom;
   float* vel;
-  // activations
+  // activations; h_in[l] ([act_rows[l], act_cols[l]] fp32) is what
+  // sat_activation_read returns for layer l
   std::vector<float*> h_in;
+  std::vector<long> act_rows;
+  std::vector<int> act_cols;
+  std::shared_ptr<ResNetPlan> rn;  // RESNET: layout and buffers of the convolutional step
   std::vector<LayerActs> acts;
   bf16* f;
   float* meanf;
@@ -161,3 +184,13 @@ sat_status sat_run_init(sat_model* M);
 sat_status sat_refresh_transposed(sat_model* M, int only = -1);
 
 const LayerActs& sat_layer_acts(const sat_model* M, int l);
+
+// resnet.cpp: the bottleneck-ResNet architecture
+sat_status sat_resnet_validate(const sat_config* c);
+void sat_resnet_dims(const sat_config& c, Dims* d);
+void sat_resnet_build_params(const sat_config& c, const Dims& D, std::vector<ParamDesc>& P,
+                             size_t* n_total);
+void sat_resnet_carve(sat_model* M, SatCarver& c);
+double sat_resnet_flops(const Dims& D);
+sat_status sat_resnet_forward(sat_model* M, const void* inputs, const int32_t* labels);
+sat_status sat_resnet_backward(sat_model* M, const void* inputs);

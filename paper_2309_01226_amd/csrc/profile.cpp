@@ -41,7 +41,7 @@ extern "C" sat_status sat_profile_batch(const sat_config* cfg, void* inputs, int
   hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
   const uint32_t seed = (uint32_t)(cfg->seed ^ (cfg->seed >> 32)) ^ 0x51ED270Bu;
   hipError_t e;
-  if (cfg->arch == SAT_VIT) {
+  if (cfg->arch == SAT_VIT || cfg->arch == SAT_RESNET) {
     const long n_in = (long)cfg->batch * cfg->channels * cfg->img_size * cfg->img_size;
     e = launch_synth_images((float*)inputs, n_in, labels, cfg->batch, cfg->vocab, seed, s);
   } else {
@@ -78,7 +78,7 @@ extern "C" sat_status sat_profile(const sat_config* cfg, void* hip_stream, int32
   // synthetic batch of the task's shape, generated on the device
   Dims D;
   sat_model_dims(*cfg, &D);
-  const bool vit = cfg->arch == SAT_VIT;
+  const bool vit = cfg->arch == SAT_VIT || cfg->arch == SAT_RESNET;
   const long n_in = vit ? (long)cfg->batch * cfg->channels * cfg->img_size * cfg->img_size
                         : (long)cfg->batch * cfg->seq_len;
   const long n_lab = vit ? cfg->batch : (long)cfg->batch * cfg->seq_len;
@@ -143,7 +143,8 @@ extern "C" sat_status sat_profile(const sat_config* cfg, void* hip_stream, int32
   r.step_ms_mean = sum / steps;
   r.step_ms_min = mn;
   r.step_ms_max = mx;
-  const double rows = vit ? (double)cfg->batch * D.S : (double)cfg->batch * cfg->seq_len;
+  const double rows = cfg->arch == SAT_RESNET ? (double)cfg->batch
+                      : vit ? (double)cfg->batch * D.S : (double)cfg->batch * cfg->seq_len;
   r.tokens_per_s = rows / (r.step_ms_mean * 1e-3);
   r.step_tflop = sat_step_flops(D) / 1e12;
   r.achieved_tflops = r.step_tflop / (r.step_ms_mean * 1e-3);

@@ -9,13 +9,11 @@
 #include "abi_common.h"
 #include "kernels.h"
 #include "model.h"
+#include "step_common.h"
+
+using namespace satstep;
 
 namespace {
-
-enum {
-  TK_OFF = 0, TK_QKV_FWD = 1, TK_ALL_GEMM = 2, TK_ADAMW = 3, TK_ATTN_FWD = 4, TK_ATTN_BWD = 5,
-  TK_LN_FWD = 6, TK_LN_BWD = 7, TK_XENT = 8, TK_QKV_WGRAD = 9
-};
 
 // Algorithmic bytes of the bandwidth kernels (each operand read once, each
 // result written once): LayerNorm forward reads fp32 x and writes bf16 y plus
@@ -29,70 +27,12 @@ double ln_bwd_bytes(long rows, int d, bool bf) {
 }
 double xent_bytes(long rows, long V) { return rows * (double)V * (4 + 2) + rows * 8.0; }
 
-struct Timed {
-  sat_model* M;
-  TimingRec* rec = nullptr;
-  Timed(sat_model* m, int kind, double work) : M(m) {
-    if (m->timing_kind == TK_OFF) return;
-    bool match = (m->timing_kind == kind) ||
-                 (m->timing_kind == TK_ALL_GEMM &&
-                  (kind == TK_QKV_FWD || kind == TK_ALL_GEMM || kind == TK_QKV_WGRAD));
-    if (!match || m->timing_used >= m->timing.size()) return;
-    rec = &m->timing[m->timing_used++];
-    rec->flops = work;
-    hipEventRecord(rec->e0, m->stream);
-  }
-  ~Timed() {
-    if (rec) hipEventRecord(rec->e1, M->stream);
-  }
-};
-
-GemmArgs gargs(const bf16* A, long lda, const bf16* B, long ldb, int Mr, int N, int K, void* out,
-               long ldo) {
-  GemmArgs a;
-  memset(&a, 0, sizeof a);
-  a.A = A;
-  a.lda = lda;
-  a.B = B;
-  a.ldb = ldb;
-  a.M = Mr;
-  a.N = N;
-  a.K = K;
-  a.out = out;
-  a.ldo = ldo;
-  a.ldr = ldo;
-  return a;
-}
-
-sat_status gemm(sat_model* M, const GemmArgs& a, int alay, int blay, int epi,
-                int tk = TK_ALL_GEMM) {
-  Timed t(M, tk, 2.0 * a.M * a.N * (double)a.K);
-  // fp32-output products with too few tiles run split-K in this workspace
-  GemmArgs b = a;
-  b.splitk_ws = M->splitk_ws;
-  b.splitk_ws_elems = M->splitk_ws_elems;
-  SAT_HIP(launch_gemm(b, alay, blay, epi, M->stream));
-  return SAT_OK;
-}
-
-#define TRY(x)                        \
-  do {                                \
-    sat_status st_ = (x);             \
-    if (st_ != SAT_OK) return st_;    \
-  } while (0)
-
 struct PIdx {
   const sat_model* M;
   int base;
   const ParamDesc& p(int i) const { return M->params[base + i]; }
 };
 
-// Parameter accessors by table index.
-inline const float* master(const sat_model* M, int i) { return M->master + M->params[i].off; }
-inline const bf16* shadow(const sat_model* M, int i) { return M->shadow + M->params[i].off; }
-inline float* grad(sat_model* M, int i) { return M->grad + M->params[i].off; }
-// Transposed bf16 copy [cols, trows] of a weight (B operand of dX = dY W).
-inline const bf16* shadow_t(const sat_model* M, int i) { return M->shadow_t + M->params[i].toff; }
 
 // Index of the first parameter of block l and of the head group.
 int embed_count(const sat_model* M) {
@@ -238,6 +178,7 @@ static sat_status block_forward(sat_model* M, int l, bool recompute) {
 }
 
 sat_status sat_run_forward(sat_model* M, const void* inputs, const int32_t* labels) {
+  if (M->D.arch == SAT_RESNET) return sat_resnet_forward(M, inputs, labels);
   const Dims& D = M->D;
   hipStream_t s = M->stream;
   const int T = D.T, d = D.d;
@@ -339,6 +280,7 @@ static sat_status ln_bwd(sat_model* M, const float* dy, const float* x, long row
 }
 
 sat_status sat_run_backward(sat_model* M, const void* inputs) {
+  if (M->D.arch == SAT_RESNET) return sat_resnet_backward(M, inputs);
   const Dims& D = M->D;
   hipStream_t s = M->stream;
   const int T = D.T, d = D.d, m = D.m;

@@ -3,8 +3,8 @@
 Holds none of the method's arithmetic: it only draws token ids, labels and
 images.  Batch t of a run with seed s comes from numpy's generator seeded with
 (s, t).  Decoders draw tokens [B, S+1] uniform in [0, V) and use the first S as
-inputs and the last S as next-token labels; ViT draws N(0, 1) images and uniform
-class labels.  These stand in for WikiText-2 and ImageNet (the paper's
+inputs and the last S as next-token labels; ViT and the ResNet draw N(0, 1)
+images and uniform class labels.  These stand in for WikiText-2 and ImageNet (the paper's
 datasets), whose contents are not used.
 """
 
@@ -29,6 +29,6 @@ def vit_batch(batch, img_size, n_classes, channels=3, seed=0, step=0):
 def batch_for(cfg, seed=0, step=0, rows=None):
     """cfg: a dict or an object with the config fields."""
     g = (lambda k: cfg[k]) if isinstance(cfg, dict) else (lambda k: getattr(cfg, k))
-    if g("arch") == "vit":
+    if g("arch") in ("vit", "resnet"):
         return vit_batch(g("batch"), g("img_size"), g("vocab"), g("channels"), seed, step)
     return decoder_batch(g("batch"), g("seq_len"), g("vocab"), seed, step, rows)

@@ -12,10 +12,10 @@ import torch
 from . import _lib
 
 
-def make_config(arch, n_layers, d_model, n_heads, d_mlp, vocab, seq_len=0, batch=1,
+def make_config(arch, n_layers, d_model=0, n_heads=0, d_mlp=0, vocab=2, seq_len=0, batch=1,
                 frozen_layers=0, rotary_dim=0, img_size=0, patch=0, channels=3, lr=1e-3,
                 beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01, init_std=0.02, ln_eps=1e-5,
-                seed=0, checkpoint=0):
+                seed=0, checkpoint=0, res_blocks=(0, 0, 0, 0), res_width=0):
     c = _lib.sat_config()
     c.struct_size = C.sizeof(_lib.sat_config)
     c.arch = _lib.ARCH[arch]
@@ -26,6 +26,9 @@ def make_config(arch, n_layers, d_model, n_heads, d_mlp, vocab, seq_len=0, batch
     c.checkpoint = int(checkpoint)
     c.lr, c.beta1, c.beta2, c.eps, c.weight_decay = lr, beta1, beta2, eps, weight_decay
     c.init_std, c.ln_eps, c.seed = init_std, ln_eps, seed
+    for i, b in enumerate(res_blocks):
+        c.res_blocks[i] = int(b)
+    c.res_width = res_width
     return c
 
 
@@ -152,16 +155,20 @@ class Model:
         raise KeyError(name)
 
     def activation(self, layer):
-        T = self.rows()
-        return self._read("sat_activation_read", layer, (T, self.kw["d_model"]))
+        shape = (C.c_int64 * 2)()
+        _lib.call("sat_activation_shape", self.h, layer, shape)
+        return self._read("sat_activation_read", layer, (shape[0], shape[1]))
 
     def logits(self):
-        R = self.kw["batch"] if self.kw["arch"] == "vit" else self.rows()
+        R = self.kw["batch"] if self.kw["arch"] in ("vit", "resnet") else self.rows()
         buf = np.empty((R, self.kw["vocab"]), np.float32)
         _lib.call("sat_logits_read", self.h, buf.ctypes.data_as(C.c_void_p))
         return buf
 
     def rows(self):
+        """Rows entering the loss per step (tokens; images for the ResNet)."""
+        if self.kw["arch"] == "resnet":
+            return self.kw["batch"]
         if self.kw["arch"] == "vit":
             g = self.kw["img_size"] // self.kw["patch"]
             return self.kw["batch"] * (g * g + 1)

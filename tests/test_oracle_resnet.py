@@ -231,3 +231,41 @@ def test_step_flops_counts():
     k2 = R.ResNetConfig(blocks=(3, 4, 6, 3), width=64, batch=1, frozen_layers=16)
     head = 2.0 * 2048 * 1000
     assert abs(R.step_flops(k2) - (R.forward_flops(k2) + 2.0 * head)) < 1.0
+
+
+def test_bf16_rounding():
+    """Round to nearest, ties to even, on hand values; and torch's own
+    float32 -> bfloat16 conversion on random values of every magnitude."""
+    assert R.bf16_round(np.array([1.0]))[0] == 1.0
+    assert R.bf16_round(np.array([1.0 + 2.0 ** -8]))[0] == 1.0                 # tie -> even (1.0)
+    assert R.bf16_round(np.array([1.0 + 3 * 2.0 ** -8]))[0] == 1.0 + 2.0 ** -6  # tie -> even (odd lsb up)
+    assert R.bf16_round(np.array([1.0 + 2.0 ** -8 + 2.0 ** -12]))[0] == 1.0 + 2.0 ** -7
+    assert R.bf16_round(np.array([-3.0 - 2.0 ** -7]))[0] == -3.0
+    assert R.bf16_round(np.array([0.0, -0.0, np.inf]))[2] == np.inf
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(7)
+    x = rng.normal(size=4000) * np.exp(rng.uniform(-30, 30, size=4000))
+    ref = torch.tensor(x, dtype=torch.float32).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(R.bf16_round(x), ref)
+
+
+def test_bf16_operands_mode():
+    """With operands already bfloat16-exact (small dyadic values) the first
+    convolution is unchanged by the rounding mode; with general operands the
+    mode changes the result (every product sees rounded operands)."""
+    cfg = _small(blocks=(1, 1, 1, 1), width=4, img_size=32, batch=2, classes=5)
+    cfgb = _small(blocks=(1, 1, 1, 1), width=4, img_size=32, batch=2, classes=5, operands="bf16")
+    rng = np.random.default_rng(8)
+    P = {n: np.round(v * 64) / 64 for n, v in _rough(cfg, rng).items()}
+    x = np.round(rng.normal(size=(2, 3, 32, 32)) * 8) / 8
+    y = rng.integers(0, 5, size=2)
+    l0, c0 = R.forward(cfg, P, x, y)
+    l1, c1 = R.forward(cfgb, P, x, y)
+    # the first convolution's operands are exact, so the stem activation agrees
+    assert np.allclose(c0["acts"][0], c1["acts"][0], rtol=1e-12, atol=1e-12)
+    assert abs(l0 - l1) < 0.05 * abs(l0)
+    # general operands: every rounded product sees operands within 2^-8 relative
+    P2 = _rough(cfg, rng)
+    l2, _ = R.forward(cfg, P2, x, y)
+    l3, _ = R.forward(cfgb, P2, x, y)
+    assert l2 != l3 and np.isfinite(l3)
