@@ -149,6 +149,43 @@ sat_status sat_op_colsum(const float* X, int64_t ldx, int32_t rows, int32_t cols
 sat_status sat_op_transpose_bf16(const void* src, int64_t lds, void* dst, int64_t ldd,
                                  int32_t rows, int32_t cols, void* stream);
 
+/* ---- the ResNet workload's own kernels (Table 3: the ResNet fine-tuned on
+ * ImageNet-shaped images).  Activations are NHWC: [N, H, W, C] is the
+ * row-major matrix [N * H * W, C]; Ho = (H + 2 pad - k) / stride + 1.
+ *
+ * im2col: col [N * Ho * Wo, k * k * C] bf16, col[(n Ho + i) Wo + j,
+ * (a k + b) C + c] = x[n, i stride - pad + a, j stride - pad + b, c] (zero
+ * outside the image), from x bf16; C a positive multiple of 8.  The operand of
+ * a k x k convolution computed as one GEMM against the weight [Cout, k k C]. */
+sat_status sat_op_im2col(const void* x, void* col, int32_t N, int32_t H, int32_t W, int32_t C,
+                         int32_t k, int32_t stride, int32_t pad, void* stream);
+/* col2im, the transpose of im2col: dx [N, H, W, C] fp32 = (accumulate: dx +)
+ * the sum over the taps that read each input element of dcol [N * Ho * Wo,
+ * k * k * C] fp32, in tap order; C a positive multiple of 4. */
+sat_status sat_op_col2im(const float* dcol, float* dx, int32_t N, int32_t H, int32_t W, int32_t C,
+                         int32_t k, int32_t stride, int32_t pad, int32_t accumulate, void* stream);
+/* Batch norm in training mode over x [P, C] fp32 (statistics of the P rows,
+ * biased variance): mean, rstd = 1 / sqrt(var + eps) [C]; y = (x - mean) rstd
+ * g + b, with ReLU when relu, as bf16 (y, may be NULL) and fp32 (yf, may be
+ * NULL, not both).  part: fp32 scratch of 2 * 1024 * C.  C % 4 == 0. */
+sat_status sat_op_batchnorm_fwd(const float* x, int64_t P, int32_t C, const float* g,
+                                const float* b, float eps, int32_t relu, float* part, float* mean,
+                                float* rstd, void* y, float* yf, void* stream);
+/* Its backward from dy [P, C] fp32, through a ReLU when mask_kind is 1 (dy
+ * where the bf16 mask > 0) or 2 (fp32 mask > 0): dg = sum g' xhat, db = sum
+ * g' (written), dx = rstd g (g' - db / P - xhat dg / P) as bf16. */
+sat_status sat_op_batchnorm_bwd(const float* dy, int32_t mask_kind, const void* mask,
+                                const float* x, const float* mean, const float* rstd,
+                                const float* g, int64_t P, int32_t C, float* part, float* dg,
+                                float* db, void* dx, void* stream);
+/* 3 x 3 max pool, stride 2, padding 1: y fp32, yb bf16 and the winning tap
+ * arg (row-major index 0..8, the first maximum) [N, Ho, Wo, C]; the backward
+ * routes dy to the winning taps: dx [N, H, W, C] fp32. */
+sat_status sat_op_maxpool_fwd(const float* x, int32_t N, int32_t H, int32_t W, int32_t C, float* y,
+                              void* yb, uint8_t* arg, void* stream);
+sat_status sat_op_maxpool_bwd(const float* dy, const uint8_t* arg, int32_t N, int32_t H, int32_t W,
+                              int32_t C, float* dx, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -110,6 +110,14 @@ SIGNATURES = {
     "sat_op_embed_bwd": (C.c_int, [_VP, _VP, _VP, _I32, _I32, _I32, _VP, _VP]),
     "sat_op_colsum": (C.c_int, [_VP, _I64, _I32, _I32, _VP, _VP, _VP]),
     "sat_op_transpose_bf16": (C.c_int, [_VP, _I64, _VP, _I64, _I32, _I32, _VP]),
+    "sat_op_im2col": (C.c_int, [_VP, _VP, _I32, _I32, _I32, _I32, _I32, _I32, _I32, _VP]),
+    "sat_op_col2im": (C.c_int, [_VP, _VP, _I32, _I32, _I32, _I32, _I32, _I32, _I32, _I32, _VP]),
+    "sat_op_batchnorm_fwd": (C.c_int, [_VP, _I64, _I32, _VP, _VP, _F32, _I32, _VP, _VP, _VP, _VP, _VP,
+                                       _VP]),
+    "sat_op_batchnorm_bwd": (C.c_int, [_VP, _I32, _VP, _VP, _VP, _VP, _VP, _I64, _I32, _VP, _VP, _VP,
+                                       _VP, _VP]),
+    "sat_op_maxpool_fwd": (C.c_int, [_VP, _I32, _I32, _I32, _I32, _VP, _VP, _VP, _VP]),
+    "sat_op_maxpool_bwd": (C.c_int, [_VP, _VP, _I32, _I32, _I32, _I32, _VP, _VP]),
 }
 
 _lib = None

@@ -274,3 +274,75 @@ extern "C" sat_status sat_op_transpose_bf16(const void* src, int64_t lds, void* 
   SAT_HIP(launch_transpose_bf16((const bf16*)src, lds, (bf16*)dst, ldd, rows, cols, S(stream)));
   return SAT_OK;
 }
+
+// ---- ResNet kernels (conv.hip)
+
+static int conv_hw(int H, int k, int st, int pad) { return (H + 2 * pad - k) / st + 1; }
+
+extern "C" sat_status sat_op_im2col(const void* x, void* col, int32_t N, int32_t H, int32_t W,
+                                    int32_t C, int32_t k, int32_t stride, int32_t pad,
+                                    void* stream) {
+  SAT_CHECK_ARG(x && col, "im2col: null pointer");
+  SAT_CHECK_ARG(N >= 1 && H >= 1 && W >= 1 && C >= 8 && C % 8 == 0 && k >= 1 && stride >= 1 &&
+                    pad >= 0 && H + 2 * pad >= k && W + 2 * pad >= k,
+                "im2col: bad sizes (C must be a positive multiple of 8)");
+  const int Ho = conv_hw(H, k, stride, pad), Wo = conv_hw(W, k, stride, pad);
+  SAT_HIP(launch_im2col((const bf16*)x, (bf16*)col, (long)k * k * C, N, H, W, C, k, stride, pad, Ho,
+                        Wo, S(stream)));
+  return SAT_OK;
+}
+
+extern "C" sat_status sat_op_col2im(const float* dcol, float* dx, int32_t N, int32_t H, int32_t W,
+                                    int32_t C, int32_t k, int32_t stride, int32_t pad,
+                                    int32_t accumulate, void* stream) {
+  SAT_CHECK_ARG(dcol && dx, "col2im: null pointer");
+  SAT_CHECK_ARG(N >= 1 && H >= 1 && W >= 1 && C >= 4 && C % 4 == 0 && k >= 1 && stride >= 1 &&
+                    pad >= 0 && H + 2 * pad >= k && W + 2 * pad >= k,
+                "col2im: bad sizes (C must be a positive multiple of 4)");
+  const int Ho = conv_hw(H, k, stride, pad), Wo = conv_hw(W, k, stride, pad);
+  SAT_HIP(launch_col2im(dcol, (long)k * k * C, dx, N, H, W, C, k, stride, pad, Ho, Wo, accumulate,
+                        S(stream)));
+  return SAT_OK;
+}
+
+extern "C" sat_status sat_op_batchnorm_fwd(const float* x, int64_t P, int32_t C, const float* g,
+                                           const float* b, float eps, int32_t relu, float* part,
+                                           float* mean, float* rstd, void* y, float* yf,
+                                           void* stream) {
+  SAT_CHECK_ARG(x && g && b && part && mean && rstd && (y || yf), "batchnorm_fwd: null pointer");
+  SAT_CHECK_ARG(P >= 1 && C >= 4 && C % 4 == 0 && eps > 0.f, "batchnorm_fwd: bad sizes");
+  SAT_HIP(launch_bn_stats(x, P, C, eps, part, mean, rstd, S(stream)));
+  SAT_HIP(launch_bn_apply(x, P, C, mean, rstd, g, b, relu, (bf16*)y, yf, S(stream)));
+  return SAT_OK;
+}
+
+extern "C" sat_status sat_op_batchnorm_bwd(const float* dy, int32_t mask_kind, const void* mask,
+                                           const float* x, const float* mean, const float* rstd,
+                                           const float* g, int64_t P, int32_t C, float* part,
+                                           float* dg, float* db, void* dx, void* stream) {
+  SAT_CHECK_ARG(dy && x && mean && rstd && g && part && dg && db && dx, "batchnorm_bwd: null pointer");
+  SAT_CHECK_ARG(mask_kind >= 0 && mask_kind <= 2 && (mask_kind == 0 || mask != nullptr),
+                "batchnorm_bwd: mask_kind must be 0 (none), 1 (bf16) or 2 (fp32) with a mask");
+  SAT_CHECK_ARG(P >= 1 && C >= 4 && C % 4 == 0, "batchnorm_bwd: bad sizes");
+  SAT_HIP(launch_bn_bwd(dy, mask_kind, mask, x, mean, rstd, g, P, C, part, dg, db, (bf16*)dx,
+                        S(stream)));
+  return SAT_OK;
+}
+
+extern "C" sat_status sat_op_maxpool_fwd(const float* x, int32_t N, int32_t H, int32_t W, int32_t C,
+                                         float* y, void* yb, uint8_t* arg, void* stream) {
+  SAT_CHECK_ARG(x && y && yb && arg, "maxpool_fwd: null pointer");
+  SAT_CHECK_ARG(N >= 1 && H >= 2 && W >= 2 && C >= 1, "maxpool_fwd: bad sizes");
+  SAT_HIP(launch_maxpool_fwd(x, N, H, W, C, conv_hw(H, 3, 2, 1), conv_hw(W, 3, 2, 1), y, (bf16*)yb,
+                             arg, S(stream)));
+  return SAT_OK;
+}
+
+extern "C" sat_status sat_op_maxpool_bwd(const float* dy, const uint8_t* arg, int32_t N, int32_t H,
+                                         int32_t W, int32_t C, float* dx, void* stream) {
+  SAT_CHECK_ARG(dy && arg && dx, "maxpool_bwd: null pointer");
+  SAT_CHECK_ARG(N >= 1 && H >= 2 && W >= 2 && C >= 1, "maxpool_bwd: bad sizes");
+  SAT_HIP(launch_maxpool_bwd(dy, arg, N, H, W, C, conv_hw(H, 3, 2, 1), conv_hw(W, 3, 2, 1), dx,
+                             S(stream)));
+  return SAT_OK;
+}

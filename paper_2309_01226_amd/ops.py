@@ -160,3 +160,80 @@ def transpose_bf16(src, dst, rows, cols, *, lds=None, ldd=None):
     _need(dst, torch.bfloat16, "dst")
     _lib.call("sat_op_transpose_bf16", _p(src), lds or cols, _p(dst), ldd or rows, rows, cols,
               _stream())
+
+
+# ---------------------------------------------------------------- ResNet kernels
+
+def _hw(H, k, stride, pad):
+    return (H + 2 * pad - k) // stride + 1
+
+
+def im2col(x, N, H, W, C, k, stride, pad):
+    """x bf16 [N*H*W, C] -> col bf16 [N*Ho*Wo, k*k*C]."""
+    _need(x, torch.bfloat16, "x")
+    Ho, Wo = _hw(H, k, stride, pad), _hw(W, k, stride, pad)
+    if x.numel() < N * H * W * C:
+        raise ValueError("im2col: x too small")
+    col = torch.empty(N * Ho * Wo, k * k * C, device=x.device, dtype=torch.bfloat16)
+    _lib.call("sat_op_im2col", _p(x), _p(col), N, H, W, C, k, stride, pad, _stream())
+    return col
+
+
+def col2im(dcol, N, H, W, C, k, stride, pad, dx=None):
+    """dcol fp32 [N*Ho*Wo, k*k*C] -> dx fp32 [N*H*W, C] (accumulated into dx when given)."""
+    _need(dcol, torch.float32, "dcol")
+    Ho, Wo = _hw(H, k, stride, pad), _hw(W, k, stride, pad)
+    if dcol.numel() < N * Ho * Wo * k * k * C:
+        raise ValueError("col2im: dcol too small")
+    acc = dx is not None
+    if dx is None:
+        dx = torch.empty(N * H * W, C, device=dcol.device, dtype=torch.float32)
+    _lib.call("sat_op_col2im", _p(dcol), _p(dx), N, H, W, C, k, stride, pad, int(acc), _stream())
+    return dx
+
+
+def batchnorm_fwd(x, g, b, eps, relu=False):
+    """Training-mode batch norm of x fp32 [P, C]: (y bf16, yf fp32, mean, rstd)."""
+    _need(x, torch.float32, "x")
+    P, Cc = x.shape
+    part = torch.empty(2 * 1024 * Cc, device=x.device, dtype=torch.float32)
+    mean = torch.empty(Cc, device=x.device, dtype=torch.float32)
+    rstd = torch.empty_like(mean)
+    y = torch.empty(P, Cc, device=x.device, dtype=torch.bfloat16)
+    yf = torch.empty(P, Cc, device=x.device, dtype=torch.float32)
+    _lib.call("sat_op_batchnorm_fwd", _p(x), P, Cc, _p(g), _p(b), C.c_float(eps), int(relu), _p(part),
+              _p(mean), _p(rstd), _p(y), _p(yf), _stream())
+    return y, yf, mean, rstd
+
+
+def batchnorm_bwd(dy, x, mean, rstd, g, mask=None):
+    """Backward of batchnorm_fwd (through a ReLU whose output is `mask`, bf16 or
+    fp32, when given): (dx bf16, dg, db)."""
+    _need(dy, torch.float32, "dy")
+    P, Cc = dy.shape
+    kind = 0 if mask is None else (1 if mask.dtype == torch.bfloat16 else 2)
+    part = torch.empty(2 * 1024 * Cc, device=dy.device, dtype=torch.float32)
+    dg = torch.empty(Cc, device=dy.device, dtype=torch.float32)
+    db = torch.empty_like(dg)
+    dx = torch.empty(P, Cc, device=dy.device, dtype=torch.bfloat16)
+    _lib.call("sat_op_batchnorm_bwd", _p(dy), kind, _p(mask), _p(x), _p(mean), _p(rstd), _p(g), P, Cc,
+              _p(part), _p(dg), _p(db), _p(dx), _stream())
+    return dx, dg, db
+
+
+def maxpool_fwd(x, N, H, W, C):
+    """3 x 3 / 2 max pool (padding 1) of x fp32 [N*H*W, C]: (y fp32, y bf16, arg uint8)."""
+    _need(x, torch.float32, "x")
+    Ho, Wo = _hw(H, 3, 2, 1), _hw(W, 3, 2, 1)
+    y = torch.empty(N * Ho * Wo, C, device=x.device, dtype=torch.float32)
+    yb = torch.empty(N * Ho * Wo, C, device=x.device, dtype=torch.bfloat16)
+    arg = torch.empty(N * Ho * Wo, C, device=x.device, dtype=torch.uint8)
+    _lib.call("sat_op_maxpool_fwd", _p(x), N, H, W, C, _p(y), _p(yb), _p(arg), _stream())
+    return y, yb, arg
+
+
+def maxpool_bwd(dy, arg, N, H, W, C):
+    _need(dy, torch.float32, "dy")
+    dx = torch.empty(N * H * W, C, device=dy.device, dtype=torch.float32)
+    _lib.call("sat_op_maxpool_bwd", _p(dy), _p(arg), N, H, W, C, _p(dx), _stream())
+    return dx
