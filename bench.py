@@ -63,6 +63,9 @@ WORKLOADS = {
     "gpt2m": "GPT-2-medium-shaped fine-tuning step: 24 layers, d_model 1024, 16 heads, MLP 4096, "
              "vocab 50257, seq 512, batch 8",
     "tiny": "tiny GPT-2-style decoder: 2 layers, d_model 64, 4 heads, MLP 256, vocab 512, seq 32, batch 2",
+    "resnet": "ResNet (200M) fine-tuning step: bottleneck ResNet-152 depth (3, 8, 36, 3) at twice the width "
+              "(stem 128, 236 M parameters), batch norm in training mode, 224x224x3 images, 1000 classes, "
+              "batch 64, AdamW on all params",
     "grid": "model-selection grid: 8 GPT-2-medium-shaped decoders (24 layers, d_model 1024, 16 heads, "
             "MLP 4096, vocab 50257, seq 512), lr {1e-5,3e-5,1e-4,3e-4} x batch {8,16}, bottom 12 blocks "
             "frozen where (lr index + batch index) is odd, one HIP stream each, one shared seed",
@@ -94,10 +97,71 @@ def step_flops(kw):
     return f
 
 
+def _resnet_cfg(kw, **over):
+    from oracle import resnet as OR
+    c = dict(blocks=tuple(kw["res_blocks"]), width=kw["res_width"], classes=kw["vocab"],
+             img_size=kw["img_size"], channels=kw.get("channels", 3), batch=kw["batch"],
+             frozen_layers=kw.get("frozen_layers", 0), lr=kw["lr"])
+    c.update(over)
+    return OR.ResNetConfig(**c)
+
+
 def n_params(kw):
+    import numpy as np
+    if kw["arch"] == "resnet":
+        from oracle import resnet as OR
+        return sum(int(np.prod(s)) for _, s, _ in OR.param_spec(_resnet_cfg(kw)))
     import oracle
     cfg = oracle.Config(**{k: v for k, v in kw.items() if k in oracle.Config.__dataclass_fields__})
-    return sum(int(__import__("numpy").prod(s)) for _, s, _ in oracle.param_spec(cfg))
+    return sum(int(np.prod(s)) for _, s, _ in oracle.param_spec(cfg))
+
+
+def cpu_baseline_resnet(kw, seed):
+    """Oracle fwd+bwd of one image through one block per stage at the full
+    width (the stem, every stage's projection block and the head), and AdamW
+    over that sample's tensors; scaled to the full step by algorithmic FLOPs
+    (forward + backward) and by parameter count (AdamW)."""
+    import numpy as np
+
+    from oracle import resnet as OR
+    from paper_2309_01226_amd.inputs import batch_for
+    cpu_model, blas, threads = _cpu_info()
+    scfg = _resnet_cfg(kw, blocks=(1, 1, 1, 1), batch=1)
+    full = _resnet_cfg(kw)
+    rng = np.random.default_rng(seed)
+    P = OR.init_params(scfg, rng)
+    x, y = batch_for(dict(kw, batch=1), seed=seed, step=0)
+    t0 = time.perf_counter()
+    _, cache = OR.forward(scfg, P, x, y)
+    G = OR.backward(scfg, P, cache)
+    t_fb = time.perf_counter() - t0
+    del cache
+    t0 = time.perf_counter()
+    for n in G:
+        z = np.zeros_like(P[n])
+        OR.adamw_update(scfg, P[n], G[n], z, z, 1)
+    t_opt = time.perf_counter() - t0
+    p_s = sum(P[n].size for n in G)
+    f_s, f_full = OR.step_flops(scfg), OR.step_flops(full)
+    p_full = n_params(kw)
+    est = t_fb * f_full / f_s + t_opt * p_full / p_s
+    return {
+        "value": kw["batch"] / est,
+        "unit": "images/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"float64 numpy oracle, one 224x224 image through one block per stage at the full width "
+                   f"plus stem and head: fwd+bwd {t_fb:.2f} s scaled by FLOPs x{f_full / f_s:.1f} "
+                   f"(extrapolated to {full.n_blocks} blocks and batch {kw['batch']}); AdamW over the "
+                   f"sample's {p_s / 1e6:.0f} M params {t_opt:.2f} s scaled by params x{p_full / p_s:.1f}; "
+                   f"estimated full step {est:.1f} s"),
+        "sample_seconds": round(t_fb + t_opt, 2),
+        "extrapolated": True,
+        "cpu_model": cpu_model,
+        "blas": blas,
+        "blas_threads": threads,
+        "host_cpus": os.cpu_count(),
+    }
 
 
 def _cpu_info():
@@ -208,7 +272,7 @@ def bandwidth_summary(diag, sep_ms, sep_bytes, n_trainable):
     may partly hit the 256 MB Infinity Cache, as they do in the step."""
     out = {}
     for name in ("ln_fwd", "ln_bwd", "xent"):
-        ms, n, nbytes = diag[name]
+        ms, n, nbytes = diag.get(name, (0.0, 0, 0.0))
         if n and ms > 0:
             gbs = nbytes / (ms * 1e-3) / 1e9
             out[name] = {"launches": n, "us_per_launch": ms / n * 1e3, "bytes_per_launch": nbytes / n,
@@ -403,7 +467,9 @@ def main():
     if args.separate_adamw:
         m.set_option("fused_adamw", 0)
     n_all, n_train, flops = m.stats()
-    assert abs(flops - step_flops(kw)) <= 1e-9 * flops, (flops, step_flops(kw))
+    resnet = kw["arch"] == "resnet"
+    if not resnet:
+        assert abs(flops - step_flops(kw)) <= 1e-9 * flops, (flops, step_flops(kw))
     K, W = args.steps, args.warmup
     batches = [device_batch(kw, seed=args.seed, step=t) for t in range(W + K)]
     tokens = m.rows() if kw["arch"] != "vit" else m.rows()
@@ -411,7 +477,10 @@ def main():
         m.train_step(*batches[t], sync=False)
     torch.cuda.synchronize()
     per_step = kw["n_layers"] - kw.get("frozen_layers", 0)
-    m.set_timing(TIMING["qkv_wgrad_gemm"], per_step * K + 8)
+    # the dominant kernel class: the fused QKV (+ fc1) weight-gradient product
+    # with its AdamW epilogue; for the ResNet, the 3x3 convolution forward products
+    dominant = "qkv_fwd_gemm" if resnet else "qkv_wgrad_gemm"
+    m.set_timing(TIMING[dominant], (kw["n_layers"] if resnet else per_step) * K + 8)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -430,7 +499,9 @@ def main():
     # over all parameters is the optimizer's bandwidth kernel, and the GEMM
     # time without the fused epilogues gives the optimizer's share of the step
     diag = {}
-    for name in ("qkv_fwd_gemm", "adamw", "all_gemm", "attn_fwd", "attn_bwd", "ln_fwd", "ln_bwd", "xent"):
+    diag_kinds = ("adamw", "all_gemm", "xent") if resnet else \
+        ("qkv_fwd_gemm", "adamw", "all_gemm", "attn_fwd", "attn_bwd", "ln_fwd", "ln_bwd", "xent")
+    for name in diag_kinds:
         m.set_timing(TIMING[name], 4096)
         m.train_step(*batches[0], sync=False)
         diag[name] = m.timing_read()
@@ -452,9 +523,10 @@ def main():
     # what the fused epilogues add to the GEMMs
     opt_ms = adamw_ms + max(diag["all_gemm"][0] - diag["all_gemm_separate"][0], 0.0)
     out = {
-        "metric": METRIC,
+        "metric": ("training images/sec + % bf16 MFMA peak, ResNet (200M) step, 1 MI355X" if resnet
+                   else METRIC),
         "value": tokens * K / dt,
-        "unit": "tokens/s",
+        "unit": "images/s" if resnet else "tokens/s",
         "n_gpus": 1,
         "steps": K,
         "warmup": W,
@@ -469,7 +541,7 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": WORKLOADS[args.config], "name": args.config,
-                   "global_batch": kw["batch"], "seq_len": m.rows() // kw["batch"],
+                   "global_batch": kw["batch"], "seq_len": 1 if resnet else m.rows() // kw["batch"],
                    "tokens_per_step": tokens, "params": n_all, "trainable_params": n_train,
                    "frozen_layers": kw.get("frozen_layers", 0), "checkpoint": kw.get("checkpoint", 0),
                    "arena_gb": m.nbytes / 1e9},
@@ -490,15 +562,25 @@ def main():
                      "ms_without_fused_optimizer": diag["all_gemm_separate"][0],
                      "tflops_without_fused_optimizer":
                          diag["all_gemm_separate"][2] / (diag["all_gemm_separate"][0] * 1e-3) / 1e12},
-        "attention": {"fwd_ms": diag["attn_fwd"][0], "bwd_ms": diag["attn_bwd"][0],
-                      "fwd_tflops": diag["attn_fwd"][2] / max(diag["attn_fwd"][0], 1e-9) / 1e9,
-                      "bwd_tflops": diag["attn_bwd"][2] / max(diag["attn_bwd"][0], 1e-9) / 1e9},
         "bandwidth_kernels": bandwidth_summary(diag, sep_ms, sep_bytes, n_train),
         "loss_after": loss,
         "paper_context": PAPER_CONTEXT,
     }
-    ncols = 3 * kw["d_model"] + kw["d_mlp"] if kw["arch"] == "gptj" else 3 * kw["d_model"]
-    if w_n:
+    if not resnet:
+        out["attention"] = {"fwd_ms": diag["attn_fwd"][0], "bwd_ms": diag["attn_bwd"][0],
+                            "fwd_tflops": diag["attn_fwd"][2] / max(diag["attn_fwd"][0], 1e-9) / 1e9,
+                            "bwd_tflops": diag["attn_bwd"][2] / max(diag["attn_bwd"][0], 1e-9) / 1e9}
+    ncols = 3 * kw.get("d_model", 0) + kw.get("d_mlp", 0) if kw["arch"] == "gptj" else 3 * kw.get("d_model", 0)
+    if w_n and resnet:
+        achieved = w_fl / w_n / (w_ms / w_n * 1e-3) / 1e12
+        out["roofline"] = {
+            "kernel": "3x3 convolution forward products (im2col operand x weight, fp32 out), "
+                      "mean over the 50 per step",
+            "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+            "launches": w_n, "avg_ms": w_ms / w_n, "flop_per_launch": w_fl / w_n,
+        }
+    elif w_n:
         fused = not args.separate_adamw
         achieved = w_fl / w_n / (w_ms / w_n * 1e-3) / 1e12
         opt_bytes = 28.0 * ncols * kw["d_model"] if fused else 0.0
@@ -520,7 +602,7 @@ def main():
             "note": "dominant kernel by time per step; serial bound = FLOPs at the MFMA peak plus the "
                     "fused AdamW bytes at the 8 TB/s HBM peak",
         }
-    q_ms, q_n, q_fl = diag["qkv_fwd_gemm"]
+    q_ms, q_n, q_fl = diag["qkv_fwd_gemm"] if "qkv_fwd_gemm" in diag else (0.0, 0, 0.0)
     if q_n:
         achieved = q_fl / q_n / (q_ms / q_n * 1e-3) / 1e12
         out["roofline_qkv_fwd"] = {
@@ -532,7 +614,7 @@ def main():
             "launches": q_n, "avg_ms": q_ms / q_n, "flop_per_launch": q_fl / q_n,
         }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(kw, args.seed)
+        out["cpu_baseline"] = cpu_baseline_resnet(kw, args.seed) if resnet else cpu_baseline(kw, args.seed)
     m.close()
     print(json.dumps(out), flush=True)
 

@@ -165,16 +165,45 @@ __global__ void bn_stats_partial_kernel(const float* __restrict__ x, long P, int
   }
 }
 
-__global__ void bn_stats_final_kernel(const float* __restrict__ x, const float* __restrict__ part,
-                                      int nb, long P, int C, float eps, float* __restrict__ mean,
-                                      float* __restrict__ rstd) {
-  const int c = blockIdx.x * NT + threadIdx.x;
-  if (c >= C) return;
-  double s1 = 0.0, s2 = 0.0;
-  for (int b = 0; b < nb; ++b) {
-    s1 += part[(long)b * C + c];
-    s2 += part[((long)nb + b) * C + c];
+// The final reductions over the nb partial rows: a workgroup of FL_T
+// threads owns FL_C consecutive columns; lane group l (of FL_L) sums rows
+// l, l + FL_L, ..., then the lane groups are added in order.
+constexpr int FL_C = 64, FL_L = 16, FL_T = FL_C * FL_L;
+
+template <typename T>
+__device__ void final_sums(const float* __restrict__ part, int nb, int C, T& s1, T& s2) {
+  __shared__ T r1[FL_T], r2[FL_T];
+  const int t = threadIdx.x, cl = t % FL_C, l = t / FL_C;
+  const int c = blockIdx.x * FL_C + cl;
+  T a = 0, b2 = 0;
+  if (c < C) {
+#pragma unroll 4
+    for (int b = l; b < nb; b += FL_L) {
+      a += (T)part[(long)b * C + c];
+      b2 += (T)part[((long)nb + b) * C + c];
+    }
   }
+  r1[t] = a;
+  r2[t] = b2;
+  __syncthreads();
+  s1 = 0;
+  s2 = 0;
+  if (l == 0)
+    for (int k = 0; k < FL_L; ++k) {
+      s1 += r1[k * FL_C + cl];
+      s2 += r2[k * FL_C + cl];
+    }
+}
+
+__global__ __launch_bounds__(FL_T) void bn_stats_final_kernel(const float* __restrict__ x,
+                                                              const float* __restrict__ part, int nb,
+                                                              long P, int C, float eps,
+                                                              float* __restrict__ mean,
+                                                              float* __restrict__ rstd) {
+  double s1, s2;
+  final_sums<double>(part, nb, C, s1, s2);
+  const int c = blockIdx.x * FL_C + threadIdx.x % FL_C;
+  if (threadIdx.x >= FL_C || c >= C) return;
   const double m1 = s1 / (double)P;
   double var = s2 / (double)P - m1 * m1;
   if (var < 0.0) var = 0.0;
@@ -267,15 +296,13 @@ __global__ void bn_bwd_partial_kernel(const float* __restrict__ dy, const void* 
 }
 
 // dbeta = sum g, dgamma = sum g xhat (written to the gradient arena).
-__global__ void bn_bwd_final_kernel(const float* __restrict__ part, int nb, int C,
-                                    float* __restrict__ dg, float* __restrict__ db) {
-  const int c = blockIdx.x * NT + threadIdx.x;
-  if (c >= C) return;
-  float s1 = 0.f, s2 = 0.f;
-  for (int b = 0; b < nb; ++b) {
-    s1 += part[(long)b * C + c];
-    s2 += part[((long)nb + b) * C + c];
-  }
+__global__ __launch_bounds__(FL_T) void bn_bwd_final_kernel(const float* __restrict__ part, int nb,
+                                                            int C, float* __restrict__ dg,
+                                                            float* __restrict__ db) {
+  float s1, s2;
+  final_sums<float>(part, nb, C, s1, s2);
+  const int c = blockIdx.x * FL_C + threadIdx.x % FL_C;
+  if (threadIdx.x >= FL_C || c >= C) return;
   db[c] = s1;
   dg[c] = s2;
 }
@@ -485,8 +512,8 @@ hipError_t launch_bn_stats(const float* x, long P, int C, float eps, float* part
   const long rpb = (P + nb - 1) / nb;
   hipLaunchKernelGGL(bn_stats_partial_kernel, dim3(nb, (C + NT - 1) / NT), dim3(NT), 0, st, x, P,
                      C, rpb, part);
-  hipLaunchKernelGGL(bn_stats_final_kernel, dim3((C + NT - 1) / NT), dim3(NT), 0, st, x, part, nb,
-                     P, C, eps, mean, rstd);
+  hipLaunchKernelGGL(bn_stats_final_kernel, dim3((C + FL_C - 1) / FL_C), dim3(FL_T), 0, st, x, part,
+                     nb, P, C, eps, mean, rstd);
   return hipGetLastError();
 }
 
@@ -527,8 +554,8 @@ hipError_t launch_bn_bwd(const float* dy, int mask_kind, const void* mask, const
   else
     hipLaunchKernelGGL(bn_bwd_partial_kernel<2>, g2, dim3(NT), 0, st, dy, mask, x, mean, rstd, P, C,
                        rpb, part);
-  hipLaunchKernelGGL(bn_bwd_final_kernel, dim3((C + NT - 1) / NT), dim3(NT), 0, st, part, nb, C, dg,
-                     db);
+  hipLaunchKernelGGL(bn_bwd_final_kernel, dim3((C + FL_C - 1) / FL_C), dim3(FL_T), 0, st, part, nb, C,
+                     dg, db);
   const long n4 = P * C / 4;
   const float inv_p = (float)(1.0 / (double)P);
   const dim3 g1(grid_for(n4));

@@ -348,7 +348,7 @@ void sat_resnet_carve(sat_model* M, SatCarver& c) {
   auto wneed = [&](int Mr, int Nc, long K) {
     ws = std::max(ws, gemm_splitk_ws_elems(Mr, Nc, (int)K, kSplitMax));
   };
-  wneed(R.width, 49 * R.C, R.Ps);
+  wneed(R.width, R.stem_kp, R.Ps);
   for (const RBlock& b : R.blocks) {
     wneed(b.mid, b.cin, b.Pin);
     wneed(b.mid, 9 * b.mid, b.Pout);
@@ -575,6 +575,10 @@ sat_status sat_resnet_backward(sat_model* M, const void* inputs) {
                         R.Ps, R.width, R.part, grad(M, R.stem_n.g), grad(M, R.stem_n.g + 1), R.dc, s));
   SAT_HIP(launch_im2col_nchw((const float*)inputs, R.col, R.stem_kp, R.N, R.C, R.img, R.img, 7, 2, 3,
                              R.Hs, R.Hs, s));
-  TRY(rwgrad(M, R.dc, R.width, R.col, R.stem_kp, 49 * R.C, R.stem_kp, R.Ps, grad(M, R.stem_w)));
+  // over the zero-padded columns (whole 4-column output vectors, so the
+  // product splits K), then the 7 x 7 x C columns into the gradient arena
+  TRY(rwgrad(M, R.dc, R.width, R.col, R.stem_kp, R.stem_kp, R.stem_kp, R.Ps, R.dsub));
+  SAT_HIP(hipMemcpy2DAsync(grad(M, R.stem_w), (size_t)49 * R.C * 4, R.dsub, (size_t)R.stem_kp * 4,
+                           (size_t)49 * R.C * 4, R.width, hipMemcpyDeviceToDevice, s));
   return SAT_OK;
 }
