@@ -90,14 +90,19 @@ sat_status sat_op_layernorm_bwd(const float* dy, int64_t lddy, const float* x, i
 
 /* Flash-style attention forward.  q, k, v, o: bf16, element (b, h, s, j) at
  * ptr[(b*S + s)*ld + h*dh + j].  lse: fp32 [B, H, S] natural-log
- * log-sum-exp of the scaled scores.  scale multiplies q.k. */
+ * log-sum-exp of the scaled scores.  scale multiplies q.k.  dh is one of 16,
+ * 32, 64, 80, 128, 256; for 64, 80 and 256, q, k, v must be 16-byte aligned
+ * with ld % 8 == 0, o 8-byte aligned with ldo % 4 == 0 and scale > 0
+ * (SAT_EINVAL otherwise). */
 sat_status sat_op_attention_fwd(const void* q, const void* k, const void* v, int64_t ldq,
                                 int64_t ldk, int64_t ldv, void* o, int64_t ldo, float* lse,
                                 int32_t B, int32_t H, int32_t S, int32_t dh, int32_t causal,
                                 float scale, void* stream);
 /* Attention backward from dO (bf16, addressed like o), the forward's o and
  * lse; writes dq, dk, dv (bf16, addressed like q, k, v).  delta: fp32
- * [B, H, S] scratch. */
+ * [B, H, S] scratch.  Head dims and alignment as for the forward; for 64, 80
+ * and 256, o and dout must also be 16-byte aligned with ld % 8 == 0 and dq,
+ * dk, dv 8-byte aligned with ld % 4 == 0. */
 sat_status sat_op_attention_bwd(const void* q, const void* k, const void* v, int64_t ldq,
                                 int64_t ldk, int64_t ldv, const void* o, int64_t ldo,
                                 const float* lse, const void* dout, int64_t lddo, float* delta,

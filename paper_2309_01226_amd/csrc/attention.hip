@@ -16,8 +16,11 @@
 //
 // Backward without atomics: one kernel accumulates dK and dV per key block
 // over all query blocks, a second accumulates dQ per query block over all key
-// blocks (the score and dP tiles are recomputed in both).  Large head dims are
-// split into output slices so the accumulators fit in registers.
+// blocks (the score and dP tiles are recomputed in both).
+//
+// This file serves head dims 16, 32 (first-generation kernels, whose output
+// may be split into head-dim slices) and 128 (the pipelined *_fast kernels);
+// head dims 64 and 80 run in attn_small.hip and 256 in attn256.hip.
 #include "common.h"
 #include "kernels.h"
 
@@ -885,79 +888,19 @@ __device__ __forceinline__ void kv_block(const bf16* __restrict__ cur, bf16* __r
   }
 }
 
-// Paired variant for large head dims: the two waves of a pair own the same
-// 32 keys; role 0 holds K, forms P and accumulates dV^T, role 1 holds V,
-// forms dP, takes P from its partner through LDS and accumulates dK^T.  Each
-// wave then needs one row operand and one accumulator set, and no product is
-// computed twice.
 template <int DH>
-__device__ __forceinline__ void kv_pair_block(const bf16* __restrict__ cur, bf16* __restrict__ nxt,
-                                              float* __restrict__ xw, bool copy_next,
-                                              __amdgpu_buffer_rsrc_t rsQ, __amdgpu_buffer_rsrc_t rsO,
-                                              long ldq, long ldo, int nvalid_next,
-                                              const bf16x8 (&rf)[DH / 16], floatx16 (&acc)[DH / 32],
-                                              int qs0, int key, int S, int causal, float sc, bool active,
-                                              int role, int wave, int lane) {
-  using SG = KVStage<DH>;
-  using TT = typename SG::TT;
-  using RT = typename SG::RT;
-  if (copy_next) {
-    RT::copy(rsQ, ldq, nvalid_next, nxt, wave);
-    RT::copy(rsO, ldo, nvalid_next, nxt + SG::RQ, wave);
-  }
-  const int g = lane >> 5, row = lane & 31;
-  const float* ls = SG::lse(cur);
-  floatx16 x = zero16();
-  if (active) {
-    const bf16* rs = SG::rows(cur, role);  // Q rows (role 0) or dO rows (role 1)
-#pragma unroll
-    for (int c = 0; c < DH / 16; ++c)
-      x = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(rs + RT::off(row, 2 * c + g)),
-                                                  rf[c], x, 0, 0, 0);
-    if (role == 0) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int qi = acc_row(r, g);
-        const int qq = qs0 + qi;
-        const bool ok = qq < S && key < S && !(causal && key > qq);
-        const float pr = ok ? exp2f(x[r] * sc - ls[qi]) : 0.f;
-        x[r] = pr;
-        xw[r * 64 + lane] = pr;
-      }
-    }
-  }
-  wait_lgkm0();
-  cta_barrier();
-  if (!active) return;
-  if (role == 1) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) x[r] = xw[r * 64 + lane] * (x[r] - ls[BQB + acc_row(r, g)]);
-  }
-  const bf16* T = SG::trans(cur, 1 - role);  // dO^T (role 0) or Q^T (role 1)
-#pragma unroll
-  for (int hh = 0; hh < 2; ++hh) {
-    const bf16x8 xb = acc_to_bf16(x, hh);
-#pragma unroll
-    for (int ot = 0; ot < DH / 32; ++ot)
-      acc[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(TT::read_perm(T, ot * 32 + row, hh * 16, g), xb, acc[ot],
-                                                        0, 0, 0);
-  }
-}
-
-template <int DH, bool PAIR>
 __global__ __launch_bounds__(NT) void attn_bwd_dkdv_fast(AttnBwdArgs a) {
   using SG = KVStage<DH>;
   using RT = typename SG::RT;
   using TR = KVTrans<DH, NT>;
-  constexpr int KPW = PAIR ? WG_ROWS / 2 : WG_ROWS;  // keys per workgroup
-  constexpr int XB = PAIR ? 2 * 16 * 64 * 2 : 0;     // P exchange (fp32) of two pairs, bf16 units
-  __shared__ __attribute__((aligned(1024))) bf16 smem[2 * SG::SIZE + XB];
+  constexpr int KPW = WG_ROWS;  // keys per workgroup
+  __shared__ __attribute__((aligned(1024))) bf16 smem[2 * SG::SIZE];
   const int S = a.f.S;
   const int bh = blockIdx.y, b = bh / a.f.H, h = bh % a.f.H;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 5;
-  const int grp = PAIR ? (wave >> 1) : wave, role = PAIR ? (wave & 1) : 0;
+  const int grp = wave;
   const int k0 = blockIdx.x * KPW;
   const int kmin = k0 + grp * WROWS;
   const int key = kmin + (lane & 31);
@@ -969,15 +912,11 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_fast(AttnBwdArgs a) {
   const float* lse_g = a.f.lse + hs;
   const float* dlt_g = a.delta + hs;
 
-  constexpr int NACC = PAIR ? 1 : 2;
+  constexpr int NACC = 2;  // acc[0] = dK^T, acc[1] = dV^T
   bf16x8 rf[NACC][DH / 16];
   floatx16 acc[NACC][DH / 32];
-  if (PAIR) {
-    load_row_operand<DH>(role ? Vb : Kb, role ? a.f.ldv : a.f.ldk, key, S, g, rf[0]);
-  } else {
-    load_row_operand<DH>(Kb, a.f.ldk, key, S, g, rf[0]);
-    load_row_operand<DH>(Vb, a.f.ldv, key, S, g, rf[NACC - 1]);
-  }
+  load_row_operand<DH>(Kb, a.f.ldk, key, S, g, rf[0]);
+  load_row_operand<DH>(Vb, a.f.ldv, key, S, g, rf[1]);
 #pragma unroll
   for (int i = 0; i < NACC; ++i)
 #pragma unroll
@@ -1009,13 +948,8 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_fast(AttnBwdArgs a) {
     const bool active = !(a.f.causal && qs0 + BQB - 1 < kmin);
     const auto rq = rows_rsrc(Qb, qs0 + BQB, a.f.ldq);
     const auto ro = rows_rsrc(dOb, qs0 + BQB, a.lddo);
-    if constexpr (PAIR)
-      kv_pair_block<DH>(cur, nxt, reinterpret_cast<float*>(smem + 2 * SG::SIZE) + grp * 16 * 64, next, rq, ro,
-                        a.f.ldq, a.lddo, S - qs0 - BQB, rf[0], acc[0], qs0, key, S, a.f.causal, sc, active,
-                        role, wave, lane);
-    else
-      kv_block<DH>(cur, nxt, next, rq, ro, a.f.ldq, a.lddo, S - qs0 - BQB, rf[0], rf[NACC - 1], acc[0],
-                   acc[NACC - 1], qs0, key, S, a.f.causal, sc, active, wave, lane);
+    kv_block<DH>(cur, nxt, next, rq, ro, a.f.ldq, a.lddo, S - qs0 - BQB, rf[0], rf[1], acc[0], acc[1], qs0,
+                 key, S, a.f.causal, sc, active, wave, lane);
     if (next) {
       tr.store(nxt);
       if (j + 2 < nqb)
@@ -1028,10 +962,9 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_fast(AttnBwdArgs a) {
   if (key < S) {
     bf16* ok_ = a.dk + ((long)b * S + key) * a.lddk + (long)h * DH;
     bf16* ov = a.dv + ((long)b * S + key) * a.lddv + (long)h * DH;
-    // PAIR: role 0 holds dV^T, role 1 dK^T; otherwise acc[0] = dK^T, acc[1] = dV^T
 #pragma unroll
     for (int i = 0; i < NACC; ++i) {
-      const bool is_k = PAIR ? role == 1 : i == 0;
+      const bool is_k = i == 0;
       bf16* o = is_k ? ok_ : ov;
       const float f = is_k ? a.f.scale : 1.f;
 #pragma unroll
@@ -1194,20 +1127,25 @@ __global__ __launch_bounds__(NT) void attn_bwd_dq_fast(AttnBwdArgs a) {
   }
 }
 
+// Tile shape of the first-generation kernels (head dims 16 and 32: one output
+// slice of the whole head).
 template <int DH>
 struct AttnCfg {
-  static constexpr int BKV = (DH >= 256) ? 32 : 64;
-  static constexpr int DHS = (DH > 128) ? 128 : round32(DH);
-  static constexpr int NSLICE = (round32(DH) + DHS - 1) / DHS;
-  static constexpr int BQ = (DH >= 256) ? 32 : 64;
+  static constexpr int BKV = 64;
+  static constexpr int DHS = round32(DH);
+  static constexpr int NSLICE = 1;
+  static constexpr int BQ = 64;
 };
 
+// Head dims 16 and 32: the first-generation kernels; 128: the pipelined
+// ones.  64, 80 and 256 run only in their own files' kernels (attn_small.hip,
+// attn256.hip), which the callers below pick first.
 template <int DH>
 hipError_t fwd_launch(const AttnArgs& a, hipStream_t s) {
+  static_assert(DH == 16 || DH == 32 || DH == 128, "head dim served by attn_small / attn256");
   dim3 grid((a.S + WG_ROWS - 1) / WG_ROWS, a.B * a.H);
-  if (DH == 64 || DH == 128 || DH == 256)
-    hipLaunchKernelGGL((attn_fwd_fast<(DH == 64 || DH == 128 || DH == 256) ? DH : 64>), grid,
-                       dim3(NT), 0, s, a);
+  if (DH == 128)
+    hipLaunchKernelGGL((attn_fwd_fast<128>), grid, dim3(NT), 0, s, a);
   else
     hipLaunchKernelGGL((attn_fwd_kernel<DH, AttnCfg<DH>::BKV>), grid, dim3(NT), 0, s, a);
   return hipGetLastError();
@@ -1215,26 +1153,19 @@ hipError_t fwd_launch(const AttnArgs& a, hipStream_t s) {
 
 template <int DH>
 hipError_t bwd_launch(const AttnBwdArgs& a, hipStream_t s) {
+  static_assert(DH == 16 || DH == 32 || DH == 128, "head dim served by attn_small / attn256");
   using C = AttnCfg<DH>;
-  if ((DH == 64 || DH == 80) && attn_small_bwd_eligible(a)) return launch_attn_small_bwd(a, s);
-  if (DH == 256 && attn256_bwd_eligible(a)) {  // dQ (which also writes delta), then dK / dV
-    hipError_t e = launch_attn256_bwd_dq(a, s);
-    return e != hipSuccess ? e : launch_attn256_bwd_dkdv(a, s);
-  }
   long rows = (long)a.f.B * a.f.S * a.f.H;
   hipLaunchKernelGGL(attn_delta_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (DH == 64 || DH == 128 || DH == 256) {
-    constexpr int D = (DH == 64 || DH == 128 || DH == 256) ? DH : 64;
-    constexpr bool PAIR = D == 256;
-    constexpr int KPW = PAIR ? WG_ROWS / 2 : WG_ROWS;
-    dim3 gkv((a.f.S + KPW - 1) / KPW, a.f.B * a.f.H);
-    hipLaunchKernelGGL((attn_bwd_dkdv_fast<D, PAIR>), gkv, dim3(NT), 0, s, a);
+  if (DH == 128) {
+    dim3 gkv((a.f.S + WG_ROWS - 1) / WG_ROWS, a.f.B * a.f.H);
+    hipLaunchKernelGGL((attn_bwd_dkdv_fast<128>), gkv, dim3(NT), 0, s, a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     dim3 gq((a.f.S + WG_ROWS - 1) / WG_ROWS, a.f.B * a.f.H);
-    hipLaunchKernelGGL((attn_bwd_dq_fast<D>), gq, dim3(NT), 0, s, a);
+    hipLaunchKernelGGL((attn_bwd_dq_fast<128>), gq, dim3(NT), 0, s, a);
     return hipGetLastError();
   }
   dim3 grid((a.f.S + WG_ROWS - 1) / WG_ROWS, a.f.B * a.f.H, C::NSLICE);
@@ -1254,15 +1185,13 @@ bool ok16(const void* p, long ld) {
 hipError_t launch_attention_fwd(const AttnArgs& a, hipStream_t s) {
   if (a.B * a.H * a.S == 0) return hipSuccess;
   if (!ok16(a.q, a.ldq) || !ok16(a.k, a.ldk) || !ok16(a.v, a.ldv)) return hipErrorInvalidValue;
-  if (attn256_fwd_eligible(a)) return launch_attn256_fwd(a, s);
-  if (attn_small_fwd_eligible(a)) return launch_attn_small_fwd(a, s);
   switch (a.dh) {
     case 16: return fwd_launch<16>(a, s);
     case 32: return fwd_launch<32>(a, s);
-    case 64: return fwd_launch<64>(a, s);
-    case 80: return fwd_launch<80>(a, s);
     case 128: return fwd_launch<128>(a, s);
-    case 256: return fwd_launch<256>(a, s);
+    case 64:
+    case 80: return attn_small_fwd_eligible(a) ? launch_attn_small_fwd(a, s) : hipErrorInvalidValue;
+    case 256: return attn256_fwd_eligible(a) ? launch_attn256_fwd(a, s) : hipErrorInvalidValue;
   }
   return hipErrorInvalidValue;
 }
@@ -1275,10 +1204,15 @@ hipError_t launch_attention_bwd(const AttnBwdArgs& a, hipStream_t s) {
   switch (a.f.dh) {
     case 16: return bwd_launch<16>(a, s);
     case 32: return bwd_launch<32>(a, s);
-    case 64: return bwd_launch<64>(a, s);
-    case 80: return bwd_launch<80>(a, s);
     case 128: return bwd_launch<128>(a, s);
-    case 256: return bwd_launch<256>(a, s);
+    case 64:
+    case 80: return attn_small_bwd_eligible(a) ? launch_attn_small_bwd(a, s) : hipErrorInvalidValue;
+    case 256:
+      if (!attn256_bwd_eligible(a)) return hipErrorInvalidValue;
+      {  // dQ (which also writes delta), then dK / dV
+        hipError_t e = launch_attn256_bwd_dq(a, s);
+        return e != hipSuccess ? e : launch_attn256_bwd_dkdv(a, s);
+      }
   }
   return hipErrorInvalidValue;
 }

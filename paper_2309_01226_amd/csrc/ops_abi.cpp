@@ -175,6 +175,10 @@ extern "C" sat_status sat_op_attention_fwd(const void* q, const void* k, const v
   a.ldq = ldq; a.ldk = ldk; a.ldv = ldv;
   a.o = (bf16*)o; a.ldo = ldo; a.lse = lse;
   a.B = B; a.H = H; a.S = Sq; a.dh = dh; a.causal = causal; a.scale = scale;
+  SAT_CHECK_ARG(!(dh == 64 || dh == 80 || dh == 256) ||
+                    (dh == 256 ? attn256_fwd_eligible(a) : attn_small_fwd_eligible(a)),
+                "attention_fwd: head dim %d needs 16-byte aligned q, k, v, an 8-byte aligned o "
+                "with ldo %% 4 == 0 and scale > 0", dh);
   SAT_HIP(launch_attention_fwd(a, S(stream)));
   return SAT_OK;
 }
@@ -200,6 +204,11 @@ extern "C" sat_status sat_op_attention_bwd(const void* q, const void* k, const v
   a.dout = (const bf16*)dout; a.lddo = lddo; a.delta = delta;
   a.dq = (bf16*)dq; a.dk = (bf16*)dk; a.dv = (bf16*)dv;
   a.lddq = lddq; a.lddk = lddk; a.lddv = lddv;
+  SAT_CHECK_ARG(!(dh == 64 || dh == 80 || dh == 256) ||
+                    (dh == 256 ? attn256_bwd_eligible(a) : attn_small_bwd_eligible(a)),
+                "attention_bwd: head dim %d needs 16-byte aligned q, k, v, o, dout with leading "
+                "dimensions %% 8 == 0, 8-byte aligned dq, dk, dv with leading dimensions %% 4 == 0 "
+                "and scale > 0", dh);
   SAT_HIP(launch_attention_bwd(a, S(stream)));
   return SAT_OK;
 }

@@ -123,6 +123,17 @@ def test_op_argument_checks_make_no_launch():
     assert L.sat_op_attention_fwd(C.c_void_p(16), C.c_void_p(16), C.c_void_p(16), 8, 8, 8,
                                   C.c_void_p(16), 8, C.c_void_p(16), 1, 1, 4, 48, 1,
                                   C.c_float(1.0), None) == -1  # head dim 48 unsupported
+    # head dims 64, 80, 256: q must be 16-byte aligned (here 2 bytes off)
+    for dh in (64, 80, 256):
+        assert L.sat_op_attention_fwd(C.c_void_p(18), C.c_void_p(16), C.c_void_p(16), 3 * dh, 3 * dh,
+                                      3 * dh, C.c_void_p(16), dh, C.c_void_p(16), 1, 1, 4, dh, 1,
+                                      C.c_float(1.0), None) == -1, dh
+        assert "aligned" in B.last_error()
+        p = [C.c_void_p(16)] * 3
+        assert L.sat_op_attention_bwd(C.c_void_p(18), *p[:2], 3 * dh, 3 * dh, 3 * dh, p[0], dh, p[0],
+                                      p[0], dh, p[0], p[0], p[0], p[0], dh, dh, dh, 1, 1, 4, dh, 1,
+                                      C.c_float(1.0), None) == -1, dh
+        assert "aligned" in B.last_error()
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):
