@@ -188,9 +188,22 @@ sat_status sat_model_stats(const sat_model* m, int64_t* n_params, int64_t* n_tra
  *   AdamW pass after the backward.
  * SAT_OPT_KEEP_GRADS (default 0): 1 also writes the gradients of those
  *   weights to the gradient arena, so that sat_grad_read returns them.
+ * SAT_OPT_OVERLAP_WGRAD (default 1): the blocks' weight-gradient products
+ *   (with the AdamW steps fused into them) run on a second stream that the
+ *   library creates with the model, beside the input-gradient chain of the
+ *   blocks below; they read token-contiguous copies of their operands in two
+ *   alternating sets, and the step joins that stream back into the model's
+ *   stream before the backward ends, so a caller that synchronizes the
+ *   model's stream sees the whole step.  Results are bitwise those with 0
+ *   (the same kernels on the same operands).  Needs batch * seq_len % 8 == 0
+ *   (otherwise ignored).
  * value is 0 or 1; the setting applies from the next train step.
  * Errors: SAT_EINVAL (null model, unknown option or value), SAT_ESTATE. */
-typedef enum { SAT_OPT_FUSED_ADAMW = 1, SAT_OPT_KEEP_GRADS = 2 } sat_option;
+typedef enum {
+  SAT_OPT_FUSED_ADAMW = 1,
+  SAT_OPT_KEEP_GRADS = 2,
+  SAT_OPT_OVERLAP_WGRAD = 3
+} sat_option;
 sat_status sat_model_set_option(sat_model* m, int32_t option, int32_t value);
 
 /* ---- measurement ---------------------------------------------------------

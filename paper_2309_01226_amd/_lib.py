@@ -16,7 +16,7 @@ SAT_OK, SAT_EINVAL, SAT_ENOMEM, SAT_EHIP, SAT_ESTATE, SAT_ENONFINITE, SAT_ENOTSU
 STATUS_NAMES = {0: "SAT_OK", -1: "SAT_EINVAL", -2: "SAT_ENOMEM", -3: "SAT_EHIP", -4: "SAT_ESTATE",
                 -5: "SAT_ENONFINITE", -6: "SAT_ENOTSUP"}
 ARCH = {"gpt2": 0, "gptj": 1, "vit": 2, "resnet": 3}
-OPTIONS = {"fused_adamw": 1, "keep_grads": 2}
+OPTIONS = {"fused_adamw": 1, "keep_grads": 2, "overlap_wgrad": 3}
 GEMM_NOALLOC_WS_ELEMS = 8 * 1024 * 1024   # SAT_GEMM_NOALLOC_WS_ELEMS in saturn_ops.h
 
 

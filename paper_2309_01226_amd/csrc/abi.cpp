@@ -63,6 +63,34 @@ extern "C" sat_status sat_model_arena_bytes(const sat_config* cfg, size_t* bytes
   return SAT_OK;
 }
 
+// The weight-gradient stream (default priority) and its events.
+static void side_destroy(sat_model* m) {
+  if (m->side) {
+    hipStreamSynchronize(m->side);
+    hipStreamDestroy(m->side);
+    m->side = nullptr;
+  }
+  for (hipEvent_t* e : {&m->ev_fork, &m->ev_done[0], &m->ev_done[1], &m->ev_join})
+    if (*e) {
+      hipEventDestroy(*e);
+      *e = nullptr;
+    }
+}
+
+static bool side_create(sat_model* m) {
+  hipError_t e = hipStreamCreateWithFlags(&m->side, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_fork, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_done[0], hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_done[1], hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_join, hipEventDisableTiming);
+  if (e != hipSuccess) {
+    sat_set_error("creating the weight-gradient stream failed: %s", hipGetErrorString(e));
+    side_destroy(m);
+    return false;
+  }
+  return true;
+}
+
 extern "C" sat_status sat_model_create(const sat_config* cfg, void* arena, size_t arena_bytes,
                                        void* hip_stream, sat_model** out) {
   sat_status st = sat_validate_config(cfg);
@@ -86,14 +114,20 @@ extern "C" sat_status sat_model_create(const sat_config* cfg, void* arena, size_
   m->timing_used = 0;
   m->opt_fused = true;
   m->opt_keep_grads = false;
+  m->opt_overlap = true;
   m->last_step_fused = false;
   m->last_step_kept = false;
   hipGetDevice(&m->device);
+  if (!side_create(m)) {
+    delete m;
+    return SAT_EHIP;
+  }
   size_t need = sat_model_layout(m, nullptr);
   if (arena == nullptr) {
     hipError_t e = hipMalloc(&m->arena, need);
     if (e != hipSuccess) {
       sat_set_error("hipMalloc(%zu) failed: %s", need, hipGetErrorString(e));
+      side_destroy(m);
       delete m;
       return SAT_ENOMEM;
     }
@@ -103,11 +137,13 @@ extern "C" sat_status sat_model_create(const sat_config* cfg, void* arena, size_
     if (arena_bytes < need) {
       sat_set_error("arena of %zu bytes is smaller than the %zu bytes this model needs",
                     arena_bytes, need);
+      side_destroy(m);
       delete m;
       return SAT_ENOMEM;
     }
     if (reinterpret_cast<uintptr_t>(arena) & 255) {
       sat_set_error("arena must be 256-byte aligned");
+      side_destroy(m);
       delete m;
       return SAT_EINVAL;
     }
@@ -120,6 +156,7 @@ extern "C" sat_status sat_model_create(const sat_config* cfg, void* arena, size_
   if (st == SAT_OK) st = sync(m);
   if (st != SAT_OK) {
     if (m->own_arena) hipFree(m->arena);
+    side_destroy(m);
     delete m;
     return st;
   }
@@ -130,6 +167,7 @@ extern "C" sat_status sat_model_create(const sat_config* cfg, void* arena, size_
 extern "C" sat_status sat_model_destroy(sat_model* m) {
   if (m == nullptr) return SAT_OK;
   hipStreamSynchronize(m->stream);
+  side_destroy(m);
   for (auto& r : m->timing) {
     hipEventDestroy(r.e0);
     hipEventDestroy(r.e1);
@@ -248,6 +286,7 @@ extern "C" sat_status sat_model_set_option(sat_model* m, int32_t option, int32_t
   switch (option) {
     case SAT_OPT_FUSED_ADAMW: m->opt_fused = value != 0; return SAT_OK;
     case SAT_OPT_KEEP_GRADS: m->opt_keep_grads = value != 0; return SAT_OK;
+    case SAT_OPT_OVERLAP_WGRAD: m->opt_overlap = value != 0; return SAT_OK;
   }
   sat_set_error("unknown option %d", option);
   return SAT_EINVAL;

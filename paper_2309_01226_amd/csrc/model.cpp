@@ -385,6 +385,24 @@ size_t carve(sat_model* M, char* base) {
     M->tA = na > 0 ? c.take<bf16>(na) : nullptr;
     M->tB = nb > 0 ? c.take<bf16>(nb) : nullptr;
   }
+  // operands of the blocks' weight-gradient products on the side stream (two
+  // sets), and that stream's split-K workspace
+  for (int i = 0; i < 2; ++i) {
+    WgradSet& W = M->wset[i];
+    memset(&W, 0, sizeof W);
+    if (!M->trans_blocks) continue;
+    W.dy1 = c.take<bf16>(T * d);
+    W.g = c.take<bf16>(T * m);
+    W.o = c.take<bf16>(T * d);
+    W.a = c.take<bf16>(T * d);
+    W.qkv = c.take<bf16>(T * D.qkv_ld);
+    if (!gptj) {
+      W.dy2 = c.take<bf16>(T * d);
+      W.c = c.take<bf16>(T * d);
+      W.du = c.take<bf16>(T * m);
+    }
+  }
+  M->splitk_ws2 = M->splitk_ws_elems > 0 ? c.take<float>((size_t)M->splitk_ws_elems) : nullptr;
   M->delta = c.take<float>((size_t)D.B * D.H * D.S);
   M->rope_cs = D.rd > 0 ? c.take<float2>((size_t)D.S * (D.rd / 2)) : nullptr;
   M->n_part = (int)(T < 256 ? T : 256);

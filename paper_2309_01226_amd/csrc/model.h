@@ -79,10 +79,32 @@ struct TimingRec {
   double flops;
 };
 
+// Token-contiguous copies of the operands of one block's weight-gradient
+// products, read by those products on the weight-gradient stream (two sets,
+// used by alternate blocks).  dy1: dY of fc2 (and of the out-projection in
+// the parallel GPT-J block); dy2: dY of the out-projection in the sequential
+// block (the residual gradient after the second LayerNorm's backward);
+// g, o, a, c: inputs of fc2, out-projection, QKV, fc1; du: dY of fc1; qkv: dY
+// of the QKV (GPT-J: QKV + fc1) product.
+struct WgradSet {
+  bf16 *dy1, *dy2, *g, *o, *a, *c, *du, *qkv;
+};
+
 struct sat_model {
   sat_config cfg;
   Dims D;
   hipStream_t stream;
+  // Weight-gradient stream: with opt_overlap the block's weight-gradient
+  // products (and the AdamW steps fused into them) run here, beside the
+  // input-gradient chain of the blocks below.  Created with the model.
+  hipStream_t side;
+  hipEvent_t ev_fork;     // model stream -> side: the operands are ready
+  hipEvent_t ev_done[2];  // side -> model stream: set i may be rewritten
+  hipEvent_t ev_join;     // side -> model stream: every product done
+  bool side_pending[2];
+  bool opt_overlap;
+  WgradSet wset[2];
+  float* splitk_ws2;      // split-K workspace of the side stream
   int device;
   char* arena;
   size_t arena_bytes;

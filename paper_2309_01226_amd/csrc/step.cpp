@@ -229,6 +229,31 @@ sat_status sat_run_forward(sat_model* M, const void* inputs, const int32_t* labe
 // pidx: the weight's parameter index.  When its AdamW step is fused, the
 // product's epilogue applies the step to the weight (and writes the gradient
 // only if the model keeps gradients).
+// The product on token-contiguous operands yT [Mr, T] and xT [N, T], on
+// stream st (the model's, or the weight-gradient stream).
+static sat_status wgrad_t(sat_model* M, hipStream_t st, const bf16* yT, const bf16* xT, int Mr,
+                          int N, int T, int pidx, int tk = TK_ALL_GEMM) {
+  const ParamDesc& P = M->params[pidx];
+  GemmArgs w = gargs(yT, T, xT, T, Mr, N, T, grad(M, pidx), P.cols);
+  if (M->opt_fused && P.fused_opt) {
+    if (!M->opt_keep_grads) w.out = nullptr;
+    w.opt_p = M->master + P.off;
+    w.opt_m = M->mom + P.off;
+    w.opt_v = M->vel + P.off;
+    w.opt_sh = M->shadow + P.off;
+    w.opt_sht = M->shadow_t + P.toff;
+    w.opt_trows = P.trows;
+    w.opt_c = M->adamw_c;
+    if (!gemm256_eligible(w, LAY_K, LAY_K, EPI_ADAMW)) {
+      sat_set_error("internal: fused optimizer step of %s not eligible for the 256 x 256 kernel",
+                    P.name.c_str());
+      return SAT_EINVAL;
+    }
+    return gemm(M, w, LAY_K, LAY_K, EPI_ADAMW, tk, st);
+  }
+  return gemm(M, w, LAY_K, LAY_K, EPI_F32, tk, st);
+}
+
 static sat_status wgrad(sat_model* M, bool trans, bool y_ready, const bf16* Y, long ldy,
                         int ycols, const bf16* X, long ldx, int Mr, int N, int T, int pidx,
                         int tk = TK_ALL_GEMM) {
@@ -238,27 +263,37 @@ static sat_status wgrad(sat_model* M, bool trans, bool y_ready, const bf16* Y, l
   if (trans) {
     if (!y_ready) SAT_HIP(launch_transpose_bf16(Y, ldy, M->tA, T, T, ycols, M->stream));
     SAT_HIP(launch_transpose_bf16(X, ldx, M->tB, T, T, N, M->stream));
-    GemmArgs w = gargs(M->tA, T, M->tB, T, Mr, N, T, out, ldo);
-    if (M->opt_fused && P.fused_opt) {
-      if (!M->opt_keep_grads) w.out = nullptr;
-      w.opt_p = M->master + P.off;
-      w.opt_m = M->mom + P.off;
-      w.opt_v = M->vel + P.off;
-      w.opt_sh = M->shadow + P.off;
-      w.opt_sht = M->shadow_t + P.toff;
-      w.opt_trows = P.trows;
-      w.opt_c = M->adamw_c;
-      if (!gemm256_eligible(w, LAY_K, LAY_K, EPI_ADAMW)) {
-        sat_set_error("internal: fused optimizer step of %s not eligible for the 256 x 256 kernel",
-                      P.name.c_str());
-        return SAT_EINVAL;
-      }
-      return gemm(M, w, LAY_K, LAY_K, EPI_ADAMW, tk);
-    }
-    return gemm(M, w, LAY_K, LAY_K, EPI_F32, tk);
+    return wgrad_t(M, M->stream, M->tA, M->tB, Mr, N, T, pidx, tk);
   }
   GemmArgs w = gargs(Y, ldy, X, ldx, Mr, N, T, out, ldo);
   return gemm(M, w, LAY_MN, LAY_MN, EPI_F32, tk);
+}
+
+// Weight-gradient stream.  fork: what the model's stream has enqueued so far
+// (the operand copies) precedes what the side stream enqueues next.  reuse:
+// before the model's stream rewrites operand set i, the products that read it
+// are done.  done: marks the end of the products of set i.  join: the model's
+// stream waits for everything on the side stream.
+static sat_status side_fork(sat_model* M) {
+  SAT_HIP(hipEventRecord(M->ev_fork, M->stream));
+  SAT_HIP(hipStreamWaitEvent(M->side, M->ev_fork, 0));
+  return SAT_OK;
+}
+static sat_status side_reuse(sat_model* M, int i) {
+  if (M->side_pending[i]) SAT_HIP(hipStreamWaitEvent(M->stream, M->ev_done[i], 0));
+  M->side_pending[i] = false;
+  return SAT_OK;
+}
+static sat_status side_done(sat_model* M, int i) {
+  SAT_HIP(hipEventRecord(M->ev_done[i], M->side));
+  M->side_pending[i] = true;
+  return SAT_OK;
+}
+static sat_status side_join(sat_model* M) {
+  SAT_HIP(hipEventRecord(M->ev_join, M->side));
+  SAT_HIP(hipStreamWaitEvent(M->stream, M->ev_join, 0));
+  M->side_pending[0] = M->side_pending[1] = false;
+  return SAT_OK;
 }
 
 // LayerNorm backward into the residual gradient dh, which it also rounds into
@@ -321,7 +356,14 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
   }
 
   // ---- blocks L-1 .. k
+  // With the weight-gradient stream, block l's operand copies go to set l % 2
+  // on the model's stream and its weight-gradient products run on the side
+  // stream; every input-gradient product of a weight is enqueued before the
+  // fork that releases the weight's (AdamW-fused) weight-gradient product.
+  const bool ov = M->opt_overlap && M->trans_blocks && M->side != nullptr;
   for (int l = D.L - 1; l >= D.k; --l) {
+    if (ov) TRY(side_reuse(M, l & 1));
+    WgradSet& W = M->wset[l & 1];
     if (D.ckpt) TRY(block_forward(M, l, true));
     const LayerActs& A = sat_layer_acts(M, l);
     const int pb = block_base(M, l);
@@ -361,8 +403,17 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
       TRY(gemm(M, du, LAY_K, LAY_K, EPI_DGELU_BF16));
       GemmArgs go = gargs(M->dh_bf, d, shadow_t(M, pb + J_PROJW), d, T, d, d, M->dout, d);
       TRY(gemm(M, go, LAY_K, LAY_K, EPI_BF16));
-      TRY(wgrad(M, tr, false, M->dh_bf, d, d, A.g, m, d, m, T, pb + J_FC2W));
-      TRY(wgrad(M, tr, true, M->dh_bf, d, d, A.o, d, d, d, T, pb + J_PROJW));
+      if (ov) {
+        SAT_HIP(launch_transpose_bf16(M->dh_bf, d, W.dy1, T, T, d, s));
+        SAT_HIP(launch_transpose_bf16(A.g, m, W.g, T, T, m, s));
+        SAT_HIP(launch_transpose_bf16(A.o, d, W.o, T, T, d, s));
+        TRY(side_fork(M));
+        TRY(wgrad_t(M, M->side, W.dy1, W.g, d, m, T, pb + J_FC2W));
+        TRY(wgrad_t(M, M->side, W.dy1, W.o, d, d, T, pb + J_PROJW));
+      } else {
+        TRY(wgrad(M, tr, false, M->dh_bf, d, d, A.g, m, d, m, T, pb + J_FC2W));
+        TRY(wgrad(M, tr, true, M->dh_bf, d, d, A.o, d, d, d, T, pb + J_PROJW));
+      }
       {
         Timed tm(M, TK_ATTN_BWD, attn_bwd_flops);
         SAT_HIP(launch_attention_bwd(ab, s));
@@ -371,8 +422,16 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
       GemmArgs ga = gargs(M->dqkv, D.qkv_ld, shadow_t(M, pb + J_QKVW), D.qkv_ld, T, d, D.qkv_ld,
                           M->dA, d);
       TRY(gemm(M, ga, LAY_K, LAY_K, EPI_F32));
-      TRY(wgrad(M, tr, false, M->dqkv, D.qkv_ld, D.qkv_ld, A.a, d, D.qkv_ld, d, T, pb + J_QKVW,
-                TK_QKV_WGRAD));
+      if (ov) {
+        SAT_HIP(launch_transpose_bf16(M->dqkv, D.qkv_ld, W.qkv, T, T, D.qkv_ld, s));
+        SAT_HIP(launch_transpose_bf16(A.a, d, W.a, T, T, d, s));
+        TRY(side_fork(M));
+        TRY(wgrad_t(M, M->side, W.qkv, W.a, D.qkv_ld, d, T, pb + J_QKVW, TK_QKV_WGRAD));
+        TRY(side_done(M, l & 1));
+      } else {
+        TRY(wgrad(M, tr, false, M->dqkv, D.qkv_ld, D.qkv_ld, A.a, d, D.qkv_ld, d, T, pb + J_QKVW,
+                  TK_QKV_WGRAD));
+      }
       SAT_HIP(launch_colsum_bf16(M->dqkv + 3 * d, D.qkv_ld, T, m, M->part, npT,
                                  grad(M, pb + J_FC1B), s));
       TRY(ln_bwd(M, M->dA, M->h_in[l], 1, pb + J_LN1G, A.mean1, A.rstd1, T));
@@ -386,26 +445,53 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
       TRY(gemm(M, du, LAY_K, LAY_K, EPI_DGELU_BF16));
       GemmArgs gc = gargs(M->du, m, shadow_t(M, pb + B_FC1W), m, T, d, m, M->dA, d);
       TRY(gemm(M, gc, LAY_K, LAY_K, EPI_F32));
-      TRY(wgrad(M, tr, false, M->dh_bf, d, d, A.g, m, d, m, T, pb + B_FC2W));
-      TRY(wgrad(M, tr, false, M->du, m, m, A.c, d, m, d, T, pb + B_FC1W));
+      if (ov) {
+        SAT_HIP(launch_transpose_bf16(M->dh_bf, d, W.dy1, T, T, d, s));
+        SAT_HIP(launch_transpose_bf16(A.g, m, W.g, T, T, m, s));
+        SAT_HIP(launch_transpose_bf16(M->du, m, W.du, T, T, m, s));
+        SAT_HIP(launch_transpose_bf16(A.c, d, W.c, T, T, d, s));
+        TRY(side_fork(M));
+        TRY(wgrad_t(M, M->side, W.dy1, W.g, d, m, T, pb + B_FC2W));
+        TRY(wgrad_t(M, M->side, W.du, W.c, m, d, T, pb + B_FC1W));
+      } else {
+        TRY(wgrad(M, tr, false, M->dh_bf, d, d, A.g, m, d, m, T, pb + B_FC2W));
+        TRY(wgrad(M, tr, false, M->du, m, m, A.c, d, m, d, T, pb + B_FC1W));
+      }
       SAT_HIP(launch_colsum_bf16(M->du, m, T, m, M->part, npT, grad(M, pb + B_FC1B), s));
       TRY(ln_bwd(M, M->dA, A.h_mid, 1, pb + B_LN2G, A.mean2, A.rstd2, T));
       SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + B_PROJB), s));
       GemmArgs go = gargs(M->dh_bf, d, shadow_t(M, pb + B_PROJW), d, T, d, d, M->dout, d);
       TRY(gemm(M, go, LAY_K, LAY_K, EPI_BF16));
-      TRY(wgrad(M, tr, false, M->dh_bf, d, d, A.o, d, d, d, T, pb + B_PROJW));
+      if (ov) {
+        SAT_HIP(launch_transpose_bf16(M->dh_bf, d, W.dy2, T, T, d, s));
+        SAT_HIP(launch_transpose_bf16(A.o, d, W.o, T, T, d, s));
+        TRY(side_fork(M));
+        TRY(wgrad_t(M, M->side, W.dy2, W.o, d, d, T, pb + B_PROJW));
+      } else {
+        TRY(wgrad(M, tr, false, M->dh_bf, d, d, A.o, d, d, d, T, pb + B_PROJW));
+      }
       {
         Timed tm(M, TK_ATTN_BWD, attn_bwd_flops);
         SAT_HIP(launch_attention_bwd(ab, s));
       }
       GemmArgs ga = gargs(M->dqkv, 3 * d, shadow_t(M, pb + B_QKVW), 3 * d, T, d, 3 * d, M->dA, d);
       TRY(gemm(M, ga, LAY_K, LAY_K, EPI_F32));
-      TRY(wgrad(M, tr, false, M->dqkv, 3 * d, 3 * d, A.a, d, 3 * d, d, T, pb + B_QKVW,
-                TK_QKV_WGRAD));
+      if (ov) {
+        SAT_HIP(launch_transpose_bf16(M->dqkv, 3 * d, W.qkv, T, T, 3 * d, s));
+        SAT_HIP(launch_transpose_bf16(A.a, d, W.a, T, T, d, s));
+        TRY(side_fork(M));
+        TRY(wgrad_t(M, M->side, W.qkv, W.a, 3 * d, d, T, pb + B_QKVW, TK_QKV_WGRAD));
+        TRY(side_done(M, l & 1));
+      } else {
+        TRY(wgrad(M, tr, false, M->dqkv, 3 * d, 3 * d, A.a, d, 3 * d, d, T, pb + B_QKVW,
+                  TK_QKV_WGRAD));
+      }
       SAT_HIP(launch_colsum_bf16(M->dqkv, 3 * d, T, 3 * d, M->part, npT, grad(M, pb + B_QKVB), s));
       TRY(ln_bwd(M, M->dA, M->h_in[l], 1, pb + B_LN1G, A.mean1, A.rstd1, T));
     }
   }
+
+  if (ov && D.k < D.L) TRY(side_join(M));
 
   // ---- embeddings (only when nothing is frozen)
   if (D.k == 0) {

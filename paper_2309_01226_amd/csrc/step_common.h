@@ -16,12 +16,15 @@ enum {
   TK_LN_FWD = 6, TK_LN_BWD = 7, TK_XENT = 8, TK_QKV_WGRAD = 9
 };
 
-// Records HIP events on the model's stream around the launches of one kernel
-// class (the model's timing kind) while in scope.
+// Records HIP events around the launches of one kernel class (the model's
+// timing kind) while in scope, on the stream those launches go to (default:
+// the model's stream).
 struct Timed {
   sat_model* M;
+  hipStream_t st;
   TimingRec* rec = nullptr;
-  Timed(sat_model* m, int kind, double work) : M(m) {
+  Timed(sat_model* m, int kind, double work, hipStream_t stream = nullptr)
+      : M(m), st(stream ? stream : m->stream) {
     if (m->timing_kind == TK_OFF) return;
     bool match = (m->timing_kind == kind) ||
                  (m->timing_kind == TK_ALL_GEMM &&
@@ -29,10 +32,10 @@ struct Timed {
     if (!match || m->timing_used >= m->timing.size()) return;
     rec = &m->timing[m->timing_used++];
     rec->flops = work;
-    hipEventRecord(rec->e0, m->stream);
+    hipEventRecord(rec->e0, st);
   }
   ~Timed() {
-    if (rec) hipEventRecord(rec->e1, M->stream);
+    if (rec) hipEventRecord(rec->e1, st);
   }
 };
 
@@ -54,14 +57,17 @@ inline GemmArgs gargs(const bf16* A, long lda, const bf16* B, long ldb, int Mr, 
 }
 
 // One GEMM launch; fp32-output products with too few tiles run split-K in
-// the model's workspace.
+// the workspace of the stream they go to (the model's stream, or the
+// weight-gradient stream with its own workspace).
 inline sat_status gemm(sat_model* M, const GemmArgs& a, int alay, int blay, int epi,
-                       int tk = TK_ALL_GEMM) {
-  Timed t(M, tk, 2.0 * a.M * a.N * (double)a.K);
+                       int tk = TK_ALL_GEMM, hipStream_t stream = nullptr) {
+  const bool side = stream != nullptr && stream == M->side;
+  hipStream_t st = stream ? stream : M->stream;
+  Timed t(M, tk, 2.0 * a.M * a.N * (double)a.K, st);
   GemmArgs b = a;
-  b.splitk_ws = M->splitk_ws;
+  b.splitk_ws = side ? M->splitk_ws2 : M->splitk_ws;
   b.splitk_ws_elems = M->splitk_ws_elems;
-  SAT_HIP(launch_gemm(b, alay, blay, epi, M->stream));
+  SAT_HIP(launch_gemm(b, alay, blay, epi, st));
   return SAT_OK;
 }
 

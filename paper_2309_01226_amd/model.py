@@ -181,7 +181,7 @@ class Model:
 
     # ---------------------------------------------------------------- timing
     def set_option(self, name, value):
-        """sat_model_set_option: "fused_adamw" or "keep_grads", value 0 / 1."""
+        """sat_model_set_option: "fused_adamw", "keep_grads" or "overlap_wgrad", value 0 / 1."""
         _lib.call("sat_model_set_option", self.h, _lib.OPTIONS[name], int(value))
 
     def set_timing(self, kind, max_launches=4096):
