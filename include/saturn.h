@@ -190,7 +190,8 @@ sat_status sat_model_stats(const sat_model* m, int64_t* n_params, int64_t* n_tra
  *   weights to the gradient arena, so that sat_grad_read returns them.
  * SAT_OPT_OVERLAP_WGRAD (default 1): the blocks' weight-gradient products
  *   (with the AdamW steps fused into them) run on a second stream that the
- *   library creates with the model, beside the input-gradient chain of the
+ *   library creates on the first such backward (default priority; destroyed
+ *   with the model), beside the input-gradient chain of the
  *   blocks below; they read token-contiguous copies of their operands in two
  *   alternating sets, and the step joins that stream back into the model's
  *   stream before the backward ends, so a caller that synchronizes the

@@ -63,8 +63,10 @@ extern "C" sat_status sat_model_arena_bytes(const sat_config* cfg, size_t* bytes
   return SAT_OK;
 }
 
-// The weight-gradient stream (default priority) and its events.
-static void side_destroy(sat_model* m) {
+// The weight-gradient stream (default priority) and its events, created on
+// the first backward that uses them (a model that never overlaps adds no
+// stream to the device's hardware queues).
+void sat_side_destroy(sat_model* m) {
   if (m->side) {
     hipStreamSynchronize(m->side);
     hipStreamDestroy(m->side);
@@ -77,7 +79,8 @@ static void side_destroy(sat_model* m) {
     }
 }
 
-static bool side_create(sat_model* m) {
+sat_status sat_side_ensure(sat_model* m) {
+  if (m->side) return SAT_OK;
   hipError_t e = hipStreamCreateWithFlags(&m->side, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_fork, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_done[0], hipEventDisableTiming);
@@ -85,10 +88,10 @@ static bool side_create(sat_model* m) {
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->ev_join, hipEventDisableTiming);
   if (e != hipSuccess) {
     sat_set_error("creating the weight-gradient stream failed: %s", hipGetErrorString(e));
-    side_destroy(m);
-    return false;
+    sat_side_destroy(m);
+    return SAT_EHIP;
   }
-  return true;
+  return SAT_OK;
 }
 
 extern "C" sat_status sat_model_create(const sat_config* cfg, void* arena, size_t arena_bytes,
@@ -118,16 +121,11 @@ extern "C" sat_status sat_model_create(const sat_config* cfg, void* arena, size_
   m->last_step_fused = false;
   m->last_step_kept = false;
   hipGetDevice(&m->device);
-  if (!side_create(m)) {
-    delete m;
-    return SAT_EHIP;
-  }
   size_t need = sat_model_layout(m, nullptr);
   if (arena == nullptr) {
     hipError_t e = hipMalloc(&m->arena, need);
     if (e != hipSuccess) {
       sat_set_error("hipMalloc(%zu) failed: %s", need, hipGetErrorString(e));
-      side_destroy(m);
       delete m;
       return SAT_ENOMEM;
     }
@@ -137,13 +135,11 @@ extern "C" sat_status sat_model_create(const sat_config* cfg, void* arena, size_
     if (arena_bytes < need) {
       sat_set_error("arena of %zu bytes is smaller than the %zu bytes this model needs",
                     arena_bytes, need);
-      side_destroy(m);
       delete m;
       return SAT_ENOMEM;
     }
     if (reinterpret_cast<uintptr_t>(arena) & 255) {
       sat_set_error("arena must be 256-byte aligned");
-      side_destroy(m);
       delete m;
       return SAT_EINVAL;
     }
@@ -156,7 +152,6 @@ extern "C" sat_status sat_model_create(const sat_config* cfg, void* arena, size_
   if (st == SAT_OK) st = sync(m);
   if (st != SAT_OK) {
     if (m->own_arena) hipFree(m->arena);
-    side_destroy(m);
     delete m;
     return st;
   }
@@ -167,7 +162,7 @@ extern "C" sat_status sat_model_create(const sat_config* cfg, void* arena, size_
 extern "C" sat_status sat_model_destroy(sat_model* m) {
   if (m == nullptr) return SAT_OK;
   hipStreamSynchronize(m->stream);
-  side_destroy(m);
+  sat_side_destroy(m);
   for (auto& r : m->timing) {
     hipEventDestroy(r.e0);
     hipEventDestroy(r.e1);

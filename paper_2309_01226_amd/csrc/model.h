@@ -96,7 +96,7 @@ struct sat_model {
   hipStream_t stream;
   // Weight-gradient stream: with opt_overlap the block's weight-gradient
   // products (and the AdamW steps fused into them) run here, beside the
-  // input-gradient chain of the blocks below.  Created with the model.
+  // input-gradient chain of the blocks below.  Created on first use.
   hipStream_t side;
   hipEvent_t ev_fork;     // model stream -> side: the operands are ready
   hipEvent_t ev_done[2];  // side -> model stream: set i may be rewritten
@@ -185,6 +185,10 @@ struct sat_model {
   std::vector<TimingRec> timing;
   size_t timing_used;
 };
+
+// The weight-gradient stream: created on first use, destroyed with the model.
+sat_status sat_side_ensure(sat_model* m);
+void sat_side_destroy(sat_model* m);
 
 sat_status sat_validate_config(const sat_config* c);
 void sat_model_dims(const sat_config& c, Dims* d);

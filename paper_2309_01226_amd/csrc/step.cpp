@@ -360,7 +360,8 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
   // on the model's stream and its weight-gradient products run on the side
   // stream; every input-gradient product of a weight is enqueued before the
   // fork that releases the weight's (AdamW-fused) weight-gradient product.
-  const bool ov = M->opt_overlap && M->trans_blocks && M->side != nullptr;
+  const bool ov = M->opt_overlap && M->trans_blocks && D.k < D.L;
+  if (ov) TRY(sat_side_ensure(M));
   for (int l = D.L - 1; l >= D.k; --l) {
     if (ov) TRY(side_reuse(M, l & 1));
     WgradSet& W = M->wset[l & 1];
@@ -491,7 +492,7 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
     }
   }
 
-  if (ov && D.k < D.L) TRY(side_join(M));
+  if (ov) TRY(side_join(M));
 
   // ---- embeddings (only when nothing is frozen)
   if (D.k == 0) {
