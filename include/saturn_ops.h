@@ -172,13 +172,15 @@ sat_status sat_op_col2im(const float* dcol, float* dx, int32_t N, int32_t H, int
 /* Batch norm in training mode over x [P, C] fp32 (statistics of the P rows,
  * biased variance): mean, rstd = 1 / sqrt(var + eps) [C]; y = (x - mean) rstd
  * g + b, with ReLU when relu, as bf16 (y, may be NULL) and fp32 (yf, may be
- * NULL, not both).  part: fp32 scratch of 2 * 1024 * C.  C % 4 == 0. */
+ * NULL, not both).  part: fp32 scratch of 2 * 1024 * C.  C % 4 == 0; every
+ * fp32 array 16-byte aligned, y 8-byte aligned (SAT_EINVAL otherwise). */
 sat_status sat_op_batchnorm_fwd(const float* x, int64_t P, int32_t C, const float* g,
                                 const float* b, float eps, int32_t relu, float* part, float* mean,
                                 float* rstd, void* y, float* yf, void* stream);
 /* Its backward from dy [P, C] fp32, through a ReLU when mask_kind is 1 (dy
  * where the bf16 mask > 0) or 2 (fp32 mask > 0): dg = sum g' xhat, db = sum
- * g' (written), dx = rstd g (g' - db / P - xhat dg / P) as bf16. */
+ * g' (written), dx = rstd g (g' - db / P - xhat dg / P) as bf16.  Alignment as
+ * for the forward (an fp32 mask 16-byte, a bf16 mask and dx 8-byte). */
 sat_status sat_op_batchnorm_bwd(const float* dy, int32_t mask_kind, const void* mask,
                                 const float* x, const float* mean, const float* rstd,
                                 const float* g, int64_t P, int32_t C, float* part, float* dg,

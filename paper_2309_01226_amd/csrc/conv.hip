@@ -112,56 +112,70 @@ __global__ void col2im4_kernel(const float* __restrict__ dcol, long ldc, float* 
 
 // ---------------------------------------------------------------- batch norm
 
-// Column slab of a [P, C] reduction: thread t of the workgroup owns column
-// c0 + t % CS of the slab and rows phase t / CS, CS = min(C - c0, 256) when
-// 256 % CS == 0 (all phases busy), else one phase.
-struct Slab {
-  int c, phase, phases, cs;
-  __device__ Slab(int C) {
-    const int c0 = blockIdx.y * NT;
-    cs = min(C - c0, NT);
-    phases = (NT % cs == 0) ? NT / cs : 1;
+// Column slab of a [P, C] reduction in groups of four columns (C % 4 == 0):
+// a slab is up to 4 NT columns; thread t owns columns c .. c + 3 with
+// c = c0 + 4 (t % cs4) and rows of phase t / cs4, cs4 = the slab's column
+// groups (at most NT), all NT / cs4 phases busy when cs4 divides NT, else one.
+struct Slab4 {
+  int c, phase, phases, cs4;
+  __device__ Slab4(int C) {
+    const int c0 = blockIdx.y * 4 * NT;
+    cs4 = min((C - c0) / 4, NT);
+    phases = (NT % cs4 == 0) ? NT / cs4 : 1;
     const int t = threadIdx.x;
-    phase = t / cs;
-    c = (phase < phases) ? c0 + t % cs : -1;
+    phase = t / cs4;
+    c = (phase < phases) ? c0 + 4 * (t % cs4) : -1;
   }
 };
 
-// Sum of v over the phases of each column, in phase order; the result is
-// valid in the threads of phase 0.
-__device__ float phase_sum(float v, const Slab& sl, float* red) {
+// Sum of v over the phases of each column group, in phase order; the result
+// is valid in the threads of phase 0.
+__device__ floatx4 phase_sum4(floatx4 v, const Slab4& sl, floatx4* red) {
   red[threadIdx.x] = v;
   __syncthreads();
-  float s = 0.f;
+  floatx4 s = {0.f, 0.f, 0.f, 0.f};
   if (sl.phase == 0 && sl.c >= 0)
-    for (int ph = 0; ph < sl.phases; ++ph) s += red[ph * sl.cs + threadIdx.x];
+    for (int ph = 0; ph < sl.phases; ++ph) s += red[ph * sl.cs4 + threadIdx.x];
   __syncthreads();
   return s;
 }
 
+constexpr int BN_U = 8;  // rows whose loads a thread has in flight together
+
 // Per-channel partial sums of (x - K_c) and (x - K_c)^2 over the rows of
 // workgroup x's block, with the shift K_c = x[0, c] (the shifted-data form of
 // the variance: no cancellation when the mean is large next to the spread).
+// Each thread adds its rows in increasing order.
 __global__ void bn_stats_partial_kernel(const float* __restrict__ x, long P, int C, long rpb,
                                         float* __restrict__ part) {
-  __shared__ float red[NT];
-  const Slab sl(C);
-  float s1 = 0.f, s2 = 0.f;
+  __shared__ floatx4 red[NT];
+  const Slab4 sl(C);
+  floatx4 s1 = {0.f, 0.f, 0.f, 0.f}, s2 = s1;
   if (sl.c >= 0) {
-    const float K = x[sl.c];
+    const floatx4 K = *reinterpret_cast<const floatx4*>(x + sl.c);
     const long r0 = (long)blockIdx.x * rpb;
     const long r1 = min(P, r0 + rpb);
-    for (long r = r0 + sl.phase; r < r1; r += sl.phases) {
-      const float d = x[r * C + sl.c] - K;
-      s1 += d;
-      s2 += d * d;
+    for (long rb = r0 + sl.phase; rb < r1; rb += (long)BN_U * sl.phases) {
+      floatx4 v[BN_U];
+#pragma unroll
+      for (int i = 0; i < BN_U; ++i) {
+        const long r = rb + (long)i * sl.phases;
+        if (r < r1) v[i] = *reinterpret_cast<const floatx4*>(x + r * C + sl.c);
+      }
+#pragma unroll
+      for (int i = 0; i < BN_U; ++i)
+        if (rb + (long)i * sl.phases < r1) {
+          const floatx4 d = v[i] - K;
+          s1 += d;
+          s2 += d * d;
+        }
     }
   }
-  s1 = phase_sum(s1, sl, red);
-  s2 = phase_sum(s2, sl, red);
+  s1 = phase_sum4(s1, sl, red);
+  s2 = phase_sum4(s2, sl, red);
   if (sl.phase == 0 && sl.c >= 0) {
-    part[(long)blockIdx.x * C + sl.c] = s1;
-    part[((long)gridDim.x + blockIdx.x) * C + sl.c] = s2;
+    *reinterpret_cast<floatx4*>(part + (long)blockIdx.x * C + sl.c) = s1;
+    *reinterpret_cast<floatx4*>(part + ((long)gridDim.x + blockIdx.x) * C + sl.c) = s2;
   }
 }
 
@@ -211,7 +225,23 @@ __global__ __launch_bounds__(FL_T) void bn_stats_final_kernel(const float* __res
   rstd[c] = (float)(1.0 / sqrt(var + (double)eps));
 }
 
+// Four consecutive per-channel values p[c .. c + 3] (c % 4 == 0): one
+// 16-byte load when the arrays are 16-byte aligned (V), else four.  The
+// elementwise kernels read up to ten such parameters per four elements, so
+// their instruction count, not their bytes, set their time with scalar loads.
+template <bool V>
+__device__ __forceinline__ floatx4 ld4(const float* __restrict__ p, int c) {
+  if constexpr (V) return *reinterpret_cast<const floatx4*>(p + c);
+  floatx4 r = {p[c], p[c + 1], p[c + 2], p[c + 3]};
+  return r;
+}
+
+__host__ __device__ inline bool a16(const void* p) {
+  return (reinterpret_cast<uintptr_t>(p) & 15) == 0;
+}
+
 // y = (x - mean) rstd g + b, ReLU when relu, as bf16 (when y) and fp32 (when yf).
+template <bool V>
 __global__ void bn_apply_kernel(const float* __restrict__ x, long n4, int C,
                                 const float* __restrict__ mean, const float* __restrict__ rstd,
                                 const float* __restrict__ g, const float* __restrict__ b, int relu,
@@ -219,10 +249,11 @@ __global__ void bn_apply_kernel(const float* __restrict__ x, long n4, int C,
   for (long t = (long)blockIdx.x * NT + threadIdx.x; t < n4; t += (long)gridDim.x * NT) {
     const int c = (int)((4 * t) % C);
     const floatx4 v = reinterpret_cast<const floatx4*>(x)[t];
+    const floatx4 m4 = ld4<V>(mean, c), r4 = ld4<V>(rstd, c), g4 = ld4<V>(g, c), b4 = ld4<V>(b, c);
     floatx4 o;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      float z = (v[e] - mean[c + e]) * rstd[c + e] * g[c + e] + b[c + e];
+      float z = (v[e] - m4[e]) * r4[e] * g4[e] + b4[e];
       o[e] = relu ? fmaxf(z, 0.f) : z;
     }
     if (y) {
@@ -234,6 +265,7 @@ __global__ void bn_apply_kernel(const float* __restrict__ x, long n4, int C,
 }
 
 // out = ReLU(BN_a(xa) + (xs2 ? BN_s(xs) : xs)), fp32 and bf16.
+template <bool V>
 __global__ void bn_add_relu_kernel(const float* __restrict__ xa, const float* __restrict__ ma,
                                    const float* __restrict__ ra, const float* __restrict__ ga,
                                    const float* __restrict__ ba, const float* __restrict__ xs,
@@ -245,12 +277,22 @@ __global__ void bn_add_relu_kernel(const float* __restrict__ xa, const float* __
     const int c = (int)((4 * t) % C);
     const floatx4 a = reinterpret_cast<const floatx4*>(xa)[t];
     const floatx4 sv = reinterpret_cast<const floatx4*>(xs)[t];
+    const floatx4 ma4 = ld4<V>(ma, c), ra4 = ld4<V>(ra, c), ga4 = ld4<V>(ga, c), ba4 = ld4<V>(ba, c);
     floatx4 o;
+    if (ms) {
+      const floatx4 ms4 = ld4<V>(ms, c), rs4 = ld4<V>(rs, c), gs4 = ld4<V>(gs, c), bs4 = ld4<V>(bs, c);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float za = (a[e] - ma[c + e]) * ra[c + e] * ga[c + e] + ba[c + e];
-      const float zs = ms ? (sv[e] - ms[c + e]) * rs[c + e] * gs[c + e] + bs[c + e] : sv[e];
-      o[e] = fmaxf(za + zs, 0.f);
+      for (int e = 0; e < 4; ++e) {
+        const float za = (a[e] - ma4[e]) * ra4[e] * ga4[e] + ba4[e];
+        const float zs = (sv[e] - ms4[e]) * rs4[e] * gs4[e] + bs4[e];
+        o[e] = fmaxf(za + zs, 0.f);
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float za = (a[e] - ma4[e]) * ra4[e] * ga4[e] + ba4[e];
+        o[e] = fmaxf(za + sv[e], 0.f);
+      }
     }
     reinterpret_cast<floatx4*>(out)[t] = o;
     bf16x4 ob = {f2bf(o[0]), f2bf(o[1]), f2bf(o[2]), f2bf(o[3])};
@@ -267,31 +309,64 @@ __device__ __forceinline__ float masked(float dy, const void* m, long i) {
   return dy;
 }
 
-// Per-channel partial sums of g and g * xhat, xhat = (x - mean) rstd.
+// The same for four consecutive elements 4 t .. 4 t + 3 (one vector load of
+// the mask when V, i.e. when the mask is aligned for it).
+template <int MASK, bool V>
+__device__ __forceinline__ floatx4 masked4(floatx4 dy, const void* m, long t) {
+  if constexpr (!V) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) dy[e] = masked<MASK>(dy[e], m, 4 * t + e);
+  } else if constexpr (MASK == 1) {
+    const bf16x4 a = reinterpret_cast<const bf16x4*>(m)[t];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) dy[e] = bf2f(a[e]) > 0.f ? dy[e] : 0.f;
+  } else if constexpr (MASK == 2) {
+    const floatx4 a = reinterpret_cast<const floatx4*>(m)[t];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) dy[e] = a[e] > 0.f ? dy[e] : 0.f;
+  }
+  return dy;
+}
+
+// Per-channel partial sums of g and g * xhat, xhat = (x - mean) rstd, each
+// thread over its rows in increasing order.
 template <int MASK>
 __global__ void bn_bwd_partial_kernel(const float* __restrict__ dy, const void* __restrict__ msk,
                                       const float* __restrict__ x, const float* __restrict__ mean,
                                       const float* __restrict__ rstd, long P, int C, long rpb,
                                       float* __restrict__ part) {
-  __shared__ float red[NT];
-  const Slab sl(C);
-  float s1 = 0.f, s2 = 0.f;
+  __shared__ floatx4 red[NT];
+  const Slab4 sl(C);
+  floatx4 s1 = {0.f, 0.f, 0.f, 0.f}, s2 = s1;
   if (sl.c >= 0) {
-    const float mu = mean[sl.c], rs = rstd[sl.c];
+    const floatx4 mu = *reinterpret_cast<const floatx4*>(mean + sl.c);
+    const floatx4 rs = *reinterpret_cast<const floatx4*>(rstd + sl.c);
     const long r0 = (long)blockIdx.x * rpb;
     const long r1 = min(P, r0 + rpb);
-    for (long r = r0 + sl.phase; r < r1; r += sl.phases) {
-      const long i = r * C + sl.c;
-      const float gv = masked<MASK>(dy[i], msk, i);
-      s1 += gv;
-      s2 += gv * (x[i] - mu) * rs;
+    for (long rb = r0 + sl.phase; rb < r1; rb += (long)BN_U * sl.phases) {
+      floatx4 gv[BN_U], xv[BN_U];
+#pragma unroll
+      for (int i = 0; i < BN_U; ++i) {
+        const long r = rb + (long)i * sl.phases;
+        if (r < r1) {
+          const long i4 = (r * C + sl.c) / 4;
+          gv[i] = masked4<MASK, true>(reinterpret_cast<const floatx4*>(dy)[i4], msk, i4);
+          xv[i] = reinterpret_cast<const floatx4*>(x)[i4];
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < BN_U; ++i)
+        if (rb + (long)i * sl.phases < r1) {
+          s1 += gv[i];
+          s2 += gv[i] * ((xv[i] - mu) * rs);
+        }
     }
   }
-  s1 = phase_sum(s1, sl, red);
-  s2 = phase_sum(s2, sl, red);
+  s1 = phase_sum4(s1, sl, red);
+  s2 = phase_sum4(s2, sl, red);
   if (sl.phase == 0 && sl.c >= 0) {
-    part[(long)blockIdx.x * C + sl.c] = s1;
-    part[((long)gridDim.x + blockIdx.x) * C + sl.c] = s2;
+    *reinterpret_cast<floatx4*>(part + (long)blockIdx.x * C + sl.c) = s1;
+    *reinterpret_cast<floatx4*>(part + ((long)gridDim.x + blockIdx.x) * C + sl.c) = s2;
   }
 }
 
@@ -308,7 +383,7 @@ __global__ __launch_bounds__(FL_T) void bn_bwd_final_kernel(const float* __restr
 }
 
 // dx = rstd g_c (g - dbeta / P - xhat dgamma / P), as bf16.
-template <int MASK>
+template <int MASK, bool V>
 __global__ void bn_bwd_apply_kernel(const float* __restrict__ dy, const void* __restrict__ msk,
                                     const float* __restrict__ x, const float* __restrict__ mean,
                                     const float* __restrict__ rstd, const float* __restrict__ gam,
@@ -316,14 +391,15 @@ __global__ void bn_bwd_apply_kernel(const float* __restrict__ dy, const void* __
                                     long n4, int C, float inv_p, bf16* __restrict__ dx) {
   for (long t = (long)blockIdx.x * NT + threadIdx.x; t < n4; t += (long)gridDim.x * NT) {
     const int c = (int)((4 * t) % C);
-    const floatx4 d = reinterpret_cast<const floatx4*>(dy)[t];
+    const floatx4 d = masked4<MASK, V>(reinterpret_cast<const floatx4*>(dy)[t], msk, t);
     const floatx4 v = reinterpret_cast<const floatx4*>(x)[t];
+    const floatx4 m4 = ld4<V>(mean, c), r4 = ld4<V>(rstd, c), g4 = ld4<V>(gam, c);
+    const floatx4 dg4 = ld4<V>(dg, c), db4 = ld4<V>(db, c);
     bf16x4 o;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const float gv = masked<MASK>(d[e], msk, 4 * t + e);
-      const float xh = (v[e] - mean[c + e]) * rstd[c + e];
-      o[e] = f2bf(rstd[c + e] * gam[c + e] * (gv - db[c + e] * inv_p - xh * dg[c + e] * inv_p));
+      const float xh = (v[e] - m4[e]) * r4[e];
+      o[e] = f2bf(r4[e] * g4[e] * (d[e] - db4[e] * inv_p - xh * dg4[e] * inv_p));
     }
     reinterpret_cast<bf16x4*>(dx)[t] = o;
   }
@@ -471,7 +547,7 @@ hipError_t launch_pad_cols_bf16(const bf16* src, int rows, int cols, bf16* dst, 
 // Row blocks of the batch-norm reductions: about 1024 workgroups in all,
 // at least 32 rows each.
 int bn_parts(long P, int C) {
-  const int slabs = (C + NT - 1) / NT;
+  const int slabs = (C + 4 * NT - 1) / (4 * NT);
   long nb = 1024 / slabs;
   nb = nb < 1 ? 1 : nb;
   const long by_rows = (P + 31) / 32;
@@ -510,7 +586,7 @@ hipError_t launch_bn_stats(const float* x, long P, int C, float eps, float* part
   if (P <= 0 || C <= 0) return hipErrorInvalidValue;
   const int nb = bn_parts(P, C);
   const long rpb = (P + nb - 1) / nb;
-  hipLaunchKernelGGL(bn_stats_partial_kernel, dim3(nb, (C + NT - 1) / NT), dim3(NT), 0, st, x, P,
+  hipLaunchKernelGGL(bn_stats_partial_kernel, dim3(nb, (C + 4 * NT - 1) / (4 * NT)), dim3(NT), 0, st, x, P,
                      C, rpb, part);
   hipLaunchKernelGGL(bn_stats_final_kernel, dim3((C + FL_C - 1) / FL_C), dim3(FL_T), 0, st, x, part,
                      nb, P, C, eps, mean, rstd);
@@ -522,8 +598,12 @@ hipError_t launch_bn_apply(const float* x, long P, int C, const float* mean, con
                            hipStream_t st) {
   if (C % 4) return hipErrorInvalidValue;
   const long n4 = P * C / 4;
-  hipLaunchKernelGGL(bn_apply_kernel, dim3(grid_for(n4)), dim3(NT), 0, st, x, n4, C, mean, rstd, g,
-                     b, relu, y, yf);
+  if (a16(mean) && a16(rstd) && a16(g) && a16(b))
+    hipLaunchKernelGGL(bn_apply_kernel<true>, dim3(grid_for(n4)), dim3(NT), 0, st, x, n4, C, mean, rstd,
+                       g, b, relu, y, yf);
+  else
+    hipLaunchKernelGGL(bn_apply_kernel<false>, dim3(grid_for(n4)), dim3(NT), 0, st, x, n4, C, mean, rstd,
+                       g, b, relu, y, yf);
   return hipGetLastError();
 }
 
@@ -533,8 +613,14 @@ hipError_t launch_bn_add_relu(const float* xa, const float* ma, const float* ra,
                               bf16* outb, hipStream_t st) {
   if (C % 4) return hipErrorInvalidValue;
   const long n4 = P * C / 4;
-  hipLaunchKernelGGL(bn_add_relu_kernel, dim3(grid_for(n4)), dim3(NT), 0, st, xa, ma, ra, ga, ba,
-                     xs, ms, rs, gs, bs, n4, C, out, outb);
+  const bool v = a16(ma) && a16(ra) && a16(ga) && a16(ba) &&
+                 (ms == nullptr || (a16(ms) && a16(rs) && a16(gs) && a16(bs)));
+  if (v)
+    hipLaunchKernelGGL(bn_add_relu_kernel<true>, dim3(grid_for(n4)), dim3(NT), 0, st, xa, ma, ra, ga,
+                       ba, xs, ms, rs, gs, bs, n4, C, out, outb);
+  else
+    hipLaunchKernelGGL(bn_add_relu_kernel<false>, dim3(grid_for(n4)), dim3(NT), 0, st, xa, ma, ra, ga,
+                       ba, xs, ms, rs, gs, bs, n4, C, out, outb);
   return hipGetLastError();
 }
 
@@ -544,7 +630,7 @@ hipError_t launch_bn_bwd(const float* dy, int mask_kind, const void* mask, const
   if (C % 4 || P <= 0 || mask_kind < 0 || mask_kind > 2) return hipErrorInvalidValue;
   const int nb = bn_parts(P, C);
   const long rpb = (P + nb - 1) / nb;
-  const dim3 g2(nb, (C + NT - 1) / NT);
+  const dim3 g2(nb, (C + 4 * NT - 1) / (4 * NT));
   if (mask_kind == 0)
     hipLaunchKernelGGL(bn_bwd_partial_kernel<0>, g2, dim3(NT), 0, st, dy, mask, x, mean, rstd, P, C,
                        rpb, part);
@@ -559,15 +645,20 @@ hipError_t launch_bn_bwd(const float* dy, int mask_kind, const void* mask, const
   const long n4 = P * C / 4;
   const float inv_p = (float)(1.0 / (double)P);
   const dim3 g1(grid_for(n4));
-  if (mask_kind == 0)
-    hipLaunchKernelGGL(bn_bwd_apply_kernel<0>, g1, dim3(NT), 0, st, dy, mask, x, mean, rstd, gam, dg,
-                       db, n4, C, inv_p, dx);
-  else if (mask_kind == 1)
-    hipLaunchKernelGGL(bn_bwd_apply_kernel<1>, g1, dim3(NT), 0, st, dy, mask, x, mean, rstd, gam, dg,
-                       db, n4, C, inv_p, dx);
-  else
-    hipLaunchKernelGGL(bn_bwd_apply_kernel<2>, g1, dim3(NT), 0, st, dy, mask, x, mean, rstd, gam, dg,
-                       db, n4, C, inv_p, dx);
+  const bool v = a16(mean) && a16(rstd) && a16(gam) && a16(dg) && a16(db) &&
+                 (mask_kind != 1 || (reinterpret_cast<uintptr_t>(mask) & 7) == 0) &&
+                 (mask_kind != 2 || a16(mask));
+#define BNB(M, VV)                                                                              \
+  hipLaunchKernelGGL((bn_bwd_apply_kernel<M, VV>), g1, dim3(NT), 0, st, dy, mask, x, mean, rstd, \
+                     gam, dg, db, n4, C, inv_p, dx)
+  if (mask_kind == 0) {
+    if (v) BNB(0, true); else BNB(0, false);
+  } else if (mask_kind == 1) {
+    if (v) BNB(1, true); else BNB(1, false);
+  } else {
+    if (v) BNB(2, true); else BNB(2, false);
+  }
+#undef BNB
   return hipGetLastError();
 }
 

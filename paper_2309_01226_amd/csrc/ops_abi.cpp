@@ -320,6 +320,10 @@ extern "C" sat_status sat_op_batchnorm_fwd(const float* x, int64_t P, int32_t C,
                                            void* stream) {
   SAT_CHECK_ARG(x && g && b && part && mean && rstd && (y || yf), "batchnorm_fwd: null pointer");
   SAT_CHECK_ARG(P >= 1 && C >= 4 && C % 4 == 0 && eps > 0.f, "batchnorm_fwd: bad sizes");
+  auto al = [](const void* q, int n) { return q == nullptr || (reinterpret_cast<uintptr_t>(q) % n) == 0; };
+  SAT_CHECK_ARG(al(x, 16) && al(g, 16) && al(b, 16) && al(part, 16) && al(mean, 16) && al(rstd, 16) &&
+                    al(yf, 16) && al(y, 8),
+                "batchnorm_fwd: fp32 arrays must be 16-byte aligned and y 8-byte aligned");
   SAT_HIP(launch_bn_stats(x, P, C, eps, part, mean, rstd, S(stream)));
   SAT_HIP(launch_bn_apply(x, P, C, mean, rstd, g, b, relu, (bf16*)y, yf, S(stream)));
   return SAT_OK;
@@ -333,6 +337,10 @@ extern "C" sat_status sat_op_batchnorm_bwd(const float* dy, int32_t mask_kind, c
   SAT_CHECK_ARG(mask_kind >= 0 && mask_kind <= 2 && (mask_kind == 0 || mask != nullptr),
                 "batchnorm_bwd: mask_kind must be 0 (none), 1 (bf16) or 2 (fp32) with a mask");
   SAT_CHECK_ARG(P >= 1 && C >= 4 && C % 4 == 0, "batchnorm_bwd: bad sizes");
+  auto al = [](const void* q, int n) { return q == nullptr || (reinterpret_cast<uintptr_t>(q) % n) == 0; };
+  SAT_CHECK_ARG(al(dy, 16) && al(x, 16) && al(mean, 16) && al(rstd, 16) && al(g, 16) && al(part, 16) &&
+                    al(dg, 16) && al(db, 16) && al(dx, 8) && al(mask, mask_kind == 2 ? 16 : 8),
+                "batchnorm_bwd: fp32 arrays must be 16-byte aligned, dx and a bf16 mask 8-byte aligned");
   SAT_HIP(launch_bn_bwd(dy, mask_kind, mask, x, mean, rstd, g, P, C, part, dg, db, (bf16*)dx,
                         S(stream)));
   return SAT_OK;
