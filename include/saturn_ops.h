@@ -164,6 +164,12 @@ sat_status sat_op_transpose_bf16(const void* src, int64_t lds, void* dst, int64_
  * a k x k convolution computed as one GEMM against the weight [Cout, k k C]. */
 sat_status sat_op_im2col(const void* x, void* col, int32_t N, int32_t H, int32_t W, int32_t C,
                          int32_t k, int32_t stride, int32_t pad, void* stream);
+/* The same matrix transposed: colT [k * k * C, N * Ho * Wo] bf16 with row
+ * stride ldt (>= N Ho Wo, a multiple of 8), the token-contiguous operand of a
+ * convolution's weight-gradient product.  N Ho Wo % 8 == 0, C % 8 == 0, x and
+ * colT 16-byte aligned (SAT_EINVAL otherwise). */
+sat_status sat_op_im2col_t(const void* x, void* colT, int64_t ldt, int32_t N, int32_t H, int32_t W,
+                           int32_t C, int32_t k, int32_t stride, int32_t pad, void* stream);
 /* col2im, the transpose of im2col: dx [N, H, W, C] fp32 = (accumulate: dx +)
  * the sum over the taps that read each input element of dcol [N * Ho * Wo,
  * k * k * C] fp32, in tap order; C a positive multiple of 4. */

@@ -111,6 +111,7 @@ SIGNATURES = {
     "sat_op_colsum": (C.c_int, [_VP, _I64, _I32, _I32, _VP, _VP, _VP]),
     "sat_op_transpose_bf16": (C.c_int, [_VP, _I64, _VP, _I64, _I32, _I32, _VP]),
     "sat_op_im2col": (C.c_int, [_VP, _VP, _I32, _I32, _I32, _I32, _I32, _I32, _I32, _VP]),
+    "sat_op_im2col_t": (C.c_int, [_VP, _VP, _I64, _I32, _I32, _I32, _I32, _I32, _I32, _I32, _VP]),
     "sat_op_col2im": (C.c_int, [_VP, _VP, _I32, _I32, _I32, _I32, _I32, _I32, _I32, _I32, _VP]),
     "sat_op_batchnorm_fwd": (C.c_int, [_VP, _I64, _I32, _VP, _VP, _F32, _I32, _VP, _VP, _VP, _VP, _VP,
                                        _VP]),

@@ -48,6 +48,71 @@ __global__ void im2col8_kernel(const bf16* __restrict__ x, bf16* __restrict__ co
   }
 }
 
+// The im2col matrix transposed, colT[(a k + b) C + c, p] (row stride ldt >=
+// P = N Ho Wo), which the weight-gradient product reads token-contiguous:
+// im2col and the transpose in one pass.  A lane gathers eight consecutive
+// output pixels' 16-byte pieces (8 channels of one tap, zeros outside the
+// image), transposes the 8 x 8 block with byte permutes (element j of pixels
+// 2e and 2e + 1 into one dword) and stores eight 16-byte rows of 8 pixels.
+// A workgroup covers 128 pixels x 512 columns; TB column blocks per lane
+// keep 8 TB loads in flight.  P % 8 == 0 and C % 8 == 0.
+constexpr int I2T_TB = 4;
+__global__ __launch_bounds__(NT) void im2col_t_kernel(const bf16* __restrict__ x, bf16* __restrict__ colT,
+                                                      long ldt, int N, int H, int W, int C, int k,
+                                                      int s, int pad, int Ho, int Wo) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const long P = (long)N * Ho * Wo;
+  const int cols = k * k * C;
+  const long p0 = (long)blockIdx.y * 128 + (wave >> 1) * 64 + (lane >> 3) * 8;
+  const int cb = blockIdx.x * 128 * I2T_TB + (wave & 1) * 64 * I2T_TB + (lane & 7) * 8;
+  if (p0 >= P) return;
+  // the eight pixels' image row / column origins and image offsets
+  int hi0[8], wi0[8];
+  long nb[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const long p = p0 + i;
+    const int j = (int)(p % Wo);
+    const long q = p / Wo;
+    const int ii = (int)(q % Ho);
+    const int n = (int)(q / Ho);
+    hi0[i] = ii * s - pad;
+    wi0[i] = j * s - pad;
+    nb[i] = (long)n * H;
+  }
+  u32x4 v[I2T_TB][8];
+#pragma unroll
+  for (int bk = 0; bk < I2T_TB; ++bk) {
+    const int c0 = cb + 64 * bk;
+    if (c0 < cols) {
+      const int tap = c0 / C, c = c0 - tap * C;
+      const int a = tap / k, b = tap - a * k;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int hi = hi0[i] + a, wi = wi0[i] + b;
+        u32x4 z = {0u, 0u, 0u, 0u};
+        if (hi >= 0 && hi < H && wi >= 0 && wi < W)
+          z = *reinterpret_cast<const u32x4*>(x + ((nb[i] + hi) * W + wi) * C + c);
+        v[bk][i] = z;
+      }
+    }
+  }
+#pragma unroll
+  for (int bk = 0; bk < I2T_TB; ++bk) {
+    const int c0 = cb + 64 * bk;
+    if (c0 >= cols) break;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
+      u32x4 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        o[e] = __builtin_amdgcn_perm(v[bk][2 * e + 1][j >> 1], v[bk][2 * e][j >> 1], sel);
+      *reinterpret_cast<u32x4*>(colT + (long)(c0 + j) * ldt + p0) = o;
+    }
+  }
+}
+
 // The stem: fp32 NCHW images -> bf16 columns, K = k k C (taps ordered a, b,
 // c as above), zero columns K .. ldc - 1.
 __global__ void im2col_nchw_kernel(const float* __restrict__ img, bf16* __restrict__ col, int N,
@@ -560,6 +625,19 @@ hipError_t launch_im2col(const bf16* x, bf16* col, long ldc, int N, int H, int W
   const long total = (long)N * Ho * Wo * k * k * (C / 8);
   hipLaunchKernelGGL(im2col8_kernel, dim3(grid_for(total)), dim3(NT), 0, st, x, col, N, H, W, C, k,
                      s, pad, Ho, Wo, ldc);
+  return hipGetLastError();
+}
+
+hipError_t launch_im2col_t(const bf16* x, bf16* colT, long ldt, int N, int H, int W, int C, int k,
+                           int s, int pad, int Ho, int Wo, hipStream_t st) {
+  const long P = (long)N * Ho * Wo;
+  if (C % 8 || P % 8 || ldt < P || ldt % 8 ||
+      ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(colT)) & 15))
+    return hipErrorInvalidValue;
+  const int cols = k * k * C;
+  dim3 grid((unsigned)((cols + 128 * I2T_TB - 1) / (128 * I2T_TB)), (unsigned)((P + 127) / 128));
+  hipLaunchKernelGGL(im2col_t_kernel, grid, dim3(NT), 0, st, x, colT, ldt, N, H, W, C, k, s, pad, Ho,
+                     Wo);
   return hipGetLastError();
 }
 

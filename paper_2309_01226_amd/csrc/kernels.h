@@ -246,6 +246,11 @@ hipError_t launch_sum_rows_batched(const float* dh, float* out, int B, int S, in
 // (zero outside); bf16, C % 8 == 0, ldc == k k C.
 hipError_t launch_im2col(const bf16* x, bf16* col, long ldc, int N, int H, int W, int C, int k,
                          int s, int pad, int Ho, int Wo, hipStream_t st);
+// The same matrix transposed, colT [k k C, N Ho Wo] (row stride ldt): the
+// token-contiguous operand of a convolution's weight-gradient product.
+// C % 8 == 0, N Ho Wo % 8 == 0, ldt % 8 == 0, 16-byte aligned.
+hipError_t launch_im2col_t(const bf16* x, bf16* colT, long ldt, int N, int H, int W, int C, int k,
+                           int s, int pad, int Ho, int Wo, hipStream_t st);
 // The same from fp32 NCHW images; columns k k C .. ldc - 1 are written as zeros.
 hipError_t launch_im2col_nchw(const float* img, bf16* col, long ldc, int N, int C, int H, int W,
                               int k, int s, int pad, int Ho, int Wo, hipStream_t st);

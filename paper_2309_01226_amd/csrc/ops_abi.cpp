@@ -301,6 +301,23 @@ extern "C" sat_status sat_op_im2col(const void* x, void* col, int32_t N, int32_t
   return SAT_OK;
 }
 
+extern "C" sat_status sat_op_im2col_t(const void* x, void* colT, int64_t ldt, int32_t N, int32_t H,
+                                      int32_t W, int32_t C, int32_t k, int32_t stride, int32_t pad,
+                                      void* stream) {
+  SAT_CHECK_ARG(x && colT, "im2col_t: null pointer");
+  SAT_CHECK_ARG(N >= 1 && H >= 1 && W >= 1 && C >= 8 && C % 8 == 0 && k >= 1 && stride >= 1 &&
+                    pad >= 0 && H + 2 * pad >= k && W + 2 * pad >= k,
+                "im2col_t: bad sizes (C must be a positive multiple of 8)");
+  const int Ho = conv_hw(H, k, stride, pad), Wo = conv_hw(W, k, stride, pad);
+  const long P = (long)N * Ho * Wo;
+  SAT_CHECK_ARG(P % 8 == 0 && ldt >= P && ldt % 8 == 0, "im2col_t: N Ho Wo and ldt must be multiples of 8, ldt >= N Ho Wo");
+  SAT_CHECK_ARG(((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(colT)) & 15) == 0,
+                "im2col_t: x and colT must be 16-byte aligned");
+  SAT_HIP(launch_im2col_t((const bf16*)x, (bf16*)colT, ldt, N, H, W, C, k, stride, pad, Ho, Wo,
+                          S(stream)));
+  return SAT_OK;
+}
+
 extern "C" sat_status sat_op_col2im(const float* dcol, float* dx, int32_t N, int32_t H, int32_t W,
                                     int32_t C, int32_t k, int32_t stride, int32_t pad,
                                     int32_t accumulate, void* stream) {

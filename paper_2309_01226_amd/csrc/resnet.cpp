@@ -421,6 +421,16 @@ sat_status rwgrad(sat_model* M, const bf16* dY, int cout, const bf16* X, long ld
 
 // dX [P, n] fp32 = dY [P, cout] (bf16) times weight w [cout, n] (through its
 // transposed copy); resid (may equal out) is added when not null.
+// The same with X already token-contiguous: XT [ncols, P] (row stride P).
+sat_status rwgrad_t(sat_model* M, const bf16* dY, int cout, const bf16* XT, int ncols, long P,
+                    float* out) {
+  ResNetPlan& R = *M->rn;
+  SAT_HIP(launch_transpose_bf16(dY, cout, R.tA, P, (int)P, cout, M->stream));
+  GemmArgs w = gargs(R.tA, P, XT, P, cout, ncols, (int)P, out, ncols);
+  w.splitk_max = kSplitMax;
+  return gemm(M, w, LAY_K, LAY_K, EPI_F32);
+}
+
 sat_status dgrad(sat_model* M, const bf16* dY, int cout, int w, long P, int n, float* out,
                  const float* resid) {
   const ParamDesc& p = M->params[w];
@@ -541,9 +551,15 @@ sat_status sat_resnet_backward(sat_model* M, const void* inputs) {
     TRY(dgrad(M, R.dc, b.mid, b.w2, b.Pout, 9 * b.mid, R.dcol, nullptr));
     SAT_HIP(launch_col2im(R.dcol, 9L * b.mid, R.da, R.N, b.H, b.W, b.mid, 3, b.stride, 1, b.Ho, b.Wo,
                           0, s));
-    SAT_HIP(launch_im2col(b.a1, R.col, 9L * b.mid, R.N, b.H, b.W, b.mid, 3, b.stride, 1, b.Ho, b.Wo,
-                          s));
-    TRY(rwgrad(M, R.dc, b.mid, R.col, 9L * b.mid, 9 * b.mid, 9 * b.mid, b.Pout, grad(M, b.w2)));
+    // (the im2col matrix written token-contiguous when the shapes allow)
+    if (b.Pout % 8 == 0 && b.mid % 8 == 0) {
+      SAT_HIP(launch_im2col_t(b.a1, R.tB, b.Pout, R.N, b.H, b.W, b.mid, 3, b.stride, 1, b.Ho, b.Wo, s));
+      TRY(rwgrad_t(M, R.dc, b.mid, R.tB, 9 * b.mid, b.Pout, grad(M, b.w2)));
+    } else {
+      SAT_HIP(launch_im2col(b.a1, R.col, 9L * b.mid, R.N, b.H, b.W, b.mid, 3, b.stride, 1, b.Ho, b.Wo,
+                            s));
+      TRY(rwgrad(M, R.dc, b.mid, R.col, 9L * b.mid, 9 * b.mid, 9 * b.mid, b.Pout, grad(M, b.w2)));
+    }
     SAT_HIP(launch_bn_bwd(R.da, 1, b.a1, b.c1, b.n1.mean, b.n1.rstd, gam(M, b.n1), b.Pin, b.mid,
                           R.part, grad(M, b.n1.g), grad(M, b.n1.g + 1), R.dc, s));
     // conv1 (1 x 1) and the shortcut; the input gradient only when something
@@ -552,19 +568,25 @@ sat_status sat_resnet_backward(sat_model* M, const void* inputs) {
     if (need_dx) TRY(dgrad(M, R.dc, b.mid, b.w1, b.Pin, b.cin, dx, b.proj ? nullptr : R.gdo));
     TRY(rwgrad(M, R.dc, b.mid, R.xb[i], b.cin, b.cin, b.cin, b.Pin, grad(M, b.w1)));
     if (b.proj) {
-      const bf16* sub = R.xb[i];
       if (b.stride != 1) {
         if (need_dx) {
           TRY(dgrad(M, R.dcd, b.cout, b.wd, b.Pout, b.cin, R.dsub, nullptr));
           SAT_HIP(launch_stride2_add(R.dsub, R.N, b.Ho, b.Wo, b.cin, b.H, b.W, dx, s));
         }
-        SAT_HIP(launch_im2col(R.xb[i], R.col, b.cin, R.N, b.H, b.W, b.cin, 1, b.stride, 0, b.Ho, b.Wo,
-                              s));
-        sub = R.col;
-      } else if (need_dx) {
-        TRY(dgrad(M, R.dcd, b.cout, b.wd, b.Pout, b.cin, dx, dx));
+        // the every-other-pixel subsample, token-contiguous when the shapes allow
+        if (b.Pout % 8 == 0 && b.cin % 8 == 0) {
+          SAT_HIP(launch_im2col_t(R.xb[i], R.tB, b.Pout, R.N, b.H, b.W, b.cin, 1, b.stride, 0, b.Ho,
+                                  b.Wo, s));
+          TRY(rwgrad_t(M, R.dcd, b.cout, R.tB, b.cin, b.Pout, grad(M, b.wd)));
+        } else {
+          SAT_HIP(launch_im2col(R.xb[i], R.col, b.cin, R.N, b.H, b.W, b.cin, 1, b.stride, 0, b.Ho,
+                                b.Wo, s));
+          TRY(rwgrad(M, R.dcd, b.cout, R.col, b.cin, b.cin, b.cin, b.Pout, grad(M, b.wd)));
+        }
+      } else {
+        if (need_dx) TRY(dgrad(M, R.dcd, b.cout, b.wd, b.Pout, b.cin, dx, dx));
+        TRY(rwgrad(M, R.dcd, b.cout, R.xb[i], b.cin, b.cin, b.cin, b.Pout, grad(M, b.wd)));
       }
-      TRY(rwgrad(M, R.dcd, b.cout, sub, b.cin, b.cin, b.cin, b.Pout, grad(M, b.wd)));
     }
     std::swap(dy, dx);
   }

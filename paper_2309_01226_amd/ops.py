@@ -179,6 +179,18 @@ def im2col(x, N, H, W, C, k, stride, pad):
     return col
 
 
+def im2col_t(x, N, H, W, C, k, stride, pad):
+    """x bf16 [N*H*W, C] -> colT bf16 [k*k*C, N*Ho*Wo] (im2col transposed)."""
+    _need(x, torch.bfloat16, "x")
+    Ho, Wo = _hw(H, k, stride, pad), _hw(W, k, stride, pad)
+    if x.numel() < N * H * W * C:
+        raise ValueError("im2col_t: x too small")
+    P = N * Ho * Wo
+    colT = torch.empty(k * k * C, P, device=x.device, dtype=torch.bfloat16)
+    _lib.call("sat_op_im2col_t", _p(x), _p(colT), P, N, H, W, C, k, stride, pad, _stream())
+    return colT
+
+
 def col2im(dcol, N, H, W, C, k, stride, pad, dx=None):
     """dcol fp32 [N*Ho*Wo, k*k*C] -> dx fp32 [N*H*W, C] (accumulated into dx when given)."""
     _need(dcol, torch.float32, "dcol")

@@ -63,6 +63,27 @@ def test_conv_via_im2col_gemm(N, H, W, C, Co, k, s, p):
     assert rel(host(dw), rdw) < 2e-6
 
 
+# im2col written transposed (the weight-gradient operand): bitwise the
+# transpose of im2col, for pixel counts that are multiples of 8, ragged maps,
+# strides 1 and 2, 3 x 3 and 1 x 1 (the projection subsample), and column
+# counts that end inside a workgroup's 512-column block
+IM2COL_T = [(4, 9, 6, 16, 3, 1, 1), (4, 10, 11, 8, 3, 2, 1), (2, 8, 8, 24, 1, 2, 0),
+            (8, 14, 14, 72, 3, 1, 1), (1, 16, 16, 64, 3, 1, 1)]
+
+
+@pytest.mark.parametrize("N,H,W,C,k,s,p", IM2COL_T)
+def test_im2col_transposed(N, H, W, C, k, s, p):
+    flush(f"im2col_t N={N} H={H} W={W} C={C} k={k} s={s} p={p}")
+    ops = K()
+    rng = np.random.default_rng(N + H + C + k)
+    x = to_dev_bf16(rng.normal(size=(N * H * W, C)))
+    col = ops.im2col(x, N, H, W, C, k, s, p)
+    colT = ops.im2col_t(x, N, H, W, C, k, s, p)
+    torch.cuda.synchronize()
+    assert col.shape[0] % 8 == 0
+    assert torch.equal(colT, col.t().contiguous())
+
+
 BN = [(1000, 64, 0.0), (37, 8, 0.0), (5000, 512, 0.0), (200, 200, 0.0), (3000, 96, 1000.0)]
 
 
