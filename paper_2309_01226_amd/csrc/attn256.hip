@@ -487,12 +487,23 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dkdv_kernel(AttnBwdArgs a)
 // so lse and delta are per-lane scalars.  K rows are read as row fragments and
 // transposed (K^T) from the same dual-swizzled tile.  This kernel runs before
 // the dK / dV kernel and also computes delta = rowsum(dO * O) for it.
+//
+// Four K / V stages (block j in stage j % 4, copied two blocks ahead) and two
+// P^T exchange buffers (block j in buffer j % 2) leave one barrier per block:
+// at barrier j, P^T of block j and the copies of block j + 1 are visible, and
+// every wave has finished block j - 1, so the copies of block j + 2 issued
+// after it overwrite block j - 2's stage and role A writes block j + 1's P^T
+// over block j - 1's.  Role A can thus compute the next block's scores while
+// role B accumulates the current block's dQ on the same SIMD.
 constexpr int QPW = 128;   // queries per workgroup
 constexpr int STG_Q = 2 * QT;  // K rows, V rows of a 32-key block
+constexpr int NSTG_Q = 4;      // K / V stages
+constexpr int XB = 4 * 16 * 64;  // floats of one P^T exchange buffer (4 pairs)
 
 __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dq_kernel(AttnBwdArgs a) {
-  __shared__ __attribute__((aligned(1024))) bf16 smem[2 * STG_Q + 4 * 64 * 16 * 2];
-  float* xbuf = reinterpret_cast<float*>(smem + 2 * STG_Q);
+  static_assert((NSTG_Q * STG_Q + 2 * XB * 2) * 2 <= 163840, "LDS budget");
+  __shared__ __attribute__((aligned(1024))) bf16 smem[NSTG_Q * STG_Q + 2 * XB * 2];
+  float* xbuf = reinterpret_cast<float*>(smem + NSTG_Q * STG_Q);
   const int S = a.f.S;
   const int nqb = (S + QPW - 1) / QPW;
   // one-dimensional grid, query blocks outermost, heaviest first
@@ -557,8 +568,8 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dq_kernel(AttnBwdArgs a) {
 
   const int kv_end = a.f.causal ? min(S, q0 + QPW) : S;
   const int nkb = (kv_end + BQ - 1) / BQ;
-  float* xw = xbuf + pair * 16 * 64;
-  auto stage_ptr = [&](int j) { return smem + (j & 1) * STG_Q; };
+  auto stage_ptr = [&](int j) { return smem + (j % NSTG_Q) * STG_Q; };
+  // four copy instructions per wave per block
   auto fetch = [&](int j) {
     const int kv = j * BQ;
     bf16* st = stage_ptr(j);
@@ -567,14 +578,21 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dq_kernel(AttnBwdArgs a) {
   };
 
   fetch(0);
-  wait_vm_lgkm0<0>();
+  if (nkb > 1) {
+    fetch(1);
+    wait_vm_lgkm0<4>();  // block 0 resident, block 1 may stay in flight
+  } else {
+    wait_vm_lgkm0<0>();
+  }
   cta_barrier();
 
   for (int j = 0; j < nkb; ++j) {
     const int kv0 = j * BQ;
     const bf16* Ks = stage_ptr(j);
     const bf16* Vs = Ks + QT;
-    if (j + 1 < nkb) fetch(j + 1);
+    float* xw = xbuf + (j & 1) * XB + pair * 16 * 64;
+    const bool more2 = j + 2 < nkb;
+    if (more2) fetch(j + 2);
     const bool active = !(a.f.causal && kv0 > pq0 + 31);
     floatx16 x = zero16();
     if (active) {
@@ -594,8 +612,10 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dq_kernel(AttnBwdArgs a) {
         }
       }
     }
-    wait_lgkm0();
-    cta_barrier();  // P^T of every pair visible
+    // own copies of block j + 1 landed (block j + 2's may stay in flight), P^T written
+    if (more2) wait_vm_lgkm0<4>();
+    else wait_vm_lgkm0<0>();
+    cta_barrier();  // P^T of every pair and block j + 1 visible; block j - 1 done everywhere
     if (active && role == 1) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) x[r] = xw[r * 64 + lane] * (x[r] - lsd);
@@ -614,10 +634,6 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dq_kernel(AttnBwdArgs a) {
                                                             xb, acc[ot], 0, 0, 0);
         }
       }
-    }
-    if (j + 1 < nkb) {
-      wait_vm_lgkm0<0>();
-      cta_barrier();
     }
   }
   if (role == 1 && q < S) {
