@@ -375,12 +375,14 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dkdv_kernel(AttnBwdArgs a)
     copy_rows32(rows_rsrc(Qb, qs, a.f.ldq), a.f.ldq, S - qs, st, wave);
     copy_rows32(rows_rsrc(dOb, qs, a.lddo), a.lddo, S - qs, st + QT, wave);
     if (wave == 0) {
+      // the raw value: scaling it here would make the wave wait for the
+      // copies just issued (one vmcnt counts loads in issue order)
       const int qi = qs + (lane & 31);
-      lsd = qi < S ? (g ? a.delta[hs + qi] : a.f.lse[hs + qi] * LOG2E) : 0.f;
+      lsd = qi < S ? (g ? a.delta[hs + qi] : a.f.lse[hs + qi]) : 0.f;
     }
   };
-  auto publish = [&](int j) {  // wave 0 stores lse / delta of block j (after its loads landed)
-    if (wave == 0) reinterpret_cast<float*>(stage_ptr(j) + 2 * QT)[lane] = lsd;
+  auto publish = [&](int j) {  // wave 0 stores lse2 / delta of block j (after its loads landed)
+    if (wave == 0) reinterpret_cast<float*>(stage_ptr(j) + 2 * QT)[lane] = g ? lsd : lsd * LOG2E;
   };
 
   fetch(0);
@@ -395,7 +397,6 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dkdv_kernel(AttnBwdArgs a)
     const bf16* Qs = st;
     const bf16* dOs = st + QT;
     const float* lsd_s = reinterpret_cast<const float*>(st + 2 * QT);
-    if (j + 1 < nqb) fetch(j + 1);
     const bool active = !(a.f.causal && qs0 + BQ - 1 < kmin);
     // S = Q K^T (role A) or dP = dO V^T (role B): rows = queries, column = key
     floatx16 x = zero16();
@@ -404,6 +405,13 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dkdv_kernel(AttnBwdArgs a)
 #pragma unroll
       for (int c = 0; c < DH / 16; ++c)
         x = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(rows, lane & 31, c, g), rf[c], x, 0, 0, 0);
+    }
+    // The next block's copies go out after this block's resident-operand
+    // products: the compiler keeps part of rf in scratch at this register
+    // budget, and one vmcnt counts loads in issue order, so a reload issued
+    // after the copies would wait for them.
+    if (j + 1 < nqb) fetch(j + 1);
+    if (active) {
       if (role == 0) {
         // P = exp2(S log2e - lse2); zero for queries past S and (causal) keys past the query
         const int lim_q = S - qs0 - 4 * g;            // rows r with acc_row < lim_q are valid
