@@ -39,6 +39,15 @@ constexpr uint32_t OOB = 0x80000000u;
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+// The CDNA4 transposing LDS read through a restrict-qualified pointer: once
+// inlined, the read carries alias-scope information, so the compiler does not
+// make it wait for every LDS copy still in flight (the next block's, which
+// land in another stage); the current stage's copies are waited for, and
+// published by a barrier, before any wave reads it.
+__device__ __forceinline__ bf16x4 ds_read_tr(const lds_bf16x4* __restrict__ p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16(const_cast<lds_bf16x4*>(p));
+}
 __device__ __forceinline__ lds_void* lds(const bf16* p) { return (lds_void*)(const_cast<bf16*>(p)); }
 
 __device__ __forceinline__ int swz_row(int r) { return r & 15; }
@@ -170,8 +179,8 @@ __device__ __forceinline__ void fwd_block(FwdState& st, const bf16* Ks, const bf
 #pragma unroll
     for (int ot = 0; ot < DH / 32; ++ot) {
       const int vo = st.vofs[ot & 3] + (ot >> 2) * 128;
-      const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(vb + vo));
-      const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(vb + vo + 8 * DH));
+      const bf16x4 lo = ds_read_tr((const lds_bf16x4*)lds(vb + vo));
+      const bf16x4 hi = ds_read_tr((const lds_bf16x4*)lds(vb + vo + 8 * DH));
       const bf16x8 vf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
       st.o[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[kk], st.o[ot], 0, 0, 0);
     }
@@ -455,8 +464,8 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dkdv_kernel(AttnBwdArgs a)
         for (int ot = 0; ot < DH / 32; ++ot) {
           // rows + 8 flip bit 1 of the row's swizzle group, i.e. chunk bit 1
           const int to = tofs[ot & 3] + (ot >> 2) * 128;
-          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(tb + to));
-          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(tb + ((to ^ 16) + 8 * DH)));
+          const bf16x4 lo = ds_read_tr((const lds_bf16x4*)lds(tb + to));
+          const bf16x4 hi = ds_read_tr((const lds_bf16x4*)lds(tb + ((to ^ 16) + 8 * DH)));
           acc[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7),
                                                             xb, acc[ot], 0, 0, 0);
         }
@@ -636,8 +645,8 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dq_kernel(AttnBwdArgs a) {
 #pragma unroll
         for (int ot = 0; ot < DH / 32; ++ot) {
           const int to = tofs[ot & 3] + (ot >> 2) * 128;
-          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(tb + to));
-          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(tb + ((to ^ 16) + 8 * DH)));
+          const bf16x4 lo = ds_read_tr((const lds_bf16x4*)lds(tb + to));
+          const bf16x4 hi = ds_read_tr((const lds_bf16x4*)lds(tb + ((to ^ 16) + 8 * DH)));
           acc[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7),
                                                             xb, acc[ot], 0, 0, 0);
         }

@@ -47,6 +47,15 @@ constexpr uint32_t OOB = 0x80000000u;
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+// The CDNA4 transposing LDS read through a restrict-qualified pointer: once
+// inlined, the read carries alias-scope information, so the compiler does not
+// make it wait for every LDS copy still in flight (the next block's, which
+// land in another stage); the current stage's copies are waited for, and
+// published by a barrier, before any wave reads it.
+__device__ __forceinline__ bf16x4 ds_read_tr(const lds_bf16x4* __restrict__ p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16(const_cast<lds_bf16x4*>(p));
+}
 __device__ __forceinline__ lds_void* lds(const bf16* p) { return (lds_void*)(const_cast<bf16*>(p)); }
 
 template <int DH>
@@ -151,13 +160,13 @@ struct TileOfs {
     bf16x4 lo, hi;
     if (ot < 2) {
       const int o = tr[ot & 1] + 16 * kk * 64;
-      lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(tile + o));
+      lo = ds_read_tr((const lds_bf16x4*)lds(tile + o));
       // rows + 8 flip bit 1 of swz, i.e. chunk bit 1
-      hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(tile + ((o ^ 16) + 8 * 64)));
+      hi = ds_read_tr((const lds_bf16x4*)lds(tile + ((o ^ 16) + 8 * 64)));
     } else {
       const int o = trt + 16 * kk * 8;
-      lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(tile + o));
-      hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lds(tile + o + 8 * 8));
+      lo = ds_read_tr((const lds_bf16x4*)lds(tile + o));
+      hi = ds_read_tr((const lds_bf16x4*)lds(tile + o + 8 * 8));
     }
     return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
   }
