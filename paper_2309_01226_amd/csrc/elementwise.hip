@@ -337,45 +337,67 @@ __global__ __launch_bounds__(256) void xent_kernel(const float* __restrict__ z, 
   if (threadIdx.x == 0) row_loss[row] = lse - zr[y];
 }
 
-// Rows of at most 13 * 4096 logits: one 1024-thread workgroup per row keeps
-// the row in registers (thread t holds columns 4 t + 4096 g .. + 3, g < NV4),
-// so the logits are read once and exp is taken once per element:
-// p = exp(z - max), lse = max + log(sum p), dz = (p / sum p - onehot) * inv_n.
-// Block max and sum go through LDS in a fixed order.
-template <int NV4>
-__global__ __launch_bounds__(1024) void xent_reg_kernel(const float* __restrict__ z, long ldz,
-                                                        const int32_t* __restrict__ labels, int V,
-                                                        float* __restrict__ row_loss,
-                                                        bf16* __restrict__ dz, long lddz,
-                                                        const float* __restrict__ inv_n_p) {
-  __shared__ float red[16];
+// Rows that fit in the registers of one workgroup (NT threads, thread t
+// holding columns 4 t + 4 NT g .. + 3 for g < NV4): the logits are read once
+// and exp is taken once per element: p = exp(z - max), lse = max + log(sum p),
+// dz = (p / sum p - onehot) * inv_n.  Block max and sum go through LDS in a
+// fixed order.  Row reads and writes are buffer instructions (one VGPR offset
+// per thread, the group offset in the scalar offset, so the row's addresses
+// take no registers) with the non-temporal hint: the logits are read once and
+// the gradient is consumed by the next kernel from HBM.  At 512 threads two
+// workgroups share a CU, so one row's reads overlap the other's writes.
+// FULL: the host has checked that every group but the last lies inside the
+// row (4 NT (NV4 - 1) <= V), so only the last one is tested.
+template <int NT, int NV4, bool FULL>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4, 4)))
+void xent_reg_kernel(const float* __restrict__ z, long ldz, const int32_t* __restrict__ labels,
+                     int V, float* __restrict__ row_loss, bf16* __restrict__ dz, long lddz,
+                     const float* __restrict__ inv_n_p) {
+  constexpr int NW = NT / 64, GS = 4 * NT;  // waves, columns per group
+  constexpr int NT_HINT = 2;                 // buffer cache policy: non-temporal
+  __shared__ float red[2][NW];
   const int row = blockIdx.x;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const float* zr = z + (long)row * ldz;
+  bf16* dr = dz + (long)row * lddz;
   const int y = labels[row];
+  const int cpad = (int)min((long)((V + 7) & ~7), lddz);  // zero the row padding too
+  const __amdgpu_buffer_rsrc_t rz =
+      __builtin_amdgcn_make_buffer_rsrc((void*)zr, (short)0, V * 4, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rd =
+      __builtin_amdgcn_make_buffer_rsrc((void*)dr, (short)0, cpad * 2, 0x00020000);
   floatx4 v[NV4];
-  float m = -INFINITY;
 #pragma unroll
   for (int g = 0; g < NV4; ++g) {
-    const int c = 4 * t + 4096 * g;
+    const int c = 4 * t + GS * g;
     v[g] = floatx4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-    if (c + 3 < V) {
-      v[g] = __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(zr + c));
+    // the first two tests are uniform: the whole group lies in the row
+    if ((FULL && g < NV4 - 1) || GS * (g + 1) <= V || c + 3 < V) {
+      v[g] = __builtin_bit_cast(
+          floatx4, __builtin_amdgcn_raw_buffer_load_b128(rz, 16 * t, 4 * GS * g, NT_HINT));
     } else {
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        if (c + e < V) v[g][e] = zr[c + e];
+        if (c + e < V)
+          v[g][e] = __builtin_bit_cast(
+              float, __builtin_amdgcn_raw_buffer_load_b32(rz, 16 * t + 4 * e, 4 * GS * g, NT_HINT));
     }
+  }
+  // the label's logit, read while the row is still arriving
+  const float zy = (t == 0 && y >= 0)
+                       ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rz, 4 * y, 0, 0))
+                       : 0.f;
+  float m = -INFINITY;
+#pragma unroll
+  for (int g = 0; g < NV4; ++g)
 #pragma unroll
     for (int e = 0; e < 4; ++e) m = fmaxf(m, v[g][e]);
-  }
   m = wave_max(m);
-  if (lane == 0) red[wave] = m;
+  if (lane == 0) red[0][wave] = m;
   __syncthreads();
-  float M = red[0];
+  float M = red[0][0];
 #pragma unroll
-  for (int w = 1; w < 16; ++w) M = fmaxf(M, red[w]);
-  __syncthreads();
+  for (int w = 1; w < NW; ++w) M = fmaxf(M, red[0][w]);
   float s = 0.f;
 #pragma unroll
   for (int g = 0; g < NV4; ++g)
@@ -385,19 +407,17 @@ __global__ __launch_bounds__(1024) void xent_reg_kernel(const float* __restrict_
       s += v[g][e];
     }
   s = wave_sum(s);
-  if (lane == 0) red[wave] = s;
+  if (lane == 0) red[1][wave] = s;
   __syncthreads();
   float tot = 0.f;
 #pragma unroll
-  for (int w = 0; w < 16; ++w) tot += red[w];
+  for (int w = 0; w < NW; ++w) tot += red[1][w];
   const float lse = M + __logf(tot);
-  bf16* dr = dz + (long)row * lddz;
-  const int cpad = (int)min((long)((V + 7) & ~7), lddz);  // zero the row padding too
   const float inv_n = y < 0 ? 0.f : *inv_n_p;
   const float rt = 1.f / tot;
 #pragma unroll
   for (int g = 0; g < NV4; ++g) {
-    const int c = 4 * t + 4096 * g;
+    const int c = 4 * t + GS * g;
     if (c >= cpad) continue;
     bf16x4 o;
 #pragma unroll
@@ -405,15 +425,18 @@ __global__ __launch_bounds__(1024) void xent_reg_kernel(const float* __restrict_
       const float pr = c + e < V ? v[g][e] * rt : 0.f;
       o[e] = f2bf((pr - (c + e == y ? 1.f : 0.f)) * inv_n);
     }
-    if (c + 3 < cpad) {
-      __builtin_nontemporal_store(o, reinterpret_cast<bf16x4*>(dr + c));
+    if ((FULL && g < NV4 - 1) || GS * (g + 1) <= cpad || c + 3 < cpad) {
+      __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, o), rd, 8 * t, 2 * GS * g,
+                                            NT_HINT);
     } else {
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        if (c + e < cpad) dr[c + e] = o[e];
+        if (c + e < cpad)
+          __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, o[e]), rd,
+                                                8 * t + 2 * e, 2 * GS * g, NT_HINT);
     }
   }
-  if (t == 0) row_loss[row] = y < 0 ? 0.f : lse - zr[y];
+  if (t == 0) row_loss[row] = y < 0 ? 0.f : lse - zy;
 }
 
 // Single block: out[0] = (sum of row_loss in a fixed tree order) * inv_n.
@@ -659,16 +682,20 @@ hipError_t launch_sum_rows_batched(const float* dh, float* out, int B, int S, in
 hipError_t launch_xent(const float* z, long ldz, const int32_t* labels, int N, int V,
                        float* row_loss, bf16* dz, long lddz, const float* inv_n, hipStream_t s) {
   if (N <= 0) return hipSuccess;
-  const int nv4 = (V + 4095) / 4096;
-  // 1024 threads leave 128 VGPRs per thread: up to 13 groups of 4 logits stay in registers
-  const bool reg = nv4 <= 13 && ldz % 4 == 0 && lddz % 4 == 0 &&
+  // rows in registers: 512 threads (two workgroups per CU) for up to 12
+  // groups of 2048 logits and for exactly 25 (the GPT vocabularies), 1024
+  // threads for up to 13 groups of 4096
+  const bool reg = V <= 13 * 4096 && ldz % 4 == 0 && lddz % 4 == 0 &&
                    (reinterpret_cast<uintptr_t>(z) & 15) == 0 && (reinterpret_cast<uintptr_t>(dz) & 7) == 0;
-#define XREG(NV) hipLaunchKernelGGL(xent_reg_kernel<NV>, dim3(N), dim3(1024), 0, s, z, ldz, labels, V, \
-                                    row_loss, dz, lddz, inv_n)
-  if (reg && nv4 <= 1) XREG(1);
-  else if (reg && nv4 <= 4) XREG(4);
-  else if (reg && nv4 <= 8) XREG(8);
-  else if (reg) XREG(13);
+  const int g512 = (V + 2047) / 2048;
+#define XREG(NT, NV, FULL) hipLaunchKernelGGL((xent_reg_kernel<NT, NV, FULL>), dim3(N), dim3(NT), 0, s, \
+                                              z, ldz, labels, V, row_loss, dz, lddz, inv_n)
+  if (reg && g512 <= 1) XREG(512, 1, false);
+  else if (reg && g512 <= 4) XREG(512, 4, false);
+  else if (reg && g512 <= 8) XREG(512, 8, false);
+  else if (reg && g512 <= 12) XREG(512, 12, false);
+  else if (reg && g512 == 25) XREG(512, 25, true);
+  else if (reg) XREG(1024, 13, false);
   else
     hipLaunchKernelGGL(xent_kernel, dim3(N), dim3(256), 0, s, z, ldz, labels, V, row_loss, dz, lddz,
                        inv_n);

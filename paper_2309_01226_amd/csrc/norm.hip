@@ -151,12 +151,51 @@ __global__ __launch_bounds__(256) void ln_fwd_wg_kernel(const float* __restrict_
   }
 }
 
+// s_waitcnt lgkmcnt(0) only: vector loads may stay in flight across it.
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xF | (3 << 14) | (7 << 4)); }
+// Workgroup barrier with no implied wait for vector memory (the compiler's
+// fence before __syncthreads would also wait for the next row's loads).
+__device__ __forceinline__ void cta_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_sched_barrier(0);
+}
+// Raw buffer resource over `bytes` bytes at p: accesses past the end read 0
+// and write nothing.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, 0x00020000);
+}
+__device__ __forceinline__ float4 bload4(__amdgpu_buffer_rsrc_t r, int vo, int so) {
+  const floatx4 v = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(r, vo, so, 0));
+  return make_float4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ void bstore4(float4 v, __amdgpu_buffer_rsrc_t r, int vo, int so) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, floatx4{v.x, v.y, v.z, v.w}), r, vo,
+                                         so, 0);
+}
+
+// One row of the backward's operands: dy, x and the residual gradient for
+// the thread's columns (j * 256 + tid) * 4 .. +3, with the row's statistics.
+template <int NC4>
+struct LnBwdRow {
+  float4 dy[NC4], x[NC4], res[NC4];
+  float mu, rs;
+};
+
 // Backward: workgroup p owns rows [p * rpb, (p + 1) * rpb); each thread owns
 // the columns (j * 256 + tid) * 4 .. +3 and keeps their dg / db partial sums
 // in registers, so the workgroup writes one partial row per tensor and needs
-// no cross-wave reduction of the columns.  Two rows are processed per
-// iteration; their two row sums go through LDS (fixed order: lane tree, then
-// waves 0..3), one barrier per iteration.  dy and x are read once.
+// no cross-wave reduction of the columns.  The row loop is software
+// pipelined: the next row's dy, x and residual gradient are loaded before the
+// current row is reduced and written, into the other of two register sets
+// (the loop is unrolled by two, so no set is ever copied and no wait for the
+// next row is implied).  Every row access is a buffer instruction, so columns
+// past d and a next row that does not exist need no branch (their reads give
+// 0, their writes are dropped) and the wait counts stay exact.  The two row
+// sums go through LDS in a fixed order (lane tree, then waves 0..3), one
+// barrier per row.  dy, x and the residual gradient are read once.
 template <int NC4>
 __global__ __launch_bounds__(256) void ln_bwd_kernel(
     const float* __restrict__ dy, long lddy, const float* __restrict__ x, long ldx,
@@ -164,116 +203,110 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(
     const float* __restrict__ rstd, float* __restrict__ dres, long ldres,
     float* __restrict__ part_g, float* __restrict__ part_b, int rows, int d, int rpb,
     bf16* __restrict__ dres_bf, long ldbf) {
-  __shared__ float red[2][4][4];
+  __shared__ float red[2][2][4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r0 = blockIdx.x * rpb, r1 = min(rows, r0 + rpb);
+  const int vo = 16 * tid;  // byte offset of the thread's columns; column block j adds 4096 j
   float4 gg[NC4], pg[NC4], pb[NC4];
+  {
+    const auto rg = rsrc(g, 4 * d);
 #pragma unroll
-  for (int j = 0; j < NC4; ++j) {
-    const int col = (j * 256 + tid) * 4;
-    gg[j] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (col < d) gg[j] = *reinterpret_cast<const float4*>(g + col);
-    pg[j] = make_float4(0.f, 0.f, 0.f, 0.f);
-    pb[j] = pg[j];
-  }
-  int it = 0;
-  for (int row = r0; row < r1; row += 2, ++it) {
-    const bool two = row + 1 < r1;
-    float4 dv[2][NC4], xh[2][NC4], rv[2][NC4];
-    float mu[2], rs[2], s[2][2];
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const int rr = two ? row + q : row;  // a lone last row is processed twice, counted once
-      mu[q] = mean[rr];
-      rs[q] = rstd[rr];
-      const float* dyr = dy + (long)rr * lddy;
-      const float* xr = x + (long)rr * row_stride * ldx;
-      const float* drr = dres + (long)rr * row_stride * ldres;
-      s[q][0] = s[q][1] = 0.f;
-#pragma unroll
-      for (int j = 0; j < NC4; ++j) {
-        const int col = (j * 256 + tid) * 4;
-        float4 xv = make_float4(0.f, 0.f, 0.f, 0.f);
-        dv[q][j] = xv;
-        rv[q][j] = xv;
-        if (col < d) {
-          // the residual gradient is loaded with dy and x, not after the row sums
-          dv[q][j] = *reinterpret_cast<const float4*>(dyr + col);
-          xv = *reinterpret_cast<const float4*>(xr + col);
-          rv[q][j] = *reinterpret_cast<const float4*>(drr + col);
-        }
-        float4 h = make_float4((xv.x - mu[q]) * rs[q], (xv.y - mu[q]) * rs[q], (xv.z - mu[q]) * rs[q],
-                               (xv.w - mu[q]) * rs[q]);
-        if (col >= d) h = make_float4(0.f, 0.f, 0.f, 0.f);
-        xh[q][j] = h;
-        const float4 v = dv[q][j];
-        const float4 gy = make_float4(v.x * gg[j].x, v.y * gg[j].y, v.z * gg[j].z, v.w * gg[j].w);
-        s[q][0] += gy.x + gy.y + gy.z + gy.w;
-        s[q][1] += gy.x * h.x + gy.y * h.y + gy.z * h.z + gy.w * h.w;
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const float a0 = wave_sum(s[q][0]), a1 = wave_sum(s[q][1]);
-      if (lane == 0) {
-        red[it & 1][wave][2 * q] = a0;
-        red[it & 1][wave][2 * q + 1] = a1;
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      if (q == 1 && !two) continue;
-      const int rr = row + q;
-      float t0 = red[it & 1][0][2 * q], t1 = red[it & 1][0][2 * q + 1];
-#pragma unroll
-      for (int w = 1; w < 4; ++w) {
-        t0 += red[it & 1][w][2 * q];
-        t1 += red[it & 1][w][2 * q + 1];
-      }
-      const float m1 = t0 / d, m2 = t1 / d;
-      float* dr = dres + (long)rr * row_stride * ldres;
-#pragma unroll
-      for (int j = 0; j < NC4; ++j) {
-        const int col = (j * 256 + tid) * 4;
-        if (col < d) {
-          const float4 v = dv[q][j], h = xh[q][j];
-          float4 o = rv[q][j];
-          o.x += rs[q] * (v.x * gg[j].x - m1 - h.x * m2);
-          o.y += rs[q] * (v.y * gg[j].y - m1 - h.y * m2);
-          o.z += rs[q] * (v.z * gg[j].z - m1 - h.z * m2);
-          o.w += rs[q] * (v.w * gg[j].w - m1 - h.w * m2);
-          *reinterpret_cast<float4*>(dr + col) = o;
-          if (dres_bf != nullptr) {
-            const bf16x4 ob = {f2bf(o.x), f2bf(o.y), f2bf(o.z), f2bf(o.w)};
-            *reinterpret_cast<bf16x4*>(dres_bf + (long)rr * ldbf + col) = ob;
-          }
-          pg[j].x += v.x * h.x; pg[j].y += v.y * h.y; pg[j].z += v.z * h.z; pg[j].w += v.w * h.w;
-          pb[j].x += v.x; pb[j].y += v.y; pb[j].z += v.z; pb[j].w += v.w;
-        }
-      }
+    for (int j = 0; j < NC4; ++j) {
+      gg[j] = bload4(rg, vo, 4096 * j);
+      pg[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+      pb[j] = pg[j];
     }
   }
+  // row rr's operands, or zeros when !ok (the statistics then come from row
+  // r0, an existing row, and are not used)
+  auto load = [&](int rr, bool ok, LnBwdRow<NC4>& o) {
+    const int rc = ok ? rr : r0;
+    o.mu = mean[rc];
+    o.rs = rstd[rc];
+    const int nb = ok ? 4 * d : 0;
+    const auto rd = rsrc(dy + (long)rc * lddy, nb);
+    const auto rx = rsrc(x + (long)rc * row_stride * ldx, nb);
+    const auto rr_ = rsrc(dres + (long)rc * row_stride * ldres, nb);
+#pragma unroll
+    for (int j = 0; j < NC4; ++j) {
+      o.dy[j] = bload4(rd, vo, 4096 * j);
+      o.x[j] = bload4(rx, vo, 4096 * j);
+      o.res[j] = bload4(rr_, vo, 4096 * j);
+    }
+  };
+  auto process = [&](int row, int par, const LnBwdRow<NC4>& c) {
+    float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+    for (int j = 0; j < NC4; ++j) {
+      const float4 v = c.dy[j], xv = c.x[j];
+      const float4 h = make_float4((xv.x - c.mu) * c.rs, (xv.y - c.mu) * c.rs,
+                                   (xv.z - c.mu) * c.rs, (xv.w - c.mu) * c.rs);
+      const float4 gy = make_float4(v.x * gg[j].x, v.y * gg[j].y, v.z * gg[j].z, v.w * gg[j].w);
+      s0 += gy.x + gy.y + gy.z + gy.w;  // columns past d: dy = 0, g = 0
+      s1 += gy.x * h.x + gy.y * h.y + gy.z * h.z + gy.w * h.w;
+    }
+    s0 = wave_sum(s0);
+    s1 = wave_sum(s1);
+    if (lane == 0) {
+      red[par][0][wave] = s0;
+      red[par][1][wave] = s1;
+    }
+    wait_lgkm0();
+    cta_barrier();
+    const float m1 = (red[par][0][0] + red[par][0][1] + red[par][0][2] + red[par][0][3]) / d;
+    const float m2 = (red[par][1][0] + red[par][1][1] + red[par][1][2] + red[par][1][3]) / d;
+    const auto rw = rsrc(dres + (long)row * row_stride * ldres, 4 * d);
+    const auto rb = dres_bf != nullptr ? rsrc(dres_bf + (long)row * ldbf, 2 * d) : rsrc(dres, 0);
+#pragma unroll
+    for (int j = 0; j < NC4; ++j) {
+      const float4 v = c.dy[j], xv = c.x[j];
+      const float4 h = make_float4((xv.x - c.mu) * c.rs, (xv.y - c.mu) * c.rs,
+                                   (xv.z - c.mu) * c.rs, (xv.w - c.mu) * c.rs);
+      float4 o = c.res[j];
+      o.x += c.rs * (v.x * gg[j].x - m1 - h.x * m2);
+      o.y += c.rs * (v.y * gg[j].y - m1 - h.y * m2);
+      o.z += c.rs * (v.z * gg[j].z - m1 - h.z * m2);
+      o.w += c.rs * (v.w * gg[j].w - m1 - h.w * m2);
+      bstore4(o, rw, vo, 4096 * j);
+      const bf16x4 ob = {f2bf(o.x), f2bf(o.y), f2bf(o.z), f2bf(o.w)};
+      __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, ob), rb, 8 * tid, 2048 * j, 0);
+      // columns past d: dy = 0, so the partial sums gain nothing there
+      pg[j].x += v.x * h.x; pg[j].y += v.y * h.y; pg[j].z += v.z * h.z; pg[j].w += v.w * h.w;
+      pb[j].x += v.x; pb[j].y += v.y; pb[j].z += v.z; pb[j].w += v.w;
+    }
+  };
+  LnBwdRow<NC4> A, B;
+  if (r0 < r1) load(r0, true, A);
+  for (int row = r0; row < r1; row += 2) {
+    load(row + 1, row + 1 < r1, B);
+    process(row, 0, A);
+    if (row + 1 >= r1) break;
+    load(row + 2, row + 2 < r1, A);
+    process(row + 1, 1, B);
+  }
+  // every workgroup writes its partial rows (zeros when it owns no row)
+  const auto rpg = rsrc(part_g + (long)blockIdx.x * d, 4 * d);
+  const auto rpb_ = rsrc(part_b + (long)blockIdx.x * d, 4 * d);
 #pragma unroll
   for (int j = 0; j < NC4; ++j) {
-    const int col = (j * 256 + tid) * 4;
-    if (col < d) {
-      *reinterpret_cast<float4*>(part_g + (long)blockIdx.x * d + col) = pg[j];
-      *reinterpret_cast<float4*>(part_b + (long)blockIdx.x * d + col) = pb[j];
-    }
+    bstore4(pg[j], rpg, vo, 4096 * j);
+    bstore4(pb[j], rpb_, vo, 4096 * j);
   }
 }
 
-// out[c] = sum_p part[p, c] in a fixed order: wave w sums p = w, w + 8, ...,
-// then the eight wave sums are added in order.  64 columns per workgroup.
 // out[c] = sum over p of part[p * d + c].  A workgroup owns 16 columns: 64
 // row lanes of 4 threads (4 columns each, one 16-byte load per row), then a
 // fixed-order tree over the row lanes, so the sum does not depend on timing.
+// blockIdx.y = 1 sums the second array of partials, part + n_part * d, into
+// out1 (the LayerNorm backward's gain and shift partials in one launch).
 template <bool VEC>
-__global__ __launch_bounds__(256) void colsum_partials_kernel(const float* __restrict__ part,
+__global__ __launch_bounds__(256) void colsum_partials_kernel(const float* __restrict__ part0,
                                                               int n_part, int d,
-                                                              float* __restrict__ out) {
+                                                              float* __restrict__ out0,
+                                                              float* __restrict__ out1) {
   __shared__ float4 red[64][4];
+  const float* part = part0 + (long)blockIdx.y * n_part * d;
+  float* out = blockIdx.y ? out1 : out0;
   const int c4 = threadIdx.x & 3, rl = threadIdx.x >> 2;
   const int c = blockIdx.x * 16 + 4 * c4;
   float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -421,20 +454,39 @@ hipError_t launch_layernorm_bwd(const float* dy, long lddy, const float* x, long
 #undef LNB
 }
 
-int ln_bwd_parts(int rows) { return rows < 1024 ? rows : 1024; }
+// Workgroups (and partial rows) of the backward: 512 for rows wider than 1024
+// (two per CU, each with two rows of 3 x 4 d bytes in flight), 1024 for
+// narrower rows, which need more workgroups for the same bytes in flight.
+// Fewer partial rows also shorten the column sums that follow.
+int ln_bwd_parts(int rows, int d) {
+  const int cap = d > 1024 ? 512 : 1024;
+  return rows < cap ? rows : cap;
+}
+
+static hipError_t colsum_partials(const float* part, int n_part, int d, float* out0, float* out1,
+                                  int n_arrays, hipStream_t s) {
+  if (d <= 0) return hipSuccess;
+  const bool vec = d % 4 == 0 && (reinterpret_cast<uintptr_t>(part) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(out0) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(out1) & 15) == 0;
+  const dim3 grid(sat_cdiv(d, 16), n_arrays);
+  if (vec)
+    hipLaunchKernelGGL(colsum_partials_kernel<true>, grid, dim3(256), 0, s, part, n_part, d, out0,
+                       out1);
+  else
+    hipLaunchKernelGGL(colsum_partials_kernel<false>, grid, dim3(256), 0, s, part, n_part, d, out0,
+                       out1);
+  return hipGetLastError();
+}
 
 hipError_t launch_colsum_partials(const float* part, int n_part, int d, float* out,
                                   hipStream_t s) {
-  if (d <= 0) return hipSuccess;
-  const bool vec = d % 4 == 0 && (reinterpret_cast<uintptr_t>(part) & 15) == 0 &&
-                   (reinterpret_cast<uintptr_t>(out) & 15) == 0;
-  if (vec)
-    hipLaunchKernelGGL(colsum_partials_kernel<true>, dim3(sat_cdiv(d, 16)), dim3(256), 0, s, part,
-                       n_part, d, out);
-  else
-    hipLaunchKernelGGL(colsum_partials_kernel<false>, dim3(sat_cdiv(d, 16)), dim3(256), 0, s, part,
-                       n_part, d, out);
-  return hipGetLastError();
+  return colsum_partials(part, n_part, d, out, out, 1, s);
+}
+
+hipError_t launch_ln_bwd_colsums(const float* part, int n_part, int d, float* dg, float* db,
+                                 hipStream_t s) {
+  return colsum_partials(part, n_part, d, dg, db, 2, s);
 }
 
 template <typename T>

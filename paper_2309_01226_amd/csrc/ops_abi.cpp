@@ -151,11 +151,10 @@ extern "C" sat_status sat_op_layernorm_bwd(const float* dy, int64_t lddy, const 
   SAT_CHECK_ARG(lddy >= d && lddy % 4 == 0 && ldx >= d && ldx % 4 == 0 && ldres >= d &&
                     ldres % 4 == 0 && row_stride >= 1,
                 "layernorm_bwd: bad leading dimensions");
-  const int n_part = ln_bwd_parts(rows);
+  const int n_part = ln_bwd_parts(rows, d);
   SAT_HIP(launch_layernorm_bwd(dy, lddy, x, ldx, row_stride, g, mean, rstd, dres, ldres, work,
                                work + (long)n_part * d, rows, d, n_part, S(stream)));
-  SAT_HIP(launch_colsum_partials(work, n_part, d, dg, S(stream)));
-  SAT_HIP(launch_colsum_partials(work + (long)n_part * d, n_part, d, db, S(stream)));
+  SAT_HIP(launch_ln_bwd_colsums(work, n_part, d, dg, db, S(stream)));
   return SAT_OK;
 }
 

@@ -301,7 +301,7 @@ static sat_status side_join(sat_model* M) {
 static sat_status ln_bwd(sat_model* M, const float* dy, const float* x, long row_stride,
                          int gidx, const float* mean, const float* rstd, int rows) {
   const int d = M->D.d;
-  const int np_ = ln_bwd_parts(rows);
+  const int np_ = ln_bwd_parts(rows, d);
   float* pg = M->part;
   float* pbb = M->part + (size_t)np_ * d;
   {
@@ -309,8 +309,7 @@ static sat_status ln_bwd(sat_model* M, const float* dy, const float* x, long row
     SAT_HIP(launch_layernorm_bwd(dy, d, x, d, row_stride, master(M, gidx), mean, rstd, M->dh, d, pg,
                                  pbb, rows, d, np_, M->stream, M->dh_bf, d));
   }
-  SAT_HIP(launch_colsum_partials(pg, np_, d, grad(M, gidx), M->stream));
-  SAT_HIP(launch_colsum_partials(pbb, np_, d, grad(M, gidx + 1), M->stream));
+  SAT_HIP(launch_ln_bwd_colsums(pg, np_, d, grad(M, gidx), grad(M, gidx + 1), M->stream));
   return SAT_OK;
 }
 
@@ -340,7 +339,7 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
     SAT_HIP(launch_zero(M->dh, (long)T * d * 4, s));
     const long rstride = (D.arch == SAT_VIT) ? D.S : 1;
     // LN_f backward writes rows r * rstride of dh (CLS rows for ViT)
-    const int np_ = ln_bwd_parts(R);
+    const int np_ = ln_bwd_parts(R, d);
     float* pg = M->part;
     float* pbb = M->part + (size_t)np_ * d;
     {
@@ -351,8 +350,7 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
     }
     if (rstride != 1)  // ViT: only the CLS rows of dh were written
       SAT_HIP(launch_f32_to_bf16(M->dh, d, M->dh_bf, d, T, d, s));
-    SAT_HIP(launch_colsum_partials(pg, np_, d, grad(M, hb + 0), s));
-    SAT_HIP(launch_colsum_partials(pbb, np_, d, grad(M, hb + 1), s));
+    SAT_HIP(launch_ln_bwd_colsums(pg, np_, d, grad(M, hb + 0), grad(M, hb + 1), s));
   }
 
   // ---- blocks L-1 .. k

@@ -216,22 +216,38 @@ def test_rotary(inverse, dh, rd):
 
 # ------------------------------------------------------------------ cross-entropy
 
-# rows of at most 53248 logits with 16-byte aligned rows stay in registers
-@pytest.mark.parametrize("N,V", [(7, 50257), (64, 512), (3, 1000), (7, 50400), (5, 53248), (4, 53256)])
-def test_cross_entropy(N, V):
-    flush(f"xent N={N} V={V}")
+# Rows of at most 53248 logits with 16-byte aligned rows stay in registers:
+# 512 threads for up to 12 groups of 2048 and for exactly 25 (the GPT
+# vocabularies, where only the last group can be ragged), 1024 threads for
+# the rest; wider or unaligned rows take the streaming kernel.  `pad` gives
+# the rows a leading dimension rounded up to 8 (as the model's logits have),
+# whose padding columns the kernel zeroes in dz.
+@pytest.mark.parametrize("N,V,pad", [
+    (7, 50257, True), (7, 50400, False), (3, 49153, True),   # 512 x 25, last group ragged
+    (64, 512, False), (3, 1000, False), (6, 6000, False),     # 512 x 1, 512 x 4
+    (5, 16000, False), (3, 20481, True),                      # 512 x 8, 512 x 12
+    (4, 40000, False), (5, 53248, False), (3, 51201, True),   # 1024 x 13
+    (4, 53256, False), (7, 50257, False)])                    # streaming kernel
+def test_cross_entropy(N, V, pad):
+    flush(f"xent N={N} V={V} pad={pad}")
     rng = np.random.default_rng(N + V)
     z = rng.normal(0, 3, size=(N, V)).astype(np.float32)
     lab = rng.integers(0, V, size=N).astype(np.int32)
     lab[1] = -1
+    lab[2] = V - 1
+    ld = (V + 7) // 8 * 8 if pad else V
+    zd = torch.zeros(N, ld, device="cuda")
+    zd[:, :V] = to_dev_f32(z)
     row = torch.empty(N, device="cuda")
-    dz = torch.empty(N, V, device="cuda", dtype=torch.bfloat16)
+    dz = torch.full((N, ld), 7.0, device="cuda", dtype=torch.bfloat16)
     inv_n = torch.empty(1, device="cuda")
-    ops().cross_entropy(to_dev_f32(z), torch.as_tensor(lab).cuda(), row, dz, inv_n, N, V)
+    ops().cross_entropy(zd, torch.as_tensor(lab).cuda(), row, dz, inv_n, N, V, ldz=ld, lddz=ld)
     torch.cuda.synchronize()
     rrow, rdz, _ = O.cross_entropy(z, lab)
     assert rel(host(row), rrow) < 1e-5
-    assert rel(host(dz), rdz) < 4e-3
+    got = host(dz)
+    assert rel(got[:, :V], rdz) < 4e-3
+    assert np.all(got[:, V:] == 0.0)
     assert abs(host(inv_n)[0] * (N - 1) - 1.0) < 1e-7
 
 
