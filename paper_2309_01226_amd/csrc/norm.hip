@@ -13,6 +13,9 @@
 namespace {
 
 constexpr int LN_MAXC = 32;  // float4 chunks per lane: d <= 64 * 4 * 32 = 8192
+#ifndef LN_FWD_GRID
+#define LN_FWD_GRID 1024
+#endif
 
 template <int NC>
 __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x, long ldx,
@@ -66,91 +69,6 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x
   }
 }
 
-// Wide rows (d >= 1024): each workgroup walks the rows blockIdx.x,
-// blockIdx.x + gridDim.x, ..., each thread holding NCH float4 chunks of a row
-// (columns (c * 256 + tid) * 4 .. +3); the two row sums are combined across
-// the four waves through LDS in a fixed order.  The next row's loads are
-// issued before the current row is reduced and stored, so every workgroup
-// keeps reads in flight while it writes (a grid of one workgroup per row
-// gets the same overlap only between dispatch rounds).  The gain and shift
-// chunks are loaded once per workgroup.
-template <int NCH>
-__global__ __launch_bounds__(256) void ln_fwd_wg_kernel(const float* __restrict__ x, long ldx,
-                                                        long row_stride,
-                                                        const float* __restrict__ g,
-                                                        const float* __restrict__ b,
-                                                        bf16* __restrict__ y, long ldy,
-                                                        float* __restrict__ mean,
-                                                        float* __restrict__ rstd, int rows, int d,
-                                                        float eps) {
-  __shared__ float red[2][4];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  float4 v[NCH], vn[NCH], gg[NCH], bb[NCH];
-  int row = blockIdx.x;
-#pragma unroll
-  for (int c = 0; c < NCH; ++c) {
-    const int col = (c * 256 + tid) * 4;
-    const float* xr = x + (long)row * row_stride * ldx;
-    v[c] = col < d ? *reinterpret_cast<const float4*>(xr + col) : make_float4(0.f, 0.f, 0.f, 0.f);
-  }
-#pragma unroll
-  for (int c = 0; c < NCH; ++c) {
-    const int col = (c * 256 + tid) * 4;
-    gg[c] = col < d ? *reinterpret_cast<const float4*>(g + col) : make_float4(0.f, 0.f, 0.f, 0.f);
-    bb[c] = col < d ? *reinterpret_cast<const float4*>(b + col) : make_float4(0.f, 0.f, 0.f, 0.f);
-  }
-  for (; row < rows; row += gridDim.x) {
-    const int nrow = row + (int)gridDim.x;
-    if (nrow < rows) {
-      const float* xn = x + (long)nrow * row_stride * ldx;
-#pragma unroll
-      for (int c = 0; c < NCH; ++c) {
-        const int col = (c * 256 + tid) * 4;
-        vn[c] = col < d ? *reinterpret_cast<const float4*>(xn + col) : make_float4(0.f, 0.f, 0.f, 0.f);
-      }
-    }
-    float s = 0.f;
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) s += v[c].x + v[c].y + v[c].z + v[c].w;
-    s = wave_sum(s);
-    if (lane == 0) red[0][wave] = s;
-    __syncthreads();
-    const float mu = (red[0][0] + red[0][1] + red[0][2] + red[0][3]) / d;
-    float q = 0.f;
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      const int col = (c * 256 + tid) * 4;
-      if (col < d) {
-        const float a0 = v[c].x - mu, a1 = v[c].y - mu, a2 = v[c].z - mu, a3 = v[c].w - mu;
-        q += a0 * a0 + a1 * a1 + a2 * a2 + a3 * a3;
-      }
-    }
-    q = wave_sum(q);
-    if (lane == 0) red[1][wave] = q;
-    __syncthreads();
-    const float rs = rsqrtf((red[1][0] + red[1][1] + red[1][2] + red[1][3]) / d + eps);
-    bf16* yr = y + (long)row * ldy;
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      const int col = (c * 256 + tid) * 4;
-      if (col < d) {
-        bf16x4 o;
-        o[0] = f2bf((v[c].x - mu) * rs * gg[c].x + bb[c].x);
-        o[1] = f2bf((v[c].y - mu) * rs * gg[c].y + bb[c].y);
-        o[2] = f2bf((v[c].z - mu) * rs * gg[c].z + bb[c].z);
-        o[3] = f2bf((v[c].w - mu) * rs * gg[c].w + bb[c].w);
-        *reinterpret_cast<bf16x4*>(yr + col) = o;
-      }
-    }
-    if (tid == 0) {
-      mean[row] = mu;
-      rstd[row] = rs;
-    }
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) v[c] = vn[c];
-  }
-}
-
 // s_waitcnt lgkmcnt(0) only: vector loads may stay in flight across it.
 __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xF | (3 << 14) | (7 << 4)); }
 // Workgroup barrier with no implied wait for vector memory (the compiler's
@@ -174,6 +92,105 @@ __device__ __forceinline__ float4 bload4(__amdgpu_buffer_rsrc_t r, int vo, int s
 __device__ __forceinline__ void bstore4(float4 v, __amdgpu_buffer_rsrc_t r, int vo, int so) {
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, floatx4{v.x, v.y, v.z, v.w}), r, vo,
                                          so, 0);
+}
+// N stores into an empty buffer range (dropped by the range check, counted by
+// the vector-memory counter).  Issued between the first row's loads and the
+// loop, they give the loop's entry the same count of operations after those
+// loads as its back edge has (the previous row's stores), so the compiler's
+// wait at the loop head does not also wait for the previous row's stores.
+template <int N>
+__device__ __forceinline__ void vm_pad(const void* any) {
+  const auto r = rsrc(any, 0);
+  // volatile (bit 31 of the auxiliary argument): kept one by one, never merged
+#pragma unroll
+  for (int i = 0; i < N; ++i) __builtin_amdgcn_raw_buffer_store_b32(0u, r, 4 * i, 0, (int)0x80000000u);
+}
+
+// Wide rows (d >= 1024): workgroup w walks the rows w, w + gridDim.x, ...,
+// each thread holding NCH float4 chunks of a row (columns (c * 256 + tid) * 4
+// .. +3).  The loop is software pipelined like the backward's: the next row
+// is loaded into the other of two register sets before the current one is
+// reduced and written (unrolled by two, so no set is copied), and every row
+// access is a buffer instruction, so columns past d need no branch (reads give
+// 0, writes are dropped) and the compiler's wait counts stay exact.  Mean and
+// variance are two passes over the register copy (x is read from HBM once);
+// the row sums are combined across the four waves through LDS in a fixed
+// order, with barriers that do not wait for the next row's loads.  The gain
+// and shift chunks are loaded once per workgroup.
+template <int NCH>
+__global__ __launch_bounds__(256) void ln_fwd_wg_kernel(const float* __restrict__ x, long ldx,
+                                                        long row_stride,
+                                                        const float* __restrict__ g,
+                                                        const float* __restrict__ b,
+                                                        bf16* __restrict__ y, long ldy,
+                                                        float* __restrict__ mean,
+                                                        float* __restrict__ rstd, int rows, int d,
+                                                        float eps) {
+  __shared__ float red[2][2][4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int vo = 16 * tid;  // byte offset of the thread's columns; chunk c adds 4096 c
+  float4 gg[NCH], bb[NCH];
+  bool in[NCH];
+  {
+    const auto rg = rsrc(g, 4 * d), rb = rsrc(b, 4 * d);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      gg[c] = bload4(rg, vo, 4096 * c);
+      bb[c] = bload4(rb, vo, 4096 * c);
+      in[c] = (c * 256 + tid) * 4 < d;
+    }
+  }
+  auto load = [&](int row, bool ok, float4* v) {
+    const auto rx = rsrc(x + (long)(ok ? row : 0) * row_stride * ldx, ok ? 4 * d : 0);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) v[c] = bload4(rx, vo, 4096 * c);
+  };
+  auto process = [&](int row, int par, const float4* v) {
+    float s = 0.f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) s += v[c].x + v[c].y + v[c].z + v[c].w;  // 0 past d
+    s = wave_sum(s);
+    if (lane == 0) red[par][0][wave] = s;
+    wait_lgkm0();
+    cta_barrier();
+    const float mu = (red[par][0][0] + red[par][0][1] + red[par][0][2] + red[par][0][3]) / d;
+    float q = 0.f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const float a0 = v[c].x - mu, a1 = v[c].y - mu, a2 = v[c].z - mu, a3 = v[c].w - mu;
+      q += in[c] ? a0 * a0 + a1 * a1 + a2 * a2 + a3 * a3 : 0.f;
+    }
+    q = wave_sum(q);
+    if (lane == 0) red[par][1][wave] = q;
+    wait_lgkm0();
+    cta_barrier();
+    const float rs = rsqrtf((red[par][1][0] + red[par][1][1] + red[par][1][2] + red[par][1][3]) / d + eps);
+    const auto ry = rsrc(y + (long)row * ldy, 2 * d);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const bf16x4 o = {f2bf((v[c].x - mu) * rs * gg[c].x + bb[c].x),
+                        f2bf((v[c].y - mu) * rs * gg[c].y + bb[c].y),
+                        f2bf((v[c].z - mu) * rs * gg[c].z + bb[c].z),
+                        f2bf((v[c].w - mu) * rs * gg[c].w + bb[c].w)};
+      __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, o), ry, 8 * tid, 2048 * c, 0);
+    }
+    // the statistics: every lane stores, all but thread 0 past the 4-byte range
+    const int so = tid == 0 ? 0 : 4;
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, mu), rsrc(mean + row, 4), so, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, rs), rsrc(rstd + row, 4), so, 0, 0);
+  };
+  const int step = gridDim.x;
+  float4 A[NCH], B[NCH];
+  int row = blockIdx.x;
+  if (row < rows) load(row, true, A);
+  vm_pad<NCH + 2>(y);  // a row's stores: NCH chunks of y, mean, rstd
+  for (; row < rows; row += 2 * step) {
+    load(row + step, row + step < rows, B);
+    process(row, 0, A);
+    if (row + step >= rows) break;
+    load(row + 2 * step, row + 2 * step < rows, A);
+    process(row + step, 1, B);
+  }
 }
 
 // One row of the backward's operands: dy, x and the residual gradient for
@@ -277,6 +294,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(
   };
   LnBwdRow<NC4> A, B;
   if (r0 < r1) load(r0, true, A);
+  vm_pad<2 * NC4>(dres);  // a row's stores: NC4 chunks of the residual gradient and its bf16 copy
   for (int row = r0; row < r1; row += 2) {
     load(row + 1, row + 1 < r1, B);
     process(row, 0, A);
@@ -391,8 +409,8 @@ template <int NCH>
 hipError_t ln_fwd_wg_launch(const float* x, long ldx, long rs, const float* g, const float* b,
                             bf16* y, long ldy, float* mean, float* rstd, int rows, int d, float eps,
                             hipStream_t s) {
-  // enough workgroups for 8 per CU on 256 CUs; each walks rows / grid rows
-  const int grid = rows < 2048 ? rows : 2048;
+  // workgroups that walk rows / grid rows each, two rows in flight per workgroup
+  const int grid = rows < LN_FWD_GRID ? rows : LN_FWD_GRID;
   hipLaunchKernelGGL(ln_fwd_wg_kernel<NCH>, dim3(grid), dim3(256), 0, s, x, ldx, rs, g, b, y, ldy,
                      mean, rstd, rows, d, eps);
   return hipGetLastError();
