@@ -386,6 +386,9 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, floatx16 (&acc)[4][4
 // which the transposed copy is written as 16-byte pieces of 8 rows.  Element
 // loads and stores stream past the caches: every byte is touched once.
 constexpr int TP = 40;  // bf16 pitch of one column of the transposed staging
+#ifndef ADAMW_PD
+#define ADAMW_PD 2  // groups of four rows whose loads run ahead of the update
+#endif
 
 __device__ __forceinline__ void epilogue_adamw(const GemmArgs& p, floatx16 (&acc)[4][4],
                                                float* stage, int m0, int n0, int wave, int lane) {
@@ -413,6 +416,34 @@ __device__ __forceinline__ void epilogue_adamw(const GemmArgs& p, floatx16 (&acc
   const bool keep = p.out != nullptr;
   const __amdgpu_buffer_rsrc_t rG =
       rsrc(keep ? reinterpret_cast<float*>(p.out) + (long)m0 * p.ldo : p.opt_p);
+  // The wave's 128 rows are 16 groups of four rows per lane (slab k / 4, group
+  // k % 4 of it), software-pipelined across the slabs: the loads of group
+  // k + ADAMW_PD are issued before group k is updated and stored, so
+  // ADAMW_PD groups (12 KB per wave each) are in flight while the wave
+  // computes.  A wave's one vmcnt counts loads and stores in issue order, so
+  // the loads must precede the stores they are to overlap.
+  auto offs = [&](int k, int u, uint32_t& oe, uint32_t& og) {
+    const int r0 = wm * 128 + 32 * (k >> 2);
+    const int rl = 2 * (4 * (k & 3) + u) + (lane >> 5);
+    const bool ok = colok && m0 + r0 + rl < p.M;
+    oe = ok ? (uint32_t)(((long)(r0 + rl) * N + col) * 4) : OOB;
+    og = ok ? (uint32_t)(((long)(r0 + rl) * p.ldo + col) * 4) : OOB;
+  };
+  constexpr int NB = ADAMW_PD + 1;
+  floatx4 pv[NB][4], mv[NB][4], vv[NB][4];
+  auto load = [&](int k) {
+    const int buf = k % NB;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      uint32_t oe, og;
+      offs(k, u, oe, og);
+      pv[buf][u] = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(rP, oe, 0, NT_AUX));
+      mv[buf][u] = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(rM, oe, 0, NT_AUX));
+      vv[buf][u] = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(rV, oe, 0, NT_AUX));
+    }
+  };
+#pragma unroll
+  for (int k = 0; k < ADAMW_PD; ++k) load(k);
   // fully unrolled: a slab index that is not a compile-time constant would put
   // the accumulators in scratch memory
 #pragma unroll
@@ -424,36 +455,15 @@ __device__ __forceinline__ void epilogue_adamw(const GemmArgs& p, floatx16 (&acc
 #pragma unroll
       for (int r = 0; r < 16; ++r)
         st[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * EP + 32 * j + (lane & 31)] = acc[i][j][r];
-    // Four groups of four rows per lane, software-pipelined: the loads of
-    // group g + 1 are issued before the stores of group g, because a wave's
-    // one vmcnt counts loads and stores in issue order.
-    auto offs = [&](int g, int u, uint32_t& oe, uint32_t& og) {
-      const int rl = 2 * (4 * g + u) + (lane >> 5);
-      const bool ok = colok && rowbase + rl < p.M;
-      oe = ok ? (uint32_t)(((long)(r0 + rl) * N + col) * 4) : OOB;
-      og = ok ? (uint32_t)(((long)(r0 + rl) * p.ldo + col) * 4) : OOB;
-    };
-    floatx4 pv[2][4], mv[2][4], vv[2][4];
-    auto load = [&](int g, int buf) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        uint32_t oe, og;
-        offs(g, u, oe, og);
-        pv[buf][u] = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(rP, oe, 0, NT_AUX));
-        mv[buf][u] = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(rM, oe, 0, NT_AUX));
-        vv[buf][u] = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(rV, oe, 0, NT_AUX));
-      }
-    };
-    load(0, 0);
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const int buf = g & 1;
-      if (g + 1 < 4) load(g + 1, buf ^ 1);
+      const int k = 4 * i + g, buf = k % NB;
+      if (k + ADAMW_PD < 16) load(k + ADAMW_PD);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int rl = 2 * (4 * g + u) + (lane >> 5);
         uint32_t oe, og;
-        offs(g, u, oe, og);
+        offs(k, u, oe, og);
         const floatx4 gv = *reinterpret_cast<const floatx4*>(st + rl * EP + cl);
         floatx4 pp = pv[buf][u], mm = mv[buf][u], vq = vv[buf][u];
         adamw_four(pp, gv, mm, vq, c);
