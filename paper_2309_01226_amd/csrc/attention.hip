@@ -386,18 +386,6 @@ struct VtTile {  // V^T block in LDS: DH rows (head dims) of FBKV keys
   }
 };
 
-template <int VM>
-__device__ __forceinline__ void wait_vm_lgkm0() {
-  static_assert(VM >= 0 && VM < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4));
-}
-__device__ __forceinline__ void cta_barrier() {
-  __builtin_amdgcn_sched_barrier(0);
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_s_barrier();
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_sched_barrier(0);
-}
 // Wait until at most n' vector loads of this wave are in flight (and all LDS
 // operations are done), n' the largest of {0, 2, 4, 6, 8, 10, 12, 16} not
 // above `n` (wave-uniform).
@@ -763,10 +751,6 @@ __global__ __launch_bounds__(NT) void attn_bwd_dkdv_kernel(AttnBwdArgs a) {
 // blocks ahead; one barrier per block.
 constexpr int BQB = 32;  // query rows per block (dK/dV kernels)
 constexpr int BKB = 32;  // key rows per block (dQ kernel)
-
-__device__ __forceinline__ void wait_lgkm0() {
-  __builtin_amdgcn_s_waitcnt(0xF | (3 << 14) | (7 << 4));  // lgkmcnt(0), vmcnt and expcnt untouched
-}
 
 // dK/dV stage: Q rows, dO rows, Q^T, dO^T, lse * log2(e) and delta of 32 queries.
 template <int DH>

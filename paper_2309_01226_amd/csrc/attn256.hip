@@ -53,21 +53,6 @@ __device__ __forceinline__ lds_void* lds(const bf16* p) { return (lds_void*)(con
 __device__ __forceinline__ int swz_row(int r) { return r & 15; }
 __device__ __forceinline__ int swz_tr(int r) { return (0xEA40 >> ((r & 3) << 2)) & 15; }
 
-template <int VM>
-__device__ __forceinline__ void wait_vm_lgkm0() {
-  static_assert(VM >= 0 && VM < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4));
-}
-// s_waitcnt lgkmcnt(0) only (vector loads may stay in flight)
-__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xF | (3 << 14) | (7 << 4)); }
-__device__ __forceinline__ void cta_barrier() {
-  __builtin_amdgcn_sched_barrier(0);
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_s_barrier();
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_sched_barrier(0);
-}
-
 __device__ __forceinline__ floatx16 zero16() {
   floatx16 z;
 #pragma unroll

@@ -1,6 +1,7 @@
 // Shared device-side helpers for the gfx950 (CDNA4) kernels of the
 // fine-tuning step: bf16 storage type, vector types for the MFMA operands,
-// wavefront reductions and the launch-error plumbing.
+// wavefront reductions, explicit waits and barriers, and the launch-error
+// plumbing.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -18,6 +19,31 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ float bf2f(bf16 x) { return (float)x; }
 __device__ __forceinline__ bf16 f2bf(float x) { return (bf16)x; }
+
+// Explicit waits.  A wave's vmcnt counts its vector loads, stores and LDS
+// copies in issue order; the compiler's own waits are only as precise as its
+// view of that order, so the pipelined kernels wait for exactly what they
+// need.  The encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8.
+// s_waitcnt vmcnt(VM) lgkmcnt(0): at most VM vector memory operations of the
+// wave still in flight, every LDS and scalar memory operation done.
+template <int VM>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4));
+}
+// s_waitcnt lgkmcnt(0) only: vector memory operations may stay in flight.
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xF | (3 << 14) | (7 << 4)); }
+// Workgroup barrier with no implied wait: __syncthreads' fence would also
+// wait for every vector load in flight (the next block's copies, the next
+// row's loads).  Callers wait for what the barrier publishes first; the
+// scheduling barriers keep the compiler from moving work across it.
+__device__ __forceinline__ void cta_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_sched_barrier(0);
+}
 
 // Sum / max over the 64 lanes of a wavefront (butterfly through DPP-capable
 // shuffles; every lane receives the result).

@@ -407,21 +407,6 @@ __global__ __launch_bounds__(NT) void gemm_kernel_simple(GemmArgs p) {
 // tells the compiler that reads of one stage never wait on copies into the
 // other.
 
-// s_waitcnt vmcnt(VM) lgkmcnt(0)
-template <int VM>
-__device__ __forceinline__ void wait_vm_lgkm0() {
-  static_assert(VM >= 0 && VM < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4));
-}
-
-__device__ __forceinline__ void cta_barrier() {
-  __builtin_amdgcn_sched_barrier(0);
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_s_barrier();
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_sched_barrier(0);
-}
-
 // Operand of the pipelined loop: MODE OP_DMA (K-contiguous, straight to LDS)
 // or OP_MN (M/N-contiguous, through registers).
 template <int MODE, int ROWS>

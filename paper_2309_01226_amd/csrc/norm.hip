@@ -70,16 +70,6 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x
 }
 
 // s_waitcnt lgkmcnt(0) only: vector loads may stay in flight across it.
-__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xF | (3 << 14) | (7 << 4)); }
-// Workgroup barrier with no implied wait for vector memory (the compiler's
-// fence before __syncthreads would also wait for the next row's loads).
-__device__ __forceinline__ void cta_barrier() {
-  __builtin_amdgcn_sched_barrier(0);
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_s_barrier();
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_sched_barrier(0);
-}
 // Raw buffer resource over `bytes` bytes at p: accesses past the end read 0
 // and write nothing.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* p, int bytes) {
