@@ -179,13 +179,18 @@ __global__ __launch_bounds__(256) void embed_bwd_rows_kernel(const int32_t* __re
 }
 
 // ---------------------------------------------------------------- ViT
+// Rows of pitch ldo >= pd; the padding columns pd .. ldo - 1 are written as 0.
 __global__ void patchify_kernel(const float* __restrict__ img, bf16* __restrict__ out, int B,
-                                int C, int I, int p) {
+                                int C, int I, int p, int ldo) {
   const int g = I / p, np = g * g, pd = C * p * p;
   long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (long)B * np * pd) return;
-  int col = idx % pd;
-  long row = idx / pd;
+  if (idx >= (long)B * np * ldo) return;
+  int col = idx % ldo;
+  long row = idx / ldo;
+  if (col >= pd) {
+    out[idx] = f2bf(0.f);
+    return;
+  }
   int i = row % np, b = row / np;
   int c = col / (p * p), kh = (col / p) % p, kw = col % p;
   int pr = i / g, pc = i % g;
@@ -627,12 +632,13 @@ hipError_t launch_embed_bwd(const int32_t* tok, const float* dh, float* dwte, in
   return hipGetLastError();
 }
 
-hipError_t launch_patchify(const float* img, bf16* out, int B, int C, int I, int p,
+hipError_t launch_patchify(const float* img, bf16* out, int B, int C, int I, int p, int ldo,
                            hipStream_t s) {
-  long total = (long)B * (I / p) * (I / p) * C * p * p;
+  if (ldo < C * p * p) return hipErrorInvalidValue;
+  long total = (long)B * (I / p) * (I / p) * ldo;
   if (total <= 0) return hipSuccess;
   hipLaunchKernelGGL(patchify_kernel, dim3(blocks_for(total)), dim3(256), 0, s, img, out, B, C, I,
-                     p);
+                     p, ldo);
   return hipGetLastError();
 }
 

@@ -184,7 +184,7 @@ hipError_t launch_embed_fwd(const int32_t* tok, const float* wte, const float* w
 hipError_t launch_embed_bwd(const int32_t* tok, const float* dh, float* dwte, int T, int d,
                             int V, int32_t* work, hipStream_t s);
 // ViT: images [B, C, I, I] fp32 -> patches [B * np, C * p * p] bf16, (c, kh, kw) order.
-hipError_t launch_patchify(const float* img, bf16* out, int B, int C, int I, int p,
+hipError_t launch_patchify(const float* img, bf16* out, int B, int C, int I, int p, int ldo,
                            hipStream_t s);
 // ViT: h[b, 0] = cls + pos[0]; h[b, 1 + i] = z[b * np + i] + pos[1 + i]  (z holds bias).
 hipError_t launch_vit_assemble(const float* z, const float* cls, const float* pos, float* h,

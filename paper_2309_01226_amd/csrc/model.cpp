@@ -101,10 +101,12 @@ void sat_model_dims(const sat_config& c, Dims* d) {
     int g = c.img_size / c.patch;
     d->np = g * g;
     d->pd = c.channels * c.patch * c.patch;
+    d->pdp = (d->pd + 7) / 8 * 8;
     d->S = d->np + 1;
   } else {
     d->np = 0;
     d->pd = 0;
+    d->pdp = 0;
     d->S = c.seq_len;
   }
   d->T = d->B * d->S;
@@ -345,6 +347,7 @@ size_t carve(sat_model* M, char* base) {
     need(D.V, di, R);
     need(R, di, D.Vp);
     need(R, D.V, di);
+    if (D.arch == SAT_VIT) need(di, D.pd, D.B * D.np);  // the patch weight's gradient
     M->splitk_ws_elems = ws;
     M->splitk_ws = ws > 0 ? c.take<float>((size_t)ws) : nullptr;
   }
@@ -359,7 +362,7 @@ size_t carve(sat_model* M, char* base) {
   M->scal = c.take<float>(8);  // [0] loss, [1] 1 / n_valid
   // ViT input side
   if (D.arch == SAT_VIT) {
-    M->patches = c.take<bf16>((size_t)D.B * D.np * D.pd);
+    M->patches = c.take<bf16>((size_t)D.B * D.np * D.pdp);
     M->zpatch = c.take<float>((size_t)D.B * D.np * d);
     M->dzpatch = c.take<bf16>((size_t)D.B * D.np * d);
   }

@@ -18,6 +18,7 @@ struct Dims {
   int arch;
   int L, d, H, dh, m, V, Vp, B, S, T, k, rd;
   int np, pd;      // ViT: patches per image, values per patch
+  int pdp;         // ViT: pitch of a row of patch values (pd rounded up to 8)
   int rows_head;   // rows entering the head (T, or B for ViT)
   int qkv_ld;      // row pitch of the q|k|v (|u for GPT-J) buffer
   bool ckpt;       // activation checkpointing: one saved-activation set, recomputed per block

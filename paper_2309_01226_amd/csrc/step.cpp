@@ -187,8 +187,8 @@ sat_status sat_run_forward(sat_model* M, const void* inputs, const int32_t* labe
   // ---- embeddings
   if (D.arch == SAT_VIT) {
     SAT_HIP(launch_patchify((const float*)inputs, M->patches, D.B, M->cfg.channels,
-                            M->cfg.img_size, M->cfg.patch, s));
-    GemmArgs a = gargs(M->patches, D.pd, shadow(M, 0), D.pd, D.B * D.np, d, D.pd, M->zpatch, d);
+                            M->cfg.img_size, M->cfg.patch, D.pdp, s));
+    GemmArgs a = gargs(M->patches, D.pdp, shadow(M, 0), D.pd, D.B * D.np, d, D.pd, M->zpatch, d);
     a.bias = master(M, 1);
     TRY(gemm(M, a, LAY_K, LAY_K, EPI_F32));
     SAT_HIP(launch_vit_assemble(M->zpatch, master(M, 2), master(M, 3), M->h_in[0], D.B, D.np, d, s));
@@ -498,9 +498,17 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
       SAT_HIP(launch_sum_rows_batched(M->dh, grad(M, 3), D.B, D.S, d, s));
       SAT_HIP(hipMemcpyAsync(grad(M, 2), grad(M, 3), (size_t)d * 4, hipMemcpyDeviceToDevice, s));
       SAT_HIP(launch_vit_patch_grad(M->dh, M->dzpatch, D.B, D.np, d, s));
-      GemmArgs wp = gargs(M->dzpatch, d, M->patches, D.pd, d, D.pd, D.B * D.np, grad(M, 0), D.pd);
-      TRY(gemm(M, wp, LAY_MN, LAY_MN, EPI_F32));
-      int rows = D.B * D.np;
+      const int rows = D.B * D.np;
+      if (M->trans_blocks && rows % 8 == 0 && d % 8 == 0) {
+        // a reduction over every patch of the batch into a 1280 x 588 weight: on
+        // token-contiguous copies it runs split-K over the whole chip
+        SAT_HIP(launch_transpose_bf16(M->dzpatch, d, M->tA, rows, rows, d, s));
+        SAT_HIP(launch_transpose_bf16(M->patches, D.pdp, M->tB, rows, rows, D.pdp, s));
+        TRY(wgrad_t(M, s, M->tA, M->tB, d, D.pd, rows, 0));
+      } else {
+        GemmArgs wp = gargs(M->dzpatch, d, M->patches, D.pdp, d, D.pd, rows, grad(M, 0), D.pd);
+        TRY(gemm(M, wp, LAY_MN, LAY_MN, EPI_F32));
+      }
       SAT_HIP(launch_colsum_bf16(M->dzpatch, d, rows, d, M->part, rows < 256 ? rows : 256,
                                  grad(M, 1), s));
     } else {

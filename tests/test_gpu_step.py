@@ -42,6 +42,10 @@ CASES = {
                        seq_len=40, batch=2, rotary_dim=16, lr=1e-3),
     "small_vit": dict(arch="vit", n_layers=2, d_model=160, n_heads=2, d_mlp=320, vocab=10,
                       img_size=28, patch=14, channels=3, batch=4, lr=1e-3),
+    # 40 tokens and 32 patches: the weight-gradient products (and the patch
+    # weight's, over 588 values per patch) on token-contiguous copies
+    "small_vit_b8": dict(arch="vit", n_layers=2, d_model=160, n_heads=2, d_mlp=320, vocab=10,
+                         img_size=28, patch=14, channels=3, batch=8, lr=1e-3),
     "tiny_gpt2_k1": dict(arch="gpt2", n_layers=3, d_model=64, n_heads=4, d_mlp=256, vocab=512,
                          seq_len=32, batch=2, lr=1e-3, frozen_layers=1),
     "small_gptj_k1": dict(arch="gptj", n_layers=2, d_model=128, n_heads=2, d_mlp=256, vocab=97,
