@@ -314,7 +314,10 @@ def bandwidth_cold(kw, calls=8):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         # a bounded spin kernel ahead of the calls keeps the GPU behind the host,
         # so the calls run back to back and the Python launch path is not timed
-        torch.cuda._sleep(20_000_000)
+        # (without it, the figure includes the host's launch time)
+        spin = getattr(torch.cuda, "_sleep", None)
+        if spin is not None:
+            spin(20_000_000)
         e0.record()
         for i in range(1, n + 1):  # set 0 was just warmed: start past it
             fn(i)
