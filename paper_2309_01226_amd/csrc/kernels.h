@@ -111,9 +111,10 @@ hipError_t launch_layernorm_bwd(const float* dy, long lddy, const float* x, long
                                 long row_stride, const float* g, const float* mean,
                                 const float* rstd, float* dres, long ldres, float* part_g,
                                 float* part_b, int rows, int d, int n_part, hipStream_t s,
-                                bf16* dres_bf = nullptr, long ldbf = 0);
+                                bf16* dres_bf = nullptr, long ldbf = 0, float* part_o = nullptr);
 // dres_bf (row_stride 1 only; null: none): also writes the updated dres rows
-// rounded to bf16 at dres_bf + r * ldbf.
+// rounded to bf16 at dres_bf + r * ldbf.  part_o (null: none): a third array
+// of n_part partial rows, the column sums of the updated dres.
 // Partial-sum rows (workgroups) the LayerNorm backward uses for `rows` rows
 // of d: the dg / db partials take 2 * ln_bwd_parts(rows, d) * d floats (at
 // most 2 * min(rows, 1024) * d).
@@ -121,9 +122,10 @@ int ln_bwd_parts(int rows, int d);
 hipError_t launch_colsum_partials(const float* part, int n_part, int d, float* out,
                                   hipStream_t s);
 // dg = colsum of part[0 : n_part], db = colsum of part[n_part : 2 n_part]
-// (rows of d), one launch.
+// (rows of d), and with dbias also dbias = colsum of part[2 n_part : 3 n_part],
+// one launch.
 hipError_t launch_ln_bwd_colsums(const float* part, int n_part, int d, float* dg, float* db,
-                                 hipStream_t s);
+                                 hipStream_t s, float* dbias = nullptr);
 // out[c] = sum_r X[r, c] for a bf16 or fp32 matrix, deterministic two-pass.
 hipError_t launch_colsum_bf16(const bf16* X, long ldx, int rows, int cols, float* part,
                               int n_part, float* out, hipStream_t s);

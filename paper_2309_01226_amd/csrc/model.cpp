@@ -412,8 +412,10 @@ size_t carve(sat_model* M, char* base) {
   long wide = D.qkv_ld > D.Vp ? D.qkv_ld : D.Vp;
   if (D.arch == SAT_VIT && D.pd > wide) wide = D.pd;
   // column-sum partials: n_part rows of the widest bias; LayerNorm partials:
-  // ln_bwd_parts(rows, d) rows of d, for dg and db
-  const size_t lnp = (size_t)2 * ln_bwd_parts((int)std::max<long>(T, D.rows_head), d) * d;
+  // ln_bwd_parts(rows, d) rows of d, for dg and db (and the bias gradient of
+  // the residual product below, when the LayerNorm backward reduces it)
+  const size_t lnp = (size_t)(sat_bias_in_ln_bwd(D) ? 3 : 2) *
+                     ln_bwd_parts((int)std::max<long>(T, D.rows_head), d) * d;
   M->part = c.take<float>(std::max((size_t)2 * M->n_part * (wide > d ? wide : d), lnp));
   M->sortbuf = c.take<int32_t>(T > 0 ? T : 1);
   return align_up(c.off, kAlignBytes);

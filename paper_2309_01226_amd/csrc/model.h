@@ -189,6 +189,9 @@ struct sat_model {
 
 // The weight-gradient stream: created on first use, destroyed with the model.
 sat_status sat_side_ensure(sat_model* m);
+// Whether the LayerNorm backward also reduces the bias gradient of the residual
+// product below it (rows up to 2048 wide; wider rows use a separate column sum).
+inline bool sat_bias_in_ln_bwd(const Dims& D) { return D.d <= 2048; }
 void sat_side_destroy(sat_model* m);
 
 sat_status sat_validate_config(const sat_config* c);

@@ -202,19 +202,21 @@ struct LnBwdRow {
 // past d and a next row that does not exist need no branch (their reads give
 // 0, their writes are dropped) and the wait counts stay exact.  The two row
 // sums go through LDS in a fixed order (lane tree, then waves 0..3), one
-// barrier per row.  dy, x and the residual gradient are read once.
-template <int NC4>
+// barrier per row.  dy, x and the residual gradient are read once.  BIAS: a
+// third partial row at part_o, the column sums of the updated residual
+// gradient (the bias gradient of the product that last fed the residual).
+template <int NC4, bool BIAS>
 __global__ __launch_bounds__(256) void ln_bwd_kernel(
     const float* __restrict__ dy, long lddy, const float* __restrict__ x, long ldx,
     long row_stride, const float* __restrict__ g, const float* __restrict__ mean,
     const float* __restrict__ rstd, float* __restrict__ dres, long ldres,
     float* __restrict__ part_g, float* __restrict__ part_b, int rows, int d, int rpb,
-    bf16* __restrict__ dres_bf, long ldbf) {
+    bf16* __restrict__ dres_bf, long ldbf, float* __restrict__ part_o) {
   __shared__ float red[2][2][4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r0 = blockIdx.x * rpb, r1 = min(rows, r0 + rpb);
   const int vo = 16 * tid;  // byte offset of the thread's columns; column block j adds 4096 j
-  float4 gg[NC4], pg[NC4], pb[NC4];
+  float4 gg[NC4], pg[NC4], pb[NC4], po[NC4];
   {
     const auto rg = rsrc(g, 4 * d);
 #pragma unroll
@@ -222,6 +224,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(
       gg[j] = bload4(rg, vo, 4096 * j);
       pg[j] = make_float4(0.f, 0.f, 0.f, 0.f);
       pb[j] = pg[j];
+      po[j] = pg[j];
     }
   }
   // row rr's operands, or zeros when !ok (the statistics then come from row
@@ -277,9 +280,13 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(
       bstore4(o, rw, vo, 4096 * j);
       const bf16x4 ob = {f2bf(o.x), f2bf(o.y), f2bf(o.z), f2bf(o.w)};
       __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, ob), rb, 8 * tid, 2048 * j, 0);
-      // columns past d: dy = 0, so the partial sums gain nothing there
+      // columns past d: dy = 0, so the partial sums gain nothing there (the
+      // sums of o there are not stored)
       pg[j].x += v.x * h.x; pg[j].y += v.y * h.y; pg[j].z += v.z * h.z; pg[j].w += v.w * h.w;
       pb[j].x += v.x; pb[j].y += v.y; pb[j].z += v.z; pb[j].w += v.w;
+      if (BIAS) {
+        po[j].x += o.x; po[j].y += o.y; po[j].z += o.z; po[j].w += o.w;
+      }
     }
   };
   LnBwdRow<NC4> A, B;
@@ -300,21 +307,27 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(
     bstore4(pg[j], rpg, vo, 4096 * j);
     bstore4(pb[j], rpb_, vo, 4096 * j);
   }
+  if (BIAS) {
+    const auto rpo = rsrc(part_o + (long)blockIdx.x * d, 4 * d);
+#pragma unroll
+    for (int j = 0; j < NC4; ++j) bstore4(po[j], rpo, vo, 4096 * j);
+  }
 }
 
 // out[c] = sum over p of part[p * d + c].  A workgroup owns 16 columns: 64
 // row lanes of 4 threads (4 columns each, one 16-byte load per row), then a
 // fixed-order tree over the row lanes, so the sum does not depend on timing.
-// blockIdx.y = 1 sums the second array of partials, part + n_part * d, into
-// out1 (the LayerNorm backward's gain and shift partials in one launch).
+// blockIdx.y = 1 and 2 sum the next arrays of partials, part + y n_part d,
+// into out1 and out2 (the LayerNorm backward's partials in one launch).
 template <bool VEC>
 __global__ __launch_bounds__(256) void colsum_partials_kernel(const float* __restrict__ part0,
                                                               int n_part, int d,
                                                               float* __restrict__ out0,
-                                                              float* __restrict__ out1) {
+                                                              float* __restrict__ out1,
+                                                              float* __restrict__ out2) {
   __shared__ float4 red[64][4];
   const float* part = part0 + (long)blockIdx.y * n_part * d;
-  float* out = blockIdx.y ? out1 : out0;
+  float* out = blockIdx.y == 0 ? out0 : blockIdx.y == 1 ? out1 : out2;
   const int c4 = threadIdx.x & 3, rl = threadIdx.x >> 2;
   const int c = blockIdx.x * 16 + 4 * c4;
   float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -410,11 +423,15 @@ template <int NC4>
 hipError_t ln_bwd_launch(const float* dy, long lddy, const float* x, long ldx, long rs,
                          const float* g, const float* mean, const float* rstd, float* dres,
                          long ldres, float* pg, float* pb, int rows, int d, int n_part,
-                         hipStream_t s, bf16* dres_bf, long ldbf) {
+                         hipStream_t s, bf16* dres_bf, long ldbf, float* po) {
   // exactly n_part workgroups, so every partial row is written (zeros past the last row)
   const int rpb = sat_cdiv(rows, n_part);
-  hipLaunchKernelGGL(ln_bwd_kernel<NC4>, dim3(n_part), dim3(256), 0, s, dy, lddy, x,
-                     ldx, rs, g, mean, rstd, dres, ldres, pg, pb, rows, d, rpb, dres_bf, ldbf);
+  if (po != nullptr)
+    hipLaunchKernelGGL((ln_bwd_kernel<NC4, true>), dim3(n_part), dim3(256), 0, s, dy, lddy, x,
+                       ldx, rs, g, mean, rstd, dres, ldres, pg, pb, rows, d, rpb, dres_bf, ldbf, po);
+  else
+    hipLaunchKernelGGL((ln_bwd_kernel<NC4, false>), dim3(n_part), dim3(256), 0, s, dy, lddy, x,
+                       ldx, rs, g, mean, rstd, dres, ldres, pg, pb, rows, d, rpb, dres_bf, ldbf, po);
   return hipGetLastError();
 }
 
@@ -446,7 +463,7 @@ hipError_t launch_layernorm_bwd(const float* dy, long lddy, const float* x, long
                                 long row_stride, const float* g, const float* mean,
                                 const float* rstd, float* dres, long ldres, float* part_g,
                                 float* part_b, int rows, int d, int n_part, hipStream_t s,
-                                bf16* dres_bf, long ldbf) {
+                                bf16* dres_bf, long ldbf, float* part_o) {
   if (rows <= 0) return hipSuccess;
   if (dres_bf != nullptr && (row_stride != 1 || ldbf % 4 != 0 ||
                              (reinterpret_cast<uintptr_t>(dres_bf) & 7) != 0))
@@ -455,7 +472,7 @@ hipError_t launch_layernorm_bwd(const float* dy, long lddy, const float* x, long
       n_part <= 0)
     return hipErrorInvalidValue;
   const int nc = sat_cdiv(d, 1024);
-#define LNB(NC) ln_bwd_launch<NC>(dy, lddy, x, ldx, row_stride, g, mean, rstd, dres, ldres, part_g, part_b, rows, d, n_part, s, dres_bf, ldbf)
+#define LNB(NC) ln_bwd_launch<NC>(dy, lddy, x, ldx, row_stride, g, mean, rstd, dres, ldres, part_g, part_b, rows, d, n_part, s, dres_bf, ldbf, part_o)
   if (nc <= 1) return LNB(1);
   if (nc <= 2) return LNB(2);
   return LNB(4);
@@ -472,29 +489,28 @@ int ln_bwd_parts(int rows, int d) {
 }
 
 static hipError_t colsum_partials(const float* part, int n_part, int d, float* out0, float* out1,
-                                  int n_arrays, hipStream_t s) {
+                                  float* out2, int n_arrays, hipStream_t s) {
   if (d <= 0) return hipSuccess;
-  const bool vec = d % 4 == 0 && (reinterpret_cast<uintptr_t>(part) & 15) == 0 &&
-                   (reinterpret_cast<uintptr_t>(out0) & 15) == 0 &&
-                   (reinterpret_cast<uintptr_t>(out1) & 15) == 0;
+  auto a16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+  const bool vec = d % 4 == 0 && a16(part) && a16(out0) && a16(out1) && a16(out2);
   const dim3 grid(sat_cdiv(d, 16), n_arrays);
   if (vec)
     hipLaunchKernelGGL(colsum_partials_kernel<true>, grid, dim3(256), 0, s, part, n_part, d, out0,
-                       out1);
+                       out1, out2);
   else
     hipLaunchKernelGGL(colsum_partials_kernel<false>, grid, dim3(256), 0, s, part, n_part, d, out0,
-                       out1);
+                       out1, out2);
   return hipGetLastError();
 }
 
 hipError_t launch_colsum_partials(const float* part, int n_part, int d, float* out,
                                   hipStream_t s) {
-  return colsum_partials(part, n_part, d, out, out, 1, s);
+  return colsum_partials(part, n_part, d, out, out, out, 1, s);
 }
 
 hipError_t launch_ln_bwd_colsums(const float* part, int n_part, int d, float* dg, float* db,
-                                 hipStream_t s) {
-  return colsum_partials(part, n_part, d, dg, db, 2, s);
+                                 hipStream_t s, float* dbias) {
+  return colsum_partials(part, n_part, d, dg, db, dbias ? dbias : db, dbias ? 3 : 2, s);
 }
 
 template <typename T>

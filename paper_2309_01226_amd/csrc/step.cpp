@@ -297,20 +297,39 @@ static sat_status side_join(sat_model* M) {
 }
 
 // LayerNorm backward into the residual gradient dh, which it also rounds into
-// dh_bf, the bf16 copy the next products read.
+// dh_bf, the bf16 copy the next products read.  dbias (may be null): the bias
+// gradient of the residual product below, the column sums of the updated dh,
+// reduced in the same pass.
 static sat_status ln_bwd(sat_model* M, const float* dy, const float* x, long row_stride,
-                         int gidx, const float* mean, const float* rstd, int rows) {
+                         int gidx, const float* mean, const float* rstd, int rows,
+                         float* dbias = nullptr) {
   const int d = M->D.d;
   const int np_ = ln_bwd_parts(rows, d);
   float* pg = M->part;
   float* pbb = M->part + (size_t)np_ * d;
+  float* po = dbias ? M->part + (size_t)2 * np_ * d : nullptr;
   {
     Timed tm(M, TK_LN_BWD, ln_bwd_bytes(rows, d, true));
     SAT_HIP(launch_layernorm_bwd(dy, d, x, d, row_stride, master(M, gidx), mean, rstd, M->dh, d, pg,
-                                 pbb, rows, d, np_, M->stream, M->dh_bf, d));
+                                 pbb, rows, d, np_, M->stream, M->dh_bf, d, po));
   }
-  SAT_HIP(launch_ln_bwd_colsums(pg, np_, d, grad(M, gidx), grad(M, gidx + 1), M->stream));
+  SAT_HIP(launch_ln_bwd_colsums(pg, np_, d, grad(M, gidx), grad(M, gidx + 1), M->stream, dbias));
   return SAT_OK;
+}
+
+// The bias gradients of the residual products (fc2; for GPT-2 / ViT also the
+// out-projection) are the column sums of the residual gradient dh that the
+// LayerNorm backward above them leaves.  For rows up to 2048 wide that pass
+// reduces them as a third partial row (no separate read of dh).  For wider
+// rows the extra registers and adds in it cost more than a separate column
+// sum (GPT-J's 4096-wide rows: 0.6 ms per step slower).
+static bool bias_in_ln_bwd(const sat_model* M) { return sat_bias_in_ln_bwd(M->D); }
+
+// Where the LayerNorm backward above block l reduces block l's fc2 bias
+// gradient: null when block l is frozen or the sum runs separately.
+static float* fc2_bias_grad(sat_model* M, int l) {
+  if (l < M->D.k || l < 0 || !bias_in_ln_bwd(M)) return nullptr;
+  return grad(M, block_base(M, l) + (M->D.arch == SAT_GPTJ ? J_FC2B : B_FC2B));
 }
 
 sat_status sat_run_backward(sat_model* M, const void* inputs) {
@@ -339,18 +358,22 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
     SAT_HIP(launch_zero(M->dh, (long)T * d * 4, s));
     const long rstride = (D.arch == SAT_VIT) ? D.S : 1;
     // LN_f backward writes rows r * rstride of dh (CLS rows for ViT)
+    // (the column sums of dh, zero outside those rows, are the top block's fc2
+    // bias gradient)
     const int np_ = ln_bwd_parts(R, d);
     float* pg = M->part;
     float* pbb = M->part + (size_t)np_ * d;
+    float* dbias_top = fc2_bias_grad(M, D.L - 1);
+    float* po = dbias_top ? M->part + (size_t)2 * np_ * d : nullptr;
     {
       Timed tm(M, TK_LN_BWD, ln_bwd_bytes(R, d, rstride == 1));
       SAT_HIP(launch_layernorm_bwd(M->dA, d, M->h_in[D.L], d, rstride, master(M, hb + 0),
                                    M->meanf, M->rstdf, M->dh, d, pg, pbb, R, d, np_, s,
-                                   rstride == 1 ? M->dh_bf : nullptr, d));
+                                   rstride == 1 ? M->dh_bf : nullptr, d, po));
     }
     if (rstride != 1)  // ViT: only the CLS rows of dh were written
       SAT_HIP(launch_f32_to_bf16(M->dh, d, M->dh_bf, d, T, d, s));
-    SAT_HIP(launch_ln_bwd_colsums(pg, np_, d, grad(M, hb + 0), grad(M, hb + 1), s));
+    SAT_HIP(launch_ln_bwd_colsums(pg, np_, d, grad(M, hb + 0), grad(M, hb + 1), s, dbias_top));
   }
 
   // ---- blocks L-1 .. k
@@ -394,7 +417,8 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
     // updated dh (the head's, or the block above's)
     if (gptj) {
       const bool tr = M->trans_blocks;
-      SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + J_FC2B), s));
+      if (!bias_in_ln_bwd(M))
+        SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + J_FC2B), s));
       GemmArgs du = gargs(M->dh_bf, d, shadow_t(M, pb + J_FC2W), d, T, m, d, M->dqkv + 3 * d, D.qkv_ld);
       du.aux = A.qkv + 3 * d;
       du.ldaux = D.qkv_ld;
@@ -433,10 +457,12 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
       }
       SAT_HIP(launch_colsum_bf16(M->dqkv + 3 * d, D.qkv_ld, T, m, M->part, npT,
                                  grad(M, pb + J_FC1B), s));
-      TRY(ln_bwd(M, M->dA, M->h_in[l], 1, pb + J_LN1G, A.mean1, A.rstd1, T));
+      TRY(ln_bwd(M, M->dA, M->h_in[l], 1, pb + J_LN1G, A.mean1, A.rstd1, T,
+                 fc2_bias_grad(M, l - 1)));
     } else {
       const bool tr = M->trans_blocks;
-      SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + B_FC2B), s));
+      if (!bias_in_ln_bwd(M))
+        SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + B_FC2B), s));
       GemmArgs du = gargs(M->dh_bf, d, shadow_t(M, pb + B_FC2W), d, T, m, d, M->du, m);
       du.aux = A.u;
       du.ldaux = m;
@@ -457,8 +483,10 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
         TRY(wgrad(M, tr, false, M->du, m, m, A.c, d, m, d, T, pb + B_FC1W));
       }
       SAT_HIP(launch_colsum_bf16(M->du, m, T, m, M->part, npT, grad(M, pb + B_FC1B), s));
-      TRY(ln_bwd(M, M->dA, A.h_mid, 1, pb + B_LN2G, A.mean2, A.rstd2, T));
-      SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + B_PROJB), s));
+      TRY(ln_bwd(M, M->dA, A.h_mid, 1, pb + B_LN2G, A.mean2, A.rstd2, T,
+                 bias_in_ln_bwd(M) ? grad(M, pb + B_PROJB) : nullptr));
+      if (!bias_in_ln_bwd(M))
+        SAT_HIP(launch_colsum_f32(M->dh, d, T, d, M->part, npT, grad(M, pb + B_PROJB), s));
       GemmArgs go = gargs(M->dh_bf, d, shadow_t(M, pb + B_PROJW), d, T, d, d, M->dout, d);
       TRY(gemm(M, go, LAY_K, LAY_K, EPI_BF16));
       if (ov) {
@@ -486,7 +514,8 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
                   TK_QKV_WGRAD));
       }
       SAT_HIP(launch_colsum_bf16(M->dqkv, 3 * d, T, 3 * d, M->part, npT, grad(M, pb + B_QKVB), s));
-      TRY(ln_bwd(M, M->dA, M->h_in[l], 1, pb + B_LN1G, A.mean1, A.rstd1, T));
+      TRY(ln_bwd(M, M->dA, M->h_in[l], 1, pb + B_LN1G, A.mean1, A.rstd1, T,
+                 fc2_bias_grad(M, l - 1)));
     }
   }
 
