@@ -384,17 +384,35 @@ __global__ __launch_bounds__(256) void colsum_pass1(const T* __restrict__ X, lon
   float s[V];
 #pragma unroll
   for (int v = 0; v < V; ++v) s[v] = 0.f;
-  for (int r = r0; r < r1; ++r) {
-    const T* src = X + (long)r * ldx + c;
+  auto add = [&](const T* src) {
     if constexpr (VEC) {
-      u32x4 raw = *reinterpret_cast<const u32x4*>(src);
+      const u32x4 raw = *reinterpret_cast<const u32x4*>(src);
       const T* e = reinterpret_cast<const T*>(&raw);
 #pragma unroll
       for (int v = 0; v < V; ++v) s[v] += (float)e[v];
     } else {
       s[0] += (float)src[0];
     }
+  };
+  int r = r0;
+  // eight rows' loads issued together (one row at a time waited for each
+  // load's full latency); the rows are still added in order
+  for (; r + 8 <= r1; r += 8) {
+    u32x4 raw[8];
+    if constexpr (VEC) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) raw[u] = *reinterpret_cast<const u32x4*>(X + (long)(r + u) * ldx + c);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) add(reinterpret_cast<const T*>(&raw[u]));
+    } else {
+      T x[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) x[u] = X[(long)(r + u) * ldx + c];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s[0] += (float)x[u];
+    }
   }
+  for (; r < r1; ++r) add(X + (long)r * ldx + c);
 #pragma unroll
   for (int v = 0; v < V; ++v) part[(long)p * cols + c + v] = s[v];
 }
