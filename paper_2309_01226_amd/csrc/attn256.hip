@@ -84,9 +84,19 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const bf16* base, in
                                            0x00020000);
 }
 
-// Max / sum over the two 32-lane halves (lanes l and l + 32 hold the same query).
-__device__ __forceinline__ float halves_max(float x) { return fmaxf(x, __shfl_xor(x, 32, 64)); }
-__device__ __forceinline__ float halves_sum(float x) { return x + __shfl_xor(x, 32, 64); }
+// Max / sum over the two 32-lane halves (lanes l and l + 32 hold the same
+// query).  v_permlane32_swap on a register and itself leaves every lane with
+// its own value and its partner's, in one VALU instruction (a cross-lane
+// shuffle would go through the LDS unit and wait for it); both lanes of a
+// pair then form the same result (IEEE max and add are commutative).
+__device__ __forceinline__ float halves_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float halves_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 // Per-lane state of one wave: 32 queries, lane = query (two lanes per query).
 struct FwdState {
@@ -97,44 +107,56 @@ struct FwdState {
   int vofs[4];          // V^T transposed-read offsets of ot = 0..3 (+128 for 4..7)
 };
 
-// One 64-key block: S^T = K Q^T, masked (MASK) online softmax, O^T += V^T P^T.
+// One 64-key block: S^T = K Q^T, online softmax (masked only where the block
+// crosses the causal diagonal or the sequence end), O^T += V^T P^T.
+//
+// Both products keep their LDS operand reads a fixed number of MFMAs ahead:
+// the reads of step i + PF are issued before the MFMAs of step i, and a
+// scheduling barrier after every step pins that order.  Left to itself the
+// compiler issued each fragment read right before the MFMA that consumes it
+// and waited for it there, so every MFMA of the block paid a full LDS
+// latency.
+constexpr int PF_K = 3;  // k-steps (two MFMAs each) of K fragments in flight
+constexpr int PF_V = 3;  // MFMAs of V^T fragments in flight
+
 __device__ __forceinline__ void fwd_block(FwdState& st, const bf16* Ks, const bf16* Vs, float sc,
-                                          int kv0, int q, int S, int causal, int g) {
+                                          int kv0, int q, int S, int causal, int g, bool mask) {
   floatx16 s0 = zero16(), s1 = zero16();
+  // K fragment of k-step c, tile t (keys kv0 + 32 t ..): k-steps 8..15 sit 16 chunks further
+  auto kread = [&](int c, int t) -> bf16x8 {
+    return *reinterpret_cast<const bf16x8*>(Ks + t * 32 * DH + st.kofs[c & 7] + (c >> 3) * 128);
+  };
+  bf16x8 kf[PF_K + 1][2];
+#pragma unroll
+  for (int c = 0; c < PF_K; ++c) {
+    kf[c][0] = kread(c, 0);
+    kf[c][1] = kread(c, 1);
+  }
 #pragma unroll
   for (int c = 0; c < DH / 16; ++c) {
-    const int co = st.kofs[c & 7] + (c >> 3) * 128;
-    const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(Ks + co);
-    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(Ks + 32 * DH + co);
-    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, st.qf[c], s0, 0, 0, 0);
-    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, st.qf[c], s1, 0, 0, 0);
+    if (c + PF_K < DH / 16) {
+      kf[(c + PF_K) % (PF_K + 1)][0] = kread(c + PF_K, 0);
+      kf[(c + PF_K) % (PF_K + 1)][1] = kread(c + PF_K, 1);
+    }
+    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[c % (PF_K + 1)][0], st.qf[c], s0, 0, 0, 0);
+    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[c % (PF_K + 1)][1], st.qf[c], s1, 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
   }
-  // keep at most two k-steps of K fragments in flight (register budget)
-  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+  if (mask) {
+    // keys past the end, or (causal) past the query, score -inf; lim = first key excluded
+    const int lim = min(S, causal ? q + 1 : S) - kv0 - 4 * g;
 #pragma unroll
-  for (int i = 0; i < 14; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    for (int r = 0; r < 16; ++r) {
+      const int kr = 8 * (r >> 2) + (r & 3);  // key - kv0 - 4 g in the first tile
+      s0[r] = kr < lim ? s0[r] : -INFINITY;
+      s1[r] = kr + 32 < lim ? s1[r] : -INFINITY;
+    }
   }
-  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-  __builtin_amdgcn_sched_barrier(0);
-  float x[32];
+  // the scale is positive, so the largest scaled score is the scaled largest score
+  float mraw = fmaxf(s0[0], s1[0]);
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    x[r] = s0[r] * sc;
-    x[16 + r] = s1[r] * sc;
-  }
-  // keys past the end, or (causal) past the query, score -inf; lim = first key excluded
-  const int lim = min(S, causal ? q + 1 : S) - kv0 - 4 * g;
-#pragma unroll
-  for (int r = 0; r < 32; ++r) {
-    const int kr = 32 * (r >> 4) + 8 * ((r & 15) >> 2) + (r & 3);  // key - kv0 - 4 g
-    x[r] = kr < lim ? x[r] : -INFINITY;
-  }
-  float mloc = x[0];
-#pragma unroll
-  for (int r = 1; r < 32; ++r) mloc = fmaxf(mloc, x[r]);
-  mloc = halves_max(mloc);
+  for (int r = 1; r < 16; ++r) mraw = fmaxf(mraw, fmaxf(s0[r], s1[r]));
+  const float mloc = halves_max(mraw) * sc;
   // lazy max: raise m only when a score exceeds it by more than the slack
   const bool raise = mloc > st.m + RESCALE_SLACK;
   if (__builtin_amdgcn_ballot_w64(raise) != 0) {
@@ -147,37 +169,35 @@ __device__ __forceinline__ void fwd_block(FwdState& st, const bf16* Ks, const bf
       for (int r = 0; r < 16; ++r) st.o[ot][r] *= alpha;
     st.m = raise ? mloc : st.m;
   }
-  const float mm = (st.m == -INFINITY) ? 0.f : st.m;  // all-masked rows: x = -inf gives p = 0
+  const float nm = (st.m == -INFINITY) ? 0.f : -st.m;  // all-masked rows: -inf scores give p = 0
   float lsum = 0.f;
   bf16x8 pb[4];
 #pragma unroll
   for (int r = 0; r < 32; ++r) {
-    const float pr = __builtin_amdgcn_exp2f(x[r] - mm);
+    const float pr = __builtin_amdgcn_exp2f(__builtin_fmaf(r < 16 ? s0[r] : s1[r - 16], sc, nm));
     lsum += pr;
     pb[r >> 3][r & 7] = f2bf(pr);
   }
   st.l += halves_sum(lsum);
   __builtin_amdgcn_sched_barrier(0);
+  // MFMA i = 8 kk + ot: 16-key step kk (keys 16 kk + {4g .. 4g+3, 8+4g .. 8+4g+3}),
+  // head dims 32 ot ..; each accumulator still takes its key steps in order
+  auto vread = [&](int i) -> bf16x8 {
+    const int kk = i >> 3, ot = i & 7;
+    const bf16* vb = Vs + 16 * kk * DH + st.vofs[ot & 3] + (ot >> 2) * 128;
+    const bf16x4 lo = ds_read_tr((const lds_bf16x4*)lds(vb));
+    const bf16x4 hi = ds_read_tr((const lds_bf16x4*)lds(vb + 8 * DH));
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  };
+  bf16x8 vf[PF_V + 1];
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {  // 16-key steps: keys 16 kk + {4g .. 4g+3, 8+4g .. 8+4g+3}
-    const bf16* vb = Vs + 16 * kk * DH;
+  for (int i = 0; i < PF_V; ++i) vf[i] = vread(i);
 #pragma unroll
-    for (int ot = 0; ot < DH / 32; ++ot) {
-      const int vo = st.vofs[ot & 3] + (ot >> 2) * 128;
-      const bf16x4 lo = ds_read_tr((const lds_bf16x4*)lds(vb + vo));
-      const bf16x4 hi = ds_read_tr((const lds_bf16x4*)lds(vb + vo + 8 * DH));
-      const bf16x8 vf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-      st.o[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[kk], st.o[ot], 0, 0, 0);
-    }
+  for (int i = 0; i < 4 * (DH / 32); ++i) {
+    if (i + PF_V < 4 * (DH / 32)) vf[(i + PF_V) % (PF_V + 1)] = vread(i + PF_V);
+    st.o[i & 7] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i % (PF_V + 1)], pb[i >> 3], st.o[i & 7], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
   }
-  // two transposed reads per MFMA, two MFMAs of reads in flight
-  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-#pragma unroll
-  for (int i = 0; i < 30; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-  }
-  __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
 }
 
 __global__ __launch_bounds__(NT, 1) void attn256_fwd_kernel(AttnArgs a) {
@@ -247,7 +267,8 @@ __global__ __launch_bounds__(NT, 1) void attn256_fwd_kernel(AttnArgs a) {
       copy_block<1>(rows_rsrc(Vb, kv0 + KB, a.ldv), a.ldv, S - kv0 - KB, nxt + TILE, wave);
     }
     if (!(a.causal && kv0 > wq0 + WQ - 1)) {
-      fwd_block(st, Ks, Ks + TILE, sc, kv0, q, S, a.causal, g);
+      const bool mask = kv0 + KB > S || (a.causal && kv0 + KB - 1 > wq0);
+      fwd_block(st, Ks, Ks + TILE, sc, kv0, q, S, a.causal, g, mask);
     }
     if (j + 1 < nblk) {
       wait_vm_lgkm0<0>();
