@@ -10,7 +10,9 @@ import ctypes as C
 import os
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libsaturn.so")
+# SAT_LIBRARY selects another build of the same library (for instance the
+# AddressSanitizer build of the host code); by default the in-tree one.
+LIB_PATH = os.environ.get("SAT_LIBRARY") or os.path.join(_PKG, "libsaturn.so")
 
 SAT_OK, SAT_EINVAL, SAT_ENOMEM, SAT_EHIP, SAT_ESTATE, SAT_ENONFINITE, SAT_ENOTSUP = 0, -1, -2, -3, -4, -5, -6
 STATUS_NAMES = {0: "SAT_OK", -1: "SAT_EINVAL", -2: "SAT_ENOMEM", -3: "SAT_EHIP", -4: "SAT_ESTATE",

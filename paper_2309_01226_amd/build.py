@@ -1,6 +1,7 @@
 """Compile the gfx950 HIP sources into the in-tree shared library libsaturn.so.
 
 Usage: python -m paper_2309_01226_amd.build   (or call build()).
+       python -m paper_2309_01226_amd.build --asan   (host code under AddressSanitizer)
 """
 
 import concurrent.futures as cf
@@ -70,6 +71,56 @@ def build(verbose=True, incremental=False):
     return OUT
 
 
+# Host translation units (argument checks, arena planning, launch sequences):
+# the AddressSanitizer build instruments these for host code only; the
+# device code objects of every source are the regular ones.
+HOST_SOURCES = [s for s in SOURCES if s.endswith(".cpp")]
+ASAN_DIR = os.path.join(BUILD_DIR, "asan")
+ASAN_OUT = os.path.join(ASAN_DIR, "libsaturn_asan.so")
+ASAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fno-omit-frame-pointer"]
+
+
+def asan_runtime():
+    """Path of the compiler's shared AddressSanitizer runtime (to preload)."""
+    r = subprocess.run([HIPCC, "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True,
+                       text=True)
+    path = r.stdout.strip()
+    return path if r.returncode == 0 and os.path.isabs(path) and os.path.exists(path) else None
+
+
+def build_asan(verbose=True):
+    """Link ASAN_OUT: the host sources compiled with AddressSanitizer (host
+    side only), the .hip sources' regular objects.  Loaded by a process that
+    preloads asan_runtime(), for host-only checks of the C ABI."""
+    build(verbose=False, incremental=True)
+    os.makedirs(ASAN_DIR, exist_ok=True)
+
+    def one(src):
+        obj = os.path.join(ASAN_DIR, src + ".o")
+        cmd = ([HIPCC] + COMMON + ASAN_FLAGS + EXTRA.get(src, []) +
+               ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj])
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"compile failed: {src}\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+        return obj
+
+    with cf.ThreadPoolExecutor(max_workers=max(1, min(8, len(HOST_SOURCES)))) as ex:
+        list(ex.map(one, HOST_SOURCES))
+    objs = [os.path.join(ASAN_DIR if s in HOST_SOURCES else BUILD_DIR, os.path.basename(s) + ".o")
+            for s in SOURCES]
+    cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=gfx950", "-shared-libasan"] + ASAN_FLAGS[:2] + \
+        ["-o", ASAN_OUT] + objs
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed\n{r.stdout}\n{r.stderr}")
+    if verbose:
+        print(f"built {ASAN_OUT}")
+    return ASAN_OUT
+
+
 if __name__ == "__main__":
-    build(incremental="--incremental" in sys.argv)
+    if "--asan" in sys.argv:
+        build_asan()
+    else:
+        build(incremental="--incremental" in sys.argv)
     sys.exit(0)
