@@ -132,8 +132,10 @@ sat_status sat_op_adamw(float* p, const float* g, float* m, float* v, void* shad
 
 /* Token embedding forward h[t] = wte[tok[t]] (+ wpe[t % S]) and its
  * deterministic backward dwte[v] = sum over t with tok[t] == v of dh[t] in
- * increasing t, written for every v < V (zero rows for absent tokens).
- * work: int32 scratch of T entries.  Backward limits: T <= 16384, V < 65536
+ * increasing t, written for every v < V (zero rows for absent tokens).  Past
+ * 16384 positions the sum is formed per chunk of 16384 positions, in order,
+ * and the chunks' sums are added in order.
+ * work: int32 scratch of min(T, 16384) entries.  Backward limit: V < 65536
  * (SAT_EINVAL otherwise). */
 sat_status sat_op_embed_fwd(const int32_t* tok, const float* wte, const float* wpe, float* h,
                             int32_t T, int32_t S, int32_t d, int32_t V, void* stream);

@@ -119,6 +119,7 @@ __global__ void embed_fwd_kernel(const int32_t* __restrict__ tok, const float* _
 
 // Sorts the keys (token << 15 | position) of T <= 16384 tokens with a bitonic
 // network in LDS (one workgroup); keys are unique, so the order is unique.
+// Longer inputs are processed in chunks of this many positions.
 constexpr int EMB_MAXT = 16384;
 __global__ __launch_bounds__(1024) void embed_sort_kernel(const int32_t* __restrict__ tok, int T,
                                                           int32_t* __restrict__ sorted) {
@@ -150,6 +151,9 @@ __global__ __launch_bounds__(1024) void embed_sort_kernel(const int32_t* __restr
 // One wavefront per vocabulary row v: binary-search v's run in the sorted
 // keys, sum the matching dh rows in increasing position order, write the row
 // (zeros when v does not occur).
+// Row v of dwte = the sum, in position order, of dh over the positions holding
+// token v (ACC: added to the row's current value, for the chunks after the first).
+template <bool ACC>
 __global__ __launch_bounds__(256) void embed_bwd_rows_kernel(const int32_t* __restrict__ sorted,
                                                              int T, const float* __restrict__ dh,
                                                              float* __restrict__ dwte, int d,
@@ -173,6 +177,10 @@ __global__ __launch_bounds__(256) void embed_bwd_rows_kernel(const int32_t* __re
       int t = sorted[j] & 0x7FFF;
       float4 x = *reinterpret_cast<const float4*>(dh + (long)t * d + c);
       s.x += x.x; s.y += x.y; s.z += x.z; s.w += x.w;
+    }
+    if (ACC) {
+      const float4 o = *reinterpret_cast<const float4*>(out + c);
+      s.x = o.x + s.x; s.y = o.y + s.y; s.z = o.z + s.z; s.w = o.w + s.w;
     }
     *reinterpret_cast<float4*>(out + c) = s;
   }
@@ -623,15 +631,28 @@ hipError_t launch_embed_fwd(const int32_t* tok, const float* wte, const float* w
   return hipGetLastError();
 }
 
+// Positions are taken in chunks of EMB_MAXT, in order, one after the other on
+// the stream: the first chunk writes every row's sum, later chunks add theirs.
+// work holds one chunk's sorted keys (min(T, EMB_MAXT) entries).
 hipError_t launch_embed_bwd(const int32_t* tok, const float* dh, float* dwte, int T, int d, int V,
                             int32_t* work, hipStream_t s) {
-  if (T <= 0 || T > EMB_MAXT || d % 4 || V <= 0 || V >= (1 << 16)) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(embed_sort_kernel, dim3(1), dim3(1024), 0, s, tok, T, work);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(embed_bwd_rows_kernel, dim3(sat_cdiv(V, 4)), dim3(256), 0, s, work, T, dh,
-                     dwte, d, V);
-  return hipGetLastError();
+  if (T <= 0 || d % 4 || V <= 0 || V >= (1 << 16)) return hipErrorInvalidValue;
+  for (int t0 = 0; t0 < T; t0 += EMB_MAXT) {
+    const int n = T - t0 < EMB_MAXT ? T - t0 : EMB_MAXT;
+    hipLaunchKernelGGL(embed_sort_kernel, dim3(1), dim3(1024), 0, s, tok + t0, n, work);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const float* dhc = dh + (long)t0 * d;
+    if (t0 == 0)
+      hipLaunchKernelGGL(embed_bwd_rows_kernel<false>, dim3(sat_cdiv(V, 4)), dim3(256), 0, s, work,
+                         n, dhc, dwte, d, V);
+    else
+      hipLaunchKernelGGL(embed_bwd_rows_kernel<true>, dim3(sat_cdiv(V, 4)), dim3(256), 0, s, work,
+                         n, dhc, dwte, d, V);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_patchify(const float* img, bf16* out, int B, int C, int I, int p, int ldo,

@@ -71,9 +71,8 @@ sat_status sat_validate_config(const sat_config* c) {
                     "rotary_dim must be even and <= head dim");
     else
       SAT_CHECK_ARG(c->rotary_dim == 0, "rotary_dim must be 0 for GPT2");
-    long T = (long)c->batch * c->seq_len;
-    SAT_CHECK_ARG(c->frozen_layers > 0 || (T <= 16384 && c->vocab < 65536),
-                  "training the token embedding needs batch*seq_len <= 16384 and vocab < 65536");
+    SAT_CHECK_ARG(c->frozen_layers > 0 || c->vocab < 65536,
+                  "training the token embedding needs vocab < 65536");
   }
   return SAT_OK;
 }
@@ -417,7 +416,7 @@ size_t carve(sat_model* M, char* base) {
   const size_t lnp = (size_t)(sat_bias_in_ln_bwd(D) ? 3 : 2) *
                      ln_bwd_parts((int)std::max<long>(T, D.rows_head), d) * d;
   M->part = c.take<float>(std::max((size_t)2 * M->n_part * (wide > d ? wide : d), lnp));
-  M->sortbuf = c.take<int32_t>(T > 0 ? T : 1);
+  M->sortbuf = c.take<int32_t>(T > 16384 ? 16384 : (T > 0 ? T : 1));  // one chunk of sorted keys
   return align_up(c.off, kAlignBytes);
 }
 

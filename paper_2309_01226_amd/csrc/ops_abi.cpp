@@ -256,8 +256,8 @@ extern "C" sat_status sat_op_embed_bwd(const int32_t* tok, const float* dh, floa
                                        int32_t T, int32_t d, int32_t V, int32_t* work,
                                        void* stream) {
   SAT_CHECK_ARG(tok && dh && dwte && work, "embed_bwd: null pointer");
-  SAT_CHECK_ARG(T > 0 && T <= 16384 && d > 0 && d % 4 == 0 && V > 0 && V < 65536,
-                "embed_bwd: needs 0 < T <= 16384, d %% 4 == 0, 0 < V < 65536");
+  SAT_CHECK_ARG(T > 0 && d > 0 && d % 4 == 0 && V > 0 && V < 65536,
+                "embed_bwd: needs T > 0, d %% 4 == 0, 0 < V < 65536");
   SAT_HIP(launch_embed_bwd(tok, dh, dwte, T, d, V, work, S(stream)));
   return SAT_OK;
 }

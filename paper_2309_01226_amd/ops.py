@@ -145,7 +145,7 @@ def embed_fwd(tok, wte, wpe, h, T, S, d, V):
 
 
 def embed_bwd(tok, dh, dwte, T, d, V):
-    work = torch.empty(max(T, 1), device=dh.device, dtype=torch.int32)
+    work = torch.empty(max(min(T, 16384), 1), device=dh.device, dtype=torch.int32)
     _lib.call("sat_op_embed_bwd", _p(tok), _p(dh), _p(dwte), T, d, V, _p(work), _stream())
 
 

@@ -85,7 +85,7 @@ def test_arena_bytes_gptj_full_fits_hbm():
     dict(arch="vit", img_size=30, patch=14),
     dict(beta1=1.0),
     dict(eps=0.0),
-    dict(seq_len=20000, batch=1),        # token embedding backward limit
+    dict(vocab=70000),                   # token ids of the embedding backward: 16 bits
 ])
 def test_invalid_configs_rejected(bad):
     st, _ = _bytes(_cfg(**bad))
@@ -108,9 +108,13 @@ def test_destroy_null_and_null_args():
     assert L.sat_model_arena_bytes(None, None) == -1
 
 
-def test_frozen_embedding_limit_lifted_when_frozen():
-    # training the embedding is limited to 16384 tokens; freezing it lifts that
-    st, _ = _bytes(_cfg(seq_len=20000, batch=1, frozen_layers=1))
+def test_embedding_limits():
+    # more than 16384 positions: the embedding backward takes them in chunks
+    st, _ = _bytes(_cfg(seq_len=20000, batch=1))
+    assert st == 0
+    # the 16-bit token ids of its sort keys bound the vocabulary, unless the
+    # embedding is frozen
+    st, _ = _bytes(_cfg(vocab=70000, frozen_layers=1))
     assert st == 0
 
 

@@ -272,8 +272,10 @@ def test_adamw_against_oracle(n):
 
 # ------------------------------------------------------------------ embedding
 
-@pytest.mark.parametrize("T,d,V", [(64, 64, 512), (1000, 256, 97), (4096, 128, 50400)])
+# 40000 positions: three sort chunks of at most 16384, the later ones added in order
+@pytest.mark.parametrize("T,d,V", [(64, 64, 512), (1000, 256, 97), (4096, 128, 50400), (40000, 64, 300)])
 def test_embedding(T, d, V):
+    flush(f"embedding T={T} d={d} V={V}")
     rng = np.random.default_rng(T)
     S = 32
     wte = rng.normal(size=(V, d)).astype(np.float32)

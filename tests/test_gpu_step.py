@@ -54,6 +54,9 @@ CASES = {
     # fc1 input gradient and the fc2 forward (K = 1024) run split-K
     "gpt2_splitk": dict(arch="gpt2", n_layers=2, d_model=256, n_heads=4, d_mlp=1024, vocab=512,
                         seq_len=1024, batch=2, lr=1e-3),
+    # 18432 tokens: the token embedding's backward sums two chunks of positions
+    "gpt2_long_t": dict(arch="gpt2", n_layers=1, d_model=128, n_heads=2, d_mlp=256, vocab=300,
+                        seq_len=256, batch=72, lr=1e-3),
 }
 
 
