@@ -34,9 +34,12 @@ extern "C" {
  * with it, an epilogue-0/1 product on layout-0 operands that has fewer than
  * 256 output tiles of 256 x 256 and K >= 1024 runs split-K: K slices of at
  * least 512 write fp32 partials there, then one reduction adds them in slice
- * order with bias and residual.  Results then differ from the unsplit
+ * order with bias and residual.  Such a product with more than 256 tiles
+ * whose last round of 256 tiles would run mostly empty instead runs its
+ * first rows (whole rounds) unsplit and only the remaining rows split-K,
+ * when that is estimated faster.  Results then differ from the unsplit
  * product by summation order only.  The scratch is used only when it holds
- * slices * M * N elements; the call makes no allocation. */
+ * slices * (split rows) * N elements; the call makes no allocation. */
 typedef struct {
   const void* A;
   const void* B;

@@ -621,6 +621,34 @@ inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 
 
 }  // namespace
 
+bool gemm_tail_split(int M, int N, int K, int smax, int* M1, int* S, int* kc) {
+  const long mt = sat_cdiv(M, 256), nt = sat_cdiv(N, 256), tiles = mt * nt;
+  if (tiles <= 256 || tiles % 256 == 0 || nt > 256) return false;
+  // head: the rows whose tiles fill whole rounds of 256 workgroups
+  const long mh = 256 * (tiles / 256) / nt;
+  if (mh <= 0 || mh >= mt) return false;
+  const int m2 = M - (int)mh * 256;
+  int c = 0;
+  const int s = gemm_splitk(m2, N, K, &c, smax);
+  if (s <= 1) return false;
+  // the same estimate as gemm_splitk, in K-tile steps of one tile: the head's
+  // rounds, the tail's slices and their reduction, against every round unsplit
+  const double kt = (double)sat_cdiv(K, 64);
+  const double head = (double)((mh * nt + 255) / 256) * kt;
+  const double tail = (double)((sat_cdiv(m2, 256) * nt * s + 255) / 256) * (c / 64) +
+                      (double)(s + 1) * m2 * N * 4.0 / 9e6;
+  if (head + tail >= (double)((tiles + 255) / 256) * kt) return false;
+  *M1 = (int)mh * 256;
+  *S = s;
+  *kc = c;
+  return true;
+}
+
+long gemm_tail_ws_elems(int M, int N, int K, int smax) {
+  int m1 = 0, s = 0, c = 0;
+  return gemm_tail_split(M, N, K, smax, &m1, &s, &c) ? (long)s * (M - m1) * N : 0;
+}
+
 hipError_t launch_gemm(const GemmArgs& a, int alay, int blay, int epi, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   if (a.K <= 0) return hipErrorInvalidValue;
@@ -645,6 +673,38 @@ hipError_t launch_gemm(const GemmArgs& a, int alay, int blay, int epi, hipStream
         return launch_splitk_reduce(a.splitk_ws, S, b.split_stride, a.M, a.N,
                                     reinterpret_cast<float*>(a.out), a.ldo, a.bias, a.bias_col0,
                                     epi == EPI_RESID_F32 ? a.resid : nullptr, a.ldr, s);
+      }
+    }
+  }
+  // more than 256 tiles with a mostly empty last round: whole rounds of rows
+  // unsplit, the remaining rows split-K into the workspace
+  if ((epi == EPI_F32 || epi == EPI_RESID_F32) && alay == LAY_K && blay == LAY_K &&
+      a.splitk <= 1 && a.splitk_ws != nullptr) {
+    int M1 = 0, S = 0, kc = 0;
+    if (gemm_tail_split(a.M, a.N, a.K, a.splitk_max, &M1, &S, &kc) &&
+        (long)S * (a.M - M1) * a.N <= a.splitk_ws_elems) {
+      GemmArgs h = a;
+      h.M = M1;
+      GemmArgs t = a;
+      t.A = a.A + (long)M1 * a.lda;
+      t.M = a.M - M1;
+      t.out = a.splitk_ws;
+      t.ldo = a.N;
+      t.bias = nullptr;
+      t.resid = nullptr;
+      t.splitk = S;
+      t.splitk_kc = kc;
+      t.split_stride = (long)t.M * a.N;
+      if (gemm256_eligible(h, LAY_K, LAY_K, epi) && gemm256_eligible(t, LAY_K, LAY_K, EPI_F32)) {
+        hipError_t e = launch_gemm256(h, LAY_K, LAY_K, epi, s);
+        if (e != hipSuccess) return e;
+        e = launch_gemm256(t, LAY_K, LAY_K, EPI_F32, s);
+        if (e != hipSuccess) return e;
+        return launch_splitk_reduce(a.splitk_ws, S, t.split_stride, t.M, a.N,
+                                    reinterpret_cast<float*>(a.out) + (long)M1 * a.ldo, a.ldo,
+                                    a.bias, a.bias_col0,
+                                    epi == EPI_RESID_F32 ? a.resid + (long)M1 * a.ldr : nullptr,
+                                    a.ldr, s);
       }
     }
   }

@@ -90,6 +90,14 @@ hipError_t launch_gemm256(const GemmArgs& a, int alay, int blay, int epi, hipStr
 // give every CU a tile where K allows, each at least 512 deep, at most smax.
 int gemm_splitk(int M, int N, int K, int* kc, int smax = 16);
 long gemm_splitk_ws_elems(int M, int N, int K, int smax = 16);
+// An fp32-output product with more than 256 tiles whose last round of 256
+// workgroups would run mostly empty: the first *M1 rows (whole rounds) run
+// unsplit, the remaining rows as *S K slices of depth *kc plus a reduction,
+// when the same estimate as gemm_splitk says that is faster.  launch_gemm
+// takes this plan when the workspace holds S * (M - M1) * N elements (the
+// figure gemm_tail_ws_elems gives; 0 when the plan does not apply).
+bool gemm_tail_split(int M, int N, int K, int smax, int* M1, int* S, int* kc);
+long gemm_tail_ws_elems(int M, int N, int K, int smax = 16);
 // out[m, n] = sum over s of ws[s * stride + m * N + n] (s in order) + bias[n -
 // bias_col0] (n >= bias_col0; null: none) + resid[m * ldr + n] (null: none).
 hipError_t launch_splitk_reduce(const float* ws, int S, long stride, int M, int N, float* out,

@@ -335,7 +335,9 @@ size_t carve(sat_model* M, char* base) {
   {
     const int Ti = (int)T, di = (int)d, mi = (int)m, R = D.rows_head;
     long ws = 0;
-    auto need = [&](int Mg, int Ng, int Kg) { ws = std::max(ws, gemm_splitk_ws_elems(Mg, Ng, Kg)); };
+    auto need = [&](int Mg, int Ng, int Kg) {
+      ws = std::max(ws, std::max(gemm_splitk_ws_elems(Mg, Ng, Kg), gemm_tail_ws_elems(Mg, Ng, Kg)));
+    };
     need(D.qkv_ld, di, Ti);
     need(di, di, Ti);
     need(mi, di, Ti);

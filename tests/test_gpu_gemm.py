@@ -171,3 +171,46 @@ def test_gemm_splitk(M, N, K, resid):
     # the split path ran: at least two slices of partial products were written
     n_used = int(torch.isfinite(ws).sum().item())
     assert n_used >= 2 * M * N, n_used
+
+
+# Tail split: fp32-output products with more than 256 tiles of 256 x 256 whose
+# last round would run mostly empty (ViT-H/14's 16448 x 1280 products have 325
+# tiles), given a workspace: whole rounds of rows unsplit, the remaining rows
+# split-K, then the reduction with bias and residual.  Shapes: the ViT-H
+# products, a ragged last row tile, ragged columns, and a second shape family.
+TAIL = [(16448, 1280, 5120, 1), (16448, 1280, 1280, 0), (16400, 1280, 3840, 1),
+        (16448, 1272, 5120, 0), (9000, 2048, 2048, 1)]
+
+
+@pytest.mark.parametrize("M,N,K,resid", TAIL)
+def test_gemm_tail_split(M, N, K, resid):
+    from paper_2309_01226_amd import ops
+    flush(f"gemm tail split M={M} N={N} K={K} resid={resid}")
+    rng = np.random.default_rng(M + N + K + 1)
+    A, B, Ad, Bd, lda, ldb = _operands(rng, M, N, K, 0, 0)
+    bias = rng.normal(size=N)
+    R = rng.normal(size=(M, N)).astype(np.float32)
+    ws = torch.full((16 * 1024 * 1024,), float("nan"), device="cuda", dtype=torch.float32)
+    out = to_dev_f32(R) if resid else torch.empty(M, N, device="cuda", dtype=torch.float32)
+    kw = dict(bias=to_dev_f32(bias), epilogue=ops.EPI_RESID_F32 if resid else ops.EPI_F32)
+    if resid:
+        kw.update(resid=out, ldr=N)
+    ops.gemm(Ad, Bd, M, N, K, out, lda=lda, ldb=ldb, splitk_ws=ws, **kw)
+    out1 = to_dev_f32(R) if resid else torch.empty(M, N, device="cuda", dtype=torch.float32)
+    if resid:
+        kw.update(resid=out1)
+    ops.gemm(Ad, Bd, M, N, K, out1, lda=lda, ldb=ldb, **kw)
+    torch.cuda.synchronize()
+    got = host(out)
+    assert np.isfinite(got).all()
+    # rows from the unsplit head, from the split tail and the last row
+    head_rows = rng.choice(M // 2, size=150, replace=False)
+    tail_rows = M - 1 - rng.choice(2048, size=150, replace=False)
+    rows = np.unique(np.concatenate([head_rows, tail_rows, [M - 1]]))
+    ref = O.gemm(A[rows], B) + bias + (R[rows].astype(np.float64) if resid else 0.0)
+    assert rel(got[rows], ref) < 2e-6
+    assert rel(got, host(out1)) < 2e-6
+    # the tail ran split-K: partials of at least two slices were written, but
+    # fewer than a split of every row would write
+    n_used = int(torch.isfinite(ws).sum().item())
+    assert 2 * N * 16 <= n_used < 2 * M * N, n_used

@@ -64,6 +64,26 @@ def test_noalloc_two_calls_second_smaller():
     _check(300, 520, 4160, resid=False, seed=2)
 
 
+def test_noalloc_tail_split():
+    """A product with 288 tiles (one whole round of rows, then 32 tiles split
+    four ways: 6.6 M partials) takes the same plan as sat_op_gemm with a
+    workspace, and gives the same bits."""
+    from paper_2309_01226_amd import ops
+    M, N, K = 9000, 2048, 2048
+    flush(f"no-alloc gemm tail split M={M} N={N} K={K}")
+    rng = np.random.default_rng(5)
+    Ad, Bd, kw, fresh, ref = _case(rng, M, N, K, resid=True)
+    out_na = fresh()
+    ops.gemm_noalloc(Ad, Bd, M, N, K, out_na, resid=out_na, ldr=N, **kw)
+    ws = torch.full((8 * 1024 * 1024,), float("nan"), device="cuda", dtype=torch.float32)
+    out_ws = fresh()
+    ops.gemm(Ad, Bd, M, N, K, out_ws, splitk_ws=ws, resid=out_ws, ldr=N, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(out_na, out_ws), "differs from sat_op_gemm with a workspace"
+    assert rel(host(out_na), ref) < 2e-6
+    assert int(torch.isfinite(ws).sum().item()) > 0
+
+
 def test_noalloc_unsplit_product():
     """A product that never splits K (K < 1024) uses no scratch and equals
     sat_op_gemm."""
