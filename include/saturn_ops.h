@@ -71,7 +71,9 @@ sat_status sat_op_gemm(const sat_gemm_desc* d, void* stream);
  * SAT_GEMM_NOALLOC_WS_ELEMS fp32 elements (32 MiB) that the library holds on
  * every device it runs on until the process ends.  The call allocates
  * nothing.  A product whose split-K partials would exceed the scratch is
- * rejected with SAT_EINVAL before any launch.  All calls on one device share
+ * rejected with SAT_EINVAL before any launch, except one that would split
+ * only the rows of its last round: that runs unsplit, with the result of
+ * sat_op_gemm without a workspace.  All calls on one device share
  * that device's scratch: calls whose products split K and that may overlap
  * (different streams, or different host threads) race and must be ordered
  * by the caller. */

@@ -110,8 +110,11 @@ extern "C" sat_status sat_op_gemm_noalloc(const sat_gemm_desc* d, void* stream) 
   // the same split-K plan sat_op_gemm takes with a large enough workspace
   const bool may_split = (d->epilogue == 0 || d->epilogue == 1) && d->a_layout == 0 &&
                          d->b_layout == 0;
+  // a product split for want of tiles must fit the scratch; one that would
+  // only split the rows of its last round runs unsplit when those do not fit
+  const long tail = may_split ? gemm_tail_ws_elems(d->M, d->N, d->K) : 0;
   const long need = may_split ? std::max(gemm_splitk_ws_elems(d->M, d->N, d->K),
-                                         gemm_tail_ws_elems(d->M, d->N, d->K))
+                                         tail <= SAT_GEMM_NOALLOC_WS_ELEMS ? tail : 0L)
                               : 0;
   SAT_CHECK_ARG(need <= SAT_GEMM_NOALLOC_WS_ELEMS,
                 "sat_op_gemm_noalloc: M=%d N=%d K=%d runs split-K with %ld fp32 partials, beyond "

@@ -82,6 +82,19 @@ def test_noalloc_tail_split():
     assert torch.equal(out_na, out_ws), "differs from sat_op_gemm with a workspace"
     assert rel(host(out_na), ref) < 2e-6
     assert int(torch.isfinite(ws).sum().item()) > 0
+    # 16448 x 1280 x 1280 (325 tiles): its tail plan needs 8.7 M partials,
+    # beyond the scratch, so it runs unsplit, as sat_op_gemm without a workspace
+    M, N, K = 16448, 1280, 1280
+    flush(f"no-alloc gemm tail split beyond the scratch M={M} N={N} K={K}")
+    rng = np.random.default_rng(6)
+    Ad, Bd, kw, fresh, ref = _case(rng, M, N, K, resid=False)
+    out_na = fresh()
+    ops.gemm_noalloc(Ad, Bd, M, N, K, out_na, **kw)
+    out_plain = fresh()
+    ops.gemm(Ad, Bd, M, N, K, out_plain, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(out_na, out_plain)
+    assert rel(host(out_na), ref) < 2e-6
 
 
 def test_noalloc_unsplit_product():
