@@ -709,8 +709,8 @@ hipError_t launch_gemm(const GemmArgs& a, int alay, int blay, int epi, hipStream
     }
   }
   if (gemm256_eligible(a, alay, blay, epi)) return launch_gemm256(a, alay, blay, epi, s);
-  // the optimizer epilogue exists in the 256 x 256 kernel only
-  if (epi == EPI_ADAMW) return hipErrorInvalidValue;
+  // the optimizer epilogue and the fused column sums exist in the 256 x 256 kernel only
+  if (epi == EPI_ADAMW || a.colsum_part != nullptr) return hipErrorInvalidValue;
   // 16-byte loads need aligned rows.  Along K a partial vector would mix in
   // values past K, so K must be a multiple of 8; along M / N a partial vector
   // only feeds output rows / columns that are never stored, so it suffices that

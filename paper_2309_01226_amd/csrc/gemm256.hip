@@ -220,6 +220,11 @@ __device__ __forceinline__ void epilogue_bf16_wide(const GemmArgs& p, floatx16 (
     }
   }
   const bool gel = EPI == EPI_BF16 && p.out2 != nullptr && col >= p.gelu_col0;
+  // DGELU with column sums: this lane's 8 columns over its rows of the wave's 128
+  const bool csum_on = EPI == EPI_DGELU_BF16 && p.colsum_part != nullptr;
+  float csum[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) csum[e] = 0.f;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const long rowbase = m0 + wm * 128 + 32 * i;
@@ -264,7 +269,23 @@ __device__ __forceinline__ void epilogue_bf16_wide(const GemmArgs& p, floatx16 (
           y[4 + e] = f2bf(x1[e] * gelu_grad_t<GE>(bf2f(uv[s][4 + e])));
         }
         store_nt(reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(p.out) + row * p.ldo + col), y);
+        if (csum_on) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) csum[e] += bf2f(y[e]);
+        }
       }
+    }
+  }
+  if (csum_on) {
+    // the four lane groups of a column (rows 4 s + group), added in group order
+#pragma unroll
+    for (int e = 0; e < 8; ++e) st[(lane >> 4) * 128 + 8 * (lane & 15) + e] = csum[e];
+    float* part = p.colsum_part + (long)((m0 + wm * 128) / 128) * p.N + n0 + wn * 128;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int c = lane + 64 * h;
+      const float v = ((st[c] + st[128 + c]) + st[256 + c]) + st[384 + c];
+      if (n0 + wn * 128 + c < p.N) part[c] = v;
     }
   }
 }
@@ -286,6 +307,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, floatx16 (&acc)[4][4
   // whose residual / pre-activation loads for a slab are all issued before the
   // slab is staged, so their latency overlaps the LDS traffic.
   const bool interior = m0 + BT <= p.M && n0 + BT <= p.N;
+  float csum4[4] = {0.f, 0.f, 0.f, 0.f};  // DGELU column sums of the ragged path
   if (EPI == EPI_BF16 || EPI == EPI_DGELU_BF16) {
     auto a16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
     const bool wide = interior && a16(p.out) && p.ldo % 8 == 0 &&
@@ -356,7 +378,30 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, floatx16 (&acc)[4][4
         const long row = rowbase + rl;
         floatx4 x = *reinterpret_cast<const floatx4*>(st + rl * EP + cl) + bias;
         if (row < p.M) store4<EPI, GE>(p, row, col, x);
+        if (EPI == EPI_DGELU_BF16 && p.colsum_part != nullptr) {
+          // the values store4 writes, zero past M or N
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int c = col + e;
+            const float y = (row < p.M && c < p.N)
+                                ? bf2f(f2bf(x[e] * gelu_grad_t<GE>(bf2f(p.aux[row * p.ldaux + c]))))
+                                : 0.f;
+            csum4[e] += y;
+          }
+        }
       }
+    }
+  }
+  if (EPI == EPI_DGELU_BF16 && p.colsum_part != nullptr && m0 + wm * 128 < p.M) {
+    // the two lane groups of a column (rows 2 s + group), added in group order
+#pragma unroll
+    for (int e = 0; e < 4; ++e) st[(lane >> 5) * 128 + cl + e] = csum4[e];
+    float* part = p.colsum_part + (long)((m0 + wm * 128) / 128) * p.N + n0 + wn * 128;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int c = lane + 64 * h;
+      const float v = st[c] + st[128 + c];
+      if (n0 + wn * 128 + c < p.N) part[c] = v;
     }
   }
 }
@@ -921,7 +966,16 @@ bool gemm256_eligible(const GemmArgs& a, int alay, int blay, int epi) {
   // 1.9 %, 3.1 % and 2.1 % per step), even when half of every tile is padding
   // (128 output columns); split-K products are small by construction and run
   // whatever their tile count
-  if (a.splitk <= 1 && (long)sat_cdiv(a.M, BT) * sat_cdiv(a.N, BT) < 64) return false;
+  if (a.splitk <= 1 && (long)sat_cdiv(a.M, BT) * sat_cdiv(a.N, BT) < 64 && a.colsum_part == nullptr)
+    return false;
+  if (a.colsum_part != nullptr) {
+    // DGELU column sums: K-contiguous operands and the 16-byte epilogue for
+    // every interior tile
+    auto a16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
+    if (epi != EPI_DGELU_BF16 || alay != LAY_K || blay != LAY_K || !a16(a.out) || a.ldo % 8 ||
+        !a16(a.aux) || a.ldaux % 8)
+      return false;
+  }
   auto r8 = [](long x) { return (x + 7) / 8 * 8; };
   const long lim = 1L << 31;
   // operands: 16-byte copies, 32-bit buffer offsets

@@ -76,6 +76,11 @@ struct GemmArgs {
   // output tiles and very long K (the convolution weight gradients, K =
   // pixels) fill the chip only with more.
   int splitk_max;
+  // EPI_DGELU_BF16 in the 256 x 256 kernel: when not null, also the column
+  // sums of the bf16 results over each block of 128 rows, block b at
+  // colsum_part[b * N + n] (cdiv(M, 128) rows; launch_colsum_partials then
+  // adds them in order).  Needs gemm256_eligible to hold with it set.
+  float* colsum_part;
 };
 
 hipError_t launch_gemm(const GemmArgs& a, int alay, int blay, int epi, hipStream_t s);

@@ -417,7 +417,8 @@ size_t carve(sat_model* M, char* base) {
   // the residual product below, when the LayerNorm backward reduces it)
   const size_t lnp = (size_t)(sat_bias_in_ln_bwd(D) ? 3 : 2) *
                      ln_bwd_parts((int)std::max<long>(T, D.rows_head), d) * d;
-  M->part = c.take<float>(std::max((size_t)2 * M->n_part * (wide > d ? wide : d), lnp));
+  M->part_elems = (long)std::max((size_t)2 * M->n_part * (wide > d ? wide : d), lnp);
+  M->part = c.take<float>((size_t)M->part_elems);
   M->sortbuf = c.take<int32_t>(T > 16384 ? 16384 : (T > 0 ? T : 1));  // one chunk of sorted keys
   return align_up(c.off, kAlignBytes);
 }

@@ -179,6 +179,7 @@ struct sat_model {
   float* delta;
   float2* rope_cs;  // rotary (cos, sin) per (position, pair); null without rotary
   float* part;
+  long part_elems;  // fp32 elements of part
   int n_part;
   int32_t* sortbuf;
   // optional per-launch timing of one kernel class

@@ -269,6 +269,18 @@ static sat_status wgrad(sat_model* M, bool trans, bool y_ready, const bf16* Y, l
   return gemm(M, w, LAY_MN, LAY_MN, EPI_F32, tk);
 }
 
+// The fc1 bias gradient is the column sum of the fc2 input-gradient product's
+// output.  Where the 256 x 256 kernel runs that product, its epilogue writes
+// the column sums of every 128-row block into the partial buffer, which one
+// launch of the partial-sum kernel then adds in order; otherwise the output is
+// summed by the column-sum kernels afterwards.
+static bool with_colsums(sat_model* M, GemmArgs& a) {
+  a.colsum_part = M->part;
+  if (((long)a.M + 127) / 128 * a.N > M->part_elems || !gemm256_eligible(a, LAY_K, LAY_K, EPI_DGELU_BF16))
+    a.colsum_part = nullptr;
+  return a.colsum_part != nullptr;
+}
+
 // Weight-gradient stream.  fork: what the model's stream has enqueued so far
 // (the operand copies) precedes what the side stream enqueues next.  reuse:
 // before the model's stream rewrites operand set i, the products that read it
@@ -423,7 +435,10 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
       du.aux = A.qkv + 3 * d;
       du.ldaux = D.qkv_ld;
       du.gelu_erf = 0;
+      const bool fc1b_fused = with_colsums(M, du);
       TRY(gemm(M, du, LAY_K, LAY_K, EPI_DGELU_BF16));
+      if (fc1b_fused)
+        SAT_HIP(launch_colsum_partials(M->part, (int)((T + 127) / 128), m, grad(M, pb + J_FC1B), s));
       GemmArgs go = gargs(M->dh_bf, d, shadow_t(M, pb + J_PROJW), d, T, d, d, M->dout, d);
       TRY(gemm(M, go, LAY_K, LAY_K, EPI_BF16));
       if (ov) {
@@ -455,8 +470,9 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
         TRY(wgrad(M, tr, false, M->dqkv, D.qkv_ld, D.qkv_ld, A.a, d, D.qkv_ld, d, T, pb + J_QKVW,
                   TK_QKV_WGRAD));
       }
-      SAT_HIP(launch_colsum_bf16(M->dqkv + 3 * d, D.qkv_ld, T, m, M->part, npT,
-                                 grad(M, pb + J_FC1B), s));
+      if (!fc1b_fused)
+        SAT_HIP(launch_colsum_bf16(M->dqkv + 3 * d, D.qkv_ld, T, m, M->part, npT,
+                                   grad(M, pb + J_FC1B), s));
       TRY(ln_bwd(M, M->dA, M->h_in[l], 1, pb + J_LN1G, A.mean1, A.rstd1, T,
                  fc2_bias_grad(M, l - 1)));
     } else {
@@ -467,7 +483,10 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
       du.aux = A.u;
       du.ldaux = m;
       du.gelu_erf = gelu_erf;
+      const bool fc1b_fused = with_colsums(M, du);
       TRY(gemm(M, du, LAY_K, LAY_K, EPI_DGELU_BF16));
+      if (fc1b_fused)
+        SAT_HIP(launch_colsum_partials(M->part, (int)((T + 127) / 128), m, grad(M, pb + B_FC1B), s));
       GemmArgs gc = gargs(M->du, m, shadow_t(M, pb + B_FC1W), m, T, d, m, M->dA, d);
       TRY(gemm(M, gc, LAY_K, LAY_K, EPI_F32));
       if (ov) {
@@ -482,7 +501,8 @@ sat_status sat_run_backward(sat_model* M, const void* inputs) {
         TRY(wgrad(M, tr, false, M->dh_bf, d, d, A.g, m, d, m, T, pb + B_FC2W));
         TRY(wgrad(M, tr, false, M->du, m, m, A.c, d, m, d, T, pb + B_FC1W));
       }
-      SAT_HIP(launch_colsum_bf16(M->du, m, T, m, M->part, npT, grad(M, pb + B_FC1B), s));
+      if (!fc1b_fused)
+        SAT_HIP(launch_colsum_bf16(M->du, m, T, m, M->part, npT, grad(M, pb + B_FC1B), s));
       TRY(ln_bwd(M, M->dA, A.h_mid, 1, pb + B_LN2G, A.mean2, A.rstd2, T,
                  bias_in_ln_bwd(M) ? grad(M, pb + B_PROJB) : nullptr));
       if (!bias_in_ln_bwd(M))
