@@ -118,6 +118,7 @@ extern "C" sat_status sat_model_create(const sat_config* cfg, void* arena, size_
   m->opt_fused = true;
   m->opt_keep_grads = false;
   m->opt_overlap = true;
+  m->tail_split = cfg->arch != SAT_RESNET;
   m->last_step_fused = false;
   m->last_step_kept = false;
   hipGetDevice(&m->device);

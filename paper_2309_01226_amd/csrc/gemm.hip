@@ -679,7 +679,7 @@ hipError_t launch_gemm(const GemmArgs& a, int alay, int blay, int epi, hipStream
   // more than 256 tiles with a mostly empty last round: whole rounds of rows
   // unsplit, the remaining rows split-K into the workspace
   if ((epi == EPI_F32 || epi == EPI_RESID_F32) && alay == LAY_K && blay == LAY_K &&
-      a.splitk <= 1 && a.splitk_ws != nullptr) {
+      a.splitk <= 1 && a.splitk_ws != nullptr && !a.no_tail_split) {
     int M1 = 0, S = 0, kc = 0;
     if (gemm_tail_split(a.M, a.N, a.K, a.splitk_max, &M1, &S, &kc) &&
         (long)S * (a.M - M1) * a.N <= a.splitk_ws_elems) {

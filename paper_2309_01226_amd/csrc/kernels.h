@@ -81,6 +81,10 @@ struct GemmArgs {
   // colsum_part[b * N + n] (cdiv(M, 128) rows; launch_colsum_partials then
   // adds them in order).  Needs gemm256_eligible to hold with it set.
   float* colsum_part;
+  // Keeps launch_gemm from splitting the rows of a mostly empty last round
+  // (gemm_tail_split): a weight gradient whose AdamW step may instead be
+  // fused into this kernel's epilogue must sum in the same order either way.
+  int no_tail_split;
 };
 
 hipError_t launch_gemm(const GemmArgs& a, int alay, int blay, int epi, hipStream_t s);

@@ -335,20 +335,22 @@ size_t carve(sat_model* M, char* base) {
   {
     const int Ti = (int)T, di = (int)d, mi = (int)m, R = D.rows_head;
     long ws = 0;
-    auto need = [&](int Mg, int Ng, int Kg) {
-      ws = std::max(ws, std::max(gemm_splitk_ws_elems(Mg, Ng, Kg), gemm_tail_ws_elems(Mg, Ng, Kg)));
+    // (weight gradients, K = tokens, never split the rows of their last round)
+    auto need = [&](int Mg, int Ng, int Kg, bool wgrad) {
+      ws = std::max(ws, gemm_splitk_ws_elems(Mg, Ng, Kg));
+      if (!wgrad) ws = std::max(ws, gemm_tail_ws_elems(Mg, Ng, Kg));
     };
-    need(D.qkv_ld, di, Ti);
-    need(di, di, Ti);
-    need(mi, di, Ti);
-    need(di, mi, Ti);
-    need(Ti, di, D.qkv_ld);
-    need(Ti, di, mi);
-    need(Ti, di, di);
-    need(D.V, di, R);
-    need(R, di, D.Vp);
-    need(R, D.V, di);
-    if (D.arch == SAT_VIT) need(di, D.pd, D.B * D.np);  // the patch weight's gradient
+    need(D.qkv_ld, di, Ti, true);
+    need(di, di, Ti, true);
+    need(mi, di, Ti, true);
+    need(di, mi, Ti, true);
+    need(Ti, di, D.qkv_ld, false);
+    need(Ti, di, mi, false);
+    need(Ti, di, di, false);
+    need(D.V, di, R, true);
+    need(R, di, D.Vp, false);
+    need(R, D.V, di, false);
+    if (D.arch == SAT_VIT) need(di, D.pd, D.B * D.np, true);  // the patch weight's gradient
     M->splitk_ws_elems = ws;
     M->splitk_ws = ws > 0 ? c.take<float>((size_t)ws) : nullptr;
   }

@@ -180,6 +180,11 @@ struct sat_model {
   float2* rope_cs;  // rotary (cos, sin) per (position, pair); null without rotary
   float* part;
   long part_elems;  // fp32 elements of part
+  // Whether fp32-output products may split the rows of a mostly empty last
+  // round of tiles (launch_gemm's tail split).  The ResNet keeps every row of
+  // a product summed in one order, so a batch of copies of one image gives
+  // identical activations.
+  bool tail_split;
   int n_part;
   int32_t* sortbuf;
   // optional per-launch timing of one kernel class
@@ -193,6 +198,10 @@ sat_status sat_side_ensure(sat_model* m);
 // Whether the LayerNorm backward also reduces the bias gradient of the residual
 // product below it (rows up to 2048 wide; wider rows use a separate column sum).
 inline bool sat_bias_in_ln_bwd(const Dims& D) { return D.d <= 2048; }
+// Whether the fc2 input-gradient product sums the fc1 bias gradient in its
+// epilogue: for the same widths (at 4096 it measured no faster, and the
+// weight-gradient products beside it on the second stream slowed down).
+inline bool sat_fc1_bias_in_epilogue(const Dims& D) { return D.d <= 2048; }
 void sat_side_destroy(sat_model* m);
 
 sat_status sat_validate_config(const sat_config* c);

@@ -251,6 +251,9 @@ static sat_status wgrad_t(sat_model* M, hipStream_t st, const bf16* yT, const bf
     }
     return gemm(M, w, LAY_K, LAY_K, EPI_ADAMW, tk, st);
   }
+  // the same sums as the fused epilogue's (no row split of the last round),
+  // so that the separate AdamW pass gives the fused step's parameters
+  w.no_tail_split = 1;
   return gemm(M, w, LAY_K, LAY_K, EPI_F32, tk, st);
 }
 
@@ -275,7 +278,8 @@ static sat_status wgrad(sat_model* M, bool trans, bool y_ready, const bf16* Y, l
 // launch of the partial-sum kernel then adds in order; otherwise the output is
 // summed by the column-sum kernels afterwards.
 static bool with_colsums(sat_model* M, GemmArgs& a) {
-  a.colsum_part = M->part;
+  a.colsum_part = sat_fc1_bias_in_epilogue(M->D) ? M->part : nullptr;
+  if (!a.colsum_part) return false;
   if (((long)a.M + 127) / 128 * a.N > M->part_elems || !gemm256_eligible(a, LAY_K, LAY_K, EPI_DGELU_BF16))
     a.colsum_part = nullptr;
   return a.colsum_part != nullptr;

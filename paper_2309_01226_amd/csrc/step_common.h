@@ -67,6 +67,7 @@ inline sat_status gemm(sat_model* M, const GemmArgs& a, int alay, int blay, int 
   GemmArgs b = a;
   b.splitk_ws = side ? M->splitk_ws2 : M->splitk_ws;
   b.splitk_ws_elems = M->splitk_ws_elems;
+  if (!M->tail_split) b.no_tail_split = 1;
   SAT_HIP(launch_gemm(b, alay, blay, epi, st));
   return SAT_OK;
 }
