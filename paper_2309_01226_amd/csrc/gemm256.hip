@@ -1067,11 +1067,19 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
     const int n = (int)(t - m * n4) * 4;
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
     if (vec) {
-      for (int s = 0; s < S; ++s) {
-        const floatx4 x = __builtin_nontemporal_load(
-            reinterpret_cast<const floatx4*>(ws + s * stride + m * N + n));
+      // eight slices' loads in flight per thread, added in slice order
+      const float* base = ws + m * N + n;
+      for (int s = 0; s < S; s += 8) {
+        floatx4 x[8];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc[e] += x[e];
+        for (int u = 0; u < 8; ++u)
+          if (s + u < S) x[u] = __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(base + (s + u) * stride));
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (s + u < S) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[e] += x[u][e];
+          }
       }
     } else {
       for (int s = 0; s < S; ++s)
