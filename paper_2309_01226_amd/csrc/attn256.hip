@@ -294,8 +294,8 @@ __global__ __launch_bounds__(NT, 1) void attn256_fwd_kernel(AttnArgs a) {
 
 // ================================================================ backward, dK and dV
 // Workgroup = 8 waves = 4 pairs; pair p owns keys k0 + 32 p .. + 31 of one
-// (batch, head) and loops over 32-query blocks.  Wave p (role A) holds K in
-// registers, forms P = exp2(S log2e - lse) from S = Q K^T and accumulates
+// (batch, head) and loops over 32-query blocks.  Wave p (role A) holds K
+// (half in registers, half in LDS), forms P = exp2(S log2e - lse) from S = Q K^T and accumulates
 // dV^T += dO^T P; wave p + 4 (role B) holds V, forms dP = dO V^T, takes P from
 // its partner through LDS and accumulates dK^T += Q^T dS, dS = P (dP - delta).
 // Every SIMD hosts one wave of each role.  The Q and dO rows of a block are
@@ -308,6 +308,14 @@ constexpr int KPW = 128;        // keys per workgroup
 constexpr int NT8 = 512;        // 8 waves
 constexpr int QT = BQ * DH;     // bf16 elements of one 32-row tile
 constexpr int STG_B = 2 * QT + 2 * 2 * BQ;  // Q rows, dO rows, lse2[32], delta[32] (fp32 as bf16 pairs)
+// Fragment reads are issued ahead of the MFMAs that take them (the compiler
+// otherwise waits for each read right before its MFMA).  The first NRF of a
+// lane's 16 resident K / V fragments stay in registers and the rest in LDS,
+// which keeps the read-ahead registers within the budget of two waves per SIMD.
+constexpr int PF_R = 2;   // dK / dV: row-fragment reads in flight (S, dP products)
+constexpr int PF_T = 2;   // dK / dV: transposed reads in flight (dV, dK products)
+constexpr int NRF = 8;    // dK / dV: resident fragments kept in registers
+constexpr int PF_RQ = 1;  // dQ: row-fragment reads in flight (S^T, dP^T products)
 
 __device__ __forceinline__ int swz_dual(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
 
@@ -332,8 +340,12 @@ __device__ __forceinline__ bf16x8 row_frag(const bf16* tile, int r, int c, int g
 }
 
 __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dkdv_kernel(AttnBwdArgs a) {
-  __shared__ __attribute__((aligned(1024))) bf16 smem[2 * STG_B + 4 * 64 * 16 * 2];
+  constexpr int SMEM = 2 * STG_B + 4 * 64 * 16 * 2 + 8 * (DH / 16 - NRF) * 64 * 8;
+  static_assert(SMEM * 2 <= 163840, "LDS budget");
+  __shared__ __attribute__((aligned(1024))) bf16 smem[SMEM];
   float* xbuf = reinterpret_cast<float*>(smem + 2 * STG_B);  // P exchange: [pair][16][64 lanes]
+  // resident fragments NRF.. of every wave: [wave][fragment][lane], 16 bytes each
+  bf16* rfs = smem + 2 * STG_B + 4 * 64 * 16 * 2;
   const int S = a.f.S;
   // one-dimensional grid, key blocks outermost: with a causal mask the
   // first key blocks see the most queries and are dispatched first
@@ -354,15 +366,20 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dkdv_kernel(AttnBwdArgs a)
   const float sc = a.f.scale * LOG2E;
 
   // resident operand: K (role A) or V (role B) of this lane's key, dims 16 c + 8 g .. + 7
-  bf16x8 rf[DH / 16];
+  bf16x8 rf[NRF];
+  bf16* rfw = rfs + (wave * (DH / 16 - NRF) * 64 + lane) * 8;  // this lane's fragment NRF; next: + 512
   {
     const bf16* base = role ? Vb : Kb;
     const long ld = role ? a.f.ldv : a.f.ldk;
     const __amdgpu_buffer_rsrc_t rk = rows_rsrc(base, kmin, ld);
     const uint32_t ko = key < S ? (uint32_t)(((long)(lane & 31) * ld + 8 * g) * 2) : OOB;
 #pragma unroll
-    for (int c = 0; c < DH / 16; ++c)
+    for (int c = 0; c < NRF; ++c)
       rf[c] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, ko, 32 * c, 0));
+#pragma unroll
+    for (int c = NRF; c < DH / 16; ++c)
+      *reinterpret_cast<bf16x8*>(rfw + (c - NRF) * 512) =
+          __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, ko, 32 * c, 0));
   }
   floatx16 acc[DH / 32];  // dV^T (role A) or dK^T (role B): dims 32 ot + acc_row(r, g), key = lane
 #pragma unroll
@@ -416,15 +433,26 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dkdv_kernel(AttnBwdArgs a)
     // S = Q K^T (role A) or dP = dO V^T (role B): rows = queries, column = key
     floatx16 x = zero16();
     if (active) {
+      // fragment reads PF_R k-steps ahead of their MFMA
       const bf16* rows = role ? dOs : Qs;
+      bf16x8 fr[PF_R + 1], fb[PF_R + 1];
+      auto rread = [&](int c) {
+        fr[c % (PF_R + 1)] = row_frag(rows, lane & 31, c, g);
+        if (c >= NRF) fb[c % (PF_R + 1)] = *reinterpret_cast<const bf16x8*>(rfw + (c - NRF) * 512);
+      };
 #pragma unroll
-      for (int c = 0; c < DH / 16; ++c)
-        x = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(rows, lane & 31, c, g), rf[c], x, 0, 0, 0);
+      for (int c = 0; c < PF_R; ++c) rread(c);
+#pragma unroll
+      for (int c = 0; c < DH / 16; ++c) {
+        if (c + PF_R < DH / 16) rread(c + PF_R);
+        x = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[c % (PF_R + 1)], c < NRF ? rf[c] : fb[c % (PF_R + 1)], x,
+                                                    0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
     // The next block's copies go out after this block's resident-operand
-    // products: the compiler keeps part of rf in scratch at this register
-    // budget, and one vmcnt counts loads in issue order, so a reload issued
-    // after the copies would wait for them.
+    // products (issued before them, the kernel alone ran 1.5 % faster but
+    // the step, where it shares the chip, no faster).
     if (j + 1 < nqb) fetch(j + 1);
     if (active) {
       if (role == 0) {
@@ -458,23 +486,31 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dkdv_kernel(AttnBwdArgs a)
           for (int e = 0; e < 4; ++e) x[4 * i + e] = xw[(4 * i + e) * 64 + lane] * (x[4 * i + e] - d4[e]);
         }
       }
-      // dV^T += dO^T P (role A) or dK^T += Q^T dS (role B)
+      // dV^T += dO^T P (role A) or dK^T += Q^T dS (role B); the transposed
+      // reads run PF_T MFMAs ahead
       const bf16* tt = role ? Qs : dOs;
+      bf16x8 xb[2];
 #pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        bf16x8 xb;
+      for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) xb[e] = f2bf(x[8 * hh + e]);
+        for (int e = 0; e < 8; ++e) xb[hh][e] = f2bf(x[8 * hh + e]);
+      auto tread = [&](int i) {  // i = 8 hh + ot
+        const int hh = i >> 3, ot = i & 7;
         const bf16* tb = tt + 16 * hh * DH;
+        // rows + 8 flip bit 1 of the row's swizzle group, i.e. chunk bit 1
+        const int to = tofs[ot & 3] + (ot >> 2) * 128;
+        const bf16x4 lo = ds_read_tr((const lds_bf16x4*)lds(tb + to));
+        const bf16x4 hi = ds_read_tr((const lds_bf16x4*)lds(tb + ((to ^ 16) + 8 * DH)));
+        return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      };
+      bf16x8 tf[PF_T + 1];
 #pragma unroll
-        for (int ot = 0; ot < DH / 32; ++ot) {
-          // rows + 8 flip bit 1 of the row's swizzle group, i.e. chunk bit 1
-          const int to = tofs[ot & 3] + (ot >> 2) * 128;
-          const bf16x4 lo = ds_read_tr((const lds_bf16x4*)lds(tb + to));
-          const bf16x4 hi = ds_read_tr((const lds_bf16x4*)lds(tb + ((to ^ 16) + 8 * DH)));
-          acc[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7),
-                                                            xb, acc[ot], 0, 0, 0);
-        }
+      for (int i = 0; i < PF_T; ++i) tf[i] = tread(i);
+#pragma unroll
+      for (int i = 0; i < 2 * (DH / 32); ++i) {
+        if (i + PF_T < 2 * (DH / 32)) tf[(i + PF_T) % (PF_T + 1)] = tread(i + PF_T);
+        acc[i & 7] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tf[i % (PF_T + 1)], xb[i >> 3], acc[i & 7], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
     if (j + 1 < nqb) {
@@ -620,9 +656,15 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dq_kernel(AttnBwdArgs a) {
     floatx16 x = zero16();
     if (active) {
       const bf16* rows = role ? Vs : Ks;
+      bf16x8 fr[PF_RQ + 1];
 #pragma unroll
-      for (int c = 0; c < DH / 16; ++c)
-        x = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(rows, lane & 31, c, g), rf[c], x, 0, 0, 0);
+      for (int c = 0; c < PF_RQ; ++c) fr[c] = row_frag(rows, lane & 31, c, g);
+#pragma unroll
+      for (int c = 0; c < DH / 16; ++c) {
+        if (c + PF_RQ < DH / 16) fr[(c + PF_RQ) % (PF_RQ + 1)] = row_frag(rows, lane & 31, c + PF_RQ, g);
+        x = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[c % (PF_RQ + 1)], rf[c], x, 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
       if (role == 0) {
         // P^T = exp2(S^T log2e - lse2); zero for keys past S or (causal) past the query
         const int lim = min(S, a.f.causal ? q + 1 : S) - kv0 - 4 * g;  // keys with acc_row < lim valid
@@ -642,21 +684,21 @@ __global__ __launch_bounds__(NT8, 1) void attn256_bwd_dq_kernel(AttnBwdArgs a) {
     if (active && role == 1) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) x[r] = xw[r * 64 + lane] * (x[r] - lsd);
+      bf16x8 xb[2];
 #pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        bf16x8 xb;
+      for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) xb[e] = f2bf(x[8 * hh + e]);
-        const bf16* tb = Ks + 16 * hh * DH;
+        for (int e = 0; e < 8; ++e) xb[hh][e] = f2bf(x[8 * hh + e]);
+      auto tread = [&](int i) {  // i = 8 hh + ot
+        const bf16* tb = Ks + 16 * (i >> 3) * DH;
+        const int to = tofs[i & 3] + ((i & 7) >> 2) * 128;
+        const bf16x4 lo = ds_read_tr((const lds_bf16x4*)lds(tb + to));
+        const bf16x4 hi = ds_read_tr((const lds_bf16x4*)lds(tb + ((to ^ 16) + 8 * DH)));
+        return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      };
 #pragma unroll
-        for (int ot = 0; ot < DH / 32; ++ot) {
-          const int to = tofs[ot & 3] + (ot >> 2) * 128;
-          const bf16x4 lo = ds_read_tr((const lds_bf16x4*)lds(tb + to));
-          const bf16x4 hi = ds_read_tr((const lds_bf16x4*)lds(tb + ((to ^ 16) + 8 * DH)));
-          acc[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7),
-                                                            xb, acc[ot], 0, 0, 0);
-        }
-      }
+      for (int i = 0; i < 2 * (DH / 32); ++i)
+        acc[i & 7] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tread(i), xb[i >> 3], acc[i & 7], 0, 0, 0);
     }
   }
   if (role == 1 && q < S) {
